@@ -1,0 +1,176 @@
+"""Seeded synthetic inputs shared by the oracle, the tests and the bench.
+
+This module holds data only: shapes of the workloads and seeded random
+draws.  It contains none of the method's arithmetic (no norm, projection,
+attention, similarity or compaction), so that the CPU oracle and the HIP
+path can both consume its arrays without sharing any computation.
+
+Every generator is deterministic in (seed, tensor name): each tensor gets
+its own numpy PCG64 stream derived from the master seed and a CRC of the
+name, so adding a tensor never shifts the values of another.
+
+Values meant for a bf16 run are produced as float32 arrays whose entries are
+exactly representable in bfloat16 (round-to-nearest-even of the float32
+draw, done by torch's dtype conversion), so both sides see identical numbers.
+"""
+from __future__ import annotations
+
+import dataclasses
+import zlib
+
+import numpy as np
+
+__all__ = [
+    "DecoderShape", "EncoderShape", "TINY", "LLAMA7B", "BERT_BASE",
+    "rng", "to_bf16_values", "decoder_weights", "encoder_weights",
+    "token_ids", "normal", "gains",
+]
+
+
+@dataclasses.dataclass(frozen=True)
+class DecoderShape:
+    """Llama-style pre-norm decoder (RMSNorm, rotary positions, SwiGLU)."""
+    n_layers: int
+    d_model: int
+    n_heads: int
+    head_dim: int
+    d_ff: int
+    vocab: int
+    rms_eps: float = 1e-6
+    rope_theta: float = 10000.0
+
+    @property
+    def d_q(self) -> int:
+        return self.n_heads * self.head_dim
+
+
+@dataclasses.dataclass(frozen=True)
+class EncoderShape:
+    """BERT-style post-norm encoder (LayerNorm, learned positions, GELU)."""
+    n_layers: int
+    d_model: int
+    n_heads: int
+    head_dim: int
+    d_ff: int
+    vocab: int
+    max_pos: int
+    n_classes: int = 2
+    ln_eps: float = 1e-12
+
+    @property
+    def d_q(self) -> int:
+        return self.n_heads * self.head_dim
+
+
+# The workload shapes: a tiny decoder that the oracle runs in seconds, the
+# 7B-class decoder (32 layers, width 4096, 32 heads of 128, FFN 11008,
+# vocab 32000) and a BERT-base-class encoder (12 layers, width 768).
+TINY = DecoderShape(n_layers=4, d_model=256, n_heads=4, head_dim=64, d_ff=1024, vocab=1024)
+LLAMA7B = DecoderShape(n_layers=32, d_model=4096, n_heads=32, head_dim=128, d_ff=11008, vocab=32000)
+BERT_BASE = EncoderShape(n_layers=12, d_model=768, n_heads=12, head_dim=64, d_ff=3072,
+                         vocab=30522, max_pos=512)
+
+
+def rng(seed: int, name: str) -> np.random.Generator:
+    """Independent PCG64 stream for tensor `name` under master `seed`."""
+    return np.random.Generator(np.random.PCG64([seed & 0xFFFFFFFF, zlib.crc32(name.encode())]))
+
+
+def to_bf16_values(x: np.ndarray) -> np.ndarray:
+    """float32 array of the bfloat16 values nearest to x (RNE, via torch)."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
+
+
+def _finish(x: np.ndarray, dtype: str) -> np.ndarray:
+    x = x.astype(np.float32)
+    if dtype == "bf16":
+        return to_bf16_values(x)
+    if dtype != "f32":
+        raise ValueError(f"dtype must be 'f32' or 'bf16', got {dtype!r}")
+    return x
+
+
+def normal(seed: int, name: str, shape, std: float = 1.0, mean: float = 0.0,
+           dtype: str = "f32") -> np.ndarray:
+    """N(mean, std^2) draws of `shape`."""
+    x = rng(seed, name).standard_normal(size=shape, dtype=np.float32)
+    return _finish(x * np.float32(std) + np.float32(mean), dtype)
+
+
+def gains(seed: int, name: str, shape, dtype: str = "f32") -> np.ndarray:
+    """Norm gains 1 + 0.1 N(0,1): non-unit so that a gain applied to the
+    wrong channel or layer changes the result."""
+    return normal(seed, name, shape, std=0.1, mean=1.0, dtype=dtype)
+
+
+def token_ids(seed: int, vocab: int, batch: int, length: int, name: str = "ids") -> np.ndarray:
+    """Uniform token ids in [0, vocab), shape [batch, length], int32."""
+    return rng(seed, name).integers(0, vocab, size=(batch, length), dtype=np.int64).astype(np.int32)
+
+
+def decoder_weights(shape: DecoderShape, seed: int, dtype: str = "f32", std: float = 0.02) -> dict:
+    """Random-init weights of a Llama-style decoder.
+
+    Linear weights and the embedding are N(0, std^2) in nn.Linear
+    [out_features, in_features] order; norm gains are 1 + 0.1 N(0,1).
+    Returns {"embed", "final_norm", "lm_head", "layers": [per-layer dict]}
+    with per-layer keys attn_norm, wq, wk, wv, wo, ffn_norm, w_gate, w_up,
+    w_down.
+    """
+    D, Dq, F, V = shape.d_model, shape.d_q, shape.d_ff, shape.vocab
+    out = {
+        "embed": normal(seed, "embed", (V, D), std, dtype=dtype),
+        "final_norm": gains(seed, "final_norm", (D,), dtype),
+        "lm_head": normal(seed, "lm_head", (V, D), std, dtype=dtype),
+        "layers": [],
+    }
+    for i in range(1, shape.n_layers + 1):
+        p = f"layer{i}."
+        out["layers"].append({
+            "attn_norm": gains(seed, p + "attn_norm", (D,), dtype),
+            "wq": normal(seed, p + "wq", (Dq, D), std, dtype=dtype),
+            "wk": normal(seed, p + "wk", (Dq, D), std, dtype=dtype),
+            "wv": normal(seed, p + "wv", (Dq, D), std, dtype=dtype),
+            "wo": normal(seed, p + "wo", (D, Dq), std, dtype=dtype),
+            "ffn_norm": gains(seed, p + "ffn_norm", (D,), dtype),
+            "w_gate": normal(seed, p + "w_gate", (F, D), std, dtype=dtype),
+            "w_up": normal(seed, p + "w_up", (F, D), std, dtype=dtype),
+            "w_down": normal(seed, p + "w_down", (D, F), std, dtype=dtype),
+        })
+    return out
+
+
+def encoder_weights(shape: EncoderShape, seed: int, dtype: str = "f32", std: float = 0.02) -> dict:
+    """Random-init weights of a BERT-style post-norm encoder with a linear
+    classification head on the first ([CLS]) position.
+
+    Linear weights, biases and embeddings are N(0, std^2) (biases non-zero
+    on purpose, so that a dropped bias is visible); LayerNorm gains are
+    1 + 0.1 N(0,1) and shifts N(0, std^2).
+    """
+    D, Dq, F, V = shape.d_model, shape.d_q, shape.d_ff, shape.vocab
+    out = {
+        "word_embed": normal(seed, "word_embed", (V, D), std, dtype=dtype),
+        "pos_embed": normal(seed, "pos_embed", (shape.max_pos, D), std, dtype=dtype),
+        "type_embed": normal(seed, "type_embed", (D,), std, dtype=dtype),
+        "embed_ln_g": gains(seed, "embed_ln_g", (D,), dtype),
+        "embed_ln_b": normal(seed, "embed_ln_b", (D,), std, dtype=dtype),
+        "cls_w": normal(seed, "cls_w", (shape.n_classes, D), std, dtype=dtype),
+        "cls_b": normal(seed, "cls_b", (shape.n_classes,), std, dtype=dtype),
+        "layers": [],
+    }
+    for i in range(1, shape.n_layers + 1):
+        p = f"layer{i}."
+        lay = {}
+        for nm, shp in (("wq", (Dq, D)), ("wk", (Dq, D)), ("wv", (Dq, D)), ("wo", (D, Dq)),
+                        ("w_in", (F, D)), ("w_out", (D, F))):
+            lay[nm] = normal(seed, p + nm, shp, std, dtype=dtype)
+        for nm, n in (("bq", Dq), ("bk", Dq), ("bv", Dq), ("bo", D), ("b_in", F), ("b_out", D),
+                      ("ln1_b", D), ("ln2_b", D)):
+            lay[nm] = normal(seed, p + nm, (n,), std, dtype=dtype)
+        lay["ln1_g"] = gains(seed, p + "ln1_g", (D,), dtype)
+        lay["ln2_g"] = gains(seed, p + "ln2_g", (D,), dtype)
+        out["layers"].append(lay)
+    return out

@@ -1,0 +1,474 @@
+"""CPU oracle of ADEPT's token-level early-exit forward pass (fp64, numpy).
+
+TEST INFRASTRUCTURE ONLY.  This module is the slow, plain reference that the
+HIP path is checked against.  Only the test suite, the package smoke check
+and the bench's CPU-baseline leg may import it; the product path never calls
+it and shares no code with it.
+
+Everything is computed in float64 from the (float32 / bfloat16-valued) seeded
+inputs.  The paper fixes no precision, so fp64 is the reference arithmetic;
+the one place where floating point decides an integer (the exit decision) is
+also taken in fp64, which is the precision the GPU exit test reduces in.
+
+Notation follows the paper: layers are numbered i = 1..N (Section 3, state
+space); token j's hidden state after layer i is s^h_{i,j}, written h_i here;
+h_0 is the embedding.  "Exit at i*" means layers 1..i* run in full and the
+skipped layers r = i*+1..N only receive generated keys/values (Section 4,
+Eq. 6; Section 4.3, Eq. 9).
+
+Readings of the paper taken here (where it is silent or ambiguous):
+  * inertia at layer i is the sum of the unit-normalised states of layers
+    1..i-1 (Eq. 7); the test at layer i compares h_i with it and the update
+    with h_i happens after the test.  At i = 1 the sum is empty, the cosine
+    is 0/0 = NaN and the token continues.
+  * the test runs only for i_min <= i <= N-1 (exiting at N skips nothing).
+  * the mapped state s~ fed to the KV generation is the identity map of the
+    exit state, s~ = h_{i*} (the trained mapper is not available).
+  * generated K/V of layer r apply layer r's own pre-attention RMSNorm, its
+    own K/V projection and, for K, the rotary embedding at the token's
+    position -- i.e. s~ is treated as layer r's input (Eq. 9).
+  * generated entries are visible to every active token's attention at the
+    layers after the exit (Section 4.3; Appendix I), so K/V of tokens that
+    exit at layer i are written before the attention of layer i+1.
+  * an exited token's final state is its mapped state (Fig. 1 caption), so
+    its logits use h_{i*}.
+  * compaction keeps both lists in ascending row order (Appendix I update).
+  * the "local" metric of Appendix H.3 is cos(h_i, h_{i-1}).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+F64 = np.float64
+
+GLOBAL = "global"   # inertia metric, Section 4.1 Eq. 7-8
+LOCAL = "local"     # consecutive-layer metric, Appendix H.3
+
+
+# ---------------------------------------------------------------------------
+# Building blocks of the base model (not the paper's contribution; the base
+# model is a Llama-style pre-norm decoder used in inference mode, Section 5).
+# ---------------------------------------------------------------------------
+
+def rms_norm(x, gain, eps):
+    """y = x / sqrt(mean(x^2) + eps) * gain over the last axis."""
+    x = np.asarray(x, F64)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * np.asarray(gain, F64)
+
+
+def layer_norm(x, gain, bias, eps):
+    """(x - mean) / sqrt(var + eps) * gain + bias over the last axis."""
+    x = np.asarray(x, F64)
+    mu = np.mean(x, axis=-1, keepdims=True)
+    var = np.mean((x - mu) ** 2, axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + eps) * np.asarray(gain, F64) + np.asarray(bias, F64)
+
+
+def rope_cos_sin(pos, head_dim, theta):
+    """cos/sin of the rotary angles pos * theta^(-2k/head_dim), k < head_dim/2, in fp64."""
+    k = np.arange(head_dim // 2, dtype=F64)
+    inv_freq = np.power(F64(theta), -2.0 * k / head_dim)
+    ang = np.asarray(pos, F64)[:, None] * inv_freq[None, :]
+    return np.cos(ang), np.sin(ang)
+
+
+def apply_rope(x, pos, theta):
+    """Rotary embedding on x[n, H, hd] at positions pos[n].
+
+    Pairing is (k, k + hd/2) ("rotate half"): the first half becomes
+    x1 cos - x2 sin and the second half x2 cos + x1 sin.
+    """
+    x = np.asarray(x, F64)
+    hd = x.shape[-1]
+    c, s = rope_cos_sin(pos, hd, theta)
+    c = c[:, None, :]
+    s = s[:, None, :]
+    x1, x2 = x[..., : hd // 2], x[..., hd // 2:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def gelu_erf(x):
+    erf = np.vectorize(math.erf, otypes=[F64])
+    return 0.5 * x * (1.0 + erf(x / math.sqrt(2.0)))
+
+
+def softmax_rows(scores):
+    m = np.max(scores, axis=-1, keepdims=True)
+    e = np.exp(scores - m)
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def as64(w):
+    """Convert a weight dict tree to float64 arrays."""
+    if isinstance(w, dict):
+        return {k: as64(v) for k, v in w.items()}
+    if isinstance(w, list):
+        return [as64(v) for v in w]
+    return np.asarray(w, F64)
+
+
+# ---------------------------------------------------------------------------
+# The exit policy (Section 4.1, Eq. 7-8; local variant Appendix H.3).
+# ---------------------------------------------------------------------------
+
+def cosine(h, ref):
+    """Row-wise <h, ref> / (|h| |ref|) in fp64; NaN where either norm is 0.
+
+    For the global metric ref is the inertia sum; Eq. 8 compares the unit
+    vectors, which is this cosine.  For the local metric ref is h_{i-1}.
+    """
+    h = np.asarray(h, F64)
+    ref = np.asarray(ref, F64)
+    s_hh = np.einsum("nd,nd->n", h, h)
+    s_rr = np.einsum("nd,nd->n", ref, ref)
+    s_hr = np.einsum("nd,nd->n", h, ref)
+    den = np.sqrt(s_hh) * np.sqrt(s_rr)
+    out = np.full(h.shape[0], np.nan)
+    ok = den > 0
+    out[ok] = s_hr[ok] / den[ok]
+    return out
+
+
+def exit_decision(sim, layer, n_layers, delta, min_exit_layer):
+    """Eq. 8: exit iff sim >= delta, tested only for min_exit_layer <= layer <= N-1.
+
+    NaN (undefined cosine) never exits.  delta = +inf never fires.
+    """
+    sim = np.asarray(sim, F64)
+    if not (min_exit_layer <= layer <= n_layers - 1):
+        return np.zeros(sim.shape, bool)
+    with np.errstate(invalid="ignore"):
+        return sim >= delta
+
+
+def inertia_update(inertia, h):
+    """Eq. 7: add the unit-normalised current state to the running sum.
+
+    A zero row adds nothing (its direction is undefined)."""
+    h = np.asarray(h, F64)
+    nrm = np.sqrt(np.einsum("nd,nd->n", h, h))
+    add = np.zeros_like(h)
+    ok = nrm > 0
+    add[ok] = h[ok] / nrm[ok, None]
+    return np.asarray(inertia, F64) + add
+
+
+def compact(flags, active):
+    """Appendix I: split the active index list by the exit flags.
+
+    Returns (still_active, exited), each in the order of `active` (ascending
+    when `active` is ascending)."""
+    still = [int(a) for a, f in zip(active, flags) if not f]
+    gone = [int(a) for a, f in zip(active, flags) if f]
+    return np.array(still, np.int64), np.array(gone, np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Decoupled KV generation (Section 4, Eq. 6; Section 4.3, Eq. 9).
+# ---------------------------------------------------------------------------
+
+def layer_kv(layer_w, x, pos, shape):
+    """Layer r's own key/value path applied to input states x[n, D]:
+    K = RoPE(RMSNorm_r(x) Wk_r^T, pos), V = RMSNorm_r(x) Wv_r^T, as [n, H, hd]."""
+    n = x.shape[0]
+    u = rms_norm(x, layer_w["attn_norm"], shape.rms_eps)
+    k = (u @ layer_w["wk"].T).reshape(n, shape.n_heads, shape.head_dim)
+    v = (u @ layer_w["wv"].T).reshape(n, shape.n_heads, shape.head_dim)
+    return apply_rope(k, pos, shape.rope_theta), v
+
+
+def kv_generate(weights, shape, s_map, exit_layer, pos):
+    """Eq. 9 for a set of exited tokens: for every skipped layer r > i*_j,
+    s^{kv}_{r,j} = s~_j W_r^{kv}, with W_r^{kv} = [Wk_r | Wv_r] applied after
+    layer r's pre-attention norm and with RoPE on the key half.
+
+    s_map [n, D], exit_layer [n] (1-based i*), pos [n].
+    Returns {r: (token_idx, K [m, H, hd], V [m, H, hd])} for r = 1..N, where
+    token_idx lists the tokens with i* < r.  Layers are independent of each
+    other (Eq. 6), so each is computed on its own.
+    """
+    s_map = np.asarray(s_map, F64)
+    exit_layer = np.asarray(exit_layer)
+    pos = np.asarray(pos)
+    out = {}
+    for r in range(1, shape.n_layers + 1):
+        idx = np.nonzero(exit_layer < r)[0]
+        if idx.size == 0:
+            continue
+        k, v = layer_kv(weights["layers"][r - 1], s_map[idx], pos[idx], shape)
+        out[r] = (idx, k, v)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Attention over a key/value cache that mixes computed and generated entries
+# (Section 3, Eq. 5; Section 4.3).
+# ---------------------------------------------------------------------------
+
+def attend(q, k_cache, v_cache, slot_base, pos, key_len=None, causal=True, key_mask=None):
+    """Softmax attention of queries q[n, H, hd] over cache rows.
+
+    Query j reads cache slots slot_base[j] + t for t in [0, pos[j]] when
+    causal, else t in [0, key_len[j]); key_mask (bool [n, L]) optionally
+    removes keys.  Cache entries must all be defined (NaN-poisoned
+    unwritten slots propagate and are caught by the tests).
+    """
+    n, H, hd = q.shape
+    out = np.empty((n, H, hd), F64)
+    scale = 1.0 / math.sqrt(hd)
+    for j in range(n):
+        L = int(pos[j]) + 1 if causal else int(key_len[j])
+        sl = slice(int(slot_base[j]), int(slot_base[j]) + L)
+        K = k_cache[sl]   # [L, H, hd]
+        V = v_cache[sl]
+        s = np.einsum("hd,lhd->hl", q[j], K) * scale
+        if key_mask is not None:
+            s = np.where(key_mask[j][None, :L], s, -np.inf)
+        p = softmax_rows(s)
+        out[j] = np.einsum("hl,lhd->hd", p, V)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Generative forward with token-level exit (Section 4, Appendix I).
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class ExitConfig:
+    delta: float = math.inf        # Eq. 8 threshold; +inf never fires
+    min_exit_layer: int = 1
+    metric: str = GLOBAL
+
+
+@dataclasses.dataclass
+class KVCache:
+    """Per-layer key/value cache [N, B * s_max, H, hd]; slot of (b, p) = b * s_max + p."""
+    k: np.ndarray
+    v: np.ndarray
+    s_max: int
+
+    @classmethod
+    def empty(cls, shape, batch, s_max):
+        dims = (shape.n_layers, batch * s_max, shape.n_heads, shape.head_dim)
+        return cls(np.full(dims, np.nan), np.full(dims, np.nan), s_max)
+
+
+@dataclasses.dataclass
+class TokenPassResult:
+    h_final: np.ndarray        # [n, D]: h_{i*} for exited tokens, h_N otherwise
+    exit_layer: np.ndarray     # [n], 1-based; N means never exited
+    logits: np.ndarray         # [n, V]
+    sims: np.ndarray           # [N, n] cosine at each layer (NaN where not tested/inactive)
+    active_counts: list        # active rows entering each layer 1..N
+    hidden: list               # hidden[i] = [n, D] states after layer i (frozen rows for exited)
+    inertia: np.ndarray        # [n, D] inertia after the last test (global metric)
+
+
+def decoder_layer(layer_w, shape, h_in, pos, seq, cache, layer):
+    """One regular decoder layer for the active rows (Appendix I, "Process 1").
+
+    h_in [n, D] are the rows' states h_{i-1}; their own K/V are written to
+    the cache first, then every row attends causally over its sequence."""
+    n = h_in.shape[0]
+    H, hd = shape.n_heads, shape.head_dim
+    u = rms_norm(h_in, layer_w["attn_norm"], shape.rms_eps)
+    q = apply_rope((u @ layer_w["wq"].T).reshape(n, H, hd), pos, shape.rope_theta)
+    k, v = layer_kv(layer_w, h_in, pos, shape)
+    slots = seq * cache.s_max + pos
+    cache.k[layer - 1][slots] = k
+    cache.v[layer - 1][slots] = v
+    o = attend(q, cache.k[layer - 1], cache.v[layer - 1], seq * cache.s_max, pos)
+    h1 = h_in + o.reshape(n, H * hd) @ layer_w["wo"].T
+    u2 = rms_norm(h1, layer_w["ffn_norm"], shape.rms_eps)
+    ff = (silu(u2 @ layer_w["w_gate"].T) * (u2 @ layer_w["w_up"].T)) @ layer_w["w_down"].T
+    return h1 + ff
+
+
+def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None):
+    """Run a set of token rows through the N layers with token-level exit.
+
+    This is the prefill of Appendix I when the rows are a whole prompt batch,
+    and one generation step when the rows are the newly sampled tokens (each
+    at the end of its sequence).  Per layer i:
+      1. the active rows run the regular layer (own K/V into cache[i]);
+      2. the exit test of Eq. 8 (global: against the inertia of Eq. 7, then
+         the inertia update; local: against h_{i-1});
+      3. the active list is split into still-active and exited rows;
+      4. the exited rows' K/V for every layer r > i are generated (Eq. 9).
+    force_layer (optional int [n]): a value f > 0 replaces the policy for that
+    row by "exit exactly at layer f" (f >= N: never); 0 keeps the policy.
+    """
+    N, D = shape.n_layers, shape.d_model
+    h0 = np.asarray(h0, F64)
+    n = h0.shape[0]
+    pos = np.asarray(pos, np.int64)
+    seq = np.asarray(seq, np.int64)
+    h = h0.copy()
+    inertia = np.zeros((n, D))
+    exit_layer = np.full(n, N, np.int64)
+    active = np.arange(n)
+    sims = np.full((N, n), np.nan)
+    counts, hidden = [], []
+    for i in range(1, N + 1):
+        counts.append(int(active.size))
+        h_prev = h.copy()
+        if active.size:
+            h[active] = decoder_layer(weights["layers"][i - 1], shape, h_prev[active],
+                                      pos[active], seq[active], cache, i)
+        ref = inertia[active] if cfg.metric == GLOBAL else h_prev[active]
+        sim = cosine(h[active], ref) if active.size else np.zeros(0)
+        sims[i - 1, active] = sim
+        flags = exit_decision(sim, i, N, cfg.delta, cfg.min_exit_layer)
+        if force_layer is not None:
+            f = np.asarray(force_layer)[active]
+            forced = f > 0
+            flags = np.where(forced, (f == i) & (i <= N - 1), flags)
+        if cfg.metric == GLOBAL and active.size:
+            inertia[active] = inertia_update(inertia[active], h[active])
+        active, exited = compact(flags, active)
+        exit_layer[exited] = i
+        if exited.size and i < N:
+            gen = kv_generate(weights, shape, h[exited], exit_layer[exited], pos[exited])
+            for r, (idx, k, v) in gen.items():
+                slots = seq[exited[idx]] * cache.s_max + pos[exited[idx]]
+                cache.k[r - 1][slots] = k
+                cache.v[r - 1][slots] = v
+        hidden.append(h.copy())
+    logits = rms_norm(h, weights["final_norm"], shape.rms_eps) @ weights["lm_head"].T
+    return TokenPassResult(h, exit_layer, logits, sims, counts, hidden, inertia)
+
+
+def prefill(weights, shape, ids, cfg, s_max=None, force_layer=None):
+    """Prefill of a [B, T] prompt batch; rows are j = b*T + p (Appendix I's
+    [4N, D_h] flattening).  Returns (TokenPassResult, KVCache)."""
+    ids = np.asarray(ids)
+    B, T = ids.shape
+    s_max = T if s_max is None else s_max
+    cache = KVCache.empty(shape, B, s_max)
+    pos = np.tile(np.arange(T), B)
+    seq = np.repeat(np.arange(B), T)
+    h0 = np.asarray(weights["embed"], F64)[ids.reshape(-1)]
+    res = token_pass(weights, shape, h0, pos, seq, cache, cfg,
+                     None if force_layer is None else np.asarray(force_layer).reshape(-1))
+    return res, cache
+
+
+def greedy(logits):
+    """Greedy choice with ties going to the lowest token id."""
+    return np.argmax(np.asarray(logits), axis=-1)
+
+
+def decode_step(weights, shape, cache, ids, pos, cfg, force_layer=None):
+    """One generation step (Appendix I, generation phase): token ids[b] sits
+    at position pos[b] of sequence b; inertia starts empty for the new token."""
+    ids = np.asarray(ids)
+    B = ids.shape[0]
+    h0 = np.asarray(weights["embed"], F64)[ids]
+    return token_pass(weights, shape, h0, np.asarray(pos), np.arange(B), cache, cfg, force_layer)
+
+
+def generate(weights, shape, ids, n_steps, cfg, force_layer=None):
+    """Prefill of ids [B, T] then n_steps greedy generation steps.
+    Returns (prefill result, list of step results, generated ids [B, n_steps], cache)."""
+    B, T = np.asarray(ids).shape
+    res, cache = prefill(weights, shape, ids, cfg, s_max=T + n_steps, force_layer=force_layer)
+    last = res.logits.reshape(B, T, -1)[:, -1]
+    nxt = greedy(last)
+    steps, out = [], []
+    for s in range(n_steps):
+        out.append(nxt)
+        st = decode_step(weights, shape, cache, nxt, np.full(B, T + s), cfg)
+        steps.append(st)
+        nxt = greedy(st.logits)
+    return res, steps, np.stack(out, axis=1) if out else np.zeros((B, 0), np.int64), cache
+
+
+def full_depth_logits(weights, shape, ids):
+    """The base model without exits (delta = +inf) -- the reference point of
+    every compute-reduction figure in the paper."""
+    res, _ = prefill(weights, shape, ids, ExitConfig(delta=math.inf))
+    return res.logits
+
+
+# ---------------------------------------------------------------------------
+# Classification mode (Section 4.3, "downstream tasks"): post-norm encoder,
+# computation stops at the exit layer, no KV generation.
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class ClassifyResult:
+    logits: np.ndarray       # [B, n_classes] from the [CLS] state at its exit
+    exit_layer: np.ndarray   # [B*T]
+    cls_exit_layer: np.ndarray
+    h_final: np.ndarray
+    sims: np.ndarray
+    active_counts: list
+
+
+def classify(weights, shape, ids, cfg, force_layer=None):
+    """Token-level exit in an encoder classifier.
+
+    Readings: exited tokens stop entirely (no KV generation) and leave the
+    key set of later layers; a sequence's output is the [CLS] (position 0)
+    state at its exit, fed to the linear head.  Tokens of a sequence whose
+    [CLS] has exited no longer influence the output."""
+    ids = np.asarray(ids)
+    B, T = ids.shape
+    N, D, H, hd = shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim
+    n = B * T
+    pos = np.tile(np.arange(T), B)
+    seq = np.repeat(np.arange(B), T)
+    x = (np.asarray(weights["word_embed"], F64)[ids.reshape(-1)]
+         + np.asarray(weights["pos_embed"], F64)[pos] + np.asarray(weights["type_embed"], F64))
+    h = layer_norm(x, weights["embed_ln_g"], weights["embed_ln_b"], shape.ln_eps)
+    inertia = np.zeros((n, D))
+    exit_layer = np.full(n, N, np.int64)
+    live = np.ones(n, bool)
+    active = np.arange(n)
+    sims = np.full((N, n), np.nan)
+    counts = []
+    scale = 1.0 / math.sqrt(hd)
+    for i in range(1, N + 1):
+        counts.append(int(active.size))
+        lw = weights["layers"][i - 1]
+        h_prev = h.copy()
+        if active.size:
+            xa = h_prev[active]
+            m = active.size
+            q = (xa @ lw["wq"].T + lw["bq"]).reshape(m, H, hd)
+            kk = (xa @ lw["wk"].T + lw["bk"]).reshape(m, H, hd)
+            vv = (xa @ lw["wv"].T + lw["bv"]).reshape(m, H, hd)
+            o = np.empty((m, H, hd))
+            sa = seq[active]
+            for b in np.unique(sa):
+                rows = np.nonzero(sa == b)[0]           # live tokens of sequence b
+                s = np.einsum("qhd,khd->hqk", q[rows], kk[rows]) * scale
+                o[rows] = np.einsum("hqk,khd->qhd", softmax_rows(s), vv[rows])
+            h1 = layer_norm(xa + o.reshape(m, H * hd) @ lw["wo"].T + lw["bo"],
+                            lw["ln1_g"], lw["ln1_b"], shape.ln_eps)
+            ff = gelu_erf(h1 @ lw["w_in"].T + lw["b_in"]) @ lw["w_out"].T + lw["b_out"]
+            h[active] = layer_norm(h1 + ff, lw["ln2_g"], lw["ln2_b"], shape.ln_eps)
+        ref = inertia[active] if cfg.metric == GLOBAL else h_prev[active]
+        sim = cosine(h[active], ref) if active.size else np.zeros(0)
+        sims[i - 1, active] = sim
+        flags = exit_decision(sim, i, N, cfg.delta, cfg.min_exit_layer)
+        if force_layer is not None:
+            f = np.asarray(force_layer).reshape(-1)[active]
+            forced = f > 0
+            flags = np.where(forced, (f == i) & (i <= N - 1), flags)
+        if cfg.metric == GLOBAL and active.size:
+            inertia[active] = inertia_update(inertia[active], h[active])
+        active, exited = compact(flags, active)
+        exit_layer[exited] = i
+        live[exited] = False
+    cls_rows = np.arange(B) * T
+    logits = h[cls_rows] @ np.asarray(weights["cls_w"], F64).T + np.asarray(weights["cls_b"], F64)
+    return ClassifyResult(logits, exit_layer, exit_layer[cls_rows], h, sims, counts)
