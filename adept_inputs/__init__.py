@@ -174,3 +174,54 @@ def encoder_weights(shape: EncoderShape, seed: int, dtype: str = "f32", std: flo
         lay["ln2_g"] = gains(seed, p + "ln2_g", (D,), dtype)
         out["layers"].append(lay)
     return out
+
+
+def decoder_weights_torch(shape: DecoderShape, seed: int, device, dtype=None, std: float = 0.02):
+    """Random-init decoder weights generated directly on `device` (torch's
+    counter-based generator), stacked over layers: attn_norm/ffn_norm [N, D],
+    wq/wk/wv [N, Dq, D], wo [N, D, Dq], w_gate/w_up [N, F, D], w_down [N, D, F],
+    embed/lm_head [V, D], final_norm [D].  Linear weights N(0, std^2), gains
+    1 + 0.1 N(0,1).  Each layer slice has its own seed, so any layer can be
+    regenerated alone.  Used for the 7B-class shapes, whose weights are too
+    large to draw on the host.
+    """
+    import torch
+    dtype = torch.bfloat16 if dtype is None else dtype
+    g = torch.Generator(device=device)
+    N, D, Dq, F, V = shape.n_layers, shape.d_model, shape.d_q, shape.d_ff, shape.vocab
+
+    def fill(out, name, scale, mean):
+        g.manual_seed((seed * 1000003 + zlib.crc32(name.encode())) & 0x7FFFFFFFFFFFFFFF)
+        tmp = torch.randn(out.shape, generator=g, device=device, dtype=torch.float32)
+        out.copy_(tmp.mul_(scale).add_(mean))
+
+    def stacked(name, shp, scale, mean=0.0):
+        out = torch.empty((N,) + shp, dtype=dtype, device=device)
+        for i in range(N):
+            fill(out[i], f"layer{i + 1}.{name}", scale, mean)
+        return out
+
+    def single(name, shp, scale, mean=0.0):
+        out = torch.empty(shp, dtype=dtype, device=device)
+        fill(out, name, scale, mean)
+        return out
+
+    return {
+        "embed": single("embed", (V, D), std),
+        "final_norm": single("final_norm", (D,), 0.1, 1.0),
+        "lm_head": single("lm_head", (V, D), std),
+        "attn_norm": stacked("attn_norm", (D,), 0.1, 1.0),
+        "wq": stacked("wq", (Dq, D), std),
+        "wk": stacked("wk", (Dq, D), std),
+        "wv": stacked("wv", (Dq, D), std),
+        "wo": stacked("wo", (D, Dq), std),
+        "ffn_norm": stacked("ffn_norm", (D,), 0.1, 1.0),
+        "w_gate": stacked("w_gate", (F, D), std),
+        "w_up": stacked("w_up", (F, D), std),
+        "w_down": stacked("w_down", (D, F), std),
+    }
+
+
+def forced_exit_layers(seed: int, n: int, lo: int, hi: int) -> np.ndarray:
+    """Seeded exit schedule: exit layer of each of n tokens uniform in [lo, hi]."""
+    return rng(seed, "forced_exit").integers(lo, hi + 1, size=n).astype(np.int32)

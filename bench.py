@@ -1,0 +1,314 @@
+#!/usr/bin/env python3
+"""Throughput of the early-exit hot path on one MI355X.
+
+One step = one prefill pass of a Llama-7B-shaped decoder (32 layers, width
+4096, 32 heads x 128, SwiGLU 11008, vocab 32000; bf16, random-init weights)
+over a batch of 8 x 2048 uniform-random tokens with token-level exit: per
+layer the regular layer for the active rows, the exit test (Eq. 7-8),
+compaction of the active list, and the decoupled KV generation (Eq. 9) for
+the rows that exit; then the final norm and LM head for the last position of
+each sequence.  Inputs and weights are resident in HBM before timing.
+
+Printed: one JSON line with tokens/s, the roofline of the dominant kernel
+(timed live with HIP events inside the timed steps), the standalone KV
+generation's MFMA utilisation and the exit test's HBM bandwidth, the no-exit
+and fixed-schedule variants, and the CPU oracle on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--delta 0.95] [--metric global]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+PEAK_BF16 = 2.5e15      # dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12       # HBM3E, B/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--delta", type=float, default=0.95)
+    ap.add_argument("--metric", choices=("global", "local"), default="global")
+    ap.add_argument("--batch", type=int, default=8)
+    ap.add_argument("--seq", type=int, default=2048)
+    ap.add_argument("--no-extras", action="store_true", help="skip the variant and kernel runs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=512)
+    ap.add_argument("--cpu-layers", type=int, default=4)
+    return ap.parse_args()
+
+
+def layer_counts(exit_layer, n_layers):
+    """Active rows entering each layer i = 1..N: tokens with exit layer >= i."""
+    import torch
+    el = exit_layer.to(torch.int64)
+    return [int((el >= i).sum()) for i in range(1, n_layers + 1)]
+
+
+def step_work(shape, exit_layer, pos):
+    """Algorithmic FLOPs / bytes of one prefill step, per kernel family."""
+    import torch
+    N, D, Dq, F = shape.n_layers, shape.d_model, shape.d_q, shape.d_ff
+    el = exit_layer.to(torch.int64).cpu()
+    p1 = (pos.to(torch.int64).cpu() + 1).double()
+    cnt = layer_counts(el, N)
+    w = {
+        "gemm_qkv": sum(2.0 * m * D * 3 * Dq for m in cnt),
+        "gemm_o": sum(2.0 * m * Dq * D for m in cnt),
+        "gemm_gate_up": sum(2.0 * m * D * 2 * F for m in cnt),
+        "gemm_down": sum(2.0 * m * F * D for m in cnt),
+        # causal attention: QK^T and PV, 2 * 2 * (p+1) * Dq per active query
+        "attention": sum(float(4.0 * Dq * p1[el >= i].sum()) for i in range(1, N + 1)),
+        # skipped-layer K/V of exited tokens: 2 * D * 2Dq per (token, layer)
+        "kv_generate": float(4.0 * D * Dq * (N - el).clamp(min=0).sum()),
+    }
+    return w, cnt
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the early-exit hot path is built for a single "
+              "MI355X (no sharding, no collectives); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import adept_inputs as ai
+    from paper_2601_03700_amd import binding as B
+    from paper_2601_03700_amd.model import DecoderModel
+
+    B.lib()  # fails loudly when the HIP library is missing
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    shape = ai.LLAMA7B
+    N, D, Dq = shape.n_layers, shape.d_model, shape.d_q
+    Bn, T = args.batch, args.seq
+    n_tok = Bn * T
+    t0 = time.time()
+    weights = ai.decoder_weights_torch(shape, seed=7, device="cuda")
+    model = DecoderModel(shape, weights, dtype="bf16", rope_max_pos=T)
+    del weights
+    torch.cuda.empty_cache()
+    ids = torch.from_numpy(ai.token_ids(8, shape.vocab, Bn, T)).cuda()
+    cache = model.new_cache(Bn, T)
+    torch.cuda.synchronize()
+    log(f"weights + cache ready in {time.time() - t0:.1f}s; "
+        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated")
+
+    def run(cfg, force=None, steps=args.steps, warmup=args.warmup, timing=False):
+        for _ in range(warmup):
+            res, _ = model.prefill(ids, cfg, cache=cache, logits="last", force_layer=force)
+        torch.cuda.synchronize()
+        if timing:
+            B.timing_reset()
+            B.timing_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            res, _ = model.prefill(ids, cfg, cache=cache, logits="last", force_layer=force)
+        e1.record()
+        torch.cuda.synchronize()
+        kern = None
+        if timing:
+            B.timing_enable(False)
+            kern = B.timing_read()
+        return e0.elapsed_time(e1) / steps, res, kern
+
+    cfg = B.exit_cfg(args.delta, N, args.metric)
+    log(f"timed run: delta={args.delta} metric={args.metric}, {args.warmup} warmup + {args.steps} steps")
+    ms, res, kern = run(cfg, timing=True)
+    tok_s = n_tok / (ms / 1e3)
+    pos = torch.arange(T, dtype=torch.int32).repeat(Bn)
+    work, cnt = step_work(shape, res.exit_layer, pos)
+    exit_frac = 1.0 - cnt[-1] / n_tok
+    log(f"{ms:.1f} ms/step, {tok_s:.0f} tokens/s, exited {exit_frac:.3%}")
+
+    # dominant kernel: the one with the largest share of the timed region
+    fam = {"gemm_qkv": "gemm_qkv", "gemm_o": "gemm_o", "gemm_gate_up": "gemm_gate_up",
+           "gemm_down": "gemm_down", "attend_prefill_kernel<128>": "attention",
+           "gemm_kv_grouped_kernel": "kv_generate"}
+    per_kernel = {}
+    for name, (n_launch, tot) in sorted(kern.items(), key=lambda kv: -kv[1][1]):
+        per_kernel[name] = {"launches": n_launch, "avg_us": 1e3 * tot / max(n_launch, 1),
+                            "share": tot / (ms * args.steps)}
+        if name in fam:
+            flops = work[fam[name]] * args.steps
+            per_kernel[name]["tflops"] = flops / (tot / 1e3) / 1e12 if tot > 0 else None
+    dom = max((k for k in kern if k in fam), key=lambda k: kern[k][1])
+    d_launch, d_ms = kern[dom]
+    d_flops_launch = work[fam[dom]] * args.steps / d_launch
+    d_avg_s = d_ms / d_launch / 1e3
+    achieved = d_flops_launch / d_avg_s
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16, "traffic": None,
+                "flops_per_launch": d_flops_launch, "avg_launch_us": d_avg_s * 1e6,
+                "launches": d_launch}
+
+    out = {
+        "metric": "tokens/s (prefill+decode) at Llama-7B shape; KV-gen MFMA util %",
+        "value": tok_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded uniform token ids, random-init N(0,0.02) weights)",
+        "config": {"workload": (f"Llama-7B-shaped decoder prefill, batch {Bn} x {T}, token-level "
+                                f"exit ({args.metric} metric, delta {args.delta})"),
+                   "global_batch": Bn, "seq_len": T, "parallelism": "none (one GPU)"},
+        "roofline": roofline,
+        "exit_fraction": exit_frac,
+        "active_rows_per_layer": cnt,
+        "kernels": per_kernel,
+    }
+
+    if not args.no_extras:
+        # no-exit reference (delta = +inf) and a fixed exit schedule (i* ~ U{8..31})
+        ms_inf, _, _ = run(B.exit_cfg(math.inf, N, args.metric), steps=max(2, args.steps // 2),
+                           warmup=1)
+        sched = torch.from_numpy(ai.forced_exit_layers(3, n_tok, 8, 31)).cuda()
+        ms_f, res_f, kern_f = run(cfg, force=sched, steps=max(2, args.steps // 2), warmup=1,
+                                  timing=True)
+        work_f, cnt_f = step_work(shape, res_f.exit_layer, pos)
+        out["no_exit"] = {"tokens_per_s": n_tok / (ms_inf / 1e3), "ms_per_step": ms_inf}
+        kv_f = kern_f.get("gemm_kv_grouped_kernel", (0, 0.0))
+        out["fixed_schedule"] = {
+            "schedule": "exit layer uniform in 8..31 per token (seeded)",
+            "tokens_per_s": n_tok / (ms_f / 1e3), "ms_per_step": ms_f,
+            "speedup_vs_no_exit": ms_inf / ms_f,
+            "kv_generate_ms_per_step": kv_f[1] / max(2, args.steps // 2),
+        }
+        log(f"no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
+        out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
+        out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args, shape, ai, np)
+    print(json.dumps(out), flush=True)
+
+
+def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
+    """4096 exited tokens, exit layers uniform in 8..31 of 32, hidden N(0,1):
+    K/V for every skipped layer into a [32][4096][32][128] cache, one call."""
+    N, D, H, hd, Dq = shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.d_q
+    n = 4096
+    g = torch.Generator(device="cuda").manual_seed(11)
+    s = torch.randn((n, D), generator=g, device="cuda").to(torch.bfloat16)
+    el = torch.from_numpy(ai.forced_exit_layers(12, n, 8, 31)).cuda()
+    rows = torch.arange(n, dtype=torch.int32, device="cuda")
+    cnt = torch.tensor([n], dtype=torch.int32, device="cuda")
+    kc = torch.empty((N, n, H, hd), dtype=torch.bfloat16, device="cuda")
+    vc = torch.empty_like(kc)
+    ws = torch.empty(B.kv_generate_workspace_bytes(N, n), dtype=torch.uint8, device="cuda")
+    w_kv = model.w_qkv[:, Dq:]          # K and V rows of each layer's stacked QKV weight
+    # positions 0..4095 (token t at position t and slot t)
+    cos = torch.empty((n, hd // 2), dtype=torch.float32, device="cuda")
+    sin = torch.empty_like(cos)
+    B.rope_table(n, hd, shape.rope_theta, cos, sin)
+
+    def call():
+        B.kv_generate(N, D, H, hd, shape.rms_eps, s, rows, cnt, n, el, rows, rows, w_kv,
+                      3 * Dq * D, model.attn_norm, cos, sin, kc, vc, n, ws)
+    call()
+    torch.cuda.synchronize()
+    B.timing_reset()
+    B.timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    B.timing_enable(False)
+    k = B.timing_read()
+    pairs = int((N - el.long()).clamp(min=0).sum())
+    flops = 4.0 * D * Dq * pairs
+    call_ms = e0.elapsed_time(e1) / reps
+    g_launch, g_ms = k.get("gemm_kv_grouped_kernel", (reps, call_ms * reps))
+    gemm_ms = g_ms / g_launch
+    return {"tokens": n, "pairs": pairs, "tflop": flops / 1e12, "call_ms": call_ms,
+            "gemm_ms": gemm_ms, "mfma_util": flops / (gemm_ms / 1e3) / PEAK_BF16,
+            "mfma_util_whole_call": flops / (call_ms / 1e3) / PEAK_BF16,
+            "kernels": {kk: {"launches": v[0], "avg_us": 1e3 * v[1] / max(v[0], 1)}
+                        for kk, v in k.items()}}
+
+
+def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
+    """Exit test at the prefill shape (16384 rows x 4096, bf16, global metric):
+    reads h (2 B/elem) and the inertia (4 B/elem), writes the inertia back."""
+    D, N = shape.d_model, shape.n_layers
+    g = torch.Generator(device="cuda").manual_seed(5)
+    h = torch.randn((n_tok, D), generator=g, device="cuda").to(torch.bfloat16)
+    inertia = torch.randn((n_tok, D), generator=g, device="cuda")
+    rows = torch.arange(n_tok, dtype=torch.int32, device="cuda")
+    cnt = torch.tensor([n_tok], dtype=torch.int32, device="cuda")
+    flag = torch.empty(n_tok, dtype=torch.uint8, device="cuda")
+    cfg = B.exit_cfg(0.95, N, "global")
+    nxt = torch.empty_like(rows)
+    ext = torch.empty_like(rows)
+    cnt2 = torch.empty(2, dtype=torch.int32, device="cuda")
+    el = torch.full((n_tok,), N, dtype=torch.int32, device="cuda")
+
+    def call():
+        B.exit_test(D, 5, cfg, rows, cnt, n_tok, h, None, inertia, None, flag)
+        B.compact(5, flag, rows, cnt, n_tok, nxt, cnt2[0:1], ext, cnt2[1:2], el)
+    call()
+    torch.cuda.synchronize()
+    B.timing_reset()
+    B.timing_enable(True)
+    for _ in range(reps):
+        call()
+    torch.cuda.synchronize()
+    B.timing_enable(False)
+    k = B.timing_read()
+    name = [x for x in k if x.startswith("(exit_test_kernel")][0]
+    et_launch, et_ms = k[name]
+    comp_launch, comp_ms = k.get("compact_single", (reps, 0.0))
+    bytes_et = n_tok * (2 * D + 4 * D + 4 * D) + n_tok * (4 + 1)
+    bytes_comp = n_tok * (1 + 4 + 4)
+    et_s = et_ms / et_launch / 1e3
+    comp_s = comp_ms / comp_launch / 1e3
+    return {"rows": n_tok, "d_model": D, "exit_test_us": et_s * 1e6,
+            "exit_test_gbs": bytes_et / et_s / 1e9, "exit_test_hbm_frac": bytes_et / et_s / PEAK_HBM,
+            "compact_us": comp_s * 1e6, "compact_gbs": bytes_comp / comp_s / 1e9,
+            "note": "working set 671 MB > 256 MB MALL"}
+
+
+def cpu_baseline(args, shape, ai, np):
+    """The oracle (numpy fp64) on a bounded sample of the same workload: one
+    sequence of --cpu-tokens tokens through --cpu-layers of the 32 layers at
+    full width (plus its LM head over all rows), extrapolated per
+    (token x layer) to the 32-layer step."""
+    import dataclasses
+    from oracle import adept_oracle as O
+    L = args.cpu_layers
+    sub = dataclasses.replace(shape, n_layers=L)
+    log(f"cpu baseline: drawing {L}-layer oracle weights")
+    w = O.as64(ai.decoder_weights(sub, seed=7, dtype="bf16"))
+    ids = ai.token_ids(8, shape.vocab, 1, args.cpu_tokens)
+    cfg = O.ExitConfig(delta=args.delta, metric=args.metric)
+    t0 = time.perf_counter()
+    O.prefill(w, sub, ids, cfg)
+    dt = time.perf_counter() - t0
+    scaled = dt * shape.n_layers / L
+    cores = len(os.sched_getaffinity(0))
+    log(f"cpu baseline: {dt:.1f}s for the sample")
+    return {"value": args.cpu_tokens / scaled, "unit": "tokens/s", "cores": cores,
+            "kind": "oracle",
+            "sample": (f"1 x {args.cpu_tokens} tokens through {L} of 32 layers at full width "
+                       f"(numpy fp64, BLAS on {cores} threads), {dt:.1f}s, extrapolated x{shape.n_layers / L:g} "
+                       f"to the 32-layer step; includes the oracle's LM head over all rows"),
+            "sample_seconds": dt}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,281 @@
+/*
+ * adept.h -- C ABI of the MI355X (gfx950) hot path of ADEPT's token-level
+ * early-exit forward pass (arXiv 2601.03700).
+ *
+ * Conventions (apply to every entry point)
+ *  - Pointers are DEVICE pointers unless marked (host).  The caller owns all
+ *    memory; the library never allocates or frees device memory.  Scratch
+ *    space is passed in as `workspace` of at least the size returned by the
+ *    matching *_workspace_bytes() query.
+ *  - Calls only enqueue work on `stream` (a hipStream_t; NULL = the null
+ *    stream) and return.  Variable counts (active rows, exited rows) live in
+ *    device int32 cells; `max_*` host integers bound the launch grids and the
+ *    kernels stop at the device count, so no call reads device memory back.
+ *  - Shapes, enum values and pointer alignment (16 bytes for tensors) are
+ *    validated on the host before anything is enqueued; on an error nothing
+ *    is launched and the call returns a negative adept_status.
+ *    adept_last_error() returns a message for the calling thread's last error.
+ *  - Layers are numbered 1..N as in the paper (Section 3).  A token that exits
+ *    at layer i* ran layers 1..i* in full; layers i*+1..N are "skipped".
+ *    exit_layer[j] == N means token j never exited.
+ *  - Per-token tensors are in token-row order [n_tok][...]; with a [B, T]
+ *    prompt batch, row j = b*T + p (Appendix I flattens a batch this way).
+ *    Index lists (int32) select rows; lists produced here are ascending.
+ *  - Element types: ADEPT_F32 (float) or ADEPT_BF16 (bfloat16 stored as
+ *    uint16).  Inertia is always float, similarities double.
+ *  - Caches K and V are [N][n_slots][H][hd]; a token's slot is
+ *    b * s_max + p (sequence b, position p).
+ */
+#ifndef ADEPT_H
+#define ADEPT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ADEPT_ABI_VERSION 1
+
+typedef enum {
+  ADEPT_OK = 0,
+  ADEPT_E_INVALID = -1,     /* bad argument; nothing enqueued */
+  ADEPT_E_UNSUPPORTED = -2, /* valid but not implemented for these shapes/types */
+  ADEPT_E_WORKSPACE = -3,   /* workspace missing or too small */
+  ADEPT_E_HIP = -4          /* a HIP launch or runtime call failed */
+} adept_status;
+
+typedef enum { ADEPT_F32 = 0, ADEPT_BF16 = 1 } adept_dtype;
+
+/* Exit metric: GLOBAL compares h_i with the inertia of Section 4.1 (Eq. 7-8);
+ * LOCAL compares h_i with h_{i-1} (the "local" metric of Appendix H.3). */
+typedef enum { ADEPT_SIM_GLOBAL = 0, ADEPT_SIM_LOCAL = 1 } adept_metric;
+
+/* (host) Exit policy of Section 4.1, Eq. 8: token j exits at layer i iff
+ * min_exit_layer <= i <= n_layers-1 and cos >= delta.  An undefined cosine
+ * (a zero-norm vector, e.g. the empty inertia at layer 1) never exits, and
+ * delta = +INFINITY never fires. */
+typedef struct {
+  double delta;
+  int32_t min_exit_layer;
+  int32_t n_layers;
+  int32_t metric; /* adept_metric */
+  int32_t reserved;
+} adept_exit_cfg;
+
+int adept_abi_version(void);
+const char* adept_last_error(void);
+
+/* Rotary table used by every kernel that applies RoPE: cos_out/sin_out are
+ * [max_pos][head_dim/2] float, entry (p, k) = cos/sin(p * theta^(-2k/head_dim)),
+ * with the angle formed in double precision on the device.  (The paper's base
+ * models use rotary positions; the paper itself does not define them.) */
+adept_status adept_rope_table(int max_pos, int head_dim, double theta,
+                              float* cos_out, float* sin_out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * adept_exit_test -- the token-level exit policy (Section 4.1, Eq. 7-8;
+ * Appendix H.3 for the local variant), for the active rows at layer `layer`.
+ *
+ *  active_rows[k], k < *n_active (device count, <= max_active): rows tested.
+ *  h_cur  [n_tok][d_model] (dtype): h_i, the residual stream after layer i.
+ *  h_prev [n_tok][d_model] (dtype): h_{i-1}; read only for ADEPT_SIM_LOCAL
+ *         (may be NULL otherwise).
+ *  inertia [n_tok][d_model] float: Eq. 7's running sum of unit states of the
+ *         layers before i.  For ADEPT_SIM_GLOBAL it is read for the test and
+ *         then updated in place, inertia += h_i/|h_i| (after the test).  For
+ *         LOCAL it is not touched (may be NULL).
+ *  force_layer [n_tok] int32, nullable: f = force_layer[row] > 0 replaces the
+ *         policy for that row by "exit iff layer == f and layer <= N-1"; 0
+ *         keeps the policy (teacher forcing and fixed exit schedules).
+ *  exit_flag [max_active] uint8 out: 1 = exit, aligned with active_rows.
+ *  sim_out [max_active] double out, nullable: the cosine (NaN if undefined).
+ *
+ * The three sums <h,h>, <r,r>, <h,r> are reduced in double precision from
+ * the stored values (each product is exact in double), the decision is
+ * taken in double.  One wavefront per row; HBM-bound.
+ * ------------------------------------------------------------------------- */
+adept_status adept_exit_test(adept_dtype dt, int d_model, int layer, const adept_exit_cfg* cfg,
+                             const int32_t* active_rows, const int32_t* n_active, int max_active,
+                             const void* h_cur, const void* h_prev, float* inertia,
+                             const int32_t* force_layer, uint8_t* exit_flag, double* sim_out,
+                             void* stream);
+
+/* ---------------------------------------------------------------------------
+ * adept_compact -- the active-index update of Appendix I: split the active
+ * list by the exit flags into the rows that continue and the rows that exit.
+ *
+ *  exit_flag[k], active_rows[k] for k < *n_active.
+ *  next_rows / *n_next out: rows with flag 0, in the order of active_rows.
+ *  exited_rows / *n_exited out: rows with flag 1, same order.
+ *  exit_layer [n_tok] int32: exit_layer[row] = layer for every exited row.
+ *  Counts are exact; with an ascending active list both outputs are ascending.
+ *  next_rows / exited_rows must not alias active_rows.
+ * ------------------------------------------------------------------------- */
+size_t adept_compact_workspace_bytes(int max_active);
+adept_status adept_compact(int layer, const uint8_t* exit_flag, const int32_t* active_rows,
+                           const int32_t* n_active, int max_active, int32_t* next_rows,
+                           int32_t* n_next, int32_t* exited_rows, int32_t* n_exited,
+                           int32_t* exit_layer, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* ---------------------------------------------------------------------------
+ * adept_kv_generate -- decoupled KV generation (Section 4, Eq. 6; Section
+ * 4.3, Eq. 9): for every listed row j and every skipped layer r with
+ * exit_layer[j] < r <= n_layers, with s = s_map[j] (the mapped state s~):
+ *     u   = RMSNorm_r(s) = s / sqrt(mean(s^2) + eps) * attn_gain[r]
+ *     K[r][cache_slot[j]] = RoPE(u Wk_r^T, pos[j]),   V[r][cache_slot[j]] = u Wv_r^T
+ * All (token, layer) pairs are computed in one grouped GEMM, with no
+ * layer-sequential dependency.
+ *
+ *  s_map [n_tok][d_model] (dtype); rows[k], k < *n_rows (<= max_rows).
+ *  exit_layer, cache_slot, pos: [n_tok] int32.
+ *  w_kv: layer r's block starts at w_kv + (r-1)*w_kv_layer_stride elements and
+ *        is [2*H*hd][d_model] (nn.Linear order): H*hd rows of Wk_r, then H*hd
+ *        rows of Wv_r.  (A stacked [N][3*H*hd][D] QKV weight passes its K part
+ *        with stride 3*H*hd*D.)
+ *  attn_gain [n_layers][d_model] (dtype): layer r's pre-attention RMSNorm gain.
+ *  rope_cos/rope_sin [rope_max_pos][hd/2] float (adept_rope_table).
+ *  k_cache/v_cache [n_layers][n_slots][H][hd] (dtype): written only at the
+ *        (layer, slot) pairs above.
+ * bf16 requires d_model % 64 == 0 and head_dim in {64, 128}.
+ * ------------------------------------------------------------------------- */
+size_t adept_kv_generate_workspace_bytes(int n_layers, int max_rows);
+adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_model, int n_heads,
+                               int head_dim, float eps, const void* s_map, const int32_t* rows,
+                               const int32_t* n_rows, int max_rows, const int32_t* exit_layer,
+                               const int32_t* cache_slot, const int32_t* pos, const void* w_kv,
+                               int64_t w_kv_layer_stride, const void* attn_gain,
+                               const float* rope_cos, const float* rope_sin, int rope_max_pos,
+                               void* k_cache, void* v_cache, int64_t n_slots, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * adept_attend -- attention of the active tokens over one layer's cache,
+ * whose entries are computed (tokens still active at this layer) or
+ * generated (tokens that exited earlier) (Section 3, Eq. 5; Section 4.3).
+ *
+ *  q [max_active][H][hd] (dtype): compacted queries; entry k is for row rows[k].
+ *  rows[k], k < *n_active.  seq[row] must be non-decreasing in k.
+ *  pos, seq [n_tok] int32: position and sequence of each row.
+ *  k_layer/v_layer: this layer's cache, [n_seq*s_max][H][hd] (dtype).
+ *  causal=1: entry k attends to slots seq*s_max + t, t = 0..pos[rows[k]].
+ *  causal=0: t = 0..key_len[seq]-1 (bidirectional), key_len [n_seq] int32.
+ *  key_live [n_seq*s_max] uint8, nullable: keys with 0 are left out.
+ *  out [max_active][H][hd] (dtype): softmax(q K^T * scale) V per head, with
+ *      f32 scores and softmax statistics.
+ * ------------------------------------------------------------------------- */
+size_t adept_attend_workspace_bytes(int max_active, int n_seq);
+adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale, int causal,
+                          const void* q, const int32_t* rows, const int32_t* n_active,
+                          int max_active, const int32_t* pos, const int32_t* seq, int n_seq,
+                          const void* k_layer, const void* v_layer, int s_max,
+                          const int32_t* key_len, const uint8_t* key_live, void* out,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Whole-layer orchestration of the generative path (Appendix I):
+ * adept_layer_step(layer=i) enqueues, for the rows of active[(i-1)&1]:
+ *   RMSNorm -> QKV GEMM (+RoPE; own K/V into cache[i]) -> adept_attend ->
+ *   O GEMM (+residual: h[i&1] = h[(i-1)&1] + o Wo^T) -> RMSNorm ->
+ *   gate/up GEMM (+SwiGLU) -> down GEMM (+residual) -> adept_exit_test ->
+ *   adept_compact (next list into active[i&1], exited rows into `exited`) ->
+ *   adept_kv_generate for the rows exited at i (layers i+1..N).
+ * The residual stream ping-pongs between h[0] and h[1]: a token's final
+ * state is h[exit_layer & 1][row] (its state at exit, the identity mapped
+ * state).  Before layer 1 the caller puts h_0 in h[0], zeroes the inertia,
+ * fills active[0] with the rows, *n_active[0] = count and exit_layer = N.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int32_t dtype;        /* adept_dtype */
+  int32_t n_layers, d_model, n_heads, head_dim, d_ff;
+  float rms_eps;
+  adept_exit_cfg exit;
+  /* weights, stacked over layers (dtype) */
+  const void* attn_norm; /* [N][D] */
+  const void* w_qkv;     /* [N][3*H*hd][D]: Wq rows, Wk rows, Wv rows */
+  const void* w_o;       /* [N][D][H*hd] */
+  const void* ffn_norm;  /* [N][D] */
+  const void* w_gate;    /* [N][F][D] */
+  const void* w_up;      /* [N][F][D] */
+  const void* w_down;    /* [N][D][F] */
+  const float* rope_cos; /* [rope_max_pos][hd/2] */
+  const float* rope_sin;
+  int32_t rope_max_pos;
+  /* token state */
+  int32_t n_tok;         /* rows in the per-token tensors */
+  int32_t max_active;    /* (host) bound on the active rows entering this layer */
+  int32_t n_seq, s_max;
+  int32_t attn_tiles;    /* 1: queries are prompt tiles (prefill); 0: one query per sequence */
+  void* h[2];            /* [n_tok][D] residual stream ping-pong */
+  float* inertia;        /* [n_tok][D] (GLOBAL metric) */
+  const int32_t* pos;    /* [n_tok] */
+  const int32_t* seq;    /* [n_tok] */
+  const int32_t* slot;   /* [n_tok] */
+  int32_t* active[2];    /* [n_tok] each */
+  int32_t* n_active[2];  /* device counts */
+  int32_t* exited;       /* [n_tok] rows exited at this layer */
+  int32_t* n_exited;     /* device count */
+  int32_t* exit_layer;   /* [n_tok] */
+  uint8_t* exit_flag;    /* [n_tok] */
+  double* sim_out;       /* [n_tok] nullable, aligned with the active list */
+  const int32_t* force_layer; /* [n_tok] nullable */
+  void* k_cache;         /* [N][n_slots][H][hd] */
+  void* v_cache;
+  int64_t n_slots;
+  /* per-layer scratch (dtype), caller-allocated */
+  void* x_norm;          /* [n_tok][D] */
+  void* q_buf;           /* [n_tok][H*hd] */
+  void* attn_out;        /* [n_tok][H*hd] */
+  void* ffn_act;         /* [n_tok][F] */
+  void* workspace;
+  size_t workspace_bytes;
+} adept_layer_args;
+
+size_t adept_layer_workspace_bytes(const adept_layer_args* a);
+adept_status adept_layer_step(const adept_layer_args* a, int layer, void* stream);
+
+/* Embedding gather (support step before layer 1): h0[k] = embed[ids[k]],
+ * k < n; embed [vocab][D] (dtype), h0 [n][D] (dtype). */
+adept_status adept_embed(adept_dtype dt, int n, int d_model, int vocab, const int32_t* ids,
+                         const void* embed, void* h0, void* stream);
+
+/* Final norm and LM head (support step after layer N): for k < *n_rows,
+ * row = rows[k]: logits[k] = RMSNorm(h[exit_layer[row] & 1][row]; final_norm)
+ * lm_head^T, as float.  An exited token uses its state at exit (Fig. 1: the
+ * mapped state is propagated to the end of the layer chain).
+ * x_norm is [max_rows][D] (dtype) scratch. */
+adept_status adept_final_logits(adept_dtype dt, int d_model, int vocab, float eps,
+                                const void* h0_buf, const void* h1_buf,
+                                const int32_t* exit_layer, const int32_t* rows,
+                                const int32_t* n_rows, int max_rows, const void* final_norm,
+                                const void* lm_head, void* x_norm, float* logits, void* stream);
+
+/* State set-up before layer 1 of a token pass: active[k] = k and
+ * exit_layer[k] = n_layers for k < n_tok, *n_active = n_tok, and the inertia
+ * [n_tok][d_model] (nullable) zeroed (Eq. 7's sum starts empty). */
+adept_status adept_token_init(int n_tok, int n_layers, int d_model, int32_t* active,
+                              int32_t* n_active, int32_t* exit_layer, float* inertia,
+                              void* stream);
+
+/* Greedy next token: out[k] = argmax_v logits[k][v] for k < n, ties to the
+ * lowest id (support step of the generation loop). */
+adept_status adept_argmax(int n, int vocab, const float* logits, int32_t* out, void* stream);
+
+/* Kernel timing for measurement runs.  While enabled, every kernel the
+ * library launches is bracketed by two HIP events on its own stream, and
+ * adept_timing_get() (which waits for the pending events) reports, per
+ * kernel name, the launch count and the summed elapsed milliseconds.
+ * Names are sorted; index 0..adept_timing_count()-1.  No device memory is
+ * used.  Disabled by default; reset clears the totals. */
+adept_status adept_timing_enable(int on);
+void adept_timing_reset(void);
+int adept_timing_count(void);
+adept_status adept_timing_get(int idx, char* name, int name_len, int64_t* launches,
+                              double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ADEPT_H */

@@ -1,0 +1,172 @@
+// Internal helpers shared by the HIP sources of libadept (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <cmath>
+#include <cstdio>
+#include <string>
+
+#include "../../include/adept.h"
+
+namespace adept {
+
+// ---------------------------------------------------------------------------
+// bfloat16 storage (uint16 bit patterns) <-> float
+// ---------------------------------------------------------------------------
+typedef uint16_t bf16;
+
+__device__ __forceinline__ float bf2f(bf16 x) { return __uint_as_float(((uint32_t)x) << 16); }
+
+// Round to nearest, ties to even; NaN stays a (quiet) NaN.
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (bf16)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  __device__ __forceinline__ static float load(const float* p) { return *p; }
+  __device__ __forceinline__ static void store(float* p, float v) { *p = v; }
+};
+template <> struct Elem<bf16> {
+  __device__ __forceinline__ static float load(const bf16* p) { return bf2f(*p); }
+  __device__ __forceinline__ static void store(bf16* p, float v) { *p = f2bf(v); }
+};
+template <typename T> __device__ __forceinline__ float ld(const T* p) { return Elem<T>::load(p); }
+template <typename T> __device__ __forceinline__ void st(T* p, float v) { Elem<T>::store(p, v); }
+
+// MFMA operand / accumulator vector types.
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+
+// ---------------------------------------------------------------------------
+// wavefront (64 lanes) reductions
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_sum_f32(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max_f32(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// host-side error plumbing
+// ---------------------------------------------------------------------------
+void set_error(const char* fmt, ...);
+adept_status launch_status(const char* what);
+
+#define ADEPT_REQUIRE(cond, ...)            \
+  do {                                      \
+    if (!(cond)) {                          \
+      ::adept::set_error(__VA_ARGS__);      \
+      return ADEPT_E_INVALID;               \
+    }                                       \
+  } while (0)
+
+#define ADEPT_CHECK_LAUNCH(what)                                   \
+  do {                                                             \
+    adept_status _s = ::adept::launch_status(what);                \
+    if (_s != ADEPT_OK) return _s;                                 \
+  } while (0)
+
+#define ADEPT_TRY(expr)                       \
+  do {                                        \
+    adept_status _s = (expr);                 \
+    if (_s != ADEPT_OK) return _s;            \
+  } while (0)
+
+// Brackets the kernel launched in its scope with timing events when timing is
+// enabled (adept_timing_enable); a no-op otherwise.  `name` must be a literal.
+class TimedLaunch {
+ public:
+  TimedLaunch(const char* name, hipStream_t s);
+  ~TimedLaunch();
+  TimedLaunch(const TimedLaunch&) = delete;
+  TimedLaunch& operator=(const TimedLaunch&) = delete;
+
+ private:
+  const char* name_;
+  hipStream_t s_;
+  void* a_ = nullptr;
+  void* b_ = nullptr;
+};
+
+// hipLaunchKernelGGL under a TimedLaunch named after the kernel expression.
+#define ADEPT_LAUNCH(kernel, grid, block, smem, stream, ...)                 \
+  do {                                                                       \
+    ::adept::TimedLaunch _adept_tl(#kernel, stream);                         \
+    hipLaunchKernelGGL(kernel, grid, block, smem, stream, __VA_ARGS__);      \
+  } while (0)
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+inline hipStream_t as_stream(void* s) { return (hipStream_t)s; }
+inline int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
+
+// ---------------------------------------------------------------------------
+// internal launchers shared between translation units
+// ---------------------------------------------------------------------------
+
+// RMSNorm of gathered rows into a compact buffer:
+// out[k] = x[rows ? rows[k] : k] / sqrt(mean(x^2) + eps) * gain, k < *n (or n_host).
+adept_status rmsnorm_rows(adept_dtype dt, int d, float eps, const void* x, const int32_t* rows,
+                          const int32_t* n_dev, int max_n, const void* gain, void* out,
+                          hipStream_t s);
+
+// GEMM epilogue kinds.
+enum EpiKind {
+  EPI_STORE = 0,   // C[k][n] (dtype or float) compact
+  EPI_QKV = 1,     // RoPE on Q and K columns; Q -> q_out[k], K/V -> cache slot of rows[k]
+  EPI_RESID = 2,   // out[rows[k]][n] = resid[rows[k]][n] + acc
+  EPI_SWIGLU = 3,  // B = (gate, up) interleaved per 64 columns; out[k][n] = silu(g) * u
+  EPI_KV = 4,      // K/V-only variant of EPI_QKV (KV generation, per-layer groups)
+};
+
+struct GemmArgs {
+  int M_max;              // grid bound on rows
+  const int32_t* M_dev;   // device row count (nullable: M_max exact)
+  int N, K;
+  const void* A;          // [.][K] rows; row index = a_rows ? a_rows[m] : m
+  const int32_t* a_rows;
+  int64_t lda;
+  const void* B;          // [N][K] (nn.Linear order)
+  const void* B2;         // second matrix for SWIGLU (up); B is gate
+  int64_t ldb;
+  int epi;
+  // epilogue operands
+  void* C; int64_t ldc; int c_f32;
+  const int32_t* rows;    // token row of compact index k (QKV/RESID/KV)
+  const void* resid;      // RESID source (may equal C)
+  const int32_t* pos;     // [n_tok]
+  const int32_t* slot;    // [n_tok]
+  const float* rope_cos; const float* rope_sin;
+  int head_dim, d_q;
+  void* q_out; void* k_cache; void* v_cache;   // caches already offset to the layer
+  const char* name;       // timing label (string literal), nullable
+};
+
+adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s);       // bf16 MFMA path
+adept_status gemm_f32(const GemmArgs& g, float* tmp, hipStream_t s);      // f32 + epilogue
+adept_status gemm_f32_direct(const GemmArgs& g, hipStream_t s);           // f32, C = A B^T
+adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32_t* n_work,
+                             int max_work, const int32_t* grp_m, const int32_t* srows,
+                             const float* rinv, const void* gain, int64_t b_layer_stride,
+                             int64_t cache_layer_stride, hipStream_t s);
+adept_status rmsnorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
+                              const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
+                              int max_n, const void* gain, void* out, hipStream_t s);
+
+}  // namespace adept

@@ -1,0 +1,157 @@
+// One decoder layer of the generative early-exit forward (Appendix I):
+// regular processing of the active rows, then the exit test, the active-list
+// update and the KV generation for the rows that exit.  Everything is
+// enqueued on one stream with the variable counts kept on the device.
+#include <algorithm>
+
+#include "common.h"
+
+namespace adept {
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct LayerWs {
+  void* compact;  size_t compact_bytes;
+  void* attend;   size_t attend_bytes;
+  void* kvgen;    size_t kvgen_bytes;
+  float* gemm_tmp;  // f32 path only
+  size_t total;
+};
+
+LayerWs carve(const adept_layer_args* a, void* base) {
+  LayerWs w{};
+  char* p = (char*)base;
+  size_t off = 0;
+  const int dq = a->n_heads * a->head_dim;
+  w.compact_bytes = adept_compact_workspace_bytes(a->n_tok);
+  w.compact = p + off; off += align256(w.compact_bytes);
+  w.attend_bytes = adept_attend_workspace_bytes(a->n_tok, a->n_seq);
+  w.attend = p + off; off += align256(w.attend_bytes);
+  w.kvgen_bytes = adept_kv_generate_workspace_bytes(a->n_layers, a->n_tok);
+  w.kvgen = p + off; off += align256(w.kvgen_bytes);
+  if (a->dtype == ADEPT_F32) {
+    const size_t cols = std::max({(size_t)3 * dq, (size_t)2 * a->d_ff, (size_t)a->d_model});
+    w.gemm_tmp = (float*)(p + off);
+    off += align256((size_t)a->n_tok * cols * sizeof(float));
+  }
+  w.total = off;
+  return w;
+}
+
+adept_status run_gemm(adept_dtype dt, const GemmArgs& g, float* tmp, hipStream_t s) {
+  return dt == ADEPT_BF16 ? gemm(dt, g, s) : gemm_f32(g, tmp, s);
+}
+
+}  // namespace
+}  // namespace adept
+
+using namespace adept;
+
+extern "C" size_t adept_layer_workspace_bytes(const adept_layer_args* a) {
+  if (!a) return 0;
+  return carve(a, nullptr).total;
+}
+
+extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, void* stream) {
+  ADEPT_REQUIRE(a != nullptr, "layer_step: args is NULL");
+  const adept_dtype dt = (adept_dtype)a->dtype;
+  ADEPT_REQUIRE(dt == ADEPT_F32 || dt == ADEPT_BF16, "layer_step: bad dtype");
+  const int N = a->n_layers, D = a->d_model, H = a->n_heads, hd = a->head_dim, F = a->d_ff;
+  ADEPT_REQUIRE(N >= 1 && layer >= 1 && layer <= N, "layer_step: layer %d outside 1..%d", layer, N);
+  ADEPT_REQUIRE(a->exit.n_layers == N, "layer_step: exit.n_layers != n_layers");
+  ADEPT_REQUIRE(D > 0 && H > 0 && hd > 0 && F > 0 && a->n_tok > 0, "layer_step: bad sizes");
+  ADEPT_REQUIRE(a->max_active >= 0 && a->max_active <= a->n_tok, "layer_step: bad max_active");
+  ADEPT_REQUIRE(a->n_seq > 0 && a->s_max > 0 && a->n_slots >= (int64_t)a->n_seq * a->s_max,
+                "layer_step: cache smaller than n_seq * s_max");
+  ADEPT_REQUIRE(a->attn_norm && a->w_qkv && a->w_o && a->ffn_norm && a->w_gate && a->w_up &&
+                    a->w_down && a->rope_cos && a->rope_sin && a->h[0] && a->h[1] && a->pos &&
+                    a->seq && a->slot && a->active[0] && a->active[1] && a->n_active[0] &&
+                    a->n_active[1] && a->exited && a->n_exited && a->exit_layer &&
+                    a->exit_flag && a->k_cache && a->v_cache && a->x_norm && a->q_buf &&
+                    a->attn_out && a->ffn_act,
+                "layer_step: NULL pointer in args");
+  ADEPT_REQUIRE(a->exit.metric != ADEPT_SIM_GLOBAL || a->inertia,
+                "layer_step: GLOBAL metric needs inertia");
+  const size_t need = adept_layer_workspace_bytes(a);
+  if (!a->workspace || a->workspace_bytes < need) {
+    set_error("layer_step: workspace of %zu bytes needed", need);
+    return ADEPT_E_WORKSPACE;
+  }
+  LayerWs ws = carve(a, a->workspace);
+  hipStream_t s = as_stream(stream);
+  const int in = (layer - 1) & 1, out = layer & 1;
+  const int32_t* act = a->active[in];
+  const int32_t* nact = a->n_active[in];
+  const int maxn = a->max_active;
+  const int dq = H * hd;
+  const size_t esz = dt == ADEPT_BF16 ? 2 : 4;
+  auto off = [&](const void* base, int64_t elems) {
+    return (const void*)((const char*)base + elems * (int64_t)esz);
+  };
+  const int64_t li = layer - 1;
+  const void* wqkv = off(a->w_qkv, li * 3 * dq * D);
+  const void* wo = off(a->w_o, li * (int64_t)D * dq);
+  const void* wg = off(a->w_gate, li * (int64_t)F * D);
+  const void* wu = off(a->w_up, li * (int64_t)F * D);
+  const void* wd = off(a->w_down, li * (int64_t)D * F);
+  const void* g_attn = off(a->attn_norm, li * D);
+  const void* g_ffn = off(a->ffn_norm, li * D);
+  void* kc = (void*)off(a->k_cache, li * a->n_slots * dq);
+  void* vc = (void*)off(a->v_cache, li * a->n_slots * dq);
+
+  if (maxn > 0) {
+    // 1. pre-attention RMSNorm of the active rows (compact)
+    ADEPT_TRY(rmsnorm_rows(dt, D, a->rms_eps, a->h[in], act, nact, maxn, g_attn, a->x_norm, s));
+    // 2. Q/K/V projections, RoPE, own K/V into cache[layer]
+    GemmArgs g{};
+    g.M_max = maxn; g.M_dev = nact; g.N = 3 * dq; g.K = D;
+    g.A = a->x_norm; g.lda = D; g.B = wqkv; g.ldb = D; g.epi = EPI_QKV;
+    g.rows = act; g.pos = a->pos; g.slot = a->slot;
+    g.rope_cos = a->rope_cos; g.rope_sin = a->rope_sin; g.head_dim = hd; g.d_q = dq;
+    g.q_out = a->q_buf; g.k_cache = kc; g.v_cache = vc; g.name = "gemm_qkv";
+    ADEPT_TRY(run_gemm(dt, g, ws.gemm_tmp, s));
+    // 3. attention over the mixed cache
+    ADEPT_TRY(adept_attend(dt, H, hd, 1.0f / sqrtf((float)hd), 1, a->q_buf, act, nact, maxn,
+                           a->pos, a->seq, a->n_seq, kc, vc, a->s_max, nullptr, nullptr,
+                           a->attn_out, a->attn_tiles ? ws.attend : nullptr, ws.attend_bytes,
+                           stream));
+    // 4. output projection + residual: h[out] = h[in] + o Wo^T
+    GemmArgs go{};
+    go.M_max = maxn; go.M_dev = nact; go.N = D; go.K = dq;
+    go.A = a->attn_out; go.lda = dq; go.B = wo; go.ldb = dq; go.epi = EPI_RESID;
+    go.C = a->h[out]; go.ldc = D; go.resid = a->h[in]; go.rows = act; go.name = "gemm_o";
+    ADEPT_TRY(run_gemm(dt, go, ws.gemm_tmp, s));
+    // 5. pre-FFN RMSNorm
+    ADEPT_TRY(rmsnorm_rows(dt, D, a->rms_eps, a->h[out], act, nact, maxn, g_ffn, a->x_norm, s));
+    // 6. gate/up projections with SwiGLU
+    GemmArgs gu{};
+    gu.M_max = maxn; gu.M_dev = nact; gu.N = F; gu.K = D;
+    gu.A = a->x_norm; gu.lda = D; gu.B = wg; gu.B2 = wu; gu.ldb = D; gu.epi = EPI_SWIGLU;
+    gu.C = a->ffn_act; gu.ldc = F; gu.name = "gemm_gate_up";
+    ADEPT_TRY(run_gemm(dt, gu, ws.gemm_tmp, s));
+    // 7. down projection + residual (in place on h[out])
+    GemmArgs gd{};
+    gd.M_max = maxn; gd.M_dev = nact; gd.N = D; gd.K = F;
+    gd.A = a->ffn_act; gd.lda = F; gd.B = wd; gd.ldb = F; gd.epi = EPI_RESID;
+    gd.C = a->h[out]; gd.ldc = D; gd.resid = a->h[out]; gd.rows = act; gd.name = "gemm_down";
+    ADEPT_TRY(run_gemm(dt, gd, ws.gemm_tmp, s));
+  }
+  // 8. exit test (Eq. 7-8)
+  ADEPT_TRY(adept_exit_test(dt, D, layer, &a->exit, act, nact, maxn, a->h[out], a->h[in],
+                            a->inertia, a->force_layer, a->exit_flag, a->sim_out, stream));
+  // 9. active-list update
+  ADEPT_TRY(adept_compact(layer, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
+                          a->exited, a->n_exited, a->exit_layer, ws.compact, ws.compact_bytes,
+                          stream));
+  // 10. K/V of the skipped layers of the rows that exited here (Eq. 9)
+  if (layer < N && maxn > 0) {
+    ADEPT_TRY(adept_kv_generate(dt, N, D, H, hd, a->rms_eps, a->h[out], a->exited, a->n_exited,
+                                maxn, a->exit_layer, a->slot, a->pos,
+                                off(a->w_qkv, (int64_t)dq * D), (int64_t)3 * dq * D,
+                                a->attn_norm, a->rope_cos, a->rope_sin, a->rope_max_pos,
+                                a->k_cache, a->v_cache, a->n_slots, ws.kvgen, ws.kvgen_bytes,
+                                stream));
+  }
+  return ADEPT_OK;
+}

@@ -1,0 +1,350 @@
+"""Per-entry-point parity of the HIP path against the CPU oracle.
+
+Both sides get the same seeded inputs (adept_inputs); the GPU side goes
+through the C ABI (binding.py).  Integer outputs (exit flags, compacted
+index lists, exit layers) must match bit for bit; floating-point outputs
+within the tolerances stated at each assertion.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import adept_inputs as ai
+from oracle import adept_oracle as O
+from paper_2601_03700_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev(x, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    return t.to(DEV) if dtype is None else t.to(DEV).to(dtype)
+
+
+def host64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def i32(x):
+    return dev(np.asarray(x, np.int32))
+
+
+def count(n):
+    return i32([n])
+
+
+# ----------------------------------------------------------------------------
+# exit test (Section 4.1 Eq. 7-8; Appendix H.3)
+# ----------------------------------------------------------------------------
+
+EXIT_CASES = [("bf16", 4096, "global"), ("bf16", 4096, "local"), ("bf16", 768, "global"),
+              ("bf16", 1000, "local"), ("f32", 256, "global"), ("f32", 256, "local"),
+              ("f32", 1028, "global")]
+
+
+@pytest.mark.parametrize("dt,D,metric", EXIT_CASES)
+def test_exit_test_matches_oracle(dt, D, metric):
+    say(f"exit_test dt={dt} D={D} metric={metric}")
+    n_tok, N, layer = 700, 8, 3
+    seed = 100 + D
+    h = ai.normal(seed, "h", (n_tok, D), dtype=dt)
+    # a reference correlated with h so the cosines spread over (0, 1)
+    ref = ai.normal(seed, "ref", (n_tok, D), dtype="f32") + 1.5 * h
+    if metric == "local":
+        ref = ai.to_bf16_values(ref) if dt == "bf16" else ref.astype(np.float32)
+    h[5] = 0.0                      # zero row: undefined cosine, never exits
+    ref[9] = 0.0                    # empty reference: likewise
+    rng = np.random.default_rng(seed)
+    active = np.sort(rng.choice(n_tok, 601, replace=False)).astype(np.int32)
+    active[:2] = [5, 9]
+    active = np.sort(active)
+    sims_o = O.cosine(h[active], ref[active])
+    srt = np.sort(sims_o[np.isfinite(sims_o)])
+    delta = float(0.5 * (srt[len(srt) // 2] + srt[len(srt) // 2 + 1]))  # between two tokens
+    force = np.zeros(n_tok, np.int32)
+    force[active[10]] = layer        # forced exit at this layer
+    force[active[11]] = layer + 1    # forced "not now"
+    cfg = B.exit_cfg(delta, N, metric)
+
+    h_d = dev(h, TDT[dt])
+    ref_d = dev(ref.astype(np.float32)) if metric == "global" else dev(ref, TDT[dt])
+    act_d, n_d = i32(active), count(len(active))
+    flag_d = torch.full((len(active) + 8,), 7, dtype=torch.uint8, device=DEV)
+    sim_d = torch.full((len(active),), -5.0, dtype=torch.float64, device=DEV)
+    B.exit_test(D, layer, cfg, act_d, n_d, len(active), h_d,
+                ref_d if metric == "local" else None, ref_d if metric == "global" else None,
+                i32(force), flag_d, sim_d)
+    torch.cuda.synchronize()
+
+    flags_o = O.exit_decision(sims_o, layer, N, delta, 1)
+    f = force[active]
+    flags_o = np.where(f > 0, (f == layer) & (layer <= N - 1), flags_o)
+    sims_g = sim_d.cpu().numpy()
+    assert np.isnan(sims_g[active == 5]).all() and np.isnan(sims_g[active == 9]).all()
+    ok = np.isfinite(sims_o)
+    np.testing.assert_array_equal(np.isfinite(sims_g), ok)
+    # both reduce in fp64: only the summation order differs
+    np.testing.assert_allclose(sims_g[ok], sims_o[ok], rtol=0, atol=1e-13)
+    # no token within fp64 summation-order noise of the threshold
+    assert np.min(np.abs(sims_o[ok] - delta)) > 1e-12
+    np.testing.assert_array_equal(flag_d[:len(active)].cpu().numpy().astype(bool), flags_o)
+    assert (flag_d[len(active):].cpu().numpy() == 7).all()      # nothing written past the count
+    if metric == "global":
+        new_o = O.inertia_update(ref[active], h[active])
+        new_g = ref_d.cpu().numpy()
+        # inertia is stored as float: one float rounding of the fp64 update
+        np.testing.assert_allclose(new_g[active], new_o, rtol=2 ** -23, atol=2 ** -40)
+        untouched = np.setdiff1d(np.arange(n_tok), active)
+        np.testing.assert_array_equal(new_g[untouched], ref.astype(np.float32)[untouched])
+
+
+def test_exit_test_window_and_special_thresholds():
+    say("exit_test window")
+    D, n, N = 512, 64, 6
+    h = ai.normal(5, "h", (n, D), dtype="bf16")
+    prev = ai.to_bf16_values(h + 0.01 * ai.normal(5, "p", (n, D)))
+    act = i32(np.arange(n))
+    for layer, delta, i_min, expect in ((N, -1.0, 1, False), (2, -1.0, 3, False),
+                                        (3, -1.0, 3, True), (3, math.inf, 1, False)):
+        flag = torch.zeros(n, dtype=torch.uint8, device=DEV)
+        B.exit_test(D, layer, B.exit_cfg(delta, N, "local", i_min), act, count(n), n,
+                    dev(h, torch.bfloat16), dev(prev, torch.bfloat16), None, None, flag)
+        torch.cuda.synchronize()
+        assert (flag.cpu().numpy() == int(expect)).all(), (layer, delta, i_min)
+    # an empty active list writes nothing
+    flag = torch.full((8,), 9, dtype=torch.uint8, device=DEV)
+    B.exit_test(D, 2, B.exit_cfg(0.5, N, "local"), act, count(0), n, dev(h, torch.bfloat16),
+                dev(prev, torch.bfloat16), None, None, flag)
+    torch.cuda.synchronize()
+    assert (flag.cpu().numpy() == 9).all()
+
+
+# ----------------------------------------------------------------------------
+# compaction (Appendix I)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n_tok,n_act,p_exit", [(16, 16, 0.5), (5000, 4097, 0.3),
+                                                (16384, 16384, 0.1), (16384, 9000, 0.0),
+                                                (16384, 9000, 1.0), (300000, 200003, 0.4)])
+def test_compact_matches_oracle(n_tok, n_act, p_exit):
+    say(f"compact n_tok={n_tok} n_act={n_act} p={p_exit}")
+    rng = np.random.default_rng(n_tok + n_act)
+    active = np.sort(rng.choice(n_tok, n_act, replace=False)).astype(np.int32)
+    flags = (rng.random(n_act) < p_exit).astype(np.uint8)
+    layer = 7
+    el0 = np.full(n_tok, 32, np.int32)
+    act_d, n_d = i32(active), count(n_act)
+    flag_d = dev(np.concatenate([flags, np.zeros(8, np.uint8)]))
+    nxt = torch.full((n_tok,), -1, dtype=torch.int32, device=DEV)
+    ext = torch.full((n_tok,), -1, dtype=torch.int32, device=DEV)
+    cnt = torch.full((2,), -1, dtype=torch.int32, device=DEV)
+    el = i32(el0)
+    wsb = B.compact_workspace_bytes(n_act)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=DEV) if wsb else None
+    B.compact(layer, flag_d, act_d, n_d, n_act, nxt, cnt[0:1], ext, cnt[1:2], el, ws)
+    torch.cuda.synchronize()
+    still, gone = O.compact(flags.astype(bool), active)
+    c = cnt.cpu().numpy()
+    assert c.tolist() == [len(still), len(gone)]
+    np.testing.assert_array_equal(nxt.cpu().numpy()[:len(still)], still)
+    np.testing.assert_array_equal(ext.cpu().numpy()[:len(gone)], gone)
+    assert (nxt.cpu().numpy()[len(still):] == -1).all() and (ext.cpu().numpy()[len(gone):] == -1).all()
+    expect = el0.copy()
+    expect[gone] = layer
+    np.testing.assert_array_equal(el.cpu().numpy(), expect)
+
+
+def test_compact_worked_example():
+    """Appendix I: <am> exits after layer 1, <a> after layer 2: 4 -> 3 -> 2 rows."""
+    say("compact worked example")
+    act = i32([0, 1, 2, 3])
+    n = count(4)
+    el = i32([4, 4, 4, 4])
+    nxt1, ex1, c1 = (torch.empty(4, dtype=torch.int32, device=DEV) for _ in range(3))
+    B.compact(1, dev(np.array([0, 1, 0, 0, 0, 0, 0, 0], np.uint8)), act, n, 4, nxt1, c1[0:1],
+              ex1, c1[1:2], el)
+    nxt2, ex2, c2 = (torch.empty(4, dtype=torch.int32, device=DEV) for _ in range(3))
+    B.compact(2, dev(np.array([0, 1, 0, 0, 0, 0, 0, 0], np.uint8)), nxt1, c1[0:1], 4, nxt2,
+              c2[0:1], ex2, c2[1:2], el)
+    torch.cuda.synchronize()
+    assert int(c1[0]) == 3 and int(c2[0]) == 2
+    assert nxt2[:2].cpu().tolist() == [0, 3]
+    assert el.cpu().tolist() == [4, 1, 2, 4]
+
+
+# ----------------------------------------------------------------------------
+# decoupled KV generation (Section 4 Eq. 6, Section 4.3 Eq. 9)
+# ----------------------------------------------------------------------------
+
+def _kv_case(dt, N, D, H, hd, n_tok, seed, std, exit_lo=0, exit_hi=None):
+    shape = ai.DecoderShape(n_layers=N, d_model=D, n_heads=H, head_dim=hd, d_ff=64, vocab=8)
+    Dq = H * hd
+    s = ai.normal(seed, "s", (n_tok, D), dtype=dt)
+    wkv = ai.normal(seed, "wkv", (N, 2 * Dq, D), std=std, dtype=dt)
+    gain = ai.gains(seed, "gain", (N, D), dtype=dt)
+    exit_hi = N if exit_hi is None else exit_hi
+    el = np.random.default_rng(seed).integers(exit_lo, exit_hi + 1, n_tok).astype(np.int32)
+    return shape, s, wkv, gain, el
+
+
+def _layers_for_oracle(wkv, gain, Dq):
+    return [{"attn_norm": gain[r], "wk": wkv[r][:Dq], "wv": wkv[r][Dq:]} for r in range(len(gain))]
+
+
+def _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_slots, max_pos):
+    N, D, H, hd = shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim
+    Dq = H * hd
+    cos = torch.empty((max_pos, hd // 2), dtype=torch.float32, device=DEV)
+    sin = torch.empty_like(cos)
+    B.rope_table(max_pos, hd, shape.rope_theta, cos, sin)
+    kc = torch.full((N, n_slots, H, hd), float("nan"), dtype=TDT[dt], device=DEV)
+    vc = torch.full_like(kc, float("nan"))
+    wsb = B.kv_generate_workspace_bytes(N, len(rows))
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=DEV)
+    B.kv_generate(N, D, H, hd, shape.rms_eps, dev(s, TDT[dt]), i32(rows), count(len(rows)),
+                  len(rows), i32(el), i32(slot), i32(pos), dev(wkv, TDT[dt]), 2 * Dq * D,
+                  dev(gain, TDT[dt]), cos, sin, kc, vc, n_slots, ws)
+    torch.cuda.synchronize()
+    return kc, vc
+
+
+@pytest.mark.parametrize("dt,hd", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+def test_kv_generate_matches_oracle(dt, hd):
+    say(f"kv_generate dt={dt} hd={hd}")
+    N, D, H = 5, 256, 4 if hd == 64 else 2
+    n_tok = 300
+    shape, s, wkv, gain, el = _kv_case(dt, N, D, H, hd, n_tok, 31 + hd, std=0.0625)
+    Dq = H * hd
+    rng = np.random.default_rng(3)
+    rows = np.sort(rng.choice(n_tok, 257, replace=False)).astype(np.int32)  # ragged tile tail
+    pos = rng.integers(0, 2000, n_tok).astype(np.int32)
+    slot = rng.permutation(n_tok + 11)[:n_tok].astype(np.int32)
+    kc, vc = _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_tok + 11, 2048)
+    gen = O.kv_generate({"layers": _layers_for_oracle(wkv, gain, Dq)}, shape, s[rows], el[rows],
+                        pos[rows])
+    K, V = host64(kc), host64(vc)
+    written = np.zeros((N, n_tok + 11), bool)
+    for r, (idx, k, v) in gen.items():
+        sl = slot[rows[idx]]
+        written[r - 1, sl] = True
+        if dt == "f32":
+            # fp32: relative to the largest magnitude of the tensor (1e-5)
+            for a, b in ((K[r - 1][sl], k), (V[r - 1][sl], v)):
+                assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(b))
+        else:
+            # bf16: 2e-2 absolute, plus one bf16 ulp of |b| above magnitude 4
+            for a, b in ((K[r - 1][sl], k), (V[r - 1][sl], v)):
+                tol = np.maximum(2e-2, 2.0 ** (np.floor(np.log2(np.abs(b) + 1e-30)) - 7))
+                assert np.all(np.abs(a - b) <= tol), np.max(np.abs(a - b))
+    # exactly the (layer, slot) pairs of skipped layers were written
+    np.testing.assert_array_equal(~np.isnan(K).any(axis=(2, 3)), written)
+    np.testing.assert_array_equal(~np.isnan(V).any(axis=(2, 3)), written)
+
+
+def test_kv_generate_equals_layer_by_layer():
+    """Eq. 6: one call over all (token, layer) pairs equals calling once per
+    exit layer (each call a separate group) -- decoupling changes nothing."""
+    say("kv_generate decoupled vs per-layer")
+    dt, N, D, H, hd = "bf16", 6, 256, 2, 128
+    shape, s, wkv, gain, el = _kv_case(dt, N, D, H, hd, 200, 77, std=0.0625)
+    rows = np.arange(200, dtype=np.int32)
+    pos = np.arange(200, dtype=np.int32)
+    kc, vc = _run_kv(dt, shape, s, wkv, gain, el, rows, pos, pos, 200, 256)
+    for L in range(N):
+        sub = rows[el == L]
+        if sub.size == 0:
+            continue
+        k1, v1 = _run_kv(dt, shape, s, wkv, gain, el, sub, pos, pos, 200, 256)
+        a = torch.isfinite(k1.float())
+        assert torch.equal(k1[a], kc[a]) and torch.equal(v1[a], vc[a])
+
+
+# ----------------------------------------------------------------------------
+# attention over a mixed cache (Section 3 Eq. 5)
+# ----------------------------------------------------------------------------
+
+def _attend_case(dt, H, hd, n_seq, s_max, lens, frac_active, seed, causal=True, live=False,
+                 decode=False, with_ws=True):
+    rng = np.random.default_rng(seed)
+    kc = ai.normal(seed, "k", (n_seq * s_max, H, hd), dtype=dt)
+    vc = ai.normal(seed, "v", (n_seq * s_max, H, hd), dtype=dt)
+    # poison slots past each sequence's length: never read
+    for b in range(n_seq):
+        kc[b * s_max + lens[b]:(b + 1) * s_max] = np.nan
+        vc[b * s_max + lens[b]:(b + 1) * s_max] = np.nan
+    if decode:
+        rows_pos = np.array(lens) - 1
+        pos = rows_pos.astype(np.int32)
+        seq = np.arange(n_seq, dtype=np.int32)
+        active = np.arange(n_seq, dtype=np.int32)
+    else:
+        T = s_max
+        pos = np.tile(np.arange(T), n_seq).astype(np.int32)
+        seq = np.repeat(np.arange(n_seq), T).astype(np.int32)
+        cand = np.array([b * T + p for b in range(n_seq) for p in range(lens[b])])
+        k = max(1, int(frac_active * cand.size))
+        active = np.sort(rng.choice(cand, k, replace=False)).astype(np.int32)
+    n = active.size
+    q = ai.normal(seed, "q", (n, H, hd), dtype=dt)
+    key_live = None
+    if live:
+        key_live = (rng.random(n_seq * s_max) < 0.7).astype(np.uint8)
+        for a in active:  # a live query's own key is live
+            key_live[seq[a] * s_max + pos[a]] = 1
+    out = torch.full((n + 3, H, hd), 123.0, dtype=TDT[dt], device=DEV)
+    ws = None
+    if with_ws:
+        wsb = B.attend_workspace_bytes(n, n_seq)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    B.attend(H, hd, dev(q, TDT[dt]), i32(active), count(n), n, i32(pos), i32(seq), n_seq,
+             dev(kc, TDT[dt]), dev(vc, TDT[dt]), s_max, out, causal=causal,
+             key_len=None if causal else i32(lens),
+             key_live=None if key_live is None else dev(key_live), workspace=ws)
+    torch.cuda.synchronize()
+    kc64, vc64 = np.nan_to_num(kc.astype(np.float64)), np.nan_to_num(vc.astype(np.float64))
+    km = None
+    if key_live is not None:
+        km = np.stack([key_live[seq[a] * s_max: seq[a] * s_max + s_max].astype(bool) for a in active])
+    ref = O.attend(q.astype(np.float64), kc64, vc64, seq[active] * s_max, pos[active],
+                   key_len=np.array(lens)[seq[active]], causal=causal, key_mask=km)
+    got = host64(out)
+    assert (got[n:] == 123.0).all()
+    return got[:n], ref
+
+
+@pytest.mark.parametrize("hd,n_seq,s_max,frac", [(128, 3, 300, 1.0), (128, 2, 1000, 0.37),
+                                                 (64, 4, 200, 0.6), (128, 1, 64, 1.0),
+                                                 (128, 5, 70, 0.05)])
+def test_attend_prefill_mfma_matches_oracle(hd, n_seq, s_max, frac):
+    say(f"attend prefill hd={hd} n_seq={n_seq} s_max={s_max} frac={frac}")
+    lens = [s_max] * n_seq
+    got, ref = _attend_case("bf16", 4 if hd == 128 else 6, hd, n_seq, s_max, lens, frac, 7 + hd)
+    # bf16 output and bf16 probabilities: 2e-2 absolute on O(1) values
+    assert np.max(np.abs(got - ref)) <= 2e-2, np.max(np.abs(got - ref))
+
+
+@pytest.mark.parametrize("dt,decode,causal,live", [("f32", False, True, False),
+                                                   ("f32", True, True, False),
+                                                   ("bf16", True, True, False),
+                                                   ("bf16", False, False, True),
+                                                   ("f32", False, False, True)])
+def test_attend_generic_matches_oracle(dt, decode, causal, live):
+    say(f"attend generic dt={dt} decode={decode} causal={causal} live={live}")
+    n_seq, s_max = 3, 150
+    lens = [150, 97, 31] if (decode or not causal) else [150] * 3
+    got, ref = _attend_case(dt, 2, 64, n_seq, s_max, lens, 0.5, 11, causal=causal, live=live,
+                            decode=decode, with_ws=False)
+    if dt == "f32":
+        assert np.max(np.abs(got - ref)) <= 1e-5 * np.max(np.abs(ref))
+    else:
+        assert np.max(np.abs(got - ref)) <= 2e-2
