@@ -76,6 +76,27 @@ def step_work(shape, exit_layer, pos):
     return w, cnt
 
 
+def family(kernel_name):
+    """Work family of a timed kernel name (template arguments ignored), or None."""
+    base = kernel_name.strip("()").split("<")[0]
+    return {"gemm_qkv": "gemm_qkv", "gemm_o": "gemm_o", "gemm_gate_up": "gemm_gate_up",
+            "gemm_down": "gemm_down", "attend_prefill_kernel": "attention",
+            "gemm_kv_grouped_kernel": "kv_generate"}.get(base)
+
+
+def kernel_table(kern, work, ms, steps):
+    """Per-kernel launches, average duration, share of the timed region and,
+    for the matrix kernels, achieved TFLOP/s from the algorithmic work."""
+    out = {}
+    for name, (n_launch, tot) in sorted(kern.items(), key=lambda kv: -kv[1][1]):
+        out[name] = {"launches": n_launch, "avg_us": 1e3 * tot / max(n_launch, 1),
+                     "share": tot / (ms * steps)}
+        f = family(name)
+        if f and tot > 0:
+            out[name]["tflops"] = work[f] * steps / (tot / 1e3) / 1e12
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -135,20 +156,10 @@ def main():
     exit_frac = 1.0 - cnt[-1] / n_tok
     log(f"{ms:.1f} ms/step, {tok_s:.0f} tokens/s, exited {exit_frac:.3%}")
 
-    # dominant kernel: the one with the largest share of the timed region
-    fam = {"gemm_qkv": "gemm_qkv", "gemm_o": "gemm_o", "gemm_gate_up": "gemm_gate_up",
-           "gemm_down": "gemm_down", "attend_prefill_kernel<128>": "attention",
-           "gemm_kv_grouped_kernel": "kv_generate"}
-    per_kernel = {}
-    for name, (n_launch, tot) in sorted(kern.items(), key=lambda kv: -kv[1][1]):
-        per_kernel[name] = {"launches": n_launch, "avg_us": 1e3 * tot / max(n_launch, 1),
-                            "share": tot / (ms * args.steps)}
-        if name in fam:
-            flops = work[fam[name]] * args.steps
-            per_kernel[name]["tflops"] = flops / (tot / 1e3) / 1e12 if tot > 0 else None
-    dom = max((k for k in kern if k in fam), key=lambda k: kern[k][1])
+    per_kernel = kernel_table(kern, work, ms, args.steps)
+    dom = max((k for k in kern if family(k)), key=lambda k: kern[k][1])
     d_launch, d_ms = kern[dom]
-    d_flops_launch = work[fam[dom]] * args.steps / d_launch
+    d_flops_launch = work[family(dom)] * args.steps / d_launch
     d_avg_s = d_ms / d_launch / 1e3
     achieved = d_flops_launch / d_avg_s
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
@@ -180,12 +191,13 @@ def main():
                                   timing=True)
         work_f, cnt_f = step_work(shape, res_f.exit_layer, pos)
         out["no_exit"] = {"tokens_per_s": n_tok / (ms_inf / 1e3), "ms_per_step": ms_inf}
-        kv_f = kern_f.get("gemm_kv_grouped_kernel", (0, 0.0))
+        steps_f = max(2, args.steps // 2)
         out["fixed_schedule"] = {
             "schedule": "exit layer uniform in 8..31 per token (seeded)",
             "tokens_per_s": n_tok / (ms_f / 1e3), "ms_per_step": ms_f,
             "speedup_vs_no_exit": ms_inf / ms_f,
-            "kv_generate_ms_per_step": kv_f[1] / max(2, args.steps // 2),
+            "active_rows_per_layer": cnt_f,
+            "kernels": kernel_table(kern_f, work_f, ms_f, steps_f),
         }
         log(f"no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
         out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
@@ -217,7 +229,7 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
 
     def call():
         B.kv_generate(N, D, H, hd, shape.rms_eps, s, rows, cnt, n, el, rows, rows, w_kv,
-                      3 * Dq * D, model.attn_norm, cos, sin, kc, vc, n, ws)
+                      3 * Dq * D, None, cos, sin, kc, vc, n, ws)
     call()
     torch.cuda.synchronize()
     B.timing_reset()

@@ -135,7 +135,10 @@ adept_status adept_compact(int layer, const uint8_t* exit_flag, const int32_t* a
  *        is [2*H*hd][d_model] (nn.Linear order): H*hd rows of Wk_r, then H*hd
  *        rows of Wv_r.  (A stacked [N][3*H*hd][D] QKV weight passes its K part
  *        with stride 3*H*hd*D.)
- *  attn_gain [n_layers][d_model] (dtype): layer r's pre-attention RMSNorm gain.
+ *  attn_gain [n_layers][d_model] (dtype), nullable: layer r's pre-attention
+ *        RMSNorm gain.  NULL means the gains are already folded into the
+ *        columns of w_kv (adept_fold_gain), which the bf16 path requires; the
+ *        kernels then apply only the 1/rms(s) row factor.
  *  rope_cos/rope_sin [rope_max_pos][hd/2] float (adept_rope_table).
  *  k_cache/v_cache [n_layers][n_slots][H][hd] (dtype): written only at the
  *        (layer, slot) pairs above.
@@ -192,13 +195,14 @@ typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ff;
   float rms_eps;
   adept_exit_cfg exit;
-  /* weights, stacked over layers (dtype) */
-  const void* attn_norm; /* [N][D] */
-  const void* w_qkv;     /* [N][3*H*hd][D]: Wq rows, Wk rows, Wv rows */
+  /* weights, stacked over layers (dtype).  The pre-norm gains are folded
+   * into the matrices that consume the normalised input (adept_fold_gain):
+   * w_qkv columns carry the layer's attention-norm gain, w_gate / w_up
+   * columns its FFN-norm gain; the kernels apply only the 1/rms row factor. */
+  const void* w_qkv;     /* [N][3*H*hd][D]: Wq rows, Wk rows, Wv rows (gain folded) */
   const void* w_o;       /* [N][D][H*hd] */
-  const void* ffn_norm;  /* [N][D] */
-  const void* w_gate;    /* [N][F][D] */
-  const void* w_up;      /* [N][F][D] */
+  const void* w_gate;    /* [N][F][D] (gain folded) */
+  const void* w_up;      /* [N][F][D] (gain folded) */
   const void* w_down;    /* [N][D][F] */
   const float* rope_cos; /* [rope_max_pos][hd/2] */
   const float* rope_sin;
@@ -225,7 +229,6 @@ typedef struct {
   void* v_cache;
   int64_t n_slots;
   /* per-layer scratch (dtype), caller-allocated */
-  void* x_norm;          /* [n_tok][D] */
   void* q_buf;           /* [n_tok][H*hd] */
   void* attn_out;        /* [n_tok][H*hd] */
   void* ffn_act;         /* [n_tok][F] */
@@ -235,6 +238,16 @@ typedef struct {
 
 size_t adept_layer_workspace_bytes(const adept_layer_args* a);
 adept_status adept_layer_step(const adept_layer_args* a, int layer, void* stream);
+
+/* Folds a norm gain into the weight matrices that consume the normalised
+ * vector, in place: w[l][o][c] *= gain[l][c] for l < n_mats, o < rows,
+ * c < cols, rounded to dtype; matrix l starts at w + l*mat_stride, its gain at
+ * gain + l*gain_stride (elements).  Since (x * g) W^T = x (W diag(g))^T, an
+ * RMSNorm followed by a projection becomes a projection scaled per row by
+ * 1/rms(x), which the GEMM epilogues apply.  Done once at model load. */
+adept_status adept_fold_gain(adept_dtype dt, int n_mats, int rows, int cols, void* w,
+                             int64_t mat_stride, const void* gain, int64_t gain_stride,
+                             void* stream);
 
 /* Embedding gather (support step before layer 1): h0[k] = embed[ids[k]],
  * k < n; embed [vocab][D] (dtype), h0 [n][D] (dtype). */

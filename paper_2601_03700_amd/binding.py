@@ -38,7 +38,7 @@ class LayerArgs(ctypes.Structure):
     _fields_ = [
         ("dtype", _i32), ("n_layers", _i32), ("d_model", _i32), ("n_heads", _i32),
         ("head_dim", _i32), ("d_ff", _i32), ("rms_eps", ctypes.c_float), ("exit", ExitCfg),
-        ("attn_norm", _vp), ("w_qkv", _vp), ("w_o", _vp), ("ffn_norm", _vp), ("w_gate", _vp),
+        ("w_qkv", _vp), ("w_o", _vp), ("w_gate", _vp),
         ("w_up", _vp), ("w_down", _vp), ("rope_cos", _vp), ("rope_sin", _vp),
         ("rope_max_pos", _i32),
         ("n_tok", _i32), ("max_active", _i32), ("n_seq", _i32), ("s_max", _i32),
@@ -47,7 +47,7 @@ class LayerArgs(ctypes.Structure):
         ("active", _vp * 2), ("n_active", _vp * 2), ("exited", _vp), ("n_exited", _vp),
         ("exit_layer", _vp), ("exit_flag", _vp), ("sim_out", _vp), ("force_layer", _vp),
         ("k_cache", _vp), ("v_cache", _vp), ("n_slots", _i64),
-        ("x_norm", _vp), ("q_buf", _vp), ("attn_out", _vp), ("ffn_act", _vp),
+        ("q_buf", _vp), ("attn_out", _vp), ("ffn_act", _vp),
         ("workspace", _vp), ("workspace_bytes", _sz),
     ]
 
@@ -74,6 +74,7 @@ _SIGS = {
                                   _i32, _vp, _vp, _vp, _vp, _vp]),
     "adept_argmax": (_i32, [_i32, _i32, _vp, _vp, _vp]),
     "adept_token_init": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "adept_fold_gain": (_i32, [_i32, _i32, _i32, _i32, _vp, _i64, _vp, _i64, _vp]),
     "adept_timing_enable": (_i32, [_i32]),
     "adept_timing_reset": (None, []),
     "adept_timing_count": (_i32, []),
@@ -245,3 +246,15 @@ def timing_read():
                "adept_timing_get")
         out[buf.value.decode()] = (int(n.value), float(ms.value))
     return out
+
+
+def fold_gain(w, gain, stream=None):
+    """In place: w[l][o][c] *= gain[l][c] for a stacked weight w [L, rows, cols]
+    (or a [L, rows, cols] view with unit column stride) and gain [L, cols]."""
+    L, rows, cols = w.shape
+    assert w.stride(2) == 1 and gain.stride(-1) == 1 and gain.shape[-1] == cols
+    if rows > 1:
+        assert w.stride(1) == cols, "rows of each matrix must be contiguous"
+    _check(lib().adept_fold_gain(dtype_code(w), L, rows, cols, ptr(w), w.stride(0), ptr(gain),
+                                 gain.stride(0) if gain.dim() == 2 else 0, stream_handle(stream)),
+           "adept_fold_gain")

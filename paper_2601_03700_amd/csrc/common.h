@@ -148,6 +148,7 @@ struct GemmArgs {
   int epi;
   // epilogue operands
   void* C; int64_t ldc; int c_f32;
+  const float* row_scale; // per-row scale of the accumulators (1/rms of the row), nullable
   const int32_t* rows;    // token row of compact index k (QKV/RESID/KV)
   const void* resid;      // RESID source (may equal C)
   const int32_t* pos;     // [n_tok]
@@ -163,8 +164,10 @@ adept_status gemm_f32(const GemmArgs& g, float* tmp, hipStream_t s);      // f32
 adept_status gemm_f32_direct(const GemmArgs& g, hipStream_t s);           // f32, C = A B^T
 adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32_t* n_work,
                              int max_work, const int32_t* grp_m, const int32_t* srows,
-                             const float* rinv, const void* gain, int64_t b_layer_stride,
-                             int64_t cache_layer_stride, hipStream_t s);
+                             int64_t b_layer_stride, int64_t cache_layer_stride, hipStream_t s);
+// out[k] = 1/sqrt(mean(x[rows[k]]^2) + eps) for k < min(*n_dev, max_n) (rows nullable: k).
+adept_status row_rinv(adept_dtype dt, int d, float eps, const void* x, const int32_t* rows,
+                      const int32_t* n_dev, int max_n, float* out, hipStream_t s);
 adept_status rmsnorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
                               const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
                               int max_n, const void* gain, void* out, hipStream_t s);

@@ -5,8 +5,10 @@
 // with i* < r form a prefix of length grp_m[r]; it then lists the work items
 // (r, 256-row tile).  A wave-per-row pass computes each sorted row's
 // 1/sqrt(mean s^2 + eps).  The grouped MFMA GEMM (gemm.hip) does the rest in
-// one launch: norm and gain applied while staging A, RoPE on K in the
-// epilogue, K/V stored straight into cache[r][slot].
+// one launch.  The norm is split: layer r's gain multiplies the columns of
+// W_r beforehand (adept_fold_gain: (s * g) W^T = s (W diag g)^T), and the
+// row factor 1/rms(s) scales the accumulators; RoPE on K in the epilogue,
+// K/V stored straight into cache[r][slot].
 //
 // f32 (small configurations): one workgroup per (row, layer) pair computes
 // the normalised state in LDS and the 2*H*hd dot products directly.
@@ -128,8 +130,8 @@ __global__ __launch_bounds__(256) void kvgen_f32_kernel(
   if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
   const float rinv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
-  const float* g = gain + (int64_t)(r - 1) * d;
-  for (int c = tid; c < d; c += 256) u[c] = x[c] * rinv * g[c];
+  const float* g = gain ? gain + (int64_t)(r - 1) * d : nullptr;
+  for (int c = tid; c < d; c += 256) u[c] = x[c] * rinv * (g ? g[c] : 1.0f);
   __syncthreads();
   const int dq = H * hd;
   const float* W = w_kv + (int64_t)(r - 1) * w_stride;
@@ -179,9 +181,12 @@ extern "C" adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_mo
                 "kv_generate: bad sizes");
   ADEPT_REQUIRE(max_rows >= 0 && n_slots > 0 && rope_max_pos > 0, "kv_generate: bad sizes");
   ADEPT_REQUIRE(max_rows < (1 << 24), "kv_generate: max_rows too large");
-  ADEPT_REQUIRE(s_map && rows && n_rows && exit_layer && cache_slot && pos && w_kv && attn_gain &&
-                    rope_cos && rope_sin && k_cache && v_cache,
+  ADEPT_REQUIRE(s_map && rows && n_rows && exit_layer && cache_slot && pos && w_kv && rope_cos &&
+                    rope_sin && k_cache && v_cache,
                 "kv_generate: NULL tensor");
+  ADEPT_REQUIRE(dt == ADEPT_F32 || attn_gain == nullptr,
+                "kv_generate: bf16 takes the gains folded into w_kv (adept_fold_gain); "
+                "pass attn_gain = NULL");
   const int dq = n_heads * head_dim;
   ADEPT_REQUIRE(w_kv_layer_stride >= (int64_t)2 * dq * d_model,
                 "kv_generate: layer stride %lld below 2*H*hd*D", (long long)w_kv_layer_stride);
@@ -201,8 +206,8 @@ extern "C" adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_mo
   ADEPT_REQUIRE(d_model % 64 == 0, "kv_generate: bf16 needs d_model %% 64 == 0");
   ADEPT_REQUIRE((head_dim == 64 || head_dim == 128) && dq % 256 == 0,
                 "kv_generate: bf16 needs head_dim 64/128 and H*hd %% 256 == 0");
-  ADEPT_REQUIRE(aligned16(s_map) && aligned16(w_kv) && aligned16(attn_gain) &&
-                    aligned16(workspace),
+  ADEPT_REQUIRE(aligned16(s_map) && aligned16(w_kv) && aligned16(workspace) &&
+                    w_kv_layer_stride % 8 == 0,
                 "kv_generate: tensors must be 16-byte aligned");
   size_t need = 0;
   carve(nullptr, n_layers, max_rows, &need);
@@ -222,8 +227,8 @@ extern "C" adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_mo
   g.A = s_map; g.lda = d_model; g.B = w_kv; g.ldb = d_model;
   g.epi = EPI_KV; g.pos = pos; g.slot = cache_slot;
   g.rope_cos = rope_cos; g.rope_sin = rope_sin; g.head_dim = head_dim; g.d_q = dq;
-  g.k_cache = k_cache; g.v_cache = v_cache;
+  g.k_cache = k_cache; g.v_cache = v_cache; g.row_scale = w.rinv;
   const int max_work = n_layers * ceil_div(max_rows, kTileM);
-  return gemm_kv_grouped(g, w.work, w.n_work, max_work, w.grp_m, w.srows, w.rinv, attn_gain,
-                         w_kv_layer_stride, layer_stride, s);
+  return gemm_kv_grouped(g, w.work, w.n_work, max_work, w.grp_m, w.srows, w_kv_layer_stride,
+                         layer_stride, s);
 }

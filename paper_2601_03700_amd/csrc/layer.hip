@@ -12,6 +12,7 @@ namespace {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct LayerWs {
+  float* rinv;    // [n_tok] 1/rms of the active rows (compact order)
   void* compact;  size_t compact_bytes;
   void* attend;   size_t attend_bytes;
   void* kvgen;    size_t kvgen_bytes;
@@ -24,6 +25,7 @@ LayerWs carve(const adept_layer_args* a, void* base) {
   char* p = (char*)base;
   size_t off = 0;
   const int dq = a->n_heads * a->head_dim;
+  w.rinv = (float*)(p + off); off += align256((size_t)a->n_tok * sizeof(float));
   w.compact_bytes = adept_compact_workspace_bytes(a->n_tok);
   w.compact = p + off; off += align256(w.compact_bytes);
   w.attend_bytes = adept_attend_workspace_bytes(a->n_tok, a->n_seq);
@@ -64,12 +66,11 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   ADEPT_REQUIRE(a->max_active >= 0 && a->max_active <= a->n_tok, "layer_step: bad max_active");
   ADEPT_REQUIRE(a->n_seq > 0 && a->s_max > 0 && a->n_slots >= (int64_t)a->n_seq * a->s_max,
                 "layer_step: cache smaller than n_seq * s_max");
-  ADEPT_REQUIRE(a->attn_norm && a->w_qkv && a->w_o && a->ffn_norm && a->w_gate && a->w_up &&
-                    a->w_down && a->rope_cos && a->rope_sin && a->h[0] && a->h[1] && a->pos &&
-                    a->seq && a->slot && a->active[0] && a->active[1] && a->n_active[0] &&
-                    a->n_active[1] && a->exited && a->n_exited && a->exit_layer &&
-                    a->exit_flag && a->k_cache && a->v_cache && a->x_norm && a->q_buf &&
-                    a->attn_out && a->ffn_act,
+  ADEPT_REQUIRE(a->w_qkv && a->w_o && a->w_gate && a->w_up && a->w_down && a->rope_cos &&
+                    a->rope_sin && a->h[0] && a->h[1] && a->pos && a->seq && a->slot &&
+                    a->active[0] && a->active[1] && a->n_active[0] && a->n_active[1] &&
+                    a->exited && a->n_exited && a->exit_layer && a->exit_flag && a->k_cache &&
+                    a->v_cache && a->q_buf && a->attn_out && a->ffn_act,
                 "layer_step: NULL pointer in args");
   ADEPT_REQUIRE(a->exit.metric != ADEPT_SIM_GLOBAL || a->inertia,
                 "layer_step: GLOBAL metric needs inertia");
@@ -95,18 +96,18 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   const void* wg = off(a->w_gate, li * (int64_t)F * D);
   const void* wu = off(a->w_up, li * (int64_t)F * D);
   const void* wd = off(a->w_down, li * (int64_t)D * F);
-  const void* g_attn = off(a->attn_norm, li * D);
-  const void* g_ffn = off(a->ffn_norm, li * D);
   void* kc = (void*)off(a->k_cache, li * a->n_slots * dq);
   void* vc = (void*)off(a->v_cache, li * a->n_slots * dq);
 
   if (maxn > 0) {
-    // 1. pre-attention RMSNorm of the active rows (compact)
-    ADEPT_TRY(rmsnorm_rows(dt, D, a->rms_eps, a->h[in], act, nact, maxn, g_attn, a->x_norm, s));
-    // 2. Q/K/V projections, RoPE, own K/V into cache[layer]
+    // 1. pre-attention RMSNorm: the gain is folded into W_qkv, the row factor
+    //    1/rms(h) scales the GEMM accumulators
+    ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[in], act, nact, maxn, ws.rinv, s));
+    // 2. Q/K/V projections of the gathered active rows, RoPE, own K/V into cache[layer]
     GemmArgs g{};
     g.M_max = maxn; g.M_dev = nact; g.N = 3 * dq; g.K = D;
-    g.A = a->x_norm; g.lda = D; g.B = wqkv; g.ldb = D; g.epi = EPI_QKV;
+    g.A = a->h[in]; g.a_rows = act; g.lda = D; g.B = wqkv; g.ldb = D; g.epi = EPI_QKV;
+    g.row_scale = ws.rinv;
     g.rows = act; g.pos = a->pos; g.slot = a->slot;
     g.rope_cos = a->rope_cos; g.rope_sin = a->rope_sin; g.head_dim = hd; g.d_q = dq;
     g.q_out = a->q_buf; g.k_cache = kc; g.v_cache = vc; g.name = "gemm_qkv";
@@ -122,12 +123,13 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     go.A = a->attn_out; go.lda = dq; go.B = wo; go.ldb = dq; go.epi = EPI_RESID;
     go.C = a->h[out]; go.ldc = D; go.resid = a->h[in]; go.rows = act; go.name = "gemm_o";
     ADEPT_TRY(run_gemm(dt, go, ws.gemm_tmp, s));
-    // 5. pre-FFN RMSNorm
-    ADEPT_TRY(rmsnorm_rows(dt, D, a->rms_eps, a->h[out], act, nact, maxn, g_ffn, a->x_norm, s));
+    // 5. pre-FFN RMSNorm (gain folded into W_gate / W_up)
+    ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[out], act, nact, maxn, ws.rinv, s));
     // 6. gate/up projections with SwiGLU
     GemmArgs gu{};
     gu.M_max = maxn; gu.M_dev = nact; gu.N = F; gu.K = D;
-    gu.A = a->x_norm; gu.lda = D; gu.B = wg; gu.B2 = wu; gu.ldb = D; gu.epi = EPI_SWIGLU;
+    gu.A = a->h[out]; gu.a_rows = act; gu.lda = D; gu.B = wg; gu.B2 = wu; gu.ldb = D;
+    gu.epi = EPI_SWIGLU; gu.row_scale = ws.rinv;
     gu.C = a->ffn_act; gu.ldc = F; gu.name = "gemm_gate_up";
     ADEPT_TRY(run_gemm(dt, gu, ws.gemm_tmp, s));
     // 7. down projection + residual (in place on h[out])
@@ -149,7 +151,7 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     ADEPT_TRY(adept_kv_generate(dt, N, D, H, hd, a->rms_eps, a->h[out], a->exited, a->n_exited,
                                 maxn, a->exit_layer, a->slot, a->pos,
                                 off(a->w_qkv, (int64_t)dq * D), (int64_t)3 * dq * D,
-                                a->attn_norm, a->rope_cos, a->rope_sin, a->rope_max_pos,
+                                nullptr, a->rope_cos, a->rope_sin, a->rope_max_pos,
                                 a->k_cache, a->v_cache, a->n_slots, ws.kvgen, ws.kvgen_bytes,
                                 stream));
   }

@@ -67,6 +67,39 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int d, float eps, const T*
   for (int c = lane; c < d; c += 64) st(o + c, ld(x + c) * r * ld(gain + c));
 }
 
+// One wave per row: out[k] = 1/sqrt(mean(x[row]^2) + eps).
+template <typename T>
+__global__ __launch_bounds__(256) void row_rinv_kernel(int d, float eps, const T* __restrict__ x,
+                                                       const int32_t* __restrict__ rows,
+                                                       const int32_t* __restrict__ n_dev,
+                                                       int max_n, float* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int n = n_dev ? min(*n_dev, max_n) : max_n;
+  if (k >= n) return;
+  const T* xr = x + (int64_t)(rows ? rows[k] : k) * d;
+  float ss = 0.0f;
+  for (int c = lane; c < d; c += 64) {
+    const float v = ld(xr + c);
+    ss = fmaf(v, v, ss);
+  }
+  ss = wave_sum_f32(ss);
+  if (lane == 0) out[k] = 1.0f / sqrtf(ss / (float)d + eps);
+}
+
+// w[l][o][c] *= gain[l][c] (in place, rounded to the element type).
+template <typename T>
+__global__ void fold_gain_kernel(int rows, int cols, T* __restrict__ w, int64_t mat_stride,
+                                 const T* __restrict__ gain, int64_t gain_stride) {
+  const int l = blockIdx.y;
+  T* wm = w + (int64_t)l * mat_stride;
+  const T* g = gain + (int64_t)l * gain_stride;
+  const int64_t total = (int64_t)rows * cols;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x)
+    st(wm + e, ld(wm + e) * ld(g + e % cols));
+}
+
 template <typename T>
 __global__ void embed_kernel(int n, int d, int vocab, const int32_t* __restrict__ ids,
                              const T* __restrict__ table, T* __restrict__ out) {
@@ -126,6 +159,19 @@ adept_status rmsnorm_rows(adept_dtype dt, int d, float eps, const void* x, const
   return rmsnorm_rows_sel(dt, d, eps, x, x, nullptr, rows, n_dev, max_n, gain, out, s);
 }
 
+adept_status row_rinv(adept_dtype dt, int d, float eps, const void* x, const int32_t* rows,
+                      const int32_t* n_dev, int max_n, float* out, hipStream_t s) {
+  if (max_n <= 0) return ADEPT_OK;
+  dim3 grid(ceil_div(max_n, 4)), block(256);
+  if (dt == ADEPT_BF16)
+    ADEPT_LAUNCH(row_rinv_kernel<bf16>, grid, block, 0, s, d, eps, (const bf16*)x, rows, n_dev,
+                 max_n, out);
+  else
+    ADEPT_LAUNCH(row_rinv_kernel<float>, grid, block, 0, s, d, eps, (const float*)x, rows, n_dev,
+                 max_n, out);
+  return launch_status("row_rinv");
+}
+
 }  // namespace adept
 
 using namespace adept;
@@ -144,6 +190,27 @@ extern "C" adept_status adept_rope_table(int max_pos, int head_dim, double theta
   ADEPT_LAUNCH(rope_table_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
                      as_stream(stream), max_pos, half, theta, cos_out, sin_out);
   return launch_status("rope_table");
+}
+
+extern "C" adept_status adept_fold_gain(adept_dtype dt, int n_mats, int rows, int cols, void* w,
+                                        int64_t mat_stride, const void* gain,
+                                        int64_t gain_stride, void* stream) {
+  ADEPT_REQUIRE(dt == ADEPT_F32 || dt == ADEPT_BF16, "fold_gain: bad dtype");
+  ADEPT_REQUIRE(n_mats >= 0 && rows >= 0 && cols > 0 && n_mats <= 65535, "fold_gain: bad sizes");
+  ADEPT_REQUIRE(mat_stride >= (int64_t)rows * cols && gain_stride >= cols,
+                "fold_gain: strides smaller than a matrix / gain row");
+  ADEPT_REQUIRE(w && gain, "fold_gain: NULL tensor");
+  if (n_mats == 0 || rows == 0) return ADEPT_OK;
+  const int64_t total = (int64_t)rows * cols;
+  const int bx = (int)std::min<int64_t>((total + 255) / 256, 8192);
+  dim3 grid(bx, n_mats);
+  if (dt == ADEPT_BF16)
+    ADEPT_LAUNCH(fold_gain_kernel<bf16>, grid, dim3(256), 0, as_stream(stream), rows, cols,
+                 (bf16*)w, mat_stride, (const bf16*)gain, gain_stride);
+  else
+    ADEPT_LAUNCH(fold_gain_kernel<float>, grid, dim3(256), 0, as_stream(stream), rows, cols,
+                 (float*)w, mat_stride, (const float*)gain, gain_stride);
+  return launch_status("fold_gain");
 }
 
 extern "C" adept_status adept_embed(adept_dtype dt, int n, int d_model, int vocab,

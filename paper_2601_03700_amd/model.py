@@ -52,7 +52,6 @@ class PassState:
     exit_flag: torch.Tensor
     sim_out: torch.Tensor
     force_layer: torch.Tensor | None
-    x_norm: torch.Tensor
     q_buf: torch.Tensor
     attn_out: torch.Tensor
     ffn_act: torch.Tensor
@@ -112,6 +111,11 @@ class DecoderModel:
         self.final_norm = up(weights["final_norm"])
         self.lm_head = up(weights["lm_head"])
         assert self.w_qkv.shape == (N, 3 * Dq, D) and self.w_down.shape == (N, D, F)
+        # fold the pre-norm gains into the projections that consume the normalised
+        # state (the library applies only the 1/rms row factor)
+        B.fold_gain(self.w_qkv, self.attn_norm)
+        B.fold_gain(self.w_gate, self.ffn_norm)
+        B.fold_gain(self.w_up, self.ffn_norm)
         self.rope_max_pos = rope_max_pos
         half = shape.head_dim // 2
         self.rope_cos = torch.empty((rope_max_pos, half), dtype=torch.float32, device=dev)
@@ -145,7 +149,6 @@ class DecoderModel:
             exit_flag=torch.empty(max(n_tok, 4), dtype=torch.uint8, device=dev),
             sim_out=torch.empty(n_tok, dtype=torch.float64, device=dev),
             force_layer=force_layer,
-            x_norm=torch.empty((n_tok, s.d_model), dtype=tdt, device=dev),
             q_buf=torch.empty((n_tok, s.d_q), dtype=tdt, device=dev),
             attn_out=torch.empty((n_tok, s.d_q), dtype=tdt, device=dev),
             ffn_act=torch.empty((n_tok, s.d_ff), dtype=tdt, device=dev),
@@ -159,8 +162,7 @@ class DecoderModel:
         a.n_layers, a.d_model, a.n_heads = s.n_layers, s.d_model, s.n_heads
         a.head_dim, a.d_ff, a.rms_eps = s.head_dim, s.d_ff, s.rms_eps
         a.exit = cfg
-        a.attn_norm, a.w_qkv, a.w_o = B.ptr(self.attn_norm), B.ptr(self.w_qkv), B.ptr(self.w_o)
-        a.ffn_norm, a.w_gate = B.ptr(self.ffn_norm), B.ptr(self.w_gate)
+        a.w_qkv, a.w_o, a.w_gate = B.ptr(self.w_qkv), B.ptr(self.w_o), B.ptr(self.w_gate)
         a.w_up, a.w_down = B.ptr(self.w_up), B.ptr(self.w_down)
         a.rope_cos, a.rope_sin, a.rope_max_pos = B.ptr(self.rope_cos), B.ptr(self.rope_sin), self.rope_max_pos
         a.n_tok, a.max_active, a.n_seq, a.s_max = st.n_tok, st.n_tok, cache.n_seq, cache.s_max
@@ -174,8 +176,7 @@ class DecoderModel:
         a.sim_out = B.ptr(st.sim_out)
         a.force_layer = B.ptr(st.force_layer)
         a.k_cache, a.v_cache, a.n_slots = B.ptr(cache.k), B.ptr(cache.v), cache.n_slots
-        a.x_norm, a.q_buf, a.attn_out, a.ffn_act = (B.ptr(st.x_norm), B.ptr(st.q_buf),
-                                                    B.ptr(st.attn_out), B.ptr(st.ffn_act))
+        a.q_buf, a.attn_out, a.ffn_act = B.ptr(st.q_buf), B.ptr(st.attn_out), B.ptr(st.ffn_act)
         need = B.layer_workspace_bytes(a)
         if st.workspace is None or st.workspace.numel() < need:
             st.workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)

@@ -201,7 +201,7 @@ def _layers_for_oracle(wkv, gain, Dq):
     return [{"attn_norm": gain[r], "wk": wkv[r][:Dq], "wv": wkv[r][Dq:]} for r in range(len(gain))]
 
 
-def _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_slots, max_pos):
+def _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_slots, max_pos, fold=True):
     N, D, H, hd = shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim
     Dq = H * hd
     cos = torch.empty((max_pos, hd // 2), dtype=torch.float32, device=DEV)
@@ -211,16 +211,21 @@ def _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_slots, max_pos):
     vc = torch.full_like(kc, float("nan"))
     wsb = B.kv_generate_workspace_bytes(N, len(rows))
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=DEV)
+    w_d, g_d = dev(wkv, TDT[dt]), dev(gain, TDT[dt])
+    if fold:
+        B.fold_gain(w_d, g_d)   # gains into the columns of [Wk_r; Wv_r]
+        g_d = None
     B.kv_generate(N, D, H, hd, shape.rms_eps, dev(s, TDT[dt]), i32(rows), count(len(rows)),
-                  len(rows), i32(el), i32(slot), i32(pos), dev(wkv, TDT[dt]), 2 * Dq * D,
-                  dev(gain, TDT[dt]), cos, sin, kc, vc, n_slots, ws)
+                  len(rows), i32(el), i32(slot), i32(pos), w_d, 2 * Dq * D,
+                  g_d, cos, sin, kc, vc, n_slots, ws)
     torch.cuda.synchronize()
     return kc, vc
 
 
-@pytest.mark.parametrize("dt,hd", [("bf16", 128), ("bf16", 64), ("f32", 64)])
-def test_kv_generate_matches_oracle(dt, hd):
-    say(f"kv_generate dt={dt} hd={hd}")
+@pytest.mark.parametrize("dt,hd,fold", [("bf16", 128, True), ("bf16", 64, True),
+                                        ("f32", 64, False), ("f32", 64, True)])
+def test_kv_generate_matches_oracle(dt, hd, fold):
+    say(f"kv_generate dt={dt} hd={hd} fold={fold}")
     N, D, H = 5, 256, 4 if hd == 64 else 2
     n_tok = 300
     shape, s, wkv, gain, el = _kv_case(dt, N, D, H, hd, n_tok, 31 + hd, std=0.0625)
@@ -229,7 +234,7 @@ def test_kv_generate_matches_oracle(dt, hd):
     rows = np.sort(rng.choice(n_tok, 257, replace=False)).astype(np.int32)  # ragged tile tail
     pos = rng.integers(0, 2000, n_tok).astype(np.int32)
     slot = rng.permutation(n_tok + 11)[:n_tok].astype(np.int32)
-    kc, vc = _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_tok + 11, 2048)
+    kc, vc = _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_tok + 11, 2048, fold)
     gen = O.kv_generate({"layers": _layers_for_oracle(wkv, gain, Dq)}, shape, s[rows], el[rows],
                         pos[rows])
     K, V = host64(kc), host64(vc)
