@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=512)
     ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="copy 256 MiB device to device first (a kernel of known traffic "
+                         "for scaling hardware byte counters)")
     return ap.parse_args()
 
 
@@ -124,6 +127,11 @@ def main():
     torch.cuda.empty_cache()
     ids = torch.from_numpy(ai.token_ids(8, shape.vocab, Bn, T)).cuda()
     cache = model.new_cache(Bn, T)
+    if args.copy_calibration:
+        src = torch.ones(1 << 27, dtype=torch.int16, device="cuda")   # 256 MiB
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        del src, dst
     torch.cuda.synchronize()
     log(f"weights + cache ready in {time.time() - t0:.1f}s; "
         f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated")

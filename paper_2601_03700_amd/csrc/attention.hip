@@ -4,9 +4,11 @@
 // not distinguish the two: a generated entry is an ordinary cache row.
 //
 // Prefill (bf16, head_dim 64/128, causal): a plan kernel cuts the compacted
-// query list into tiles of <= 64 consecutive entries of one sequence; a
-// 256-thread workgroup takes one (tile, head), each wave 16 queries.  Key
-// blocks of 64 rows are staged in LDS (K row-major, V transposed), and the
+// query list into tiles of <= 128 consecutive entries of one sequence; a
+// 256-thread workgroup takes one (tile, head), each wave two groups of 16
+// queries, so every K/V fragment read from LDS feeds two MFMAs.  Key
+// blocks of 64 rows are staged in LDS (K row-major, V transposed with packed
+// 8-byte writes of 4 keys), and the
 // scores are formed transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16 so
 // that each lane owns one query column: the online softmax then needs only
 // two cross-lane steps for the running max, and the probabilities already sit
@@ -91,7 +93,7 @@ __global__ __launch_bounds__(kGenThreads) void attend_generic_kernel(
 // ---------------------------------------------------------------------------
 // prefill plan: tiles of <= 64 consecutive query entries of one sequence
 // ---------------------------------------------------------------------------
-constexpr int QT = 64;   // queries per tile
+constexpr int QT = 128;  // queries per tile (4 waves x 2 groups of 16)
 constexpr int KB = 64;   // keys per LDS block
 
 __global__ __launch_bounds__(1024) void attend_plan_kernel(const int32_t* __restrict__ rows,
@@ -136,7 +138,7 @@ __global__ __launch_bounds__(1024) void attend_plan_kernel(const int32_t* __rest
 // prefill MFMA kernel
 // ---------------------------------------------------------------------------
 template <int HD>
-__global__ __launch_bounds__(256) void attend_prefill_kernel(
+__global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     int H, float scale_log2, const bf16* __restrict__ q, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ pos, const int32_t* __restrict__ seq,
     const bf16* __restrict__ kc, const bf16* __restrict__ vc, int s_max,
@@ -145,6 +147,7 @@ __global__ __launch_bounds__(256) void attend_prefill_kernel(
   constexpr int VLD = KB + 8;     // sVt row stride
   constexpr int DS = HD / 32;     // 32-wide dim steps for S
   constexpr int DB = HD / 16;     // 16-row dim blocks of O^T
+  constexpr int QG = QT / 64;     // 16-query groups per wave
   __shared__ __attribute__((aligned(16))) bf16 sK[KB * KLD];
   __shared__ __attribute__((aligned(16))) bf16 sVt[HD * VLD];
   const int nt = *n_tiles;
@@ -159,99 +162,125 @@ __global__ __launch_bounds__(256) void attend_prefill_kernel(
   const int pmax = pos[rows[tile.x + tile.y - 1]];
   const int64_t kbase = (int64_t)b * s_max;
 
-  // this lane's query (column c16 of the wave's 16)
-  const int qi = wave * 16 + c16;
-  const bool qvalid = qi < tile.y;
-  const int qk = tile.x + (qvalid ? qi : 0);
-  const int qpos = qvalid ? pos[rows[qk]] : -1;
-
-  bf16x8_t qf[DS];
+  // this lane's queries: column c16 of each of the wave's QG groups of 16
+  int qk[QG], qpos[QG];
+  bool qvalid[QG];
+  bf16x8_t qf[QG][DS];
+  f32x4_t o[QG][DB];
+  float m_run[QG], l_run[QG];
 #pragma unroll
-  for (int s = 0; s < DS; ++s) {
-    const uint4 v = *reinterpret_cast<const uint4*>(q + (int64_t)qk * rs + h * HD + s * 32 + g * 8);
-    qf[s] = __builtin_bit_cast(bf16x8_t, v);
+  for (int qg = 0; qg < QG; ++qg) {
+    const int qi = (wave * QG + qg) * 16 + c16;
+    qvalid[qg] = qi < tile.y;
+    qk[qg] = tile.x + (qvalid[qg] ? qi : 0);
+    qpos[qg] = qvalid[qg] ? pos[rows[qk[qg]]] : -1;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      const uint4 v =
+          *reinterpret_cast<const uint4*>(q + (int64_t)qk[qg] * rs + h * HD + s * 32 + g * 8);
+      qf[qg][s] = __builtin_bit_cast(bf16x8_t, v);
+    }
+#pragma unroll
+    for (int i = 0; i < DB; ++i) o[qg][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    m_run[qg] = -INFINITY;
+    l_run[qg] = 0.0f;
   }
-
-  f32x4_t o[DB];
-#pragma unroll
-  for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.0f;
 
   const int nkb = pmax / KB + 1;
   for (int kb = 0; kb < nkb; ++kb) {
     const int t0 = kb * KB;
-    // ---- stage K [64][HD] and V^T [HD][64]; keys past pmax are zero
+    // ---- stage K [64][HD] row-major; keys past pmax are zero
     constexpr int CH = HD / 8;  // 16-byte chunks per row
+#pragma unroll
     for (int e = tid; e < KB * CH; e += 256) {
       const int r = e / CH, c = (e % CH) * 8;
       const int t = t0 + r;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (t <= pmax) {
-        kv = *reinterpret_cast<const uint4*>(kc + (kbase + t) * rs + h * HD + c);
-        vv = *reinterpret_cast<const uint4*>(vc + (kbase + t) * rs + h * HD + c);
-      }
+      uint4 kv = make_uint4(0, 0, 0, 0);
+      if (t <= pmax) kv = *reinterpret_cast<const uint4*>(kc + (kbase + t) * rs + h * HD + c);
       *reinterpret_cast<uint4*>(sK + r * KLD + c) = kv;
-      const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+    }
+    // ---- stage V^T [HD][64]: a thread takes 4 keys x 8 dims and writes eight
+    // 8-byte runs (4 keys of one dim)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sVt[(c + 2 * j) * VLD + r] = (bf16)(w[j] & 0xffff);
-        sVt[(c + 2 * j + 1) * VLD + r] = (bf16)(w[j] >> 16);
+    for (int e = tid; e < (KB / 4) * CH; e += 256) {
+      const int kg = e % (KB / 4), dc = e / (KB / 4);
+      uint32_t w[4][4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int t = t0 + 4 * kg + kk;
+        uint4 vv = make_uint4(0, 0, 0, 0);
+        if (t <= pmax) vv = *reinterpret_cast<const uint4*>(vc + (kbase + t) * rs + h * HD + dc * 8);
+        w[kk][0] = vv.x; w[kk][1] = vv.y; w[kk][2] = vv.z; w[kk][3] = vv.w;
+      }
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        const int sh = (d & 1) * 16;
+        const uint32_t e0 = (w[0][d >> 1] >> sh) & 0xffff, e1 = (w[1][d >> 1] >> sh) & 0xffff;
+        const uint32_t e2 = (w[2][d >> 1] >> sh) & 0xffff, e3 = (w[3][d >> 1] >> sh) & 0xffff;
+        *reinterpret_cast<uint2*>(sVt + (dc * 8 + d) * VLD + 4 * kg) =
+            make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
       }
     }
     __syncthreads();
 
-    // ---- S^T = K Q^T: 4 key sub-blocks of 16
-    f32x4_t s[4];
+    // ---- S^T = K Q^T: 4 key sub-blocks of 16; each K fragment serves QG groups
+    f32x4_t s[QG][4];
 #pragma unroll
     for (int sb = 0; sb < 4; ++sb) {
-      s[sb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int qg = 0; qg < QG; ++qg) s[qg][sb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
         const bf16x8_t a =
             *reinterpret_cast<const bf16x8_t*>(sK + (sb * 16 + c16) * KLD + ds * 32 + g * 8);
-        s[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[ds], s[sb], 0, 0, 0);
+#pragma unroll
+        for (int qg = 0; qg < QG; ++qg)
+          s[qg][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qg][ds], s[qg][sb], 0, 0, 0);
       }
     }
-    // ---- mask, running max
-    float mloc = -INFINITY;
+    bf16x8_t pb[QG][2];
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb)
+    for (int qg = 0; qg < QG; ++qg) {
+      // ---- mask, running max
+      float mloc = -INFINITY;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int t = t0 + sb * 16 + g * 4 + v;
-        float x = s[sb][v] * scale_log2;
-        x = (t <= qpos) ? x : -INFINITY;
-        s[sb][v] = x;
-        mloc = fmaxf(mloc, x);
-      }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);
-    const float alpha = (m_new == -INFINITY) ? 1.0f : exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
-#pragma unroll
-    for (int i = 0; i < DB; ++i)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) o[i][v] *= alpha;
-    // ---- P = exp2(S - m) packed as the B operand (key order: sub-block pairs)
-    bf16x8_t pb[2];
-#pragma unroll
-    for (int kp = 0; kp < 2; ++kp) {
-      uint16_t pv[8];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
+      for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float x = s[2 * kp + hh][v];
-          const float e = (x == -INFINITY) ? 0.0f : exp2f(x - m_new);
-          const bf16 eb = f2bf(e);
-          l_run += bf2f(eb);
-          pv[hh * 4 + v] = eb;
+          const int t = t0 + sb * 16 + g * 4 + v;
+          float x = s[qg][sb][v] * scale_log2;
+          x = (t <= qpos[qg]) ? x : -INFINITY;
+          s[qg][sb][v] = x;
+          mloc = fmaxf(mloc, x);
         }
-      pb[kp] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(pv));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m_run[qg], mloc);
+      const float alpha = (m_new == -INFINITY) ? 1.0f : exp2f(m_run[qg] - m_new);
+      m_run[qg] = m_new;
+      l_run[qg] *= alpha;
+#pragma unroll
+      for (int i = 0; i < DB; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[qg][i][v] *= alpha;
+      // ---- P = exp2(S - m) packed as the B operand (key order: sub-block pairs)
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp) {
+        uint16_t pv[8];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const float x = s[qg][2 * kp + hh][v];
+            const float ev = (x == -INFINITY) ? 0.0f : exp2f(x - m_new);
+            const bf16 eb = f2bf(ev);
+            l_run[qg] += bf2f(eb);
+            pv[hh * 4 + v] = eb;
+          }
+        pb[qg][kp] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(pv));
+      }
     }
-    // ---- O^T += V^T P^T
+    // ---- O^T += V^T P^T; each V^T fragment serves QG groups
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -260,21 +289,29 @@ __global__ __launch_bounds__(256) void attend_prefill_kernel(
         const uint2 lo = *reinterpret_cast<const uint2*>(vr);
         const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
         const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
-        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kp], o[db], 0, 0, 0);
+#pragma unroll
+        for (int qg = 0; qg < QG; ++qg)
+          o[qg][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qg][kp], o[qg][db], 0, 0, 0);
       }
     __syncthreads();
   }
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-  if (!qvalid) return;
-  const float inv = 1.0f / l_run;
-  bf16* dst = out + (int64_t)qk * rs + h * HD;
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const int d0 = db * 16 + g * 4;
-    const uint32_t w0 = (uint32_t)f2bf(o[db][0] * inv) | ((uint32_t)f2bf(o[db][1] * inv) << 16);
-    const uint32_t w1 = (uint32_t)f2bf(o[db][2] * inv) | ((uint32_t)f2bf(o[db][3] * inv) << 16);
-    *reinterpret_cast<uint2*>(dst + d0) = make_uint2(w0, w1);
+  for (int qg = 0; qg < QG; ++qg) {
+    float l = l_run[qg];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (!qvalid[qg]) continue;
+    const float inv = 1.0f / l;
+    bf16* dst = out + (int64_t)qk[qg] * rs + h * HD;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int d0 = db * 16 + g * 4;
+      const uint32_t w0 =
+          (uint32_t)f2bf(o[qg][db][0] * inv) | ((uint32_t)f2bf(o[qg][db][1] * inv) << 16);
+      const uint32_t w1 =
+          (uint32_t)f2bf(o[qg][db][2] * inv) | ((uint32_t)f2bf(o[qg][db][3] * inv) << 16);
+      *reinterpret_cast<uint2*>(dst + d0) = make_uint2(w0, w1);
+    }
   }
 }
 

@@ -300,25 +300,43 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int* 
   *nt = r / rows_in_g;
 }
 
+// The grid is sized for M_max; the tiles are numbered over the rows that are
+// actually active (device count), so when tokens exit the remaining tiles
+// still spread over all XCDs and the surplus workgroups return at once.
 template <int EPI, int HD>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GP p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
+  const int tiles_m = (M + BM - 1) / BM;
+  if ((int)blockIdx.x >= tiles_m * p.tiles_n) return;
   int mt, nt;
-  tile_of(blockIdx.x, p.tiles_m, p.tiles_n, &mt, &nt);
-  if (mt * BM >= M) return;
+  tile_of(blockIdx.x, tiles_m, p.tiles_n, &mt, &nt);
   gemm_tile<EPI, false, HD>(p, smem, 0, mt, nt, M, p.B);
 }
 
 // Persistent grouped GEMM: workgroups stride over the device-built list of
 // (layer, row tile) items times the column tiles; an empty list costs one
-// read per workgroup.
+// read per workgroup.  The items, rastered in groups of 8 row tiles, are cut
+// into 8 contiguous chunks, one per XCD, walked by that XCD's workgroups.
 template <int HD>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kv_grouped_kernel(GP p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int total = *p.n_work * p.tiles_n;
-  for (int item = blockIdx.x; item < total; item += gridDim.x) {
-    const int w = item / p.tiles_n, nt = item % p.tiles_n;
+  const int n_work = *p.n_work;
+  const int total = n_work * p.tiles_n;
+  int lo = 0, hi = total, t0 = blockIdx.x, step = gridDim.x;
+  if ((gridDim.x & 7) == 0 && total >= (int)gridDim.x) {
+    const int chunk = (total + 7) >> 3;
+    lo = (blockIdx.x & 7) * chunk;
+    hi = min(total, lo + chunk);
+    t0 = lo + (blockIdx.x >> 3);
+    step = gridDim.x >> 3;
+  }
+  for (int t = t0; t < hi; t += step) {
+    constexpr int G = 8;
+    const int gsz = G * p.tiles_n;
+    const int g = t / gsz, r = t - g * gsz;
+    const int rows_in_g = min(G, n_work - g * G);
+    const int w = g * G + r % rows_in_g, nt = r / rows_in_g;
     const int packed = p.work[w];
     const int layer = packed >> 16, mt = packed & 0xffff;
     const int M = p.grp_m[layer];
