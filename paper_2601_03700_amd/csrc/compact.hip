@@ -1,27 +1,125 @@
 // Active-index update of Appendix I: stable split of the active list by the
 // exit flags into the rows that continue and the rows that exit.
 //
-// Small lists (the per-layer case: at most a few ten thousand rows) use one
-// 1024-thread workgroup that walks the list in rounds of 4096 entries: each
-// thread takes 4 consecutive entries (one 4-byte flag load, one 16-byte row
-// load), counts its exits, and a wave scan (shuffles) plus a 16-entry LDS
-// scan over the waves gives every thread its output offsets.  Larger lists
-// use three passes over 16K-entry tiles (count, scan of tile counts, scatter)
-// with the same in-tile scheme.  Both keep the input order.
+// The split is wave-ballot based.  A workgroup of 16 waves takes a range of
+// the list; each wave owns a contiguous chunk of it (a multiple of 64
+// entries).  Pass A: per 64 entries the wave takes one 64-bit ballot of the
+// exit flags (kept in LDS) and counts exits.  The 16 wave totals are scanned
+// in LDS.  Pass B: lane l of a 64-entry step reads its row (coalesced) and
+// writes it at (wave offset + popcount of the ballot below l) among the exits
+// or at (wave offset + l - that count) among the kept rows, so stores of a
+// wave land on consecutive addresses.  Lists up to 64K entries (the
+// per-layer case) use one workgroup over the whole list; longer lists use
+// three passes over 16K-entry tiles: a count of exits per tile (16 flags per
+// thread, one 16-byte load), a scan of the tile counts, and the split of
+// each tile from its offsets.  Input order is kept in both outputs.
 #include "common.h"
 
 namespace adept {
 namespace {
 
 constexpr int kThreads = 1024;
-constexpr int kItems = 4;
-constexpr int kRound = kThreads * kItems;      // entries per round
-constexpr int kTileRounds = 4;                 // multi-pass tile = 16K entries
-constexpr int kTile = kRound * kTileRounds;
+constexpr int kWaves = kThreads / 64;
+constexpr int kTileItems = 16;                 // flags per thread in the count pass
+constexpr int kTile = kThreads * kTileItems;   // multi-pass tile = 16K entries
 constexpr int kSingleMax = 1 << 16;            // lists up to this use one workgroup
+constexpr int kMaxSteps = kSingleMax / kThreads;   // 64-entry steps per wave, at most
+constexpr int kBatch = 16;                     // steps whose loads are issued together
+
+// Splits entries [start, end) with the block's waves on consecutive chunks of
+// `chunk` entries (a multiple of 64, chunk * kWaves >= end - start).  Exits go
+// to exited[ex_base + ...], kept rows to next[keep_base + ...].  Steps are
+// taken kBatch at a time so that a batch's loads are in flight together.
+__device__ __forceinline__ void split_block(int start, int end, int chunk, int ex_base,
+                                            int keep_base, int layer,
+                                            const uint8_t* __restrict__ flags,
+                                            const int32_t* __restrict__ active,
+                                            int32_t* __restrict__ next,
+                                            int32_t* __restrict__ exited,
+                                            int32_t* __restrict__ exit_layer, uint64_t* masks,
+                                            int* sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lo = start + wave * chunk;
+  const int hi = min(end, lo + chunk);
+  const int steps = chunk >> 6;
+  uint64_t* wm = masks + wave * steps;
+  int ex = 0;
+  for (int s0 = 0; s0 < steps; s0 += kBatch) {
+    uint8_t f[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int e = lo + (s0 + b) * 64 + lane;
+      f[b] = (s0 + b < steps && e < hi) ? flags[e] : 0;
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      if (s0 + b < steps) {
+        const uint64_t m = __ballot(f[b] != 0);
+        if (lane == 0) wm[s0 + b] = m;
+        ex += __popcll(m);
+      }
+    }
+  }
+  if (lane == 0) {
+    sh[wave] = ex;
+    sh[kWaves + wave] = max(0, hi - lo) - ex;
+  }
+  __syncthreads();
+  int ex_off = ex_base, keep_off = keep_base;
+  for (int w = 0; w < wave; ++w) {
+    ex_off += sh[w];
+    keep_off += sh[kWaves + w];
+  }
+  const uint64_t lt = (1ull << lane) - 1ull;   // lanes below this one
+  for (int s0 = 0; s0 < steps && lo + s0 * 64 < hi; s0 += kBatch) {
+    int32_t r[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int e = lo + (s0 + b) * 64 + lane;
+      r[b] = (s0 + b < steps && e < hi) ? active[e] : 0;
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int base = lo + (s0 + b) * 64;
+      if (s0 + b < steps && base < hi) {
+        const uint64_t m = wm[s0 + b];
+        if (base + lane < hi) {
+          const int below = __popcll(m & lt);
+          if ((m >> lane) & 1ull) {
+            exited[ex_off + below] = r[b];
+            exit_layer[r[b]] = layer;
+          } else {
+            next[keep_off + lane - below] = r[b];
+          }
+        }
+        const int me = __popcll(m);
+        ex_off += me;
+        keep_off += min(64, hi - base) - me;
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void compact_single(
+    int layer, const uint8_t* __restrict__ flags, const int32_t* __restrict__ active,
+    const int32_t* __restrict__ n_active, int32_t* __restrict__ next, int32_t* __restrict__ n_next,
+    int32_t* __restrict__ exited, int32_t* __restrict__ n_exited,
+    int32_t* __restrict__ exit_layer, int max_n) {
+  __shared__ uint64_t masks[kWaves * kMaxSteps];
+  __shared__ int sh[2 * kWaves];
+  const int n = min(*n_active, max_n);     // max_n <= kSingleMax
+  const int chunk = ((n + kThreads - 1) / kThreads) * 64;   // ceil(n / kWaves) rounded to 64
+  split_block(0, n, chunk, 0, 0, layer, flags, active, next, exited, exit_layer, masks, sh);
+  if (threadIdx.x == 0) {
+    int ex = 0;
+    for (int w = 0; w < kWaves; ++w) ex += sh[w];
+    *n_exited = ex;
+    *n_next = n - ex;
+  }
+}
 
 // Inclusive scan of v over the workgroup; returns the exclusive prefix and
-// writes the workgroup total to *total.  `sh` holds >= 32 ints.
+// writes the workgroup total to *total.  `sh` holds >= kWaves + 1 ints.
 __device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int x = v;
@@ -34,86 +132,18 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int* total) 
   __syncthreads();
   if (threadIdx.x == 0) {
     int run = 0;
-    for (int w = 0; w < kThreads / 64; ++w) {
+    for (int w = 0; w < kWaves; ++w) {
       const int t = sh[w];
       sh[w] = run;
       run += t;
     }
-    sh[kThreads / 64] = run;
+    sh[kWaves] = run;
   }
   __syncthreads();
   const int excl = sh[wave] + x - v;
-  *total = sh[kThreads / 64];
+  *total = sh[kWaves];
   __syncthreads();
   return excl;
-}
-
-// Processes entries [start, end) of the list, writing kept rows at
-// next[keep_base + ...] and exited rows at exited[exit_base + ...].
-__device__ __forceinline__ void split_range(int start, int end, int layer,
-                                            const uint8_t* __restrict__ flags,
-                                            const int32_t* __restrict__ active,
-                                            int32_t* __restrict__ next,
-                                            int32_t* __restrict__ exited,
-                                            int32_t* __restrict__ exit_layer, int* keep_base,
-                                            int* exit_base, int* sh) {
-  for (int r0 = start; r0 < end; r0 += kRound) {
-    const int e0 = r0 + threadIdx.x * kItems;
-    uint8_t f[kItems];
-    int32_t rw[kItems];
-    if (e0 + kItems <= end) {
-      const uint32_t fw = *reinterpret_cast<const uint32_t*>(flags + e0);
-      const int4 rv = *reinterpret_cast<const int4*>(active + e0);
-      f[0] = fw & 0xff; f[1] = (fw >> 8) & 0xff; f[2] = (fw >> 16) & 0xff; f[3] = fw >> 24;
-      rw[0] = rv.x; rw[1] = rv.y; rw[2] = rv.z; rw[3] = rv.w;
-    } else {
-#pragma unroll
-      for (int q = 0; q < kItems; ++q) {
-        const bool ok = e0 + q < end;
-        f[q] = (ok && flags[e0 + q]) ? 1 : 0;
-        rw[q] = ok ? active[e0 + q] : -1;
-      }
-    }
-    int n_ex = 0, n_keep = 0;
-#pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-      const bool valid = e0 + q < end;
-      n_ex += (valid && f[q]) ? 1 : 0;
-      n_keep += (valid && !f[q]) ? 1 : 0;
-    }
-    int tot_ex, tot_keep;
-    int off_ex = block_exclusive_scan(n_ex, sh, &tot_ex);
-    int off_keep = block_exclusive_scan(n_keep, sh, &tot_keep);
-    off_ex += *exit_base;
-    off_keep += *keep_base;
-#pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-      if (e0 + q >= end) break;
-      if (f[q]) {
-        exited[off_ex++] = rw[q];
-        exit_layer[rw[q]] = layer;
-      } else {
-        next[off_keep++] = rw[q];
-      }
-    }
-    *exit_base += tot_ex;
-    *keep_base += tot_keep;
-  }
-}
-
-__global__ __launch_bounds__(kThreads) void compact_single(
-    int layer, const uint8_t* __restrict__ flags, const int32_t* __restrict__ active,
-    const int32_t* __restrict__ n_active, int32_t* __restrict__ next, int32_t* __restrict__ n_next,
-    int32_t* __restrict__ exited, int32_t* __restrict__ n_exited,
-    int32_t* __restrict__ exit_layer, int max_n) {
-  __shared__ int sh[kThreads / 64 + 1];
-  const int n = min(*n_active, max_n);
-  int keep = 0, ex = 0;
-  split_range(0, n, layer, flags, active, next, exited, exit_layer, &keep, &ex, sh);
-  if (threadIdx.x == 0) {
-    *n_next = keep;
-    *n_exited = ex;
-  }
 }
 
 // pass 1: exits per tile
@@ -121,13 +151,29 @@ __global__ __launch_bounds__(kThreads) void compact_count(const uint8_t* __restr
                                                           const int32_t* __restrict__ n_active,
                                                           int32_t* __restrict__ tile_ex,
                                                           int max_n) {
-  __shared__ int sh[kThreads / 64 + 1];
+  __shared__ int sh[kWaves + 1];
   const int n = min(*n_active, max_n);
   const int start = blockIdx.x * kTile;
   if (start >= n) return;
   const int end = min(n, start + kTile);
+  // kTileItems flags per thread: one 16-byte load, nonzero bytes counted
+  static_assert(kTileItems == 16, "one uint4 of flags per thread");
+  const int e0 = start + threadIdx.x * kTileItems;
   int cnt = 0;
-  for (int e = start + threadIdx.x; e < end; e += kThreads) cnt += flags[e] ? 1 : 0;
+  if (e0 + kTileItems <= end) {
+    const uint4 v = *reinterpret_cast<const uint4*>(flags + e0);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t x = w[q];
+      x |= x >> 4;
+      x |= x >> 2;
+      x |= x >> 1;
+      cnt += __popc(x & 0x01010101u);
+    }
+  } else {
+    for (int e = e0; e < end && e < e0 + kTileItems; ++e) cnt += flags[e] ? 1 : 0;
+  }
   int tot;
   block_exclusive_scan(cnt, sh, &tot);
   if (threadIdx.x == 0) tile_ex[blockIdx.x] = tot;
@@ -139,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void compact_scan(const int32_t* __restri
                                                          int32_t* __restrict__ n_next,
                                                          int32_t* __restrict__ n_exited,
                                                          int max_n) {
-  __shared__ int sh[kThreads / 64 + 1];
+  __shared__ int sh[kWaves + 1];
   const int n = min(*n_active, max_n);
   const int tiles = (n + kTile - 1) / kTile;
   int carry = 0;
@@ -157,25 +203,25 @@ __global__ __launch_bounds__(kThreads) void compact_scan(const int32_t* __restri
   }
 }
 
-// pass 3: scatter each tile from its offsets
+// pass 3: split each tile from its offsets
 __global__ __launch_bounds__(kThreads) void compact_scatter(
     int layer, const uint8_t* __restrict__ flags, const int32_t* __restrict__ active,
     const int32_t* __restrict__ n_active, const int32_t* __restrict__ tile_ex,
     int32_t* __restrict__ next, int32_t* __restrict__ exited, int32_t* __restrict__ exit_layer,
     int max_n) {
-  __shared__ int sh[kThreads / 64 + 1];
+  __shared__ uint64_t masks[kTile / 64];
+  __shared__ int sh[2 * kWaves];
   const int n = min(*n_active, max_n);
   const int start = blockIdx.x * kTile;
   if (start >= n) return;
   const int end = min(n, start + kTile);
-  int ex = tile_ex[blockIdx.x];
-  int keep = start - ex;
-  split_range(start, end, layer, flags, active, next, exited, exit_layer, &keep, &ex, sh);
+  const int ex = tile_ex[blockIdx.x];
+  split_block(start, end, kTile / kWaves, ex, start - ex, layer, flags, active, next, exited,
+              exit_layer, masks, sh);
 }
 
 }  // namespace
 }  // namespace adept
-
 using namespace adept;
 
 extern "C" size_t adept_compact_workspace_bytes(int max_active) {
@@ -204,6 +250,8 @@ extern "C" adept_status adept_compact(int layer, const uint8_t* exit_flag,
                        exit_layer, max_active);
     return launch_status("compact");
   }
+  ADEPT_REQUIRE(aligned16(exit_flag),
+                "compact: exit_flag must be 16-byte aligned above %d entries", kSingleMax);
   const size_t need = adept_compact_workspace_bytes(max_active);
   if (!workspace || workspace_bytes < need) {
     set_error("compact: workspace of %zu bytes needed", need);

@@ -23,20 +23,20 @@ template <typename T> struct Vec16;
 template <> struct Vec16<float> { static constexpr int n = 4; };
 template <> struct Vec16<bf16> { static constexpr int n = 8; };
 
-__device__ __forceinline__ void load16(const float* p, float* out) {
-  float4 v = *reinterpret_cast<const float4*>(p);
-  out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+// Element i of a 16-byte vector of T, as float.
+template <typename T> __device__ __forceinline__ float elem(const uint4& r, int i);
+template <> __device__ __forceinline__ float elem<float>(const uint4& r, int i) {
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+  return __uint_as_float(w[i]);
 }
-__device__ __forceinline__ void load16(const bf16* p, float* out) {
-  uint4 v = *reinterpret_cast<const uint4*>(p);
-  uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    out[2 * i] = __uint_as_float(w[i] << 16);
-    out[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-  }
+template <> __device__ __forceinline__ float elem<bf16>(const uint4& r, int i) {
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+  return __uint_as_float((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16));
 }
 
+// Values stay in registers in their stored form (16-byte vectors, bf16
+// packed) between the reduction and the inertia update, which keeps the
+// register count low enough for several rows in flight per SIMD.
 template <typename T, int CH, bool GLOBAL>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void exit_test_kernel(
     ExitParams p, int max_active, const int32_t* __restrict__ rows,
@@ -45,6 +45,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void exit_test_kernel(
     const int32_t* __restrict__ force_layer, uint8_t* __restrict__ exit_flag,
     double* __restrict__ sim_out) {
   constexpr int V = Vec16<T>::n;
+  constexpr int RV = GLOBAL ? V / 4 : 1;   // 16-byte vectors of the reference per chunk
   const int lane = threadIdx.x & 63;
   const int k = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   if (k >= min(*n_active, max_active)) return;
@@ -52,24 +53,31 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void exit_test_kernel(
   const int nvec = p.d / V;
   const T* hr = h_cur + (int64_t)row * p.d;
 
-  float hv[CH][V];
-  float rv[CH][V];
+  uint4 hv[CH];
+  uint4 rv[CH][RV];
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int vi = c * 64 + lane;
+    if (vi < nvec) {
+      hv[c] = *reinterpret_cast<const uint4*>(hr + vi * V);
+      if (GLOBAL) {
+        const float* ir = inertia + (int64_t)row * p.d + vi * V;
+#pragma unroll
+        for (int q = 0; q < RV; ++q) rv[c][q] = *reinterpret_cast<const uint4*>(ir + 4 * q);
+      } else {
+        rv[c][0] = *reinterpret_cast<const uint4*>(h_prev + (int64_t)row * p.d + vi * V);
+      }
+    }
+  }
   double s_hh = 0.0, s_rr = 0.0, s_hr = 0.0;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const int vi = c * 64 + lane;
     if (vi < nvec) {
-      load16(hr + vi * V, hv[c]);
-      if (GLOBAL) {
-        const float* ir = inertia + (int64_t)row * p.d + vi * V;
-#pragma unroll
-        for (int q = 0; q < V; q += 4) load16(ir + q, &rv[c][q]);
-      } else {
-        load16(h_prev + (int64_t)row * p.d + vi * V, rv[c]);
-      }
 #pragma unroll
       for (int v = 0; v < V; ++v) {
-        const double a = hv[c][v], b = rv[c][v];
+        const double a = elem<T>(hv[c], v);
+        const double b = GLOBAL ? elem<float>(rv[c][v >> 2], v & 3) : elem<T>(rv[c][0], v);
         s_hh = fma(a, a, s_hh);
         s_rr = fma(b, b, s_rr);
         s_hr = fma(a, b, s_hr);
@@ -100,13 +108,13 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void exit_test_kernel(
       if (vi < nvec) {
         float* ir = inertia + (int64_t)row * p.d + vi * V;
 #pragma unroll
-        for (int q = 0; q < V; q += 4) {
+        for (int q = 0; q < RV; ++q) {
           float4 o;
-          o.x = (float)((double)rv[c][q + 0] + (double)hv[c][q + 0] * inv);
-          o.y = (float)((double)rv[c][q + 1] + (double)hv[c][q + 1] * inv);
-          o.z = (float)((double)rv[c][q + 2] + (double)hv[c][q + 2] * inv);
-          o.w = (float)((double)rv[c][q + 3] + (double)hv[c][q + 3] * inv);
-          *reinterpret_cast<float4*>(ir + q) = o;
+          o.x = (float)((double)elem<float>(rv[c][q], 0) + (double)elem<T>(hv[c], 4 * q + 0) * inv);
+          o.y = (float)((double)elem<float>(rv[c][q], 1) + (double)elem<T>(hv[c], 4 * q + 1) * inv);
+          o.z = (float)((double)elem<float>(rv[c][q], 2) + (double)elem<T>(hv[c], 4 * q + 2) * inv);
+          o.w = (float)((double)elem<float>(rv[c][q], 3) + (double)elem<T>(hv[c], 4 * q + 3) * inv);
+          *reinterpret_cast<float4*>(ir + 4 * q) = o;
         }
       }
     }

@@ -133,25 +133,32 @@ def test_exit_test_window_and_special_thresholds():
 # compaction (Appendix I)
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("n_tok,n_act,p_exit", [(16, 16, 0.5), (5000, 4097, 0.3),
-                                                (16384, 16384, 0.1), (16384, 9000, 0.0),
-                                                (16384, 9000, 1.0), (300000, 200003, 0.4)])
-def test_compact_matches_oracle(n_tok, n_act, p_exit):
-    say(f"compact n_tok={n_tok} n_act={n_act} p={p_exit}")
+@pytest.mark.parametrize("n_tok,n_act,p_exit,slack", [
+    (16, 16, 0.5, 0), (5000, 4097, 0.3, 0), (16384, 16384, 0.1, 0), (16384, 9000, 0.0, 0),
+    (16384, 9000, 1.0, 0), (300000, 200003, 0.4, 0),
+    (70000, 65536, 0.5, 0),          # largest single-workgroup list
+    (70000, 65537, 0.5, 0),          # smallest multi-pass list
+    (1000, 0, 0.5, 64),              # empty list
+    (20000, 777, 0.5, 4000),         # device count below max_active (one workgroup)
+    (200000, 70001, 0.5, 40000)])    # device count below max_active (multi-pass)
+def test_compact_matches_oracle(n_tok, n_act, p_exit, slack):
+    say(f"compact n_tok={n_tok} n_act={n_act} p={p_exit} slack={slack}")
     rng = np.random.default_rng(n_tok + n_act)
     active = np.sort(rng.choice(n_tok, n_act, replace=False)).astype(np.int32)
     flags = (rng.random(n_act) < p_exit).astype(np.uint8)
     layer = 7
     el0 = np.full(n_tok, 32, np.int32)
-    act_d, n_d = i32(active), count(n_act)
-    flag_d = dev(np.concatenate([flags, np.zeros(8, np.uint8)]))
-    nxt = torch.full((n_tok,), -1, dtype=torch.int32, device=DEV)
-    ext = torch.full((n_tok,), -1, dtype=torch.int32, device=DEV)
+    # entries past the device count: row 0, flagged to exit -> must be ignored
+    max_act = n_act + slack
+    act_d, n_d = i32(np.concatenate([active, np.zeros(slack, np.int32)])), count(n_act)
+    flag_d = dev(np.concatenate([flags, np.ones(slack, np.uint8), np.zeros(8, np.uint8)]))
+    nxt = torch.full((max(n_tok, 1),), -1, dtype=torch.int32, device=DEV)
+    ext = torch.full((max(n_tok, 1),), -1, dtype=torch.int32, device=DEV)
     cnt = torch.full((2,), -1, dtype=torch.int32, device=DEV)
     el = i32(el0)
-    wsb = B.compact_workspace_bytes(n_act)
+    wsb = B.compact_workspace_bytes(max_act)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=DEV) if wsb else None
-    B.compact(layer, flag_d, act_d, n_d, n_act, nxt, cnt[0:1], ext, cnt[1:2], el, ws)
+    B.compact(layer, flag_d, act_d, n_d, max_act, nxt, cnt[0:1], ext, cnt[1:2], el, ws)
     torch.cuda.synchronize()
     still, gone = O.compact(flags.astype(bool), active)
     c = cnt.cpu().numpy()
