@@ -19,13 +19,9 @@ typedef uint16_t bf16;
 
 __device__ __forceinline__ float bf2f(bf16 x) { return __uint_as_float(((uint32_t)x) << 16); }
 
-// Round to nearest, ties to even; NaN stays a (quiet) NaN.
-__device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (bf16)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16)(u >> 16);
-}
+// float -> bf16 bits: round to nearest, ties to even; NaN stays a quiet NaN
+// (v_cvt_pk_bf16_f32 on gfx950)
+__device__ __forceinline__ bf16 f2bf(float f) { return __builtin_bit_cast(bf16, (__bf16)f); }
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
@@ -41,6 +37,7 @@ template <typename T> __device__ __forceinline__ void st(T* p, float v) { Elem<T
 
 // MFMA operand / accumulator vector types.
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(uint16_t)))) uint16_t bf16x4_t;   // 4 bf16 bit patterns
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 

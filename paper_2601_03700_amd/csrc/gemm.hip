@@ -7,12 +7,16 @@
 // 32 at a time through a ring of four LDS stages filled by direct
 // global->LDS loads (global_load_lds_dwordx4: lane l of an instruction lands
 // 16 bytes at base + 16 l), so operands never pass through registers on the
-// way in, and three stages (about 3000 cycles of MFMA work) are in flight
-// ahead of the one being consumed -- enough to cover HBM latency under load.
-// Each 64-byte tile row is stored with its four 16-byte chunks permuted,
-// chunk c of row r at position c ^ ((r >> 1) & 3); the MFMA operand reads of
-// eight consecutive rows then cover all banks once.  One vmcnt wait and one
-// barrier per stage order the ring.
+// way in; a stage is issued three stages (about 3000 cycles of MFMA work)
+// before it is consumed and waited for one stage ahead, and the operand
+// fragments of the next stage are read from LDS while the current stage's
+// MFMAs run, so neither wait sits in front of an MFMA.  Each 64-byte tile row
+// is stored with its four 16-byte chunks permuted, chunk c of row r at
+// position c ^ ((r >> 2) & 3): LDS serves a 16-byte read for 16 lanes per
+// cycle (64 banks), 16 consecutive rows fall into the 4 bank quarters by
+// r mod 4, and the permutation gives the 4 rows of a quarter 4 distinct chunk
+// positions, so the operand reads are free of bank conflicts.  One vmcnt wait
+// and one barrier per stage order the ring.
 //
 // Workgroups are mapped to tiles XCD by XCD: the hardware deals consecutive
 // workgroup ids round-robin to the 8 XCDs, so the id is remapped to give each
@@ -42,11 +46,16 @@ namespace adept {
 namespace {
 
 constexpr int BM = 256, BN = 256;
-constexpr int BK = 32;                                          // k columns per LDS stage
-constexpr int NS = 4;                                           // LDS stages (3 in flight)
+constexpr int BK = 64;                                          // k columns per stage: 128-byte rows
+constexpr int NS = 2;                                           // LDS stages (double buffer)
 constexpr int kThreads = 256;
-constexpr int kStageBytes = BM * BK * 2;                        // one operand, one stage: 16 KiB
-constexpr size_t kLdsBytes = (size_t)NS * 2 * kStageBytes;     // 4 stages x 2 operands = 128 KiB
+constexpr int kStageBytes = BM * BK * 2;                        // one operand, one stage: 32 KiB
+constexpr size_t kLdsBytes = (size_t)NS * 2 * kStageBytes;     // 2 stages x 2 operands = 128 KiB
+constexpr int kEpiStride = 136;                                 // floats per staged epilogue row
+constexpr int kEpiWaveBytes = 32 * kEpiStride * 4;              // one wave's 32 staged rows
+constexpr int kEpiMetaBytes = 128 * 3 * 4;                      // per-row scale, row/slot, position
+static_assert(4 * (kEpiWaveBytes + kEpiMetaBytes) <= (int)kLdsBytes,
+              "epilogue staging fits in the ring");
 constexpr int kPersistentBlocks = 256;                          // one workgroup per CU
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -86,18 +95,34 @@ struct GP {
   int64_t cache_layer_stride;
 };
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+// x * sigmoid(x) with the hardware reciprocal (about 1 ulp in f32, far below
+// the bf16 rounding of the output)
+__device__ __forceinline__ float silu(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+}
 
 __device__ __forceinline__ void dma16(const bf16* g, char* l) {
   __builtin_amdgcn_global_load_lds((glb_void_t*)g, (lds_void_t*)l, 16, 0, 0);
 }
 
+// s_waitcnt immediate (gfx9 encoding) that waits for all LDS operations and
+// leaves the vector-memory and export counters free: vmcnt 63, expcnt 7,
+// lgkmcnt 0.
+constexpr int kWaitLgkm0 = 0xC07F;
+
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Workgroup barrier of the K loop.  __syncthreads() would also wait for every
+// outstanding vector-memory operation, i.e. drain the direct-to-LDS loads of
+// the later stages and leave no load in flight across the barrier; here the
+// caller waits for exactly the stage it needs (vmcnt) and the memory clobber
+// keeps the compiler from moving LDS accesses across the barrier.  The
+// operand reads of the previous stage have completed by then: the MFMAs that
+// consume them were issued before it.
+__device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 // One 256x256 output tile: rows [mt*256, M) against column tile nt of Bm.
-// HD (64 or 128) is the head size of the rotary epilogues (0 otherwise); as a
-// compile-time constant it keeps the partner-column index static, so the
-// accumulators stay in registers.
+// HD (64 or 128) is the head size of the rotary epilogues (0 otherwise).
 template <int EPI, bool GROUPED, int HD>
 __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, int mt, int nt,
                                           int M, const bf16* Bm) {
@@ -105,17 +130,18 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = mt * BM;
 
-  // ---- load assignment: instruction j (0..3) of wave w fills LDS 16-byte
-  // units [(w*4+j)*64, +64) of a stage, i.e. tile rows (w*4+j)*16 .. +16;
-  // lane l -> row (w*4+j)*16 + l/4, stored position l%4, logical chunk
-  // (l%4) ^ ((row >> 1) & 3) = (l%4) ^ ((l >> 3) & 3).
-  const int lrow = lane >> 2;
-  const int lchunk = (lane & 3) ^ ((lane >> 3) & 3);
-  const bf16* a_src[4];
-  const bf16* b_src[4];
+  // ---- load assignment: DMA instruction j (0..7) of wave w fills the 1 KiB
+  // of stage rows 8q .. 8q+7, q = w*8 + j; lane l -> row 8q + l/8, stored
+  // position l%8, logical chunk (l%8) ^ ((row >> 1) & 7)
+  // = (l%8) ^ ((4q + (l >> 4)) & 7).  A row's 128 bytes are one cache line.
+  const int lrow = lane >> 3;
+  const bf16* a_src[8];
+  const bf16* b_src[8];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int r = (wave * 4 + j) * 16 + lrow;
+  for (int j = 0; j < 8; ++j) {
+    const int q = wave * 8 + j;
+    const int r = 8 * q + lrow;
+    const int lchunk = (lane & 7) ^ ((4 * q + (lane >> 4)) & 7);
     int m = m0 + r;
     if (m >= M) m = m0;  // clamp: loaded, never stored
     const int arow = GROUPED ? p.srows[m] : (p.a_rows ? p.a_rows[m] : m);
@@ -133,14 +159,10 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   }
   char* sA = smem;                        // [NS][kStageBytes]
   char* sB = smem + NS * kStageBytes;     // [NS][kStageBytes]
-  auto issue = [&](int stage, int k0) {   // 8 DMA instructions per wave
-    char* la = sA + stage * kStageBytes + wave * 4 * 1024;
-    char* lb = sB + stage * kStageBytes + wave * 4 * 1024;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      dma16(a_src[j] + k0, la + j * 1024);
-      dma16(b_src[j] + k0, lb + j * 1024);
-    }
+  // DMA instructions j (A and B) of a stage: 16 per wave in all
+  auto issue_j = [&](int stage, int k0, int j) {
+    dma16(a_src[j] + k0, sA + stage * kStageBytes + (wave * 8 + j) * 1024);
+    dma16(b_src[j] + k0, sB + stage * kStageBytes + (wave * 8 + j) * 1024);
   };
 
   f32x16_t acc[4][4];
@@ -152,138 +174,242 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
   // MFMA operand addresses: block i row R = w*128 + i*32 + lane%32; logical
-  // chunk 2*ks + lane/32 stored at chunk ^ ((R >> 1) & 3), and the block
-  // offsets are multiples of 32, so the position is chunk ^ ((lane >> 1) & 3).
+  // chunk 2*ks + lane/32 (k step ks = 0..3) stored at chunk ^ ((R >> 1) & 7),
+  // and the block offsets are multiples of 32, so the position is
+  // chunk ^ ((lane >> 1) & 7).
   const int rA = wm * 128 + (lane & 31);
   const int rB = wn * 128 + (lane & 31);
-  const int swz = (lane >> 1) & 3;
+  const int swz = (lane >> 1) & 7;
   const int KT = p.K / BK;
   // operand fragments of one 16-wide k step (4 A blocks, 4 B blocks)
   auto frags = [&](const char* cA, const char* cB, int ks, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
     const int ch = (2 * ks + (lane >> 5)) ^ swz;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      a[i] = *reinterpret_cast<const bf16x8_t*>(cA + ((rA + i * 32) * 4 + ch) * 16);
-      b[i] = *reinterpret_cast<const bf16x8_t*>(cB + ((rB + i * 32) * 4 + ch) * 16);
+      a[i] = *reinterpret_cast<const bf16x8_t*>(cA + ((rA + i * 32) * 8 + ch) * 16);
+      b[i] = *reinterpret_cast<const bf16x8_t*>(cB + ((rB + i * 32) * 8 + ch) * 16);
     }
+  };
+  auto mma_row = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], int i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   };
   auto mma = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    for (int i = 0; i < 4; ++i) mma_row(a, b, i);
   };
-  // prologue: stages 0 .. NS-2 in flight
-#pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
-    if (s < KT) issue(s, s * BK);
-  bf16x8_t a0[4], b0[4], a1[4], b1[4];
-  for (int kt = 0; kt < KT; ++kt) {
-    // stage kt has landed once at most the DMA groups of the (up to two)
-    // later stages are outstanding; the barrier makes it visible to all waves
-    // and retires all reads of the buffer refilled below (read at kt - 1).
-    const int ahead = min(NS - 2, KT - 1 - kt);
-    if (ahead >= 2) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else wait_dma();
-    __syncthreads();
-    if (kt + NS - 1 < KT) issue((kt + NS - 1) % NS, (kt + NS - 1) * BK);
-    const char* cA = sA + (kt % NS) * kStageBytes;
-    const char* cB = sB + (kt % NS) * kStageBytes;
-    // the second k step's fragments are read while the first step's 16 MFMAs run
-    frags(cA, cB, 0, a0, b0);
-    frags(cA, cB, 1, a1, b1);
-    mma(a0, b0);
-    mma(a1, b1);
-  }
 
-  // ---- epilogues.  Lane holds column (lane & 31) of each 32x32 block and
-  // rows 8*(v/4) + 4*(lane/32) + v%4, v = 0..15.
+  // Double-buffered K loop.  At the top of iteration kt stage kt has landed
+  // and is visible to every wave, and the fragments of its first k step (f)
+  // were read just before.  Each k step reads the next step's fragments
+  // before issuing its own 16 MFMAs, with at most 8 LDS reads outstanding
+  // (the 4-bit lgkm counter cannot express more).  The DMA of stage kt+1
+  // into the other buffer (whose last reads the previous barrier retired) is
+  // interleaved with the first k step's MFMAs, 4 instructions per MFMA row,
+  // so it issues while the matrix core is busy.  The last k step is split
+  // around the wait for stage kt+1 and the barrier (which publishes it and
+  // retires every read of stage kt): its first two MFMA rows cover the wait,
+  // its last two the reads of stage kt+1's first fragments.
+  issue_j(0, 0, 0); issue_j(0, 0, 1); issue_j(0, 0, 2); issue_j(0, 0, 3);
+  issue_j(0, 0, 4); issue_j(0, 0, 5); issue_j(0, 0, 6); issue_j(0, 0, 7);
+  wait_dma();
+  stage_barrier();
+  bf16x8_t fa[4], fb[4], ga[4], gb[4];
+  frags(sA, sB, 0, fa, fb);
+  for (int kt = 0; kt < KT; ++kt) {
+    const bool pre = kt + 1 < KT;
+    const int nst = (kt + 1) & 1, nk0 = (kt + 1) * BK;
+    const char* cA = sA + (kt & 1) * kStageBytes;
+    const char* cB = sB + (kt & 1) * kStageBytes;
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    frags(cA, cB, 1, ga, gb);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      mma_row(fa, fb, i);
+      if (pre) {
+        issue_j(nst, nk0, 2 * i);
+        issue_j(nst, nk0, 2 * i + 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    frags(cA, cB, 2, fa, fb);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(ga, gb);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    frags(cA, cB, 3, ga, gb);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(fa, fb);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    mma_row(ga, gb, 0);
+    mma_row(ga, gb, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_dma();
+    stage_barrier();
+    // unconditional: after the last stage this reads stale but valid LDS
+    frags(sA + nst * kStageBytes, sB + nst * kStageBytes, 0, fa, fb);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_row(ga, gb, 2);
+    mma_row(ga, gb, 3);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  stage_barrier();   // every wave is done with the ring; LDS is reused below
+
+  // ---- epilogue, staged through LDS 32 rows at a time.  Lane holds column
+  // (lane & 31) of each 32x32 block and rows 8*(v/4) + 4*(lane/32) + v%4,
+  // v = 0..15.  Block i of the wave (32 rows x its 128 columns, f32) is
+  // written to the wave's LDS area with a row stride of kEpiStride floats
+  // (the two row groups of a write then fall on disjoint banks), then read
+  // back as 4 consecutive columns per lane, so every global load and store
+  // of the epilogue covers whole rows: 32 lanes x 8 bytes = one 256-byte row
+  // of 128 bf16 columns.  The per-row inputs (scale, residual row or cache
+  // slot and position) of the wave's 128 rows are gathered into LDS first,
+  // two memory latencies per tile instead of one per store round.
+  float* stg = reinterpret_cast<float*>(smem + wave * kEpiWaveBytes);
+  float* msc = reinterpret_cast<float*>(smem + 4 * kEpiWaveBytes + wave * kEpiMetaBytes);
+  int* mrow = reinterpret_cast<int*>(msc + 128);   // residual row / cache slot
+  int* mpos = mrow + 128;                          // rotary position
   const int col_l = lane & 31;
   const int row_q = 4 * (lane >> 5);
-  const float* rsc = p.row_scale;
-  if (EPI == EPI_STORE || EPI == EPI_RESID) {
+  const int c4 = (lane & 31) * 4;         // first of the lane's 4 columns (wave space)
+  const int nw = nt * BN + wn * 128;      // first output column of this wave
+  constexpr bool kCache = EPI == EPI_QKV || EPI == EPI_KV;
+  const int sec = kCache ? nw / p.d_q : 0;    // QKV: 0 q, 1 k, 2 v;  KV: 0 k, 1 v
+  const bool is_q = EPI == EPI_QKV && sec == 0;
+  const bool is_v = EPI == EPI_QKV ? sec == 2 : (EPI == EPI_KV && sec == 1);
+  const int cbase = nw - sec * p.d_q;         // column within the section
+  constexpr int hd = HD > 0 ? HD : 128, half = hd >> 1;
+  bf16* kc = p.k_cache;
+  bf16* vc = p.v_cache;
+  if (GROUPED) {
+    kc += (int64_t)(layer - 1) * p.cache_layer_stride;
+    vc += (int64_t)(layer - 1) * p.cache_layer_stride;
+  }
+  {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + row_q + (v & 3);
-        if (m >= M) continue;
-        const float sc = rsc ? rsc[m] : 1.0f;
-        const int64_t orow = EPI == EPI_RESID ? (int64_t)p.rows[m] : (int64_t)m;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = nt * BN + wn * 128 + j * 32 + col_l;
-          float x = acc[i][j][v] * sc;
-          if (EPI == EPI_RESID) {
-            x += bf2f(p.resid[orow * p.ldc + n]);
-            reinterpret_cast<bf16*>(p.C)[orow * p.ldc + n] = f2bf(x);
-          } else if (p.c_f32) {
-            reinterpret_cast<float*>(p.C)[orow * p.ldc + n] = x;
-          } else {
-            reinterpret_cast<bf16*>(p.C)[orow * p.ldc + n] = f2bf(x);
-          }
-        }
+    for (int h = 0; h < 2; ++h) {
+      const int lr = lane + 64 * h;
+      const int mc = min(m0 + wm * 128 + lr, M - 1);   // clamped: rows past M are never stored
+      msc[lr] = p.row_scale ? p.row_scale[mc] : 1.0f;
+      if (EPI == EPI_RESID) {
+        mrow[lr] = p.rows[mc];
+      } else if (kCache) {
+        const int row = GROUPED ? p.srows[mc] : p.rows[mc];
+        mrow[lr] = is_q ? 0 : p.slot[row];
+        mpos[lr] = is_v ? 0 : p.pos[row];
       }
-  } else if (EPI == EPI_SWIGLU) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + row_q + (v & 3);
-        if (m >= M) continue;
-        const float sc = rsc ? rsc[m] : 1.0f;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int o = nt * 128 + wn * 64 + j * 32 + col_l;
-          const float g = acc[i][j][v] * sc, u = acc[i][j + 2][v] * sc;
-          reinterpret_cast<bf16*>(p.C)[(int64_t)m * p.ldc + o] = f2bf(silu(g) * u);
-        }
-      }
-  } else {  // EPI_QKV / EPI_KV
-    const int nw = nt * BN + wn * 128;          // first output column of this wave
-    const int sec = nw / p.d_q;                 // QKV: 0 q, 1 k, 2 v;  KV: 0 k, 1 v
-    const bool is_q = EPI == EPI_QKV && sec == 0;
-    const bool is_v = EPI == EPI_QKV ? sec == 2 : sec == 1;
-    const int cbase = nw - sec * p.d_q;         // column within the section
-    constexpr int hd = HD > 0 ? HD : 128, half = hd >> 1, pmask = hd >> 6;
-    bf16* kc = p.k_cache;
-    bf16* vc = p.v_cache;
-    if (GROUPED) {
-      kc += (int64_t)(layer - 1) * p.cache_layer_stride;
-      vc += (int64_t)(layer - 1) * p.cache_layer_stride;
     }
+  }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
+    const int mb = m0 + wm * 128 + i * 32;   // first row of the block
+    if (mb >= M) break;                       // the wave's remaining rows are past M
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + row_q + (v & 3);
-        if (m >= M) continue;
-        const float sc = rsc ? rsc[m] : 1.0f;
-        const int row = GROUPED ? p.srows[m] : p.rows[m];
-        bf16* dst;
-        if (is_q) dst = p.q_out + (int64_t)m * p.d_q;
-        else dst = (is_v ? vc : kc) + (int64_t)p.slot[row] * p.d_q;
-        if (is_v) {
+    for (int v = 0; v < 16; ++v) {
+      const int lr = 8 * (v >> 2) + row_q + (v & 3);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) dst[cbase + j * 32 + col_l] = f2bf(acc[i][j][v] * sc);
-        } else {
-          const int ps = p.pos[row];
-          const float* cr = p.rope_cos + (int64_t)ps * half;
-          const float* sr = p.rope_sin + (int64_t)ps * half;
+      for (int j = 0; j < 4; ++j) stg[lr * kEpiStride + j * 32 + col_l] = acc[i][j][v];
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_wave_barrier();
+    if (EPI == EPI_SWIGLU) {
+      // 64 outputs per row (gate columns 0..63 of the wave, up columns
+      // 64..127): 16 lanes per row, 4 rows per round
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int c = (cbase + j * 32 + col_l) & (hd - 1);  // column within the head
-            const int kk = c & (half - 1);
-            const float cs = cr[kk], sn = sr[kk];
-            const float x = acc[i][j][v] * sc;
-            const float y = acc[i][j ^ pmask][v] * sc;         // partner column c +- hd/2
-            const float r = c < half ? x * cs - y * sn : x * cs + y * sn;
-            dst[cbase + j * 32 + col_l] = f2bf(r);
+      for (int rr = 0; rr < 32; rr += 4) {
+        const int lr = rr + (lane >> 4);
+        const int m = mb + lr;
+        const int c = (lane & 15) * 4;
+        const float4 g = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + c);
+        const float4 u = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + 64 + c);
+        const float sc = msc[i * 32 + lr];
+        bf16x4_t o;
+        o[0] = f2bf(silu(g.x * sc) * (u.x * sc));
+        o[1] = f2bf(silu(g.y * sc) * (u.y * sc));
+        o[2] = f2bf(silu(g.z * sc) * (u.z * sc));
+        o[3] = f2bf(silu(g.w * sc) * (u.w * sc));
+        if (m < M)
+          *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc +
+                                       nt * 128 + wn * 64 + c) = o;
+      }
+    } else {
+      // 2 rows per round (32 lanes x 4 columns each), in two halves of 8
+      // rounds whose global loads are issued together
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        bf16x4_t rv[8];
+        float4 cs[8], sn[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int lr = 16 * hh + 2 * r + (lane >> 5);
+          const int ml = i * 32 + lr;
+          if (EPI == EPI_RESID)
+            rv[r] = *reinterpret_cast<const bf16x4_t*>(p.resid + (int64_t)mrow[ml] * p.ldc + nw + c4);
+          if (kCache && !is_v) {
+            const int c = (cbase + c4) & (hd - 1);
+            const int64_t t = (int64_t)mpos[ml] * half + (c & (half - 1));
+            cs[r] = *reinterpret_cast<const float4*>(p.rope_cos + t);
+            sn[r] = *reinterpret_cast<const float4*>(p.rope_sin + t);
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int lr = 16 * hh + 2 * r + (lane >> 5);
+          const int ml = i * 32 + lr;
+          const int m = mb + lr;
+          const float4 x4 = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + c4);
+          const float sc = msc[ml];
+          const float x[4] = {x4.x * sc, x4.y * sc, x4.z * sc, x4.w * sc};
+          if (EPI == EPI_STORE) {
+            const int64_t off = (int64_t)m * p.ldc + nw + c4;
+            if (m < M) {
+              if (p.c_f32) {
+                *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + off) =
+                    make_float4(x[0], x[1], x[2], x[3]);
+              } else {
+                bf16x4_t o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
+                *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
+              }
+            }
+          } else if (EPI == EPI_RESID) {
+            bf16x4_t o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e] + bf2f(rv[r][e]));
+            if (m < M)
+              *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) +
+                                           (int64_t)mrow[ml] * p.ldc + nw + c4) = o;
+          } else {  // EPI_QKV / EPI_KV
+            bf16x4_t o;
+            if (is_v) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
+            } else {
+              // rotate-half RoPE: column c pairs with c +- hd/2 of the same head
+              const float4 y4 = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + (c4 ^ half));
+              const float y[4] = {y4.x * sc, y4.y * sc, y4.z * sc, y4.w * sc};
+              const int c = (cbase + c4) & (hd - 1);   // column within the head
+              const float cv[4] = {cs[r].x, cs[r].y, cs[r].z, cs[r].w};
+              const float sv[4] = {sn[r].x, sn[r].y, sn[r].z, sn[r].w};
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                o[e] = f2bf(c < half ? x[e] * cv[e] - y[e] * sv[e] : x[e] * cv[e] + y[e] * sv[e]);
+            }
+            bf16* dst = is_q ? p.q_out + (int64_t)m * p.d_q
+                             : (is_v ? vc : kc) + (int64_t)mrow[ml] * p.d_q;
+            if (m < M) *reinterpret_cast<bf16x4_t*>(dst + cbase + c4) = o;
           }
         }
       }
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);   // block reads done before the next block's writes
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
