@@ -4,19 +4,22 @@
 // bf16 path: one 256-thread workgroup computes a 256x256 output tile with
 // v_mfma_f32_32x32x16_bf16; its four waves each own a 128x128 sub-tile
 // (4x4 MFMA blocks, 256 accumulators per lane, held in AGPRs).  K advances
-// 32 at a time through a ring of four LDS stages filled by direct
-// global->LDS loads (global_load_lds_dwordx4: lane l of an instruction lands
-// 16 bytes at base + 16 l), so operands never pass through registers on the
-// way in; a stage is issued three stages (about 3000 cycles of MFMA work)
-// before it is consumed and waited for one stage ahead, and the operand
-// fragments of the next stage are read from LDS while the current stage's
-// MFMAs run, so neither wait sits in front of an MFMA.  Each 64-byte tile row
-// is stored with its four 16-byte chunks permuted, chunk c of row r at
-// position c ^ ((r >> 2) & 3): LDS serves a 16-byte read for 16 lanes per
-// cycle (64 banks), 16 consecutive rows fall into the 4 bank quarters by
-// r mod 4, and the permutation gives the 4 rows of a quarter 4 distinct chunk
-// positions, so the operand reads are free of bank conflicts.  One vmcnt wait
-// and one barrier per stage order the ring.
+// 64 at a time.  Operands reach LDS by direct global->LDS loads
+// (global_load_lds_dwordx4: lane l of an instruction lands 16 bytes at base
+// + 16 l), eight lanes per 128-byte row, so every row of a stage is one whole
+// cache line: the load path sustains about 1.5x the bytes per cycle it does
+// with half-line requests.  The LDS (160 KiB) is a ring of five 32 KiB slots,
+// one operand of one stage each; while stage k is consumed, B of stage k+1
+// and A of stage k+2 are in flight, so the loads that miss L2 have one to
+// two stages of MFMA work (2048 cycles each) to land.  Within a row the
+// eight 16-byte chunks are permuted, chunk c of row r at position
+// c ^ ((r >> 1) & 7): LDS serves a 16-byte read for 16 lanes per cycle
+// (64 banks), the 16 rows of such a read fall into the two bank halves by
+// r mod 2, and the permutation gives the 8 rows of a half 8 distinct chunk
+// positions, so the operand reads are free of bank conflicts.  The operand
+// fragments of the next k step are read while the current step's MFMAs run,
+// and the loads of later stages are issued between MFMAs; one vmcnt wait and
+// one barrier per stage order the ring.
 //
 // Workgroups are mapped to tiles XCD by XCD: the hardware deals consecutive
 // workgroup ids round-robin to the 8 XCDs, so the id is remapped to give each
@@ -24,11 +27,13 @@
 // workgroups resident on one XCD then share A and B k-slices in its L2.
 //
 // Row gathers (active-row lists) are folded into the per-lane load
-// addresses.  A per-row scale (1/rms of the row, with the norm gain folded
-// into B beforehand) is applied to the accumulators first, then the
-// epilogue: RoPE + cache store (the wave's 128 columns cover whole heads of
-// 64 or 128, so the rotary pair of a column sits in the same lane), residual
-// add, SwiGLU (B tile = 64 gate rows + 64 up rows per wave), or plain store.
+// addresses.  The epilogue stages the accumulators through LDS, 32 rows of a
+// wave at a time, so that its global loads and stores cover whole rows; a
+// per-row scale (1/rms of the row, with the norm gain folded into B
+// beforehand) is applied first, then RoPE + cache store (the wave's 128
+// columns cover whole heads of 64 or 128, so a column's rotary partner is in
+// the same staged row), residual add, SwiGLU (B tile = 64 gate rows + 64 up
+// rows per wave), or plain store.
 //
 // The grouped variant is the decoupled KV generation of Eq. 9: a persistent
 // grid strides over (layer r, 256-row tile, column tile) items built on the
@@ -39,6 +44,7 @@
 // f32 path (small configurations only): a plain 64x64-tiled FMA GEMM into a
 // float scratch buffer followed by an element-wise epilogue kernel.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 
@@ -47,10 +53,10 @@ namespace {
 
 constexpr int BM = 256, BN = 256;
 constexpr int BK = 64;                                          // k columns per stage: 128-byte rows
-constexpr int NS = 2;                                           // LDS stages (double buffer)
+constexpr int kSlots = 5;                                       // LDS ring slots, one operand each
 constexpr int kThreads = 256;
 constexpr int kStageBytes = BM * BK * 2;                        // one operand, one stage: 32 KiB
-constexpr size_t kLdsBytes = (size_t)NS * 2 * kStageBytes;     // 2 stages x 2 operands = 128 KiB
+constexpr size_t kLdsBytes = (size_t)kSlots * kStageBytes;     // 160 KiB: all of a CU's LDS
 constexpr int kEpiStride = 136;                                 // floats per staged epilogue row
 constexpr int kEpiWaveBytes = 32 * kEpiStride * 4;              // one wave's 32 staged rows
 constexpr int kEpiMetaBytes = 128 * 3 * 4;                      // per-row scale, row/slot, position
@@ -157,12 +163,14 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     }
     b_src[j] = bbase + brow * p.ldb + lchunk * 8;
   }
-  char* sA = smem;                        // [NS][kStageBytes]
-  char* sB = smem + NS * kStageBytes;     // [NS][kStageBytes]
-  // DMA instructions j (A and B) of a stage: 16 per wave in all
-  auto issue_j = [&](int stage, int k0, int j) {
-    dma16(a_src[j] + k0, sA + stage * kStageBytes + (wave * 8 + j) * 1024);
-    dma16(b_src[j] + k0, sB + stage * kStageBytes + (wave * 8 + j) * 1024);
+  // Ring of kSlots one-operand slots: A of stage k in slot 2k mod 5, B of
+  // stage k in slot 2k+1 mod 5.  DMA instruction j (0..7) of an operand.
+  auto slot = [&](int u) { return smem + (u % kSlots) * kStageBytes; };
+  auto issue_a = [&](int k, int j) {
+    dma16(a_src[j] + k * BK, slot(2 * k) + (wave * 8 + j) * 1024);
+  };
+  auto issue_b = [&](int k, int j) {
+    dma16(b_src[j] + k * BK, slot(2 * k + 1) + (wave * 8 + j) * 1024);
   };
 
   f32x16_t acc[4][4];
@@ -200,62 +208,92 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     for (int i = 0; i < 4; ++i) mma_row(a, b, i);
   };
 
-  // Double-buffered K loop.  At the top of iteration kt stage kt has landed
-  // and is visible to every wave, and the fragments of its first k step (f)
-  // were read just before.  Each k step reads the next step's fragments
-  // before issuing its own 16 MFMAs, with at most 8 LDS reads outstanding
-  // (the 4-bit lgkm counter cannot express more).  The DMA of stage kt+1
-  // into the other buffer (whose last reads the previous barrier retired) is
-  // interleaved with the first k step's MFMAs, 4 instructions per MFMA row,
-  // so it issues while the matrix core is busy.  The last k step is split
-  // around the wait for stage kt+1 and the barrier (which publishes it and
-  // retires every read of stage kt): its first two MFMA rows cover the wait,
-  // its last two the reads of stage kt+1's first fragments.
-  issue_j(0, 0, 0); issue_j(0, 0, 1); issue_j(0, 0, 2); issue_j(0, 0, 3);
-  issue_j(0, 0, 4); issue_j(0, 0, 5); issue_j(0, 0, 6); issue_j(0, 0, 7);
-  wait_dma();
-  stage_barrier();
-  bf16x8_t fa[4], fb[4], ga[4], gb[4];
-  frags(sA, sB, 0, fa, fb);
-  for (int kt = 0; kt < KT; ++kt) {
-    const bool pre = kt + 1 < KT;
-    const int nst = (kt + 1) & 1, nk0 = (kt + 1) * BK;
-    const char* cA = sA + (kt & 1) * kStageBytes;
-    const char* cB = sB + (kt & 1) * kStageBytes;
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    frags(cA, cB, 1, ga, gb);
-    __builtin_amdgcn_sched_barrier(0);
+  // One fragment (A block i or B block i) of k step ks, for the
+  // interleaved schedule below: read n = 0..7 is A_{n/2} for even n, B_{n/2}
+  // for odd n.
+  auto frag1 = [&](const char* cA, const char* cB, int ks, int n, bf16x8_t (&a)[4],
+                   bf16x8_t (&b)[4]) {
+    const int ch = (2 * ks + (lane >> 5)) ^ swz;
+    const int i = n >> 1;
+    if (n & 1) b[i] = *reinterpret_cast<const bf16x8_t*>(cB + ((rB + i * 32) * 8 + ch) * 16);
+    else a[i] = *reinterpret_cast<const bf16x8_t*>(cA + ((rA + i * 32) * 8 + ch) * 16);
+  };
+  // One k step: 16 MFMAs on (a, b); the 8 reads of the next step's fragments
+  // (k step nks of cA/cB into na/nb) go out one after each of the first 8
+  // MFMAs, and up to 8 DMA instructions dma(0..7) one after each of the last
+  // 8, so that every non-MFMA instruction issues while the matrix core has
+  // work queued.
+  auto kstep = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], bf16x8_t (&na)[4],
+                   bf16x8_t (&nb)[4], const char* cA, const char* cB, int nks, auto&& dma,
+                   bool do_dma) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      mma_row(fa, fb, i);
-      if (pre) {
-        issue_j(nst, nk0, 2 * i);
-        issue_j(nst, nk0, 2 * i + 1);
-      }
+    for (int n = 0; n < 16; ++n) {
+      const int i = n >> 2, j = n & 3;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      if (n < 8) frag1(cA, cB, nks, n, na, nb);
+      else if (do_dma) dma(n - 8);
       __builtin_amdgcn_sched_barrier(0);
     }
+  };
+  auto no_dma = [](int) {};
+
+  // K loop over a 5-slot ring.  At the top of iteration kt stage kt (A_kt,
+  // B_kt) has landed and is visible to every wave, A_kt+1 is in flight, and
+  // the fragments of stage kt's first k step (f) were read just before.  The
+  // slots of stage kt-1, retired by the previous barrier, take B_kt+1 (during
+  // k step 0) and A_kt+2 (during k step 1): A gets two iterations of lead, B
+  // one.  Before each k step, the reads issued during the previous one are
+  // waited for; at most 8 LDS reads are ever outstanding (the 4-bit lgkm
+  // counter cannot express more).  The last k step is split around the wait
+  // for stage kt+1 (only A_kt+2 may stay outstanding) and the barrier, which
+  // publishes stage kt+1 and retires every read of stage kt; its last two
+  // MFMA rows carry the reads of stage kt+1's first fragments.
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    issue_a(0, j);
+    issue_b(0, j);
+  }
+  if (KT > 1) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) issue_a(1, j);
+    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  } else {
+    wait_dma();
+  }
+  stage_barrier();
+  bf16x8_t fa[4], fb[4], ga[4], gb[4];
+  frags(slot(0), slot(1), 0, fa, fb);
+  for (int kt = 0; kt < KT; ++kt) {
+    const char* cA = slot(2 * kt);
+    const char* cB = slot(2 * kt + 1);
+    const bool nb = kt + 1 < KT, na = kt + 2 < KT;
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    frags(cA, cB, 2, fa, fb);
     __builtin_amdgcn_sched_barrier(0);
-    mma(ga, gb);
-    __builtin_amdgcn_sched_barrier(0);
+    kstep(fa, fb, ga, gb, cA, cB, 1, [&](int j) { issue_b(kt + 1, j); }, nb);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    frags(cA, cB, 3, ga, gb);
     __builtin_amdgcn_sched_barrier(0);
-    mma(fa, fb);
-    __builtin_amdgcn_sched_barrier(0);
+    kstep(ga, gb, fa, fb, cA, cB, 2, [&](int j) { issue_a(kt + 2, j); }, na);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_sched_barrier(0);
+    kstep(fa, fb, ga, gb, cA, cB, 3, no_dma, false);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_sched_barrier(0);
     mma_row(ga, gb, 0);
     mma_row(ga, gb, 1);
     __builtin_amdgcn_sched_barrier(0);
-    wait_dma();
+    if (na) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else wait_dma();
     stage_barrier();
     // unconditional: after the last stage this reads stale but valid LDS
-    frags(sA + nst * kStageBytes, sB + nst * kStageBytes, 0, fa, fb);
-    __builtin_amdgcn_sched_barrier(0);
-    mma_row(ga, gb, 2);
-    mma_row(ga, gb, 3);
-    __builtin_amdgcn_sched_barrier(0);
+    const char* nA = slot(2 * kt + 2);
+    const char* nB = slot(2 * kt + 3);
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+      const int i = 2 + (n >> 2), j = n & 3;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[i], gb[j], acc[i][j], 0, 0, 0);
+      frag1(nA, nB, 0, n, fa, fb);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
   __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
   stage_barrier();   // every wave is done with the ring; LDS is reused below
@@ -284,11 +322,17 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   const bool is_v = EPI == EPI_QKV ? sec == 2 : (EPI == EPI_KV && sec == 1);
   const int cbase = nw - sec * p.d_q;         // column within the section
   constexpr int hd = HD > 0 ? HD : 128, half = hd >> 1;
-  bf16* kc = p.k_cache;
-  bf16* vc = p.v_cache;
-  if (GROUPED) {
-    kc += (int64_t)(layer - 1) * p.cache_layer_stride;
-    vc += (int64_t)(layer - 1) * p.cache_layer_stride;
+  // destination of the QKV / KV epilogues: Q rows by compact index, K and V
+  // rows by cache slot (in layer r's cache for the grouped variant)
+  bf16* sec_dst = nullptr;
+  if (kCache) {
+    if (is_q) {
+      sec_dst = p.q_out;
+    } else {
+      sec_dst = is_v ? p.v_cache : p.k_cache;
+      if (GROUPED) sec_dst += (int64_t)(layer - 1) * p.cache_layer_stride;
+    }
+    sec_dst += cbase;
   }
   {
 #pragma unroll
@@ -317,97 +361,120 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     }
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_wave_barrier();
-    if (EPI == EPI_SWIGLU) {
-      // 64 outputs per row (gate columns 0..63 of the wave, up columns
-      // 64..127): 16 lanes per row, 4 rows per round
-#pragma unroll
-      for (int rr = 0; rr < 32; rr += 4) {
-        const int lr = rr + (lane >> 4);
-        const int m = mb + lr;
+    // Each block is emitted in phases: all LDS reads of a group of rounds
+    // into registers, then the global loads they index, then arithmetic and
+    // stores (the stores go through generic pointers, which the compiler
+    // must otherwise keep ordered before later LDS reads).  Rows past M exist
+    // only in the last block of a ragged tile; full blocks take the variant
+    // without the per-row store check.
+    auto emit = [&](auto check) {
+      constexpr bool kCheck = decltype(check)::value;
+      if (EPI == EPI_SWIGLU) {
+        // 64 outputs per row (gate columns 0..63 of the wave, up columns
+        // 64..127): 16 lanes per row, 4 rows per round, 8 rounds
         const int c = (lane & 15) * 4;
-        const float4 g = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + c);
-        const float4 u = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + 64 + c);
-        const float sc = msc[i * 32 + lr];
-        bf16x4_t o;
-        o[0] = f2bf(silu(g.x * sc) * (u.x * sc));
-        o[1] = f2bf(silu(g.y * sc) * (u.y * sc));
-        o[2] = f2bf(silu(g.z * sc) * (u.z * sc));
-        o[3] = f2bf(silu(g.w * sc) * (u.w * sc));
-        if (m < M)
-          *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc +
-                                       nt * 128 + wn * 64 + c) = o;
-      }
-    } else {
-      // 2 rows per round (32 lanes x 4 columns each), in two halves of 8
-      // rounds whose global loads are issued together
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        bf16x4_t rv[8];
-        float4 cs[8], sn[8];
+        float4 g[8], u[8];
+        float sc[8];
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-          const int lr = 16 * hh + 2 * r + (lane >> 5);
-          const int ml = i * 32 + lr;
-          if (EPI == EPI_RESID)
-            rv[r] = *reinterpret_cast<const bf16x4_t*>(p.resid + (int64_t)mrow[ml] * p.ldc + nw + c4);
-          if (kCache && !is_v) {
-            const int c = (cbase + c4) & (hd - 1);
-            const int64_t t = (int64_t)mpos[ml] * half + (c & (half - 1));
-            cs[r] = *reinterpret_cast<const float4*>(p.rope_cos + t);
-            sn[r] = *reinterpret_cast<const float4*>(p.rope_sin + t);
-          }
+          const int lr = 4 * r + (lane >> 4);
+          g[r] = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + c);
+          u[r] = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + 64 + c);
+          sc[r] = msc[i * 32 + lr];
         }
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-          const int lr = 16 * hh + 2 * r + (lane >> 5);
-          const int ml = i * 32 + lr;
-          const int m = mb + lr;
-          const float4 x4 = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + c4);
-          const float sc = msc[ml];
-          const float x[4] = {x4.x * sc, x4.y * sc, x4.z * sc, x4.w * sc};
-          if (EPI == EPI_STORE) {
-            const int64_t off = (int64_t)m * p.ldc + nw + c4;
-            if (m < M) {
-              if (p.c_f32) {
-                *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + off) =
-                    make_float4(x[0], x[1], x[2], x[3]);
-              } else {
-                bf16x4_t o;
+          const int m = mb + 4 * r + (lane >> 4);
+          bf16x4_t o;
+          o[0] = f2bf(silu(g[r].x * sc[r]) * (u[r].x * sc[r]));
+          o[1] = f2bf(silu(g[r].y * sc[r]) * (u[r].y * sc[r]));
+          o[2] = f2bf(silu(g[r].z * sc[r]) * (u[r].z * sc[r]));
+          o[3] = f2bf(silu(g[r].w * sc[r]) * (u[r].w * sc[r]));
+          if (!kCheck || m < M)
+            *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc +
+                                         nt * 128 + wn * 64 + c) = o;
+        }
+      } else {
+        // 2 rows per round (32 lanes x 4 columns each), 16 rounds in groups of
+        // G (4 for the rotary epilogues, whose rounds hold 4 float4 each)
+        constexpr bool kRope = EPI == EPI_QKV || EPI == EPI_KV;
+        constexpr int G = kRope ? 4 : 8;
+#pragma unroll
+        for (int hh = 0; hh < 16 / G; ++hh) {
+          float4 x4[G], y4[G], cs[G], sn[G];
+          float sc[G];
+          int mr[G], mp[G];
+          bf16x4_t rv[G];
+#pragma unroll
+          for (int r = 0; r < G; ++r) {
+            const int lr = 2 * (G * hh + r) + (lane >> 5);
+            x4[r] = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + c4);
+            if (kRope && !is_v)
+              y4[r] = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + (c4 ^ half));
+            sc[r] = msc[i * 32 + lr];
+            mr[r] = mrow[i * 32 + lr];
+            mp[r] = mpos[i * 32 + lr];
+          }
+#pragma unroll
+          for (int r = 0; r < G; ++r) {
+            if (EPI == EPI_RESID)
+              rv[r] = *reinterpret_cast<const bf16x4_t*>(p.resid + (int64_t)mr[r] * p.ldc + nw + c4);
+            if (kRope && !is_v) {
+              const int c = (cbase + c4) & (hd - 1);
+              const int64_t t = (int64_t)mp[r] * half + (c & (half - 1));
+              cs[r] = *reinterpret_cast<const float4*>(p.rope_cos + t);
+              sn[r] = *reinterpret_cast<const float4*>(p.rope_sin + t);
+            }
+          }
+#pragma unroll
+          for (int r = 0; r < G; ++r) {
+            const int m = mb + 2 * (G * hh + r) + (lane >> 5);
+            const float x[4] = {x4[r].x * sc[r], x4[r].y * sc[r], x4[r].z * sc[r],
+                                x4[r].w * sc[r]};
+            bf16x4_t o;
+            if (EPI == EPI_STORE) {
+              const int64_t off = (int64_t)m * p.ldc + nw + c4;
+              if (!kCheck || m < M) {
+                if (p.c_f32) {
+                  *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + off) =
+                      make_float4(x[0], x[1], x[2], x[3]);
+                } else {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
+                  *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
+                }
+              }
+            } else if (EPI == EPI_RESID) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e] + bf2f(rv[r][e]));
+              if (!kCheck || m < M)
+                *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) +
+                                             (int64_t)mr[r] * p.ldc + nw + c4) = o;
+            } else {  // EPI_QKV / EPI_KV
+              if (is_v) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
-                *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
+              } else {
+                // rotate-half RoPE: column c pairs with c +- hd/2 of the same head
+                const float y[4] = {y4[r].x * sc[r], y4[r].y * sc[r], y4[r].z * sc[r],
+                                    y4[r].w * sc[r]};
+                const int c = (cbase + c4) & (hd - 1);   // column within the head
+                const float cv[4] = {cs[r].x, cs[r].y, cs[r].z, cs[r].w};
+                const float sv[4] = {sn[r].x, sn[r].y, sn[r].z, sn[r].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  o[e] = f2bf(c < half ? x[e] * cv[e] - y[e] * sv[e] : x[e] * cv[e] + y[e] * sv[e]);
               }
+              const int64_t drow = is_q ? (int64_t)m : (int64_t)mr[r];
+              if (!kCheck || m < M)
+                *reinterpret_cast<bf16x4_t*>(sec_dst + drow * p.d_q + c4) = o;
             }
-          } else if (EPI == EPI_RESID) {
-            bf16x4_t o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e] + bf2f(rv[r][e]));
-            if (m < M)
-              *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) +
-                                           (int64_t)mrow[ml] * p.ldc + nw + c4) = o;
-          } else {  // EPI_QKV / EPI_KV
-            bf16x4_t o;
-            if (is_v) {
-#pragma unroll
-              for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
-            } else {
-              // rotate-half RoPE: column c pairs with c +- hd/2 of the same head
-              const float4 y4 = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + (c4 ^ half));
-              const float y[4] = {y4.x * sc, y4.y * sc, y4.z * sc, y4.w * sc};
-              const int c = (cbase + c4) & (hd - 1);   // column within the head
-              const float cv[4] = {cs[r].x, cs[r].y, cs[r].z, cs[r].w};
-              const float sv[4] = {sn[r].x, sn[r].y, sn[r].z, sn[r].w};
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                o[e] = f2bf(c < half ? x[e] * cv[e] - y[e] * sv[e] : x[e] * cv[e] + y[e] * sv[e]);
-            }
-            bf16* dst = is_q ? p.q_out + (int64_t)m * p.d_q
-                             : (is_v ? vc : kc) + (int64_t)mrow[ml] * p.d_q;
-            if (m < M) *reinterpret_cast<bf16x4_t*>(dst + cbase + c4) = o;
           }
         }
       }
-    }
+    };
+    if (mb + 32 <= M) emit(std::false_type{});
+    else emit(std::true_type{});
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);   // block reads done before the next block's writes
     __builtin_amdgcn_wave_barrier();
   }
