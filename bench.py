@@ -27,6 +27,35 @@ import time
 
 PEAK_BF16 = 2.5e15      # dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12       # HBM3E, B/s
+HERE = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "llama7b_prefill_8x2048_hbm_traffic.json")
+
+
+def sources_sha256():
+    """Hash of the HIP sources, the same way the traffic summary records it."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(HERE, "paper_2601_03700_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(fam):
+    """HBM bytes per launch of a kernel family from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary (each scaled by what it reads for a
+    device copy of known size), or None when the HIP sources changed after
+    the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            d = json.load(fh)
+    except OSError:
+        return None
+    if d.get("source_sha256") != sources_sha256():
+        return None
+    k = d.get("kernels", {}).get(fam)
+    return None if k is None else k["traffic_bytes"]
 
 
 def log(*a):
@@ -171,7 +200,7 @@ def main():
     d_avg_s = d_ms / d_launch / 1e3
     achieved = d_flops_launch / d_avg_s
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16, "traffic": None,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16, "traffic": measured_traffic(family(dom)),
                 "flops_per_launch": d_flops_launch, "avg_launch_us": d_avg_s * 1e6,
                 "launches": d_launch}
 
