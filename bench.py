@@ -73,7 +73,12 @@ def parse():
     ap.add_argument("--seq", type=int, default=2048)
     ap.add_argument("--no-extras", action="store_true", help="skip the variant and kernel runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=512)
+    ap.add_argument("--no-generation", action="store_true",
+                    help="skip the generation run (batch 64, 4096-token context, decode steps)")
+    ap.add_argument("--gen-batch", type=int, default=64)
+    ap.add_argument("--gen-context", type=int, default=4096)
+    ap.add_argument("--gen-steps", type=int, default=256)
+    ap.add_argument("--cpu-tokens", type=int, default=2048)
     ap.add_argument("--cpu-layers", type=int, default=4)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="copy 256 MiB device to device first (a kernel of known traffic "
@@ -151,7 +156,8 @@ def main():
     n_tok = Bn * T
     t0 = time.time()
     weights = ai.decoder_weights_torch(shape, seed=7, device="cuda")
-    model = DecoderModel(shape, weights, dtype="bf16", rope_max_pos=T)
+    rope_pos = max(T, args.gen_context + args.gen_steps)
+    model = DecoderModel(shape, weights, dtype="bf16", rope_max_pos=rope_pos)
     del weights
     torch.cuda.empty_cache()
     ids = torch.from_numpy(ai.token_ids(8, shape.vocab, Bn, T)).cuda()
@@ -239,6 +245,11 @@ def main():
         log(f"no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
         out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
         out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
+
+    if not args.no_generation:
+        del cache, ids
+        torch.cuda.empty_cache()
+        out["generation"] = generation(args, model, shape, ai, B, torch, np)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args, shape, ai, np)
@@ -373,6 +384,97 @@ def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
             "copy_512MiB_gbs": copy_gbs,
             "note": "exit-test working set 671 MB > 256 MB MALL; per-layer compaction "
                     "(16K entries) is latency-bound, the 2^26 list measures bandwidth"}
+
+
+def generation(args, model, shape, ai, B, torch, np):
+    """Generation at the 7B shape: a batch of gen_context-token prompts is
+    prefilled with exits (exit layer uniform in 8..31 per token, seeded), so
+    the cache mixes computed and generated entries, then gen_steps greedy
+    decode steps run with the same per-token schedule.  A no-exit decode run
+    (delta = +inf) over the same cache follows for comparison."""
+    N, H, hd, Dq = shape.n_layers, shape.n_heads, shape.head_dim, shape.d_q
+    Bn, T, S = args.gen_batch, args.gen_context, args.gen_steps
+    s_max = T + S
+    t0 = time.time()
+    cache = model.new_cache(Bn, s_max)
+    ids = torch.from_numpy(ai.token_ids(9, shape.vocab, Bn, T)).cuda()
+    cfg = B.exit_cfg(args.delta, N, args.metric)
+    sched_p = torch.from_numpy(ai.forced_exit_layers(5, Bn * T, 8, 31)).cuda()
+    sched_d = torch.from_numpy(ai.forced_exit_layers(6, S * Bn, 8, 31)).cuda().view(S, Bn)
+    torch.cuda.synchronize()
+    tp = time.time()
+    res, _ = model.prefill(ids, cfg, cache=cache, logits="last", force_layer=sched_p)
+    torch.cuda.synchronize()
+    prefill_s = time.time() - tp
+    first = model.greedy(res.logits)
+    gen_frac = float((N - sched_p.to(torch.float64)).mean() / N)
+    log(f"generation: cache {2 * cache.k.numel() * 2 / 2**30:.0f} GiB, prefill of {Bn}x{T} "
+        f"in {prefill_s:.2f}s ({time.time() - t0:.1f}s with setup)")
+    del res
+    torch.cuda.empty_cache()
+
+    def decode(n_steps, force, timing=False, cfg_=cfg):
+        nxt = first
+        el = []
+        for k in range(2):      # warmup at the first two positions (rewritten below)
+            pos = torch.full((Bn,), T + k, dtype=torch.int32, device="cuda")
+            model.decode_step(cache, nxt, pos, cfg_, force_layer=None if force is None else force[k])
+        torch.cuda.synchronize()
+        if timing:
+            B.timing_reset()
+            B.timing_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for k in range(n_steps):
+            pos = torch.full((Bn,), T + k, dtype=torch.int32, device="cuda")
+            st = model.decode_step(cache, nxt, pos, cfg_,
+                                   force_layer=None if force is None else force[k])
+            nxt = model.greedy(st.logits)
+            el.append(st.exit_layer)
+        e1.record()
+        torch.cuda.synchronize()
+        kern = None
+        if timing:
+            B.timing_enable(False)
+            kern = B.timing_read()
+        return e0.elapsed_time(e1) / 1e3, torch.stack(el), kern
+
+    dec_s, el, kern = decode(S, sched_d, timing=True)
+    exited_by_layer = [float((el <= i).to(torch.float64).mean()) for i in range(1, N + 1)]
+    # decode attention: each active (query, head) streams its context's K and V rows
+    att = {k: v for k, v in kern.items() if k.startswith("attend_split")}
+    att_launch, att_ms = att.get("attend_split_kernel<128>", (0, 0.0))
+    ctx_keys = sum(T + k + 1 for k in range(S))          # keys per sequence summed over steps
+    active_q = int(sum((el >= i).sum() for i in range(1, N + 1)))   # (token, layer) queries
+    att_bytes = (active_q / (S * Bn)) * ctx_keys * Bn * H * hd * 2 * 2   # K + V, bf16
+    kinf_s, _, _ = decode(max(8, S // 4), None, cfg_=B.exit_cfg(math.inf, N, args.metric))
+    n_inf = max(8, S // 4)
+    out = {
+        "workload": (f"Llama-7B-shaped generation: batch {Bn}, {T}-token prompts prefilled with "
+                     f"exit layer uniform in 8..31 per token, then {S} greedy decode steps with "
+                     f"the same per-token schedule"),
+        "prefill_tokens_per_s": Bn * T / prefill_s,
+        "decode_tokens_per_s": Bn * S / dec_s,
+        "decode_ms_per_step": dec_s * 1e3 / S,
+        "prefill_plus_decode_tokens_per_s": Bn * (T + S) / (prefill_s + dec_s),
+        "no_exit_decode_tokens_per_s": Bn * n_inf / kinf_s,
+        "no_exit_decode_ms_per_step": kinf_s * 1e3 / n_inf,
+        "generated_cache_fraction_prompt": gen_frac,
+        "exited_fraction_by_layer": exited_by_layer,
+        "decode_attention": {
+            "launches": att_launch, "avg_us": att_ms * 1e3 / max(1, att_launch),
+            "bytes_per_step": att_bytes / S,
+            "gbs": att_bytes / (att_ms / 1e3) / 1e9 if att_ms else None,
+            "hbm_frac": att_bytes / (att_ms / 1e3) / PEAK_HBM if att_ms else None},
+        "kernels": {k: {"launches": n, "avg_us": ms * 1e3 / n, "share": ms / (dec_s * 1e3)}
+                    for k, (n, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1])[:12]},
+    }
+    log(f"generation: decode {dec_s * 1e3 / S:.1f} ms/step ({Bn * S / dec_s:.0f} tok/s), "
+        f"no-exit {kinf_s * 1e3 / n_inf:.1f} ms/step; decode attention "
+        f"{out['decode_attention']['gbs'] or 0:.0f} GB/s")
+    del cache
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(args, shape, ai, np):

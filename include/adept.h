@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define ADEPT_ABI_VERSION 1
+#define ADEPT_ABI_VERSION 2
 
 typedef enum {
   ADEPT_OK = 0,
@@ -168,8 +168,15 @@ adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_model, int n_
  *  key_live [n_seq*s_max] uint8, nullable: keys with 0 are left out.
  *  out [max_active][H][hd] (dtype): softmax(q K^T * scale) V per head, with
  *      f32 scores and softmax statistics.
+ *  workspace: adept_attend_workspace_bytes(max_active, n_seq, H, hd, s_max)
+ *      bytes (at most about 17 MB), 16-byte aligned; nullable, but then bf16
+ *      takes the slow generic kernel.  bf16 with hd 64/128 uses query tiles on
+ *      MFMA when the queries average at least 4 per sequence (causal, no
+ *      key_live: prefill), otherwise key chunks streamed per (query, head)
+ *      and merged (decode, bidirectional).
  * ------------------------------------------------------------------------- */
-size_t adept_attend_workspace_bytes(int max_active, int n_seq);
+size_t adept_attend_workspace_bytes(int max_active, int n_seq, int n_heads, int head_dim,
+                                    int s_max);
 adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale, int causal,
                           const void* q, const int32_t* rows, const int32_t* n_active,
                           int max_active, const int32_t* pos, const int32_t* seq, int n_seq,
@@ -184,7 +191,9 @@ adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale
  *   O GEMM (+residual: h[i&1] = h[(i-1)&1] + o Wo^T) -> RMSNorm ->
  *   gate/up GEMM (+SwiGLU) -> down GEMM (+residual) -> adept_exit_test ->
  *   adept_compact (next list into active[i&1], exited rows into `exited`) ->
- *   adept_kv_generate for the rows exited at i (layers i+1..N).
+ *   adept_kv_generate for the rows exited at i (layers i+1..N); with
+ *   attn_tiles = 0 (decode) the generation of every exited row is enqueued
+ *   once, by the step of layer N, after copying the exit states into h[N&1].
  * The residual stream ping-pongs between h[0] and h[1]: a token's final
  * state is h[exit_layer & 1][row] (its state at exit, the identity mapped
  * state).  Before layer 1 the caller puts h_0 in h[0], zeroes the inertia,
@@ -211,7 +220,11 @@ typedef struct {
   int32_t n_tok;         /* rows in the per-token tensors */
   int32_t max_active;    /* (host) bound on the active rows entering this layer */
   int32_t n_seq, s_max;
-  int32_t attn_tiles;    /* 1: queries are prompt tiles (prefill); 0: one query per sequence */
+  int32_t attn_tiles;    /* 1: prompt rows (prefill): attention by query tiles, K/V of
+                            the rows that exit at layer i generated right after layer i;
+                            0: one row per sequence (decode): attention by key chunks,
+                            K/V of all exited rows generated after layer N (no row of
+                            the pass reads them); the pass must then run all N layers */
   void* h[2];            /* [n_tok][D] residual stream ping-pong */
   float* inertia;        /* [n_tok][D] (GLOBAL metric) */
   const int32_t* pos;    /* [n_tok] */

@@ -64,7 +64,7 @@ _SIGS = {
     "adept_kv_generate": (_i32, [_i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp, _vp,
                                  _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _vp,
                                  _i64, _vp, _sz, _vp]),
-    "adept_attend_workspace_bytes": (_sz, [_i32, _i32]),
+    "adept_attend_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32]),
     "adept_attend": (_i32, [_i32, _i32, _i32, ctypes.c_float, _i32, _vp, _vp, _vp, _i32, _vp,
                             _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "adept_layer_workspace_bytes": (_sz, [ctypes.POINTER(LayerArgs)]),
@@ -178,8 +178,8 @@ def kv_generate(n_layers, d_model, n_heads, head_dim, eps, s_map, rows, n_rows, 
            "adept_kv_generate")
 
 
-def attend_workspace_bytes(max_active, n_seq):
-    return lib().adept_attend_workspace_bytes(max_active, n_seq)
+def attend_workspace_bytes(max_active, n_seq, n_heads, head_dim, s_max):
+    return lib().adept_attend_workspace_bytes(max_active, n_seq, n_heads, head_dim, s_max)
 
 
 def attend(n_heads, head_dim, q, rows, n_active, max_active, pos, seq, n_seq, k_layer, v_layer,

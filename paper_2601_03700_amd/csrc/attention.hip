@@ -18,6 +18,8 @@
 // Generic path (f32, decode with one query per sequence, bidirectional
 // attention with a live-key mask): one workgroup per (query, head), scores
 // for all keys in LDS, exact softmax, then a weighted sum of V rows.
+#include <algorithm>
+
 #include "common.h"
 
 namespace adept {
@@ -315,23 +317,199 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// split-K kernel (decode and bidirectional): HBM-bound streaming of K/V rows
+// ---------------------------------------------------------------------------
+constexpr int kSplitThreads = 256;
+
+// Workgroup (k, c, h): keys [c*CK, min(L, (c+1)*CK)) of query entry k, head
+// h, CK = ceil(L / nc).  A key's row of head h (HD bf16 = HD*2 bytes) is read
+// by LPK = HD/8 lanes, 16 bytes each, so every load instruction covers whole
+// rows; the wave's GPW lane groups take different keys, four per group in
+// flight.  Scores are q.k over the group (xor shuffles), and each group keeps
+// an online softmax in the exp2 domain (q is pre-scaled by scale*log2(e)).
+// The workgroup's groups are merged in LDS; with one chunk the output is
+// written directly, else (max, sum, unnormalised o) go to the workspace for
+// attend_combine_kernel.
+template <int HD>
+__global__ __launch_bounds__(kSplitThreads) void attend_split_kernel(
+    int H, float scale_log2, int causal, int nc, const bf16* __restrict__ q,
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ n_active, int max_active,
+    const int32_t* __restrict__ pos, const int32_t* __restrict__ seq,
+    const bf16* __restrict__ kc, const bf16* __restrict__ vc, int s_max,
+    const int32_t* __restrict__ key_len, const uint8_t* __restrict__ key_live,
+    bf16* __restrict__ out, float* __restrict__ part) {
+  constexpr int LPK = HD / 8;                 // lanes per key row
+  constexpr int GPW = 64 / LPK;               // key groups per wave
+  constexpr int G = GPW * (kSplitThreads / 64);
+  __shared__ float gm[G], gl[G];
+  __shared__ float go[G][HD + 4];
+  const int k = blockIdx.x / nc, c = blockIdx.x - (blockIdx.x / nc) * nc, h = blockIdx.y;
+  if (k >= min(*n_active, max_active)) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int grp = (tid >> 6) * GPW + lane / LPK;   // key group in the workgroup
+  const int sub = lane % LPK;                      // 8-dim slice of the row
+  const int row = rows[k];
+  const int b = seq[row];
+  const int L = min(causal ? pos[row] + 1 : key_len[b], s_max);
+  const int ck = (L + nc - 1) / nc;
+  const int t0 = c * ck, t1 = min(L, t0 + ck);
+  const int64_t rs = (int64_t)H * HD;               // cache row stride (elements)
+  const bf16* kb = kc + (int64_t)b * s_max * rs + h * HD + sub * 8;
+  const bf16* vb = vc + (int64_t)b * s_max * rs + h * HD + sub * 8;
+  const uint8_t* live = key_live ? key_live + (int64_t)b * s_max : nullptr;
+
+  float qf[8];
+  {
+    const uint4 qv = *reinterpret_cast<const uint4*>(q + (int64_t)k * rs + h * HD + sub * 8);
+    const uint32_t w[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      qf[2 * e] = __uint_as_float(w[e] << 16) * scale_log2;
+      qf[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u) * scale_log2;
+    }
+  }
+  float m = -INFINITY, l = 0.0f, o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = 0.0f;
+  for (int tb = t0 + grp; tb < t1; tb += 4 * G) {
+    uint4 kv[4], vv[4];
+    bool ok[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int t = tb + u * G;
+      ok[u] = t < t1;
+      const int tt = ok[u] ? t : t0;            // clamped: loaded, never used
+      kv[u] = *reinterpret_cast<const uint4*>(kb + (int64_t)tt * rs);
+      vv[u] = *reinterpret_cast<const uint4*>(vb + (int64_t)tt * rs);
+    }
+    float sc[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t w[4] = {kv[u].x, kv[u].y, kv[u].z, kv[u].w};
+      float d = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        d = fmaf(qf[2 * e], __uint_as_float(w[e] << 16), d);
+        d = fmaf(qf[2 * e + 1], __uint_as_float(w[e] & 0xffff0000u), d);
+      }
+#pragma unroll
+      for (int off = LPK / 2; off > 0; off >>= 1) d += __shfl_xor(d, off, 64);
+      const int t = tb + u * G;
+      const bool use = ok[u] && (!live || live[ok[u] ? t : t0]);
+      sc[u] = use ? d : -INFINITY;
+    }
+    const float mb = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+    const float mn = fmaxf(m, mb);
+    if (mn == -INFINITY) continue;              // nothing live yet in this group
+    const float cf = exp2f(m - mn);             // m = -inf -> 0
+    l *= cf;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] *= cf;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float pu = exp2f(sc[u] - mn);       // masked -> 0
+      l += pu;
+      const uint32_t w[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[2 * e] = fmaf(pu, __uint_as_float(w[e] << 16), o[2 * e]);
+        o[2 * e + 1] = fmaf(pu, __uint_as_float(w[e] & 0xffff0000u), o[2 * e + 1]);
+      }
+    }
+    m = mn;
+  }
+  // merge the workgroup's G groups
+  if (sub == 0) {
+    gm[grp] = m;
+    gl[grp] = l;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) go[grp][sub * 8 + e] = o[e];
+  __syncthreads();
+  if (tid < HD) {
+    float M = -INFINITY;
+    for (int g = 0; g < G; ++g) M = fmaxf(M, gm[g]);
+    float Ls = 0.0f, O = 0.0f;
+    if (M != -INFINITY) {
+      for (int g = 0; g < G; ++g) {
+        const float w = exp2f(gm[g] - M);       // empty group: -inf -> 0
+        Ls = fmaf(w, gl[g], Ls);
+        O = fmaf(w, go[g][tid], O);
+      }
+    }
+    const int64_t pq = (int64_t)k * H + h;
+    if (nc == 1) {
+      out[pq * HD + tid] = f2bf(O / Ls);
+    } else {
+      float* pp = part + (pq * nc + c) * (HD + 2);
+      pp[2 + tid] = O;
+      if (tid == 0) {
+        pp[0] = M;
+        pp[1] = Ls;
+      }
+    }
+  }
+}
+
+// Merges the nc partial results of each (query entry, head).
+template <int HD>
+__global__ __launch_bounds__(HD) void attend_combine_kernel(int H, int nc,
+                                                           const int32_t* __restrict__ n_active,
+                                                           int max_active,
+                                                           const float* __restrict__ part,
+                                                           bf16* __restrict__ out) {
+  const int k = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
+  if (k >= min(*n_active, max_active)) return;
+  const int64_t pq = (int64_t)k * H + h;
+  const float* pp = part + pq * nc * (HD + 2);
+  float M = -INFINITY;
+  for (int c = 0; c < nc; ++c) M = fmaxf(M, pp[c * (HD + 2)]);
+  float Ls = 0.0f, O = 0.0f;
+  if (M != -INFINITY) {
+    for (int c = 0; c < nc; ++c) {
+      const float* pc = pp + c * (HD + 2);
+      const float w = exp2f(pc[0] - M);
+      Ls = fmaf(w, pc[1], Ls);
+      O = fmaf(w, pc[2 + d], O);
+    }
+  }
+  out[pq * HD + d] = f2bf(O / Ls);
+}
+
+// Chunks per (query entry, head) of the split kernel: about 32K workgroups
+// in all, at most one chunk per 256 keys of s_max.
+int split_chunks(int max_active, int H, int s_max) {
+  const int64_t pairs = (int64_t)std::max(max_active, 1) * H;
+  const int64_t want = std::max<int64_t>(1, 32768 / pairs);
+  return (int)std::max<int64_t>(1, std::min<int64_t>(want, (s_max + 255) / 256));
+}
+
+size_t split_workspace_bytes(int max_active, int H, int hd, int s_max) {
+  const int nc = split_chunks(max_active, H, s_max);
+  return nc == 1 ? 0 : (size_t)max_active * H * nc * (hd + 2) * sizeof(float);
+}
+
 }  // namespace
 }  // namespace adept
 
 using namespace adept;
 
-extern "C" size_t adept_attend_workspace_bytes(int max_active, int n_seq) {
-  const size_t tiles = (size_t)(max_active / QT + n_seq + 1);
-  return 256 + tiles * sizeof(int2);
+namespace adept {
+
+size_t attend_workspace_bytes(int max_active, int n_seq, int n_heads, int head_dim, int s_max) {
+  const size_t tiles = 256 + (size_t)(max_active / QT + n_seq + 1) * sizeof(int2);
+  return std::max(tiles, split_workspace_bytes(max_active, n_heads, head_dim, s_max));
 }
 
-extern "C" adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale,
-                                     int causal, const void* q, const int32_t* rows,
-                                     const int32_t* n_active, int max_active, const int32_t* pos,
-                                     const int32_t* seq, int n_seq, const void* k_layer,
-                                     const void* v_layer, int s_max, const int32_t* key_len,
-                                     const uint8_t* key_live, void* out, void* workspace,
-                                     size_t workspace_bytes, void* stream) {
+adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float scale, int causal,
+                             const void* q, const int32_t* rows, const int32_t* n_active,
+                             int max_active, const int32_t* pos, const int32_t* seq, int n_seq,
+                             const void* k_layer, const void* v_layer, int s_max,
+                             const int32_t* key_len, const uint8_t* key_live, void* out,
+                             void* workspace, size_t workspace_bytes, bool allow_tiles,
+                             hipStream_t s) {
   ADEPT_REQUIRE(dt == ADEPT_F32 || dt == ADEPT_BF16, "attend: bad dtype");
   ADEPT_REQUIRE(n_heads > 0 && head_dim > 0 && head_dim <= 128 && 256 % head_dim == 0,
                 "attend: head_dim %d must divide 256 and be <= 128", head_dim);
@@ -341,10 +519,9 @@ extern "C" adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, 
                 "attend: NULL tensor");
   ADEPT_REQUIRE(causal || key_len, "attend: bidirectional attention needs key_len");
   if (max_active == 0) return ADEPT_OK;
-  hipStream_t s = as_stream(stream);
-  const bool mfma = dt == ADEPT_BF16 && causal && !key_live && (head_dim == 64 || head_dim == 128);
-  if (mfma && workspace) {
-    const size_t need = adept_attend_workspace_bytes(max_active, n_seq);
+  const bool fast = dt == ADEPT_BF16 && (head_dim == 64 || head_dim == 128) && workspace;
+  if (fast) {
+    const size_t need = attend_workspace_bytes(max_active, n_seq, n_heads, head_dim, s_max);
     if (workspace_bytes < need) {
       set_error("attend: workspace of %zu bytes needed", need);
       return ADEPT_E_WORKSPACE;
@@ -352,23 +529,52 @@ extern "C" adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, 
     ADEPT_REQUIRE(aligned16(q) && aligned16(k_layer) && aligned16(v_layer) && aligned16(out) &&
                       aligned16(workspace),
                   "attend: tensors must be 16-byte aligned");
+  }
+  const float sl = scale * 1.4426950408889634f;   // scores in the exp2 domain
+  // query tiles pay off when the queries of a sequence are many (prefill)
+  if (fast && allow_tiles && causal && !key_live && max_active >= 4 * n_seq) {
     int32_t* n_tiles = (int32_t*)workspace;
     int2* tiles = (int2*)((char*)workspace + 256);
     const int max_tiles = max_active / QT + n_seq + 1;
     ADEPT_LAUNCH(attend_plan_kernel, dim3(1), dim3(1024), 2 * (n_seq + 1) * sizeof(int), s,
-                       rows, n_active, max_active, seq, n_seq, tiles, n_tiles);
+                 rows, n_active, max_active, seq, n_seq, tiles, n_tiles);
     ADEPT_CHECK_LAUNCH("attend_plan");
-    const float sl = scale * 1.4426950408889634f;
     dim3 grid(max_tiles, n_heads);
     if (head_dim == 128)
       ADEPT_LAUNCH(attend_prefill_kernel<128>, grid, dim3(256), 0, s, n_heads, sl,
-                         (const bf16*)q, rows, pos, seq, (const bf16*)k_layer,
-                         (const bf16*)v_layer, s_max, tiles, n_tiles, (bf16*)out);
+                   (const bf16*)q, rows, pos, seq, (const bf16*)k_layer, (const bf16*)v_layer,
+                   s_max, tiles, n_tiles, (bf16*)out);
     else
       ADEPT_LAUNCH(attend_prefill_kernel<64>, grid, dim3(256), 0, s, n_heads, sl,
-                         (const bf16*)q, rows, pos, seq, (const bf16*)k_layer,
-                         (const bf16*)v_layer, s_max, tiles, n_tiles, (bf16*)out);
+                   (const bf16*)q, rows, pos, seq, (const bf16*)k_layer, (const bf16*)v_layer,
+                   s_max, tiles, n_tiles, (bf16*)out);
     return launch_status("attend_prefill");
+  }
+  if (fast) {
+    const int nc = split_chunks(max_active, n_heads, s_max);
+    float* part = (float*)workspace;
+    dim3 grid(max_active * nc, n_heads);
+    if (head_dim == 128)
+      ADEPT_LAUNCH(attend_split_kernel<128>, grid, dim3(kSplitThreads), 0, s, n_heads, sl,
+                   causal, nc, (const bf16*)q, rows, n_active, max_active, pos, seq,
+                   (const bf16*)k_layer, (const bf16*)v_layer, s_max, key_len, key_live,
+                   (bf16*)out, part);
+    else
+      ADEPT_LAUNCH(attend_split_kernel<64>, grid, dim3(kSplitThreads), 0, s, n_heads, sl,
+                   causal, nc, (const bf16*)q, rows, n_active, max_active, pos, seq,
+                   (const bf16*)k_layer, (const bf16*)v_layer, s_max, key_len, key_live,
+                   (bf16*)out, part);
+    ADEPT_CHECK_LAUNCH("attend_split");
+    if (nc > 1) {
+      dim3 g2(max_active, n_heads);
+      if (head_dim == 128)
+        ADEPT_LAUNCH(attend_combine_kernel<128>, g2, dim3(128), 0, s, n_heads, nc, n_active,
+                     max_active, part, (bf16*)out);
+      else
+        ADEPT_LAUNCH(attend_combine_kernel<64>, g2, dim3(64), 0, s, n_heads, nc, n_active,
+                     max_active, part, (bf16*)out);
+    }
+    return launch_status("attend_split");
   }
   const size_t smem = (size_t)(128 + s_max) * sizeof(float);
   dim3 grid(max_active, n_heads);
@@ -383,4 +589,23 @@ extern "C" adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, 
                        pos, seq, (const float*)k_layer, (const float*)v_layer, s_max, key_len,
                        key_live, (float*)out);
   return launch_status("attend_generic");
+}
+
+}  // namespace adept
+
+extern "C" size_t adept_attend_workspace_bytes(int max_active, int n_seq, int n_heads,
+                                               int head_dim, int s_max) {
+  return attend_workspace_bytes(max_active, n_seq, n_heads, head_dim, s_max);
+}
+
+extern "C" adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale,
+                                     int causal, const void* q, const int32_t* rows,
+                                     const int32_t* n_active, int max_active, const int32_t* pos,
+                                     const int32_t* seq, int n_seq, const void* k_layer,
+                                     const void* v_layer, int s_max, const int32_t* key_len,
+                                     const uint8_t* key_live, void* out, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  return attend_dispatch(dt, n_heads, head_dim, scale, causal, q, rows, n_active, max_active,
+                         pos, seq, n_seq, k_layer, v_layer, s_max, key_len, key_live, out,
+                         workspace, workspace_bytes, true, as_stream(stream));
 }

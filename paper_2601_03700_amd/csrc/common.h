@@ -154,9 +154,23 @@ struct GemmArgs {
   int head_dim, d_q;
   void* q_out; void* k_cache; void* v_cache;   // caches already offset to the layer
   const char* name;       // timing label (string literal), nullable
+  // f32 workspace of the skinny path (M_max <= 64: decode), nullable; used
+  // when at least skinny_ws_bytes(N or 2N for SWIGLU, K) bytes
+  float* skinny_ws; size_t skinny_ws_bytes;
 };
+size_t skinny_ws_bytes(int n_cols, int K);
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s);       // bf16 MFMA path
+// attention (csrc/attention.hip): adept_attend with a switch that can forbid
+// the query-tile kernel (one query per sequence: decode)
+size_t attend_workspace_bytes(int max_active, int n_seq, int n_heads, int head_dim, int s_max);
+adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float scale, int causal,
+                             const void* q, const int32_t* rows, const int32_t* n_active,
+                             int max_active, const int32_t* pos, const int32_t* seq, int n_seq,
+                             const void* k_layer, const void* v_layer, int s_max,
+                             const int32_t* key_len, const uint8_t* key_live, void* out,
+                             void* workspace, size_t workspace_bytes, bool allow_tiles,
+                             hipStream_t s);
 adept_status gemm_f32(const GemmArgs& g, float* tmp, hipStream_t s);      // f32 + epilogue
 adept_status gemm_f32_direct(const GemmArgs& g, hipStream_t s);           // f32, C = A B^T
 adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32_t* n_work,

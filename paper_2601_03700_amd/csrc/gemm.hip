@@ -654,6 +654,185 @@ adept_status launch_bf16(const GP& p, hipStream_t s, const char* name) {
   return launch_status("gemm_bf16");
 }
 
+// ---------------------------------------------------------------------------
+// Skinny path (at most 64 rows: decode).  The weights are streamed from HBM
+// once; M is too small for the 256x256 tile to give the chip enough
+// workgroups.  A workgroup owns 32 columns of the partial space (N columns,
+// or the F gate columns followed by the F up columns for SWIGLU) and one
+// slice of K; its four waves take contiguous quarters of the slice, keep
+// eight 16-wide k steps of loads in flight (operands straight from global
+// memory in the MFMA layout: 32 rows x 32 bytes per instruction, whole
+// 128-byte lines over four consecutive steps), and add up in LDS.  The
+// slices' partial tiles go to a workspace; skinny_epilogue_kernel sums them
+// in slice order (deterministic) and applies the same epilogues as the tiled
+// path.
+// ---------------------------------------------------------------------------
+constexpr int kSkinnyM = 64;
+constexpr int kSkinnyBN = 32;
+constexpr int kSkinnyU = 8;
+
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(GP p, int Nt, int nb, int k_slice,
+                                                          float* __restrict__ part) {
+  __shared__ float red[4][kSkinnyM][kSkinnyBN + 1];
+  const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
+  if (M <= 0) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.x * kSkinnyBN, slice = blockIdx.y;
+  const int k0 = slice * k_slice, k1 = min(p.K, k0 + k_slice);
+  const int steps = (k1 - k0) / 16;
+  const int w0 = k0 + 16 * ((steps * wave) / 4), w1 = k0 + 16 * ((steps * (wave + 1)) / 4);
+  const int n = n0 + (lane & 31);
+  const int koff = 8 * (lane >> 5);
+  const bf16* brow = (n >= nb ? p.B2 + (int64_t)(n - nb) * p.ldb : p.B + (int64_t)n * p.ldb) + koff;
+  const bf16* arow[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int m = min(i * 32 + (lane & 31), M - 1);   // clamped: loaded, never stored
+    const int r = p.a_rows ? p.a_rows[m] : m;
+    arow[i] = p.A + (int64_t)r * p.lda + koff;
+  }
+  f32x16_t acc[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[i][v] = 0.0f;
+  int k = w0;
+  for (; k + 16 * kSkinnyU <= w1; k += 16 * kSkinnyU) {
+    bf16x8_t a0[kSkinnyU], a1[kSkinnyU], b[kSkinnyU];
+#pragma unroll
+    for (int u = 0; u < kSkinnyU; ++u) {
+      b[u] = *reinterpret_cast<const bf16x8_t*>(brow + k + 16 * u);
+      a0[u] = *reinterpret_cast<const bf16x8_t*>(arow[0] + k + 16 * u);
+      a1[u] = *reinterpret_cast<const bf16x8_t*>(arow[1] + k + 16 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < kSkinnyU; ++u) {
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[u], b[u], acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[u], b[u], acc[1], 0, 0, 0);
+    }
+  }
+  for (; k < w1; k += 16) {
+    const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(brow + k);
+    const bf16x8_t x0 = *reinterpret_cast<const bf16x8_t*>(arow[0] + k);
+    const bf16x8_t x1 = *reinterpret_cast<const bf16x8_t*>(arow[1] + k);
+    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b0, acc[0], 0, 0, 0);
+    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b0, acc[1], 0, 0, 0);
+  }
+  // C layout: value v of block i is row i*32 + 8*(v/4) + 4*(lane/32) + v%4, column lane%32
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      red[wave][i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)][lane & 31] = acc[i][v];
+  __syncthreads();
+  for (int e = tid; e < kSkinnyM * kSkinnyBN; e += 256) {
+    const int r = e / kSkinnyBN, c = e % kSkinnyBN;
+    part[((int64_t)slice * kSkinnyM + r) * Nt + n0 + c] =
+        red[0][r][c] + red[1][r][c] + red[2][r][c] + red[3][r][c];
+  }
+}
+
+// Sum of the S slices for row m, columns c..c+3.
+__device__ __forceinline__ float4 skinny_sum(const float* __restrict__ part, int S, int Nt, int m,
+                                             int c) {
+  float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int sl = 0; sl < S; ++sl) {
+    const float4 y =
+        *reinterpret_cast<const float4*>(part + ((int64_t)sl * kSkinnyM + m) * Nt + c);
+    x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+  }
+  return x;
+}
+
+// One thread per (row, 4 output columns).
+template <int EPI>
+__global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int nout, int S,
+                                                              const float* __restrict__ part) {
+  const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
+  const int g4 = nout / 4;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int m = (int)(idx / g4), n = (int)(idx % g4) * 4;
+  if (m >= M) return;
+  const float sc = p.row_scale ? p.row_scale[m] : 1.0f;
+  const float4 x4 = skinny_sum(part, S, Nt, m, n);
+  const float x[4] = {x4.x * sc, x4.y * sc, x4.z * sc, x4.w * sc};
+  bf16x4_t o;
+  if (EPI == EPI_STORE) {
+    const int64_t off = (int64_t)m * p.ldc + n;
+    if (p.c_f32) {
+      *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + off) =
+          make_float4(x[0], x[1], x[2], x[3]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
+      *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
+    }
+  } else if (EPI == EPI_RESID) {
+    const int64_t off = (int64_t)p.rows[m] * p.ldc + n;
+    const bf16x4_t r = *reinterpret_cast<const bf16x4_t*>(p.resid + off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e] + bf2f(r[e]));
+    *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
+  } else if (EPI == EPI_SWIGLU) {
+    const float4 u4 = skinny_sum(part, S, Nt, m, nout + n);
+    const float u[4] = {u4.x * sc, u4.y * sc, u4.z * sc, u4.w * sc};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = f2bf(silu(x[e]) * u[e]);
+    *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc + n) = o;
+  } else {  // EPI_QKV
+    const int sec = n / p.d_q, cin = n - sec * p.d_q;
+    const int row = p.rows[m];
+    const bool is_v = sec == 2;
+    bf16* dst = sec == 0 ? p.q_out + (int64_t)m * p.d_q
+                         : (is_v ? p.v_cache : p.k_cache) + (int64_t)p.slot[row] * p.d_q;
+    if (is_v) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
+    } else {
+      // rotate-half RoPE: column c pairs with c +- hd/2 of the same head
+      const int hd = p.head_dim, half = hd >> 1;
+      const int c = cin & (hd - 1);
+      const float4 y4 = skinny_sum(part, S, Nt, m, n ^ half);
+      const float y[4] = {y4.x * sc, y4.y * sc, y4.z * sc, y4.w * sc};
+      const int64_t t = (int64_t)p.pos[row] * half + (c & (half - 1));
+      const float4 cs = *reinterpret_cast<const float4*>(p.rope_cos + t);
+      const float4 sn = *reinterpret_cast<const float4*>(p.rope_sin + t);
+      const float cv[4] = {cs.x, cs.y, cs.z, cs.w}, sv[4] = {sn.x, sn.y, sn.z, sn.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = f2bf(c < half ? x[e] * cv[e] - y[e] * sv[e] : x[e] * cv[e] + y[e] * sv[e]);
+    }
+    *reinterpret_cast<bf16x4_t*>(dst + cin) = o;
+  }
+}
+
+// K slices of the skinny path: about 512 workgroups in all, slices of a
+// multiple of 64 (four waves x 16).
+void skinny_split(int Nt, int K, int* S, int* k_slice) {
+  const int tiles = Nt / kSkinnyBN;
+  int want = std::max(1, std::min(8, (512 + tiles - 1) / tiles));
+  int ks = ((K + want - 1) / want + 63) / 64 * 64;
+  *k_slice = ks;
+  *S = (K + ks - 1) / ks;
+}
+
+template <int EPI>
+adept_status launch_skinny(const GP& p, int Nt, int nout, hipStream_t s, const char* name,
+                           float* part) {
+  int S, ks;
+  skinny_split(Nt, p.K, &S, &ks);
+  {
+    TimedLaunch tl(name ? name : "gemm_skinny", s);
+    hipLaunchKernelGGL(gemm_skinny_kernel, dim3(Nt / kSkinnyBN, S), dim3(256), 0, s, p, Nt,
+                       EPI == EPI_SWIGLU ? nout : Nt, ks, part);
+  }
+  ADEPT_CHECK_LAUNCH("gemm_skinny");
+  const int64_t total = (int64_t)p.M_max * (nout / 4);
+  ADEPT_LAUNCH(skinny_epilogue_kernel<EPI>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+               s, p, Nt, nout, S, part);
+  return launch_status("skinny_epilogue");
+}
+
 GP to_gp(const GemmArgs& g) {
   GP p{};
   p.M_max = g.M_max; p.M_dev = g.M_dev; p.N = g.N; p.K = g.K;
@@ -672,6 +851,12 @@ bool aligned_operands(const GemmArgs& g) {
 }
 
 }  // namespace
+
+size_t skinny_ws_bytes(int Nt, int K) {
+  int S, ks;
+  skinny_split(Nt, K, &S, &ks);
+  return (size_t)S * kSkinnyM * Nt * sizeof(float);
+}
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
   if (g.M_max <= 0) return ADEPT_OK;
@@ -697,6 +882,18 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
     return ADEPT_E_INVALID;
   }
   GP p = to_gp(g);
+  if (g.M_max <= kSkinnyM && g.skinny_ws && g.epi != EPI_KV) {
+    const int Nt = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
+    if (skinny_ws_bytes(Nt, g.K) <= g.skinny_ws_bytes) {
+      switch (g.epi) {
+        case EPI_STORE: return launch_skinny<EPI_STORE>(p, Nt, g.N, s, g.name, g.skinny_ws);
+        case EPI_QKV: return launch_skinny<EPI_QKV>(p, Nt, g.N, s, g.name, g.skinny_ws);
+        case EPI_RESID: return launch_skinny<EPI_RESID>(p, Nt, g.N, s, g.name, g.skinny_ws);
+        case EPI_SWIGLU: return launch_skinny<EPI_SWIGLU>(p, Nt, g.N, s, g.name, g.skinny_ws);
+        default: break;
+      }
+    }
+  }
   p.tiles_m = ceil_div(g.M_max, BM);
   p.tiles_n = g.N / ncols;
   switch (g.epi) {

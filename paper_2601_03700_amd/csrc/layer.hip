@@ -2,6 +2,12 @@
 // regular processing of the active rows, then the exit test, the active-list
 // update and the KV generation for the rows that exit.  Everything is
 // enqueued on one stream with the variable counts kept on the device.
+//
+// With one query row per sequence (decode) no row of the pass reads another
+// row's cache entries, so the K/V a row generates for its skipped layers
+// (Eq. 9) are needed only by later passes: the generation of all rows is
+// then deferred to the end of layer N, as one grouped GEMM in which each
+// skipped layer's Wk/Wv is read once, instead of once per exit layer.
 #include <algorithm>
 
 #include "common.h"
@@ -16,6 +22,8 @@ struct LayerWs {
   void* compact;  size_t compact_bytes;
   void* attend;   size_t attend_bytes;
   void* kvgen;    size_t kvgen_bytes;
+  int32_t* all_rows;  // [n_tok + 64]: rows 0..n_tok-1 and their count (deferred KV generation)
+  float* skinny;  size_t skinny_bytes;   // GEMM partial sums when n_tok <= 64 (decode)
   float* gemm_tmp;  // f32 path only
   size_t total;
 };
@@ -28,10 +36,18 @@ LayerWs carve(const adept_layer_args* a, void* base) {
   w.rinv = (float*)(p + off); off += align256((size_t)a->n_tok * sizeof(float));
   w.compact_bytes = adept_compact_workspace_bytes(a->n_tok);
   w.compact = p + off; off += align256(w.compact_bytes);
-  w.attend_bytes = adept_attend_workspace_bytes(a->n_tok, a->n_seq);
+  w.attend_bytes = attend_workspace_bytes(a->n_tok, a->n_seq, a->n_heads, a->head_dim, a->s_max);
   w.attend = p + off; off += align256(w.attend_bytes);
   w.kvgen_bytes = adept_kv_generate_workspace_bytes(a->n_layers, a->n_tok);
   w.kvgen = p + off; off += align256(w.kvgen_bytes);
+  w.all_rows = (int32_t*)(p + off); off += align256(((size_t)a->n_tok + 64) * sizeof(int32_t));
+  if (a->dtype == ADEPT_BF16 && a->n_tok <= 64) {
+    w.skinny_bytes = std::max({skinny_ws_bytes(3 * dq, a->d_model), skinny_ws_bytes(a->d_model, dq),
+                               skinny_ws_bytes(2 * a->d_ff, a->d_model),
+                               skinny_ws_bytes(a->d_model, a->d_ff)});
+    w.skinny = (float*)(p + off);
+    off += align256(w.skinny_bytes);
+  }
   if (a->dtype == ADEPT_F32) {
     const size_t cols = std::max({(size_t)3 * dq, (size_t)2 * a->d_ff, (size_t)a->d_model});
     w.gemm_tmp = (float*)(p + off);
@@ -39,6 +55,29 @@ LayerWs carve(const adept_layer_args* a, void* base) {
   }
   w.total = off;
   return w;
+}
+
+// Deferred KV generation, step 1: the row list 0..n_tok-1 with its count,
+// and the exit state of every row that exited at a layer of the other
+// parity than N copied into h[N & 1] (one wave per row, 16-byte copies; no
+// later kernel reads an exited row of that buffer, and the final head reads
+// the same values).
+__global__ __launch_bounds__(64) void defer_rows_kernel(int n_tok, int n_layers, int row_bytes,
+                                                        const int32_t* __restrict__ exit_layer,
+                                                        const char* __restrict__ h_other,
+                                                        char* __restrict__ h_last,
+                                                        int32_t* __restrict__ rows,
+                                                        int32_t* __restrict__ count) {
+  const int j = blockIdx.x;
+  if (threadIdx.x == 0) {
+    rows[j] = j;
+    if (j == 0) *count = n_tok;
+  }
+  const int e = exit_layer[j];
+  if (e >= n_layers || ((e ^ n_layers) & 1) == 0) return;
+  const int64_t base = (int64_t)j * row_bytes;
+  for (int o = threadIdx.x * 16; o < row_bytes; o += 64 * 16)
+    *reinterpret_cast<uint4*>(h_last + base + o) = *reinterpret_cast<const uint4*>(h_other + base + o);
 }
 
 adept_status run_gemm(adept_dtype dt, const GemmArgs& g, float* tmp, hipStream_t s) {
@@ -111,17 +150,18 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     g.rows = act; g.pos = a->pos; g.slot = a->slot;
     g.rope_cos = a->rope_cos; g.rope_sin = a->rope_sin; g.head_dim = hd; g.d_q = dq;
     g.q_out = a->q_buf; g.k_cache = kc; g.v_cache = vc; g.name = "gemm_qkv";
+    g.skinny_ws = ws.skinny; g.skinny_ws_bytes = ws.skinny_bytes;
     ADEPT_TRY(run_gemm(dt, g, ws.gemm_tmp, s));
     // 3. attention over the mixed cache
-    ADEPT_TRY(adept_attend(dt, H, hd, 1.0f / sqrtf((float)hd), 1, a->q_buf, act, nact, maxn,
-                           a->pos, a->seq, a->n_seq, kc, vc, a->s_max, nullptr, nullptr,
-                           a->attn_out, a->attn_tiles ? ws.attend : nullptr, ws.attend_bytes,
-                           stream));
+    ADEPT_TRY(attend_dispatch(dt, H, hd, 1.0f / sqrtf((float)hd), 1, a->q_buf, act, nact, maxn,
+                              a->pos, a->seq, a->n_seq, kc, vc, a->s_max, nullptr, nullptr,
+                              a->attn_out, ws.attend, ws.attend_bytes, a->attn_tiles != 0, s));
     // 4. output projection + residual: h[out] = h[in] + o Wo^T
     GemmArgs go{};
     go.M_max = maxn; go.M_dev = nact; go.N = D; go.K = dq;
     go.A = a->attn_out; go.lda = dq; go.B = wo; go.ldb = dq; go.epi = EPI_RESID;
     go.C = a->h[out]; go.ldc = D; go.resid = a->h[in]; go.rows = act; go.name = "gemm_o";
+    go.skinny_ws = ws.skinny; go.skinny_ws_bytes = ws.skinny_bytes;
     ADEPT_TRY(run_gemm(dt, go, ws.gemm_tmp, s));
     // 5. pre-FFN RMSNorm (gain folded into W_gate / W_up)
     ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[out], act, nact, maxn, ws.rinv, s));
@@ -131,12 +171,14 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     gu.A = a->h[out]; gu.a_rows = act; gu.lda = D; gu.B = wg; gu.B2 = wu; gu.ldb = D;
     gu.epi = EPI_SWIGLU; gu.row_scale = ws.rinv;
     gu.C = a->ffn_act; gu.ldc = F; gu.name = "gemm_gate_up";
+    gu.skinny_ws = ws.skinny; gu.skinny_ws_bytes = ws.skinny_bytes;
     ADEPT_TRY(run_gemm(dt, gu, ws.gemm_tmp, s));
     // 7. down projection + residual (in place on h[out])
     GemmArgs gd{};
     gd.M_max = maxn; gd.M_dev = nact; gd.N = D; gd.K = F;
     gd.A = a->ffn_act; gd.lda = F; gd.B = wd; gd.ldb = F; gd.epi = EPI_RESID;
     gd.C = a->h[out]; gd.ldc = D; gd.resid = a->h[out]; gd.rows = act; gd.name = "gemm_down";
+    gd.skinny_ws = ws.skinny; gd.skinny_ws_bytes = ws.skinny_bytes;
     ADEPT_TRY(run_gemm(dt, gd, ws.gemm_tmp, s));
   }
   // 8. exit test (Eq. 7-8)
@@ -146,8 +188,23 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   ADEPT_TRY(adept_compact(layer, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
                           a->exited, a->n_exited, a->exit_layer, ws.compact, ws.compact_bytes,
                           stream));
-  // 10. K/V of the skipped layers of the rows that exited here (Eq. 9)
-  if (layer < N && maxn > 0) {
+  // 10. K/V of the skipped layers of the rows that exited here (Eq. 9); in
+  //     decode, of every row that exited in the pass, after layer N
+  const bool defer = a->attn_tiles == 0;
+  if (defer && layer == N) {
+    const int rb = D * (dt == ADEPT_BF16 ? 2 : 4);
+    ADEPT_LAUNCH(defer_rows_kernel, dim3(a->n_tok), dim3(64), 0, s, a->n_tok, N, rb,
+                 a->exit_layer, (const char*)a->h[(N + 1) & 1], (char*)a->h[N & 1], ws.all_rows,
+                 ws.all_rows + a->n_tok);
+    ADEPT_CHECK_LAUNCH("defer_rows");
+    ADEPT_TRY(adept_kv_generate(dt, N, D, H, hd, a->rms_eps, a->h[N & 1], ws.all_rows,
+                                ws.all_rows + a->n_tok, a->n_tok, a->exit_layer, a->slot, a->pos,
+                                off(a->w_qkv, (int64_t)dq * D), (int64_t)3 * dq * D,
+                                nullptr, a->rope_cos, a->rope_sin, a->rope_max_pos,
+                                a->k_cache, a->v_cache, a->n_slots, ws.kvgen, ws.kvgen_bytes,
+                                stream));
+  }
+  if (!defer && layer < N && maxn > 0) {
     ADEPT_TRY(adept_kv_generate(dt, N, D, H, hd, a->rms_eps, a->h[out], a->exited, a->n_exited,
                                 maxn, a->exit_layer, a->slot, a->pos,
                                 off(a->w_qkv, (int64_t)dq * D), (int64_t)3 * dq * D,

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), f"{n} declared in adept.h but not exported"
     assert set(names) == set(B.EXPORTED), "binding signatures and header differ"
-    assert lib.adept_abi_version() == 1
+    assert lib.adept_abi_version() == 2
 
 
 def test_struct_layout_matches_header(tmp_path):
@@ -89,4 +89,7 @@ def test_workspace_queries_are_host_only():
     assert B.compact_workspace_bytes(1000) == 0          # one workgroup
     assert B.compact_workspace_bytes(1 << 20) > 0        # multi-pass tiles
     assert B.kv_generate_workspace_bytes(32, 4096) >= 4096 * 8
-    assert B.attend_workspace_bytes(16384, 8) >= (16384 // 128 + 8) * 8   # one int2 per query tile
+    assert B.attend_workspace_bytes(16384, 8, 32, 128, 2048) >= (16384 // 128 + 8) * 8  # query tiles
+    # decode: 64 queries x 32 heads, 16 key chunks of (max, sum, 128 partial outputs) in f32
+    assert B.attend_workspace_bytes(64, 64, 32, 128, 4352) == 64 * 32 * 16 * 130 * 4
+    assert B.attend_workspace_bytes(1 << 20, 1, 32, 128, 16384) < 64 << 20   # bounded

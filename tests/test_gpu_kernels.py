@@ -316,7 +316,7 @@ def _attend_case(dt, H, hd, n_seq, s_max, lens, frac_active, seed, causal=True, 
     out = torch.full((n + 3, H, hd), 123.0, dtype=TDT[dt], device=DEV)
     ws = None
     if with_ws:
-        wsb = B.attend_workspace_bytes(n, n_seq)
+        wsb = B.attend_workspace_bytes(n, n_seq, H, hd, s_max)
         ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
     B.attend(H, hd, dev(q, TDT[dt]), i32(active), count(n), n, i32(pos), i32(seq), n_seq,
              dev(kc, TDT[dt]), dev(vc, TDT[dt]), s_max, out, causal=causal,
@@ -345,6 +345,21 @@ def test_attend_prefill_mfma_matches_oracle(hd, n_seq, s_max, frac):
     assert np.max(np.abs(got - ref)) <= 2e-2, np.max(np.abs(got - ref))
 
 
+@pytest.mark.parametrize("hd,lens,decode,causal,live,H", [
+    (128, [1000, 999, 513, 64, 1], True, True, False, 4),   # decode, ragged, 1-key sequence
+    (64, [700, 255, 256, 257], True, True, False, 6),       # decode, chunk-boundary lengths
+    (64, [512, 300, 77], False, False, True, 2),           # bidirectional over live keys
+    (128, [130, 20], False, True, False, 3),                # few causal queries per sequence
+])
+def test_attend_split_matches_oracle(hd, lens, decode, causal, live, H):
+    """bf16 key-chunked kernel (one or few queries per sequence, bidirectional)."""
+    say(f"attend split hd={hd} lens={lens} decode={decode} causal={causal} live={live}")
+    n_seq, s_max = len(lens), max(lens)
+    got, ref = _attend_case("bf16", H, hd, n_seq, s_max, lens, 0.02 if causal and not decode
+                            else 0.5, 23 + hd, causal=causal, live=live, decode=decode)
+    assert np.max(np.abs(got - ref)) <= 2e-2, np.max(np.abs(got - ref))
+
+
 @pytest.mark.parametrize("dt,decode,causal,live", [("f32", False, True, False),
                                                    ("f32", True, True, False),
                                                    ("bf16", True, True, False),
@@ -360,3 +375,42 @@ def test_attend_generic_matches_oracle(dt, decode, causal, live):
         assert np.max(np.abs(got - ref)) <= 1e-5 * np.max(np.abs(ref))
     else:
         assert np.max(np.abs(got - ref)) <= 2e-2
+
+
+def test_attend_decode_full_shape_sampled():
+    """7B-shaped decode attention: 64 sequences, 32 heads x 128, contexts of
+    4097..4352 keys (a 4096-token prompt plus up to 256 generated tokens), the
+    launch the decode step makes (key chunks + merge).  Caches come from the
+    seeded device generator; slots past each context are NaN (never read).
+    Sampled (query, head) pairs are checked against the oracle."""
+    n_seq, H, hd, s_max = 64, 32, 128, 4352
+    say(f"attend decode full shape n_seq={n_seq} H={H} hd={hd} s_max={s_max}")
+    g = torch.Generator(device=DEV).manual_seed(41)
+    kc = torch.randn((n_seq * s_max, H, hd), generator=g, device=DEV).to(torch.bfloat16)
+    vc = torch.randn((n_seq * s_max, H, hd), generator=g, device=DEV).to(torch.bfloat16)
+    q = torch.randn((n_seq, H, hd), generator=g, device=DEV).to(torch.bfloat16)
+    rng = np.random.default_rng(41)
+    lens = rng.integers(4097, s_max + 1, n_seq)
+    lens[0], lens[1] = 4097, s_max
+    for b in range(n_seq):
+        kc[b * s_max + int(lens[b]):(b + 1) * s_max] = float("nan")
+        vc[b * s_max + int(lens[b]):(b + 1) * s_max] = float("nan")
+    pos = (lens - 1).astype(np.int32)
+    seq = np.arange(n_seq, dtype=np.int32)
+    out = torch.full((n_seq, H, hd), 123.0, dtype=torch.bfloat16, device=DEV)
+    ws = torch.empty(B.attend_workspace_bytes(n_seq, n_seq, H, hd, s_max), dtype=torch.uint8,
+                     device=DEV)
+    B.attend(H, hd, q, i32(seq), count(n_seq), n_seq, i32(pos), i32(seq), n_seq, kc, vc, s_max,
+             out, causal=True, workspace=ws)
+    torch.cuda.synchronize()
+    got = host64(out)
+    assert np.isfinite(got).all()
+    for b, h in [(0, 0), (1, 31), (2, 5), (17, 17), (33, 9), (63, 30)] + \
+            [(int(x), int(y)) for x, y in zip(rng.integers(0, n_seq, 10), rng.integers(0, H, 10))]:
+        L = int(lens[b])
+        ks = host64(kc[b * s_max:b * s_max + L, h:h + 1])
+        vs = host64(vc[b * s_max:b * s_max + L, h:h + 1])
+        ref = O.attend(host64(q[b:b + 1, h:h + 1]), ks, vs, np.array([0]), np.array([L - 1]))
+        assert np.max(np.abs(got[b, h] - ref[0, 0])) <= 2e-2, (b, h)
+    del kc, vc
+    torch.cuda.empty_cache()
