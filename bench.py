@@ -75,6 +75,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-generation", action="store_true",
                     help="skip the generation run (batch 64, 4096-token context, decode steps)")
+    ap.add_argument("--no-classification", action="store_true",
+                    help="skip the BERT-base classification run (64 x 512 tokens)")
     ap.add_argument("--gen-batch", type=int, default=64)
     ap.add_argument("--gen-context", type=int, default=4096)
     ap.add_argument("--gen-steps", type=int, default=256)
@@ -250,6 +252,11 @@ def main():
         del cache, ids
         torch.cuda.empty_cache()
         out["generation"] = generation(args, model, shape, ai, B, torch, np)
+
+    if not args.no_classification:
+        del model
+        torch.cuda.empty_cache()
+        out["classification"] = classification(args, ai, B, torch, np)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args, shape, ai, np)
@@ -475,6 +482,74 @@ def generation(args, model, shape, ai, B, torch, np):
     del cache
     torch.cuda.empty_cache()
     return out
+
+
+def classification(args, ai, B, torch, np, reps=5):
+    """BERT-base-shaped encoder classification with token-level exit: batch
+    64 x 512 uniform-random tokens, global metric at --delta; also the no-exit
+    pass (delta = +inf) and a fixed schedule (exit layer uniform in 3..11 of
+    12 per token, seeded) that shows the exit path's cost and benefit."""
+    from paper_2601_03700_amd.model import EncoderModel
+    shape = ai.BERT_BASE
+    N = shape.n_layers
+    Bn, T = 64, 512
+    n = Bn * T
+    t0 = time.time()
+    model = EncoderModel(shape, ai.encoder_weights(shape, seed=17, dtype="bf16"))
+    ids = torch.from_numpy(ai.token_ids(18, shape.vocab, Bn, T)).cuda()
+    log(f"classification: weights ready in {time.time() - t0:.1f}s")
+
+    def run(delta, force=None, timing=False):
+        cfg = B.exit_cfg(delta, N, args.metric)
+        out = model.classify(ids, cfg, force_layer=force)
+        st = out.state
+        out = model.classify(ids, cfg, force_layer=force, state=st)
+        torch.cuda.synchronize()
+        if timing:
+            B.timing_reset()
+            B.timing_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            out = model.classify(ids, cfg, force_layer=force, state=st)
+        e1.record()
+        torch.cuda.synchronize()
+        kern = None
+        if timing:
+            B.timing_enable(False)
+            kern = B.timing_read()
+        return e0.elapsed_time(e1) / reps, out, kern
+
+    ms, out, _ = run(args.delta)
+    _, _, kern = run(args.delta, timing=True)     # per-kernel HIP events (separate run)
+    el = out.exit_layer.to(torch.int64)
+    ms_inf, _, _ = run(math.inf)
+    sched = torch.from_numpy(ai.forced_exit_layers(19, n, 3, N - 1)).cuda()
+    ms_f, out_f, _ = run(math.inf, force=sched)
+    el_f = out_f.exit_layer.to(torch.int64)
+    res = {
+        "workload": (f"BERT-base-shaped encoder classification (12 layers, width 768, 12x64 heads, "
+                     f"GELU FFN 3072, 2-class head on [CLS]), batch {Bn} x {T}, token-level exit "
+                     f"({args.metric} metric, delta {args.delta})"),
+        "sequences_per_s": Bn / (ms / 1e3), "tokens_per_s": n / (ms / 1e3), "ms_per_pass": ms,
+        "exit_fraction": float((el < N).to(torch.float64).mean()),
+        "no_exit": {"sequences_per_s": Bn / (ms_inf / 1e3), "ms_per_pass": ms_inf},
+        "fixed_schedule": {
+            "schedule": "exit layer uniform in 3..11 per token (seeded)",
+            "sequences_per_s": Bn / (ms_f / 1e3), "ms_per_pass": ms_f,
+            "speedup_vs_no_exit": ms_inf / ms_f,
+            "active_rows_per_layer": [int((el_f >= i).sum()) for i in range(1, N + 1)],
+            "cls_exit_layer_histogram": np.bincount(out_f.cls_exit_layer.cpu().numpy(),
+                                                    minlength=N + 1)[1:].tolist()},
+        "kernels": {k: {"launches": c, "avg_us": t * 1e3 / c,
+                        "share": t / sum(x[1] for x in kern.values())}
+                    for k, (c, t) in sorted(kern.items(), key=lambda kv: -kv[1][1])[:10]},
+    }
+    log(f"classification: {ms:.2f} ms/pass ({Bn / (ms / 1e3):.0f} seq/s), no-exit {ms_inf:.2f}, "
+        f"fixed schedule {ms_f:.2f} ms")
+    del model
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(args, shape, ai, np):

@@ -171,9 +171,9 @@ adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_model, int n_
  *  workspace: adept_attend_workspace_bytes(max_active, n_seq, H, hd, s_max)
  *      bytes (at most about 17 MB), 16-byte aligned; nullable, but then bf16
  *      takes the slow generic kernel.  bf16 with hd 64/128 uses query tiles on
- *      MFMA when the queries average at least 4 per sequence (causal, no
- *      key_live: prefill), otherwise key chunks streamed per (query, head)
- *      and merged (decode, bidirectional).
+ *      MFMA when the queries average at least 4 per sequence (prefill,
+ *      classification), otherwise key chunks streamed per (query, head) and
+ *      merged (decode).
  * ------------------------------------------------------------------------- */
 size_t adept_attend_workspace_bytes(int max_active, int n_seq, int n_heads, int head_dim,
                                     int s_max);
@@ -288,6 +288,88 @@ adept_status adept_token_init(int n_tok, int n_layers, int d_model, int32_t* act
 /* Greedy next token: out[k] = argmax_v logits[k][v] for k < n, ties to the
  * lowest id (support step of the generation loop). */
 adept_status adept_argmax(int n, int vocab, const float* logits, int32_t* out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Classification mode (Section 4.3, downstream tasks): token-level exit in a
+ * post-norm encoder (BERT-style: biases, LayerNorm, GELU, learned positions).
+ * Exited tokens stop and leave the key set of every later layer; there is no
+ * KV generation.  A sequence's output is its first ([CLS]) row at that row's
+ * exit layer.  bf16 only.  Rows are j = b*seq_len + p for n_seq sequences.
+ *
+ * adept_encoder_layer_step(layer=i) enqueues, for the rows of
+ * active[(i-1)&1]: QKV GEMM + bias (Q into q_buf, K/V into k_buf/v_buf at
+ * row j) -> attention of each row over the rows of its sequence whose
+ * key_live byte is 1 (bidirectional, keys < key_len[b]) -> O GEMM + bias +
+ * residual into y_buf -> LayerNorm 1 (in place) -> GEMM + bias + GELU into
+ * ffn_act -> GEMM + bias + residual into h[i&1] -> LayerNorm 2 (in place)
+ * -> adept_exit_test -> adept_compact -> key_live[row] = 0 for the rows that
+ * exited.  Before layer 1 the caller runs adept_encoder_embed into h[0],
+ * adept_token_init, and sets key_live to 1 for every row.  A row's final
+ * state is h[exit_layer & 1][row].
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int32_t dtype;        /* ADEPT_BF16 */
+  int32_t n_layers, d_model, n_heads, head_dim, d_ff;
+  float ln_eps;
+  adept_exit_cfg exit;
+  /* weights stacked over layers, nn.Linear [out][in] order (bf16) */
+  const void* w_qkv;    /* [N][3*H*hd][D]: Wq rows, Wk rows, Wv rows */
+  const void* b_qkv;    /* [N][3*H*hd] */
+  const void* w_o;      /* [N][D][H*hd] */
+  const void* b_o;      /* [N][D] */
+  const void* ln1_g;    /* [N][D] */
+  const void* ln1_b;    /* [N][D] */
+  const void* w_in;     /* [N][F][D] */
+  const void* b_in;     /* [N][F] */
+  const void* w_out;    /* [N][D][F] */
+  const void* b_out;    /* [N][D] */
+  const void* ln2_g;    /* [N][D] */
+  const void* ln2_b;    /* [N][D] */
+  int32_t n_tok, n_seq, seq_len;   /* n_tok = n_seq * seq_len */
+  int32_t reserved;
+  void* h[2];            /* [n_tok][D] residual stream ping-pong */
+  float* inertia;        /* [n_tok][D] (GLOBAL metric) */
+  const int32_t* pos;    /* [n_tok] position of row j (j mod seq_len) */
+  const int32_t* seq;    /* [n_tok] sequence of row j */
+  int32_t* active[2];    /* [n_tok] ping-pong active lists */
+  int32_t* n_active[2];  /* device counts */
+  int32_t* exited;       /* [n_tok] rows that exited at this layer */
+  int32_t* n_exited;
+  int32_t* exit_layer;   /* [n_tok] */
+  uint8_t* exit_flag;    /* [n_tok] */
+  double* sim_out;       /* [n_tok] nullable */
+  const int32_t* force_layer;  /* [n_tok] nullable, as in adept_exit_test */
+  uint8_t* key_live;     /* [n_tok]: 1 while the row is a key (not exited) */
+  const int32_t* key_len;      /* [n_seq] keys per sequence (normally seq_len) */
+  void* k_buf;           /* [n_tok][H*hd] this layer's K of the active rows */
+  void* v_buf;           /* [n_tok][H*hd] */
+  void* q_buf;           /* [n_tok][H*hd] (compact order) */
+  void* attn_out;        /* [n_tok][H*hd] (compact order) */
+  void* y_buf;           /* [n_tok][D] attention sub-layer output */
+  void* ffn_act;         /* [n_tok][F] (compact order) */
+  void* workspace;       /* adept_encoder_workspace_bytes(), 256-byte aligned */
+  size_t workspace_bytes;
+} adept_encoder_args;
+
+size_t adept_encoder_workspace_bytes(const adept_encoder_args* a);
+adept_status adept_encoder_layer_step(const adept_encoder_args* a, int layer, void* stream);
+
+/* h0[j] = LayerNorm(word_emb[ids[j]] + pos_emb[pos[j]] + type_emb) * ln_g + ln_b
+ * (token type 0 for every row; f32 statistics; ids and positions clamped
+ * into the tables).  word_emb [vocab][D], pos_emb [max_pos][D], type_emb,
+ * ln_g, ln_b [D], out [n][D] (bf16). */
+adept_status adept_encoder_embed(int n, int d_model, int vocab, int max_pos, float eps,
+                                 const int32_t* ids, const int32_t* pos, const void* word_emb,
+                                 const void* pos_emb, const void* type_emb, const void* ln_g,
+                                 const void* ln_b, void* out, void* stream);
+
+/* Linear head on each sequence's [CLS] row at its exit (Section 4.3):
+ * logits[b][c] = h[exit_layer[r] & 1][r] . w_cls[c] + b_cls[c], r = b*seq_len.
+ * w_cls [n_classes][D], b_cls [n_classes] nullable (bf16); logits f32. */
+adept_status adept_classify_head(int n_seq, int seq_len, int d_model, int n_classes,
+                                 const void* h0, const void* h1, const int32_t* exit_layer,
+                                 const void* w_cls, const void* b_cls, float* logits,
+                                 void* stream);
 
 /* Kernel timing for measurement runs.  While enabled, every kernel the
  * library launches is bracketed by two HIP events on its own stream, and

@@ -52,6 +52,23 @@ class LayerArgs(ctypes.Structure):
     ]
 
 
+class EncoderArgs(ctypes.Structure):
+    _fields_ = [
+        ("dtype", _i32), ("n_layers", _i32), ("d_model", _i32), ("n_heads", _i32),
+        ("head_dim", _i32), ("d_ff", _i32), ("ln_eps", ctypes.c_float), ("exit", ExitCfg),
+        ("w_qkv", _vp), ("b_qkv", _vp), ("w_o", _vp), ("b_o", _vp), ("ln1_g", _vp),
+        ("ln1_b", _vp), ("w_in", _vp), ("b_in", _vp), ("w_out", _vp), ("b_out", _vp),
+        ("ln2_g", _vp), ("ln2_b", _vp),
+        ("n_tok", _i32), ("n_seq", _i32), ("seq_len", _i32), ("reserved", _i32),
+        ("h", _vp * 2), ("inertia", _vp), ("pos", _vp), ("seq", _vp),
+        ("active", _vp * 2), ("n_active", _vp * 2), ("exited", _vp), ("n_exited", _vp),
+        ("exit_layer", _vp), ("exit_flag", _vp), ("sim_out", _vp), ("force_layer", _vp),
+        ("key_live", _vp), ("key_len", _vp), ("k_buf", _vp), ("v_buf", _vp), ("q_buf", _vp),
+        ("attn_out", _vp), ("y_buf", _vp), ("ffn_act", _vp),
+        ("workspace", _vp), ("workspace_bytes", _sz),
+    ]
+
+
 _SIGS = {
     "adept_abi_version": (_i32, []),
     "adept_last_error": (ctypes.c_char_p, []),
@@ -75,6 +92,11 @@ _SIGS = {
     "adept_argmax": (_i32, [_i32, _i32, _vp, _vp, _vp]),
     "adept_token_init": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "adept_fold_gain": (_i32, [_i32, _i32, _i32, _i32, _vp, _i64, _vp, _i64, _vp]),
+    "adept_encoder_workspace_bytes": (_sz, [ctypes.POINTER(EncoderArgs)]),
+    "adept_encoder_layer_step": (_i32, [ctypes.POINTER(EncoderArgs), _i32, _vp]),
+    "adept_encoder_embed": (_i32, [_i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp, _vp, _vp,
+                                   _vp, _vp, _vp, _vp, _vp]),
+    "adept_classify_head": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "adept_timing_enable": (_i32, [_i32]),
     "adept_timing_reset": (None, []),
     "adept_timing_count": (_i32, []),
@@ -233,6 +255,30 @@ def timing_enable(on=True):
 
 def timing_reset():
     lib().adept_timing_reset()
+
+
+def encoder_workspace_bytes(args):
+    return lib().adept_encoder_workspace_bytes(ctypes.byref(args))
+
+
+def encoder_layer_step(args, layer, stream=None):
+    _check(lib().adept_encoder_layer_step(ctypes.byref(args), layer, stream_handle(stream)),
+           "adept_encoder_layer_step")
+
+
+def encoder_embed(n, d_model, vocab, max_pos, eps, ids, pos, word_emb, pos_emb, type_emb, ln_g,
+                  ln_b, out, stream=None):
+    _check(lib().adept_encoder_embed(n, d_model, vocab, max_pos, eps, ptr(ids), ptr(pos),
+                                     ptr(word_emb), ptr(pos_emb), ptr(type_emb), ptr(ln_g),
+                                     ptr(ln_b), ptr(out), stream_handle(stream)),
+           "adept_encoder_embed")
+
+
+def classify_head(n_seq, seq_len, d_model, n_classes, h0, h1, exit_layer, w_cls, b_cls, logits,
+                  stream=None):
+    _check(lib().adept_classify_head(n_seq, seq_len, d_model, n_classes, ptr(h0), ptr(h1),
+                                     ptr(exit_layer), ptr(w_cls), ptr(b_cls), ptr(logits),
+                                     stream_handle(stream)), "adept_classify_head")
 
 
 def timing_read():

@@ -3,8 +3,10 @@
 // from an earlier exit state (Section 3, Eq. 5; Section 4.3).  The kernels do
 // not distinguish the two: a generated entry is an ordinary cache row.
 //
-// Prefill (bf16, head_dim 64/128, causal): a plan kernel cuts the compacted
-// query list into tiles of <= 128 consecutive entries of one sequence; a
+// Query tiles (bf16, head_dim 64/128; prefill, and the bidirectional
+// attention of classification over the live keys): a plan kernel cuts the
+// compacted query list into tiles of <= 128 consecutive entries of one
+// sequence; a
 // 256-thread workgroup takes one (tile, head), each wave two groups of 16
 // queries, so every K/V fragment read from LDS feeds two MFMAs.  Key
 // blocks of 64 rows are staged in LDS (K row-major, V transposed with packed
@@ -15,9 +17,9 @@
 // in the B-operand layout of O^T += V^T P^T (the order of keys inside an
 // MFMA's reduction is free, so V^T is read in the same key order).
 //
-// Generic path (f32, decode with one query per sequence, bidirectional
-// attention with a live-key mask): one workgroup per (query, head), scores
-// for all keys in LDS, exact softmax, then a weighted sum of V rows.
+// Key chunks (bf16, few queries per sequence: decode): see
+// attend_split_kernel.  Generic path (f32): one workgroup per (query, head),
+// scores for all keys in LDS, exact softmax, then a weighted sum of V rows.
 #include <algorithm>
 
 #include "common.h"
@@ -139,11 +141,15 @@ __global__ __launch_bounds__(1024) void attend_plan_kernel(const int32_t* __rest
 // ---------------------------------------------------------------------------
 // prefill MFMA kernel
 // ---------------------------------------------------------------------------
+// causal: keys 0..pos of each query; else keys 0..key_len[b]-1 of the
+// sequence, all of them for every query (bidirectional).  key_live
+// (nullable) drops keys whose byte is 0.
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
-    int H, float scale_log2, const bf16* __restrict__ q, const int32_t* __restrict__ rows,
-    const int32_t* __restrict__ pos, const int32_t* __restrict__ seq,
-    const bf16* __restrict__ kc, const bf16* __restrict__ vc, int s_max,
+    int H, float scale_log2, int causal, const bf16* __restrict__ q,
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ pos,
+    const int32_t* __restrict__ seq, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
+    int s_max, const int32_t* __restrict__ key_len, const uint8_t* __restrict__ key_live,
     const int2* __restrict__ tiles, const int32_t* __restrict__ n_tiles, bf16* __restrict__ out) {
   constexpr int KLD = HD + 8;     // sK row stride (elements)
   constexpr int VLD = KB + 8;     // sVt row stride
@@ -152,6 +158,7 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
   constexpr int QG = QT / 64;     // 16-query groups per wave
   __shared__ __attribute__((aligned(16))) bf16 sK[KB * KLD];
   __shared__ __attribute__((aligned(16))) bf16 sVt[HD * VLD];
+  __shared__ uint8_t sLive[KB];
   const int nt = *n_tiles;
   if ((int)blockIdx.x >= nt) return;
   const int2 tile = tiles[nt - 1 - blockIdx.x];   // longest (latest) tiles first
@@ -161,7 +168,8 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
   const int64_t rs = (int64_t)H * HD;
 
   const int b = seq[rows[tile.x]];
-  const int pmax = pos[rows[tile.x + tile.y - 1]];
+  // keys [0, tend) are read; causal queries mask t > pos themselves
+  const int tend = causal ? pos[rows[tile.x + tile.y - 1]] + 1 : min(key_len[b], s_max);
   const int64_t kbase = (int64_t)b * s_max;
 
   // this lane's queries: column c16 of each of the wave's QG groups of 16
@@ -175,7 +183,7 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     const int qi = (wave * QG + qg) * 16 + c16;
     qvalid[qg] = qi < tile.y;
     qk[qg] = tile.x + (qvalid[qg] ? qi : 0);
-    qpos[qg] = qvalid[qg] ? pos[rows[qk[qg]]] : -1;
+    qpos[qg] = qvalid[qg] ? (causal ? pos[rows[qk[qg]]] : tend - 1) : -1;
 #pragma unroll
     for (int s = 0; s < DS; ++s) {
       const uint4 v =
@@ -188,17 +196,18 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     l_run[qg] = 0.0f;
   }
 
-  const int nkb = pmax / KB + 1;
+  const int nkb = (tend + KB - 1) / KB;
   for (int kb = 0; kb < nkb; ++kb) {
     const int t0 = kb * KB;
-    // ---- stage K [64][HD] row-major; keys past pmax are zero
+    if (tid < KB) sLive[tid] = (t0 + tid < tend && (!key_live || key_live[kbase + t0 + tid])) ? 1 : 0;
+    // ---- stage K [64][HD] row-major; keys past the range are zero
     constexpr int CH = HD / 8;  // 16-byte chunks per row
 #pragma unroll
     for (int e = tid; e < KB * CH; e += 256) {
       const int r = e / CH, c = (e % CH) * 8;
       const int t = t0 + r;
       uint4 kv = make_uint4(0, 0, 0, 0);
-      if (t <= pmax) kv = *reinterpret_cast<const uint4*>(kc + (kbase + t) * rs + h * HD + c);
+      if (t < tend) kv = *reinterpret_cast<const uint4*>(kc + (kbase + t) * rs + h * HD + c);
       *reinterpret_cast<uint4*>(sK + r * KLD + c) = kv;
     }
     // ---- stage V^T [HD][64]: a thread takes 4 keys x 8 dims and writes eight
@@ -211,7 +220,7 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
       for (int kk = 0; kk < 4; ++kk) {
         const int t = t0 + 4 * kg + kk;
         uint4 vv = make_uint4(0, 0, 0, 0);
-        if (t <= pmax) vv = *reinterpret_cast<const uint4*>(vc + (kbase + t) * rs + h * HD + dc * 8);
+        if (t < tend) vv = *reinterpret_cast<const uint4*>(vc + (kbase + t) * rs + h * HD + dc * 8);
         w[kk][0] = vv.x; w[kk][1] = vv.y; w[kk][2] = vv.z; w[kk][3] = vv.w;
       }
 #pragma unroll
@@ -249,9 +258,9 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
       for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int t = t0 + sb * 16 + g * 4 + v;
+          const int kl = sb * 16 + g * 4 + v;
           float x = s[qg][sb][v] * scale_log2;
-          x = (t <= qpos[qg]) ? x : -INFINITY;
+          x = (t0 + kl <= qpos[qg] && sLive[kl]) ? x : -INFINITY;
           s[qg][sb][v] = x;
           mloc = fmaxf(mloc, x);
         }
@@ -532,7 +541,7 @@ adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float sc
   }
   const float sl = scale * 1.4426950408889634f;   // scores in the exp2 domain
   // query tiles pay off when the queries of a sequence are many (prefill)
-  if (fast && allow_tiles && causal && !key_live && max_active >= 4 * n_seq) {
+  if (fast && allow_tiles && max_active >= 4 * n_seq) {
     int32_t* n_tiles = (int32_t*)workspace;
     int2* tiles = (int2*)((char*)workspace + 256);
     const int max_tiles = max_active / QT + n_seq + 1;
@@ -541,13 +550,13 @@ adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float sc
     ADEPT_CHECK_LAUNCH("attend_plan");
     dim3 grid(max_tiles, n_heads);
     if (head_dim == 128)
-      ADEPT_LAUNCH(attend_prefill_kernel<128>, grid, dim3(256), 0, s, n_heads, sl,
+      ADEPT_LAUNCH(attend_prefill_kernel<128>, grid, dim3(256), 0, s, n_heads, sl, causal,
                    (const bf16*)q, rows, pos, seq, (const bf16*)k_layer, (const bf16*)v_layer,
-                   s_max, tiles, n_tiles, (bf16*)out);
+                   s_max, key_len, key_live, tiles, n_tiles, (bf16*)out);
     else
-      ADEPT_LAUNCH(attend_prefill_kernel<64>, grid, dim3(256), 0, s, n_heads, sl,
+      ADEPT_LAUNCH(attend_prefill_kernel<64>, grid, dim3(256), 0, s, n_heads, sl, causal,
                    (const bf16*)q, rows, pos, seq, (const bf16*)k_layer, (const bf16*)v_layer,
-                   s_max, tiles, n_tiles, (bf16*)out);
+                   s_max, key_len, key_live, tiles, n_tiles, (bf16*)out);
     return launch_status("attend_prefill");
   }
   if (fast) {

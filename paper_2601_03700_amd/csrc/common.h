@@ -126,10 +126,12 @@ adept_status rmsnorm_rows(adept_dtype dt, int d, float eps, const void* x, const
 // GEMM epilogue kinds.
 enum EpiKind {
   EPI_STORE = 0,   // C[k][n] (dtype or float) compact
-  EPI_QKV = 1,     // RoPE on Q and K columns; Q -> q_out[k], K/V -> cache slot of rows[k]
+  EPI_QKV = 1,     // RoPE on Q and K columns (none when rope_cos is NULL); Q -> q_out[k],
+                   // K/V -> cache slot of rows[k]
   EPI_RESID = 2,   // out[rows[k]][n] = resid[rows[k]][n] + acc
   EPI_SWIGLU = 3,  // B = (gate, up) interleaved per 64 columns; out[k][n] = silu(g) * u
   EPI_KV = 4,      // K/V-only variant of EPI_QKV (KV generation, per-layer groups)
+  EPI_GELU = 5,    // C[k][n] = gelu(acc) (exact erf form), dtype
 };
 
 struct GemmArgs {
@@ -146,10 +148,11 @@ struct GemmArgs {
   // epilogue operands
   void* C; int64_t ldc; int c_f32;
   const float* row_scale; // per-row scale of the accumulators (1/rms of the row), nullable
+  const void* bias;       // [N] (dtype) added after the row scale, before the epilogue; nullable
   const int32_t* rows;    // token row of compact index k (QKV/RESID/KV)
   const void* resid;      // RESID source (may equal C)
   const int32_t* pos;     // [n_tok]
-  const int32_t* slot;    // [n_tok]
+  const int32_t* slot;    // [n_tok] cache slot of a row (nullable: the row itself)
   const float* rope_cos; const float* rope_sin;
   int head_dim, d_q;
   void* q_out; void* k_cache; void* v_cache;   // caches already offset to the layer

@@ -83,6 +83,7 @@ struct GP {
   const float* row_scale;   // [compact m] or nullptr
   const int32_t* rows;
   const bf16* resid;
+  const bf16* bias;         // [N] or nullptr
   const int32_t* pos;
   const int32_t* slot;
   const float* rope_cos;
@@ -105,6 +106,18 @@ struct GP {
 // the bf16 rounding of the output)
 __device__ __forceinline__ float silu(float g) {
   return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+}
+
+// x * Phi(x) with the exact erf form of the normal CDF
+__device__ __forceinline__ float gelu_erf(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.7071067811865476f));
+}
+
+// Four bias values of columns c..c+3 (zeros when there is no bias).
+__device__ __forceinline__ float4 bias4(const bf16* b, int64_t c) {
+  if (!b) return make_float4(0.f, 0.f, 0.f, 0.f);
+  const bf16x4_t v = *reinterpret_cast<const bf16x4_t*>(b + c);
+  return make_float4(bf2f(v[0]), bf2f(v[1]), bf2f(v[2]), bf2f(v[3]));
 }
 
 __device__ __forceinline__ void dma16(const bf16* g, char* l) {
@@ -344,8 +357,8 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
         mrow[lr] = p.rows[mc];
       } else if (kCache) {
         const int row = GROUPED ? p.srows[mc] : p.rows[mc];
-        mrow[lr] = is_q ? 0 : p.slot[row];
-        mpos[lr] = is_v ? 0 : p.pos[row];
+        mrow[lr] = is_q ? 0 : (p.slot ? p.slot[row] : row);
+        mpos[lr] = (is_v || !p.rope_cos) ? 0 : p.pos[row];
       }
     }
   }
@@ -399,6 +412,9 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
         // G (4 for the rotary epilogues, whose rounds hold 4 float4 each)
         constexpr bool kRope = EPI == EPI_QKV || EPI == EPI_KV;
         constexpr int G = kRope ? 4 : 8;
+        const bool rope = kRope && !is_v && p.rope_cos;   // wave-uniform
+        const float4 bx = bias4(p.bias, nw + c4);
+        const float4 by = rope ? bias4(p.bias, nw + (c4 ^ half)) : bx;
 #pragma unroll
         for (int hh = 0; hh < 16 / G; ++hh) {
           float4 x4[G], y4[G], cs[G], sn[G];
@@ -409,7 +425,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
           for (int r = 0; r < G; ++r) {
             const int lr = 2 * (G * hh + r) + (lane >> 5);
             x4[r] = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + c4);
-            if (kRope && !is_v)
+            if (rope)
               y4[r] = *reinterpret_cast<const float4*>(stg + lr * kEpiStride + (c4 ^ half));
             sc[r] = msc[i * 32 + lr];
             mr[r] = mrow[i * 32 + lr];
@@ -419,7 +435,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
           for (int r = 0; r < G; ++r) {
             if (EPI == EPI_RESID)
               rv[r] = *reinterpret_cast<const bf16x4_t*>(p.resid + (int64_t)mr[r] * p.ldc + nw + c4);
-            if (kRope && !is_v) {
+            if (rope) {
               const int c = (cbase + c4) & (hd - 1);
               const int64_t t = (int64_t)mp[r] * half + (c & (half - 1));
               cs[r] = *reinterpret_cast<const float4*>(p.rope_cos + t);
@@ -429,10 +445,16 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
 #pragma unroll
           for (int r = 0; r < G; ++r) {
             const int m = mb + 2 * (G * hh + r) + (lane >> 5);
-            const float x[4] = {x4[r].x * sc[r], x4[r].y * sc[r], x4[r].z * sc[r],
-                                x4[r].w * sc[r]};
+            const float x[4] = {x4[r].x * sc[r] + bx.x, x4[r].y * sc[r] + bx.y,
+                                x4[r].z * sc[r] + bx.z, x4[r].w * sc[r] + bx.w};
             bf16x4_t o;
-            if (EPI == EPI_STORE) {
+            if (EPI == EPI_GELU) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) o[e] = f2bf(gelu_erf(x[e]));
+              if (!kCheck || m < M)
+                *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc +
+                                             nw + c4) = o;
+            } else if (EPI == EPI_STORE) {
               const int64_t off = (int64_t)m * p.ldc + nw + c4;
               if (!kCheck || m < M) {
                 if (p.c_f32) {
@@ -451,13 +473,13 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
                 *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) +
                                              (int64_t)mr[r] * p.ldc + nw + c4) = o;
             } else {  // EPI_QKV / EPI_KV
-              if (is_v) {
+              if (!rope) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
               } else {
                 // rotate-half RoPE: column c pairs with c +- hd/2 of the same head
-                const float y[4] = {y4[r].x * sc[r], y4[r].y * sc[r], y4[r].z * sc[r],
-                                    y4[r].w * sc[r]};
+                const float y[4] = {y4[r].x * sc[r] + by.x, y4[r].y * sc[r] + by.y,
+                                    y4[r].z * sc[r] + by.z, y4[r].w * sc[r] + by.w};
                 const int c = (cbase + c4) & (hd - 1);   // column within the head
                 const float cv[4] = {cs[r].x, cs[r].y, cs[r].z, cs[r].w};
                 const float sv[4] = {sn[r].x, sn[r].y, sn[r].z, sn[r].w};
@@ -755,9 +777,14 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
   if (m >= M) return;
   const float sc = p.row_scale ? p.row_scale[m] : 1.0f;
   const float4 x4 = skinny_sum(part, S, Nt, m, n);
-  const float x[4] = {x4.x * sc, x4.y * sc, x4.z * sc, x4.w * sc};
+  const float4 bx = bias4(p.bias, n);
+  const float x[4] = {x4.x * sc + bx.x, x4.y * sc + bx.y, x4.z * sc + bx.z, x4.w * sc + bx.w};
   bf16x4_t o;
-  if (EPI == EPI_STORE) {
+  if (EPI == EPI_GELU) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = f2bf(gelu_erf(x[e]));
+    *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc + n) = o;
+  } else if (EPI == EPI_STORE) {
     const int64_t off = (int64_t)m * p.ldc + n;
     if (p.c_f32) {
       *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + off) =
@@ -784,8 +811,9 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
     const int row = p.rows[m];
     const bool is_v = sec == 2;
     bf16* dst = sec == 0 ? p.q_out + (int64_t)m * p.d_q
-                         : (is_v ? p.v_cache : p.k_cache) + (int64_t)p.slot[row] * p.d_q;
-    if (is_v) {
+                         : (is_v ? p.v_cache : p.k_cache) +
+                               (int64_t)(p.slot ? p.slot[row] : row) * p.d_q;
+    if (is_v || !p.rope_cos) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e]);
     } else {
@@ -793,7 +821,8 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
       const int hd = p.head_dim, half = hd >> 1;
       const int c = cin & (hd - 1);
       const float4 y4 = skinny_sum(part, S, Nt, m, n ^ half);
-      const float y[4] = {y4.x * sc, y4.y * sc, y4.z * sc, y4.w * sc};
+      const float4 by = bias4(p.bias, n ^ half);
+      const float y[4] = {y4.x * sc + by.x, y4.y * sc + by.y, y4.z * sc + by.z, y4.w * sc + by.w};
       const int64_t t = (int64_t)p.pos[row] * half + (c & (half - 1));
       const float4 cs = *reinterpret_cast<const float4*>(p.rope_cos + t);
       const float4 sn = *reinterpret_cast<const float4*>(p.rope_sin + t);
@@ -840,10 +869,13 @@ GP to_gp(const GemmArgs& g) {
   p.B = (const bf16*)g.B; p.B2 = (const bf16*)g.B2; p.ldb = g.ldb;
   p.C = g.C; p.ldc = g.ldc; p.c_f32 = g.c_f32; p.row_scale = g.row_scale;
   p.rows = g.rows; p.resid = (const bf16*)g.resid; p.pos = g.pos; p.slot = g.slot;
+  p.bias = (const bf16*)g.bias;
   p.rope_cos = g.rope_cos; p.rope_sin = g.rope_sin; p.head_dim = g.head_dim; p.d_q = g.d_q;
   p.q_out = (bf16*)g.q_out; p.k_cache = (bf16*)g.k_cache; p.v_cache = (bf16*)g.v_cache;
   return p;
 }
+
+bool aligned8(const void* p) { return ((uintptr_t)p & 7u) == 0; }
 
 bool aligned_operands(const GemmArgs& g) {
   return aligned16(g.A) && aligned16(g.B) && (!g.B2 || aligned16(g.B2)) && g.lda % 8 == 0 &&
@@ -873,8 +905,13 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
     set_error("gemm: N=%d not a multiple of %d", g.N, ncols);
     return ADEPT_E_UNSUPPORTED;
   }
-  if ((g.epi == EPI_QKV) && (g.d_q % 128 != 0 || (g.head_dim != 64 && g.head_dim != 128))) {
-    set_error("gemm: QKV epilogue needs head_dim 64/128 and d_q %% 128 == 0");
+  if ((g.epi == EPI_QKV) &&
+      (g.d_q % 128 != 0 || (g.rope_cos && g.head_dim != 64 && g.head_dim != 128))) {
+    set_error("gemm: QKV epilogue needs d_q %% 128 == 0 (and head_dim 64/128 with RoPE)");
+    return ADEPT_E_UNSUPPORTED;
+  }
+  if (g.bias && (g.epi == EPI_SWIGLU || g.epi == EPI_KV || !aligned8(g.bias))) {
+    set_error("gemm: bias needs an 8-byte aligned [N] vector and no SWIGLU / KV epilogue");
     return ADEPT_E_UNSUPPORTED;
   }
   if (!aligned_operands(g)) {
@@ -890,6 +927,7 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
         case EPI_QKV: return launch_skinny<EPI_QKV>(p, Nt, g.N, s, g.name, g.skinny_ws);
         case EPI_RESID: return launch_skinny<EPI_RESID>(p, Nt, g.N, s, g.name, g.skinny_ws);
         case EPI_SWIGLU: return launch_skinny<EPI_SWIGLU>(p, Nt, g.N, s, g.name, g.skinny_ws);
+        case EPI_GELU: return launch_skinny<EPI_GELU>(p, Nt, g.N, s, g.name, g.skinny_ws);
         default: break;
       }
     }
@@ -903,6 +941,7 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
                                : launch_bf16<EPI_QKV, 64>(p, s, g.name);
     case EPI_RESID: return launch_bf16<EPI_RESID, 0>(p, s, g.name);
     case EPI_SWIGLU: return launch_bf16<EPI_SWIGLU, 0>(p, s, g.name);
+    case EPI_GELU: return launch_bf16<EPI_GELU, 0>(p, s, g.name);
     default: set_error("gemm: bad epilogue"); return ADEPT_E_INVALID;
   }
 }

@@ -272,3 +272,123 @@ class DecoderModel:
             nxt = self.greedy(st.logits)
         gen = torch.stack(out, dim=1) if out else torch.zeros((Bn, 0), dtype=torch.int32)
         return res, steps, gen, cache
+
+
+@dataclasses.dataclass
+class ClassifyOutput:
+    logits: torch.Tensor          # [B, n_classes] f32, from each [CLS] row at its exit
+    exit_layer: torch.Tensor      # [B*T] int32 (n_layers: never exited)
+    cls_exit_layer: torch.Tensor  # [B]
+    state: dict                   # device buffers of the pass (h, inertia, sims, ...)
+
+
+class EncoderModel:
+    """A BERT-style post-norm encoder classifier held on the device (bf16),
+    run with token-level exit in classification mode:
+
+        adept_encoder_embed -> adept_token_init -> adept_encoder_layer_step(i),
+        i = 1..N -> adept_classify_head
+
+    weights: a dict like adept_inputs.encoder_weights() (numpy, per layer) or
+    the same keys stacked over layers as torch tensors.
+    """
+
+    def __init__(self, shape, weights, device="cuda"):
+        self.shape = shape
+        self.device = torch.device(device)
+        dev, tdt = self.device, torch.bfloat16
+
+        def up(x):
+            if isinstance(x, torch.Tensor):
+                return x.to(dev, tdt).contiguous()
+            return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(dev).to(tdt)
+
+        L = weights["layers"]
+        if isinstance(L, list):
+            stack = lambda k: up(np.stack([lw[k] for lw in L]))
+            self.w_qkv = up(np.stack([np.concatenate([lw["wq"], lw["wk"], lw["wv"]]) for lw in L]))
+            self.b_qkv = up(np.stack([np.concatenate([lw["bq"], lw["bk"], lw["bv"]]) for lw in L]))
+        else:
+            stack = lambda k: up(L[k])
+            self.w_qkv = up(torch.cat([L["wq"], L["wk"], L["wv"]], dim=1))
+            self.b_qkv = up(torch.cat([L["bq"], L["bk"], L["bv"]], dim=1))
+        self.w_o, self.b_o = stack("wo"), stack("bo")
+        self.ln1_g, self.ln1_b = stack("ln1_g"), stack("ln1_b")
+        self.w_in, self.b_in = stack("w_in"), stack("b_in")
+        self.w_out, self.b_out = stack("w_out"), stack("b_out")
+        self.ln2_g, self.ln2_b = stack("ln2_g"), stack("ln2_b")
+        self.word = up(weights["word_embed"])
+        self.pos_emb = up(weights["pos_embed"])
+        self.type_emb = up(weights["type_embed"])
+        self.eln_g, self.eln_b = up(weights["embed_ln_g"]), up(weights["embed_ln_b"])
+        self.cls_w, self.cls_b = up(weights["cls_w"]), up(weights["cls_b"])
+
+    def classify(self, ids, cfg, force_layer=None, state=None):
+        """ids [B, T] (numpy or tensor); cfg from binding.exit_cfg.  A state
+        dict from an earlier call of the same shape is reused (no allocation)."""
+        s, dev = self.shape, self.device
+        ids = torch.as_tensor(np.asarray(ids) if not isinstance(ids, torch.Tensor) else ids)
+        Bn, T = ids.shape
+        n, D, Dq, F, N = Bn * T, s.d_model, s.d_q, s.d_ff, s.n_layers
+        i32 = dict(dtype=torch.int32, device=dev)
+        bf = dict(dtype=torch.bfloat16, device=dev)
+        st = state
+        if st is None or st["n"] != n:
+            st = {
+                "n": n,
+                "h": [torch.empty((n, D), **bf) for _ in range(2)],
+                "inertia": torch.empty((n, D), dtype=torch.float32, device=dev),
+                "pos": torch.arange(T, **i32).repeat(Bn),
+                "seq": torch.arange(Bn, **i32).repeat_interleave(T),
+                "active": [torch.empty(n, **i32) for _ in range(2)],
+                "counts": torch.zeros(4, **i32),
+                "exited": torch.empty(n, **i32),
+                "exit_layer": torch.empty(n, **i32),
+                "exit_flag": torch.empty(max(n, 4), dtype=torch.uint8, device=dev),
+                "sim_out": torch.empty(n, dtype=torch.float64, device=dev),
+                "key_live": torch.empty(n, dtype=torch.uint8, device=dev),
+                "key_len": torch.full((Bn,), T, **i32),
+                "k_buf": torch.empty((n, Dq), **bf), "v_buf": torch.empty((n, Dq), **bf),
+                "q_buf": torch.empty((n, Dq), **bf), "attn_out": torch.empty((n, Dq), **bf),
+                "y_buf": torch.empty((n, D), **bf), "ffn_act": torch.empty((n, F), **bf),
+                "logits": torch.empty((Bn, s.n_classes), dtype=torch.float32, device=dev),
+                "workspace": None,
+            }
+        st["force"] = None
+        if force_layer is not None:
+            st["force"] = torch.as_tensor(np.asarray(force_layer).reshape(-1)
+                                          if not isinstance(force_layer, torch.Tensor)
+                                          else force_layer.reshape(-1)).to(dev, torch.int32)
+        a = B.EncoderArgs()
+        a.dtype, a.n_layers, a.d_model, a.n_heads = B.BF16, N, D, s.n_heads
+        a.head_dim, a.d_ff, a.ln_eps, a.exit = s.head_dim, F, s.ln_eps, cfg
+        for k in ("w_qkv", "b_qkv", "w_o", "b_o", "ln1_g", "ln1_b", "w_in", "b_in", "w_out",
+                  "b_out", "ln2_g", "ln2_b"):
+            setattr(a, k, B.ptr(getattr(self, k)))
+        a.n_tok, a.n_seq, a.seq_len = n, Bn, T
+        a.h[0], a.h[1] = B.ptr(st["h"][0]), B.ptr(st["h"][1])
+        a.inertia, a.pos, a.seq = B.ptr(st["inertia"]), B.ptr(st["pos"]), B.ptr(st["seq"])
+        a.active[0], a.active[1] = B.ptr(st["active"][0]), B.ptr(st["active"][1])
+        cp = B.ptr(st["counts"])
+        a.n_active[0], a.n_active[1], a.n_exited = cp, cp + 4, cp + 8
+        a.exited, a.exit_layer = B.ptr(st["exited"]), B.ptr(st["exit_layer"])
+        a.exit_flag, a.sim_out = B.ptr(st["exit_flag"]), B.ptr(st["sim_out"])
+        a.force_layer = B.ptr(st["force"])
+        a.key_live, a.key_len = B.ptr(st["key_live"]), B.ptr(st["key_len"])
+        for k in ("k_buf", "v_buf", "q_buf", "attn_out", "y_buf", "ffn_act"):
+            setattr(a, k, B.ptr(st[k]))
+        need = B.encoder_workspace_bytes(a)
+        if st["workspace"] is None or st["workspace"].numel() < need:
+            st["workspace"] = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        a.workspace, a.workspace_bytes = B.ptr(st["workspace"]), st["workspace"].numel()
+
+        ids_d = ids.reshape(-1).to(dev, torch.int32)
+        B.encoder_embed(n, D, s.vocab, s.max_pos, s.ln_eps, ids_d, st["pos"], self.word,
+                        self.pos_emb, self.type_emb, self.eln_g, self.eln_b, st["h"][0])
+        B.token_init(n, N, D, st["active"][0], st["counts"], st["exit_layer"], st["inertia"])
+        st["key_live"].fill_(1)
+        for i in range(1, N + 1):
+            B.encoder_layer_step(a, i)
+        B.classify_head(Bn, T, D, s.n_classes, st["h"][0], st["h"][1], st["exit_layer"],
+                        self.cls_w, self.cls_b, st["logits"])
+        return ClassifyOutput(st["logits"], st["exit_layer"], st["exit_layer"][::T], st)

@@ -30,12 +30,15 @@ def test_library_exports_every_declared_symbol():
     assert lib.adept_abi_version() == 2
 
 
-def test_struct_layout_matches_header(tmp_path):
-    fields = [f for f, _ in B.LayerArgs._fields_]
+@pytest.mark.parametrize("cname,pyname", [("adept_layer_args", "LayerArgs"),
+                                           ("adept_encoder_args", "EncoderArgs")])
+def test_struct_layout_matches_header(tmp_path, cname, pyname):
+    S = getattr(B, pyname)
+    fields = [f for f, _ in S._fields_]
     src = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', 'int main(void){',
-           'printf("%zu\\n", sizeof(adept_layer_args));']
+           f'printf("%zu\\n", sizeof({cname}));']
     for f in fields:
-        src.append(f'printf("%zu\\n", offsetof(adept_layer_args, {f}));')
+        src.append(f'printf("%zu\\n", offsetof({cname}, {f}));')
     src.append('printf("%zu\\n", sizeof(adept_exit_cfg)); return 0; }')
     c = tmp_path / "layout.c"
     c.write_text("\n".join(src))
@@ -43,9 +46,9 @@ def test_struct_layout_matches_header(tmp_path):
     subprocess.run(["gcc", "-o", str(exe), str(c)], check=True)
     vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
                                            check=True).stdout.split()]
-    assert vals[0] == ctypes.sizeof(B.LayerArgs)
+    assert vals[0] == ctypes.sizeof(S)
     for f, off in zip(fields, vals[1:-1]):
-        assert getattr(B.LayerArgs, f).offset == off, f
+        assert getattr(S, f).offset == off, f
     assert vals[-1] == ctypes.sizeof(B.ExitCfg)
 
 

@@ -1,0 +1,98 @@
+"""Classification mode (Section 4.3) on the GPU against the oracle: a
+BERT-style post-norm encoder with token-level exit, where exited tokens
+leave the key set and each sequence's [CLS] row at its exit feeds the linear
+head.  bf16 throughout: a seeded exit schedule imposed on both sides gives
+exact exit layers and logits within the bf16 bound; policy-driven decisions
+are compared where the oracle's margin exceeds the bf16 error."""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import adept_inputs as ai
+from oracle import adept_oracle as O
+from paper_2601_03700_amd import binding as B
+from paper_2601_03700_amd.model import EncoderModel
+
+pytestmark = pytest.mark.gpu
+
+ENC = ai.EncoderShape(n_layers=4, d_model=256, n_heads=4, head_dim=64, d_ff=512, vocab=300,
+                      max_pos=128)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def bf16_close(a, b, what):
+    """2e-2 on unit-scale values, scaled by the reference's largest magnitude
+    above 1, plus an RMS bound of 1e-2 relative (each layer stores its
+    activations and residual stream in bf16)."""
+    m = max(1.0, float(np.max(np.abs(b))))
+    err = np.abs(a - b)
+    rms = float(np.sqrt(np.mean(err ** 2)) / max(np.sqrt(np.mean(b ** 2)), 1e-30))
+    say(f"  {what}: max err {err.max():.4g} (bound {2e-2 * m:.4g}), rms rel {rms:.3g}")
+    assert err.max() <= 2e-2 * m and rms <= 1e-2, what
+
+
+@pytest.fixture(scope="module")
+def enc():
+    w32 = ai.encoder_weights(ENC, seed=21, dtype="bf16", std=0.05)
+    return w32, O.as64(w32), EncoderModel(ENC, w32)
+
+
+@pytest.mark.parametrize("Bn,T", [(3, 100), (2, 24)])   # tiled GEMMs; skinny GEMMs (48 rows)
+def test_classify_forced_schedule(enc, Bn, T):
+    w32, w, model = enc
+    say(f"classify forced schedule B={Bn} T={T}")
+    ids = ai.token_ids(30 + T, ENC.vocab, Bn, T)
+    force = np.random.default_rng(T).integers(0, ENC.n_layers + 1, size=ids.shape)
+    force[0, 0] = 2                       # a [CLS] row that exits early
+    out = model.classify(ids, B.exit_cfg(math.inf, ENC.n_layers, "global"), force_layer=force)
+    torch.cuda.synchronize()
+    ref = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf), force_layer=force)
+    np.testing.assert_array_equal(out.exit_layer.cpu().numpy(), ref.exit_layer)
+    np.testing.assert_array_equal(out.cls_exit_layer.cpu().numpy(), ref.cls_exit_layer)
+    bf16_close(out.logits.cpu().numpy(), ref.logits, "logits")
+    # the final states the head reads (each row's state at its exit)
+    h = [t.float().cpu().numpy().astype(np.float64) for t in out.state["h"]]
+    el = out.exit_layer.cpu().numpy()
+    hf = np.where((el & 1)[:, None] == 1, h[1], h[0])
+    bf16_close(hf, ref.h_final, "final states")
+
+
+def test_classify_full_depth(enc):
+    w32, w, model = enc
+    say("classify full depth")
+    ids = ai.token_ids(40, ENC.vocab, 2, 128)
+    out = model.classify(ids, B.exit_cfg(math.inf, ENC.n_layers, "global"))
+    torch.cuda.synchronize()
+    ref = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf))
+    assert (out.exit_layer.cpu().numpy() == ENC.n_layers).all()
+    bf16_close(out.logits.cpu().numpy(), ref.logits, "logits")
+
+
+def test_classify_policy_decisions(enc):
+    """Global metric, a threshold between the oracle's similarities: every
+    token whose margin exceeds 5e-3 at every tested layer exits at the same
+    layer on both sides."""
+    w32, w, model = enc
+    say("classify policy")
+    ids = ai.token_ids(41, ENC.vocab, 2, 96)
+    full = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf))
+    sims = full.sims[:ENC.n_layers - 1]
+    fin = np.sort(sims[np.isfinite(sims)])
+    q = np.searchsorted(fin, np.quantile(fin, 0.6))
+    delta = float(0.5 * (fin[q - 1] + fin[q]))
+    ref = O.classify(w, ENC, ids, O.ExitConfig(delta=delta))
+    out = model.classify(ids, B.exit_cfg(delta, ENC.n_layers, "global"))
+    torch.cuda.synchronize()
+    m = np.abs(ref.sims - delta)
+    safe = np.nanmin(np.where(np.isfinite(m), m, np.inf), axis=0) > 5e-3
+    el_g, el_o = out.exit_layer.cpu().numpy(), ref.exit_layer
+    assert safe.sum() > 0.3 * safe.size
+    np.testing.assert_array_equal(el_g[safe], el_o[safe])
+    assert 0 < np.sum(el_o < ENC.n_layers) < el_o.size

@@ -151,3 +151,40 @@ def test_small_bf16_free_running_decisions():
     assert safe.sum() > 0.5 * safe.size
     np.testing.assert_array_equal(el_g[safe], el_o[safe])
     assert 0 < np.sum(el_o < shape.n_layers) < el_o.size
+
+
+def test_small_bf16_decode_forced_schedule():
+    """bf16 generation with a seeded exit schedule on both sides, for the
+    prompt and every step: the decode passes (one row per sequence) take the
+    key-chunked attention, the skinny GEMMs and the KV generation deferred to
+    the end of the pass.  Step tokens are seeded (not greedy) so both sides
+    see the same ids; exit layers exact, logits and the whole cache (computed
+    and generated entries) within the bf16 bound."""
+    say("small bf16 decode forced schedule")
+    shape = SMALL_BF16
+    N = shape.n_layers
+    w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
+    w = O.as64(w32)
+    Bn, T, S = 3, 40, 6
+    ids = ai.token_ids(12, shape.vocab, Bn, T)
+    step_ids = ai.token_ids(13, shape.vocab, S, Bn)
+    rng = np.random.default_rng(6)
+    force_p = rng.integers(0, N + 1, size=ids.shape)
+    force_s = rng.integers(1, N + 1, size=(S, Bn))     # every step token exits somewhere
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512)
+    cfg_g = B.exit_cfg(math.inf, N, "global")
+    cfg_o = O.ExitConfig(delta=math.inf)
+    res_g, cache_g = model.prefill(ids, cfg_g, s_max=T + S, force_layer=force_p, logits="last")
+    res_o, cache_o = O.prefill(w, shape, ids, cfg_o, s_max=T + S, force_layer=force_p)
+    for s in range(S):
+        pos = np.full(Bn, T + s)
+        st_g = model.decode_step(cache_g, torch.from_numpy(step_ids[s]).to("cuda", torch.int32),
+                                 torch.from_numpy(pos).to("cuda", torch.int32), cfg_g,
+                                 force_layer=torch.from_numpy(force_s[s]).to("cuda", torch.int32))
+        st_o = O.decode_step(w, shape, cache_o, step_ids[s], pos, cfg_o, force_layer=force_s[s])
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(st_g.exit_layer.cpu().numpy(), st_o.exit_layer)
+        bf16_close(st_g.logits.cpu().numpy(), st_o.logits, f"step {s} logits")
+    kg, vg = cache_host(cache_g, Bn, T + S)
+    bf16_close(kg, cache_o.k, "K cache")
+    bf16_close(vg, cache_o.v, "V cache")

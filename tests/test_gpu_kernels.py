@@ -345,18 +345,31 @@ def test_attend_prefill_mfma_matches_oracle(hd, n_seq, s_max, frac):
     assert np.max(np.abs(got - ref)) <= 2e-2, np.max(np.abs(got - ref))
 
 
-@pytest.mark.parametrize("hd,lens,decode,causal,live,H", [
-    (128, [1000, 999, 513, 64, 1], True, True, False, 4),   # decode, ragged, 1-key sequence
-    (64, [700, 255, 256, 257], True, True, False, 6),       # decode, chunk-boundary lengths
-    (64, [512, 300, 77], False, False, True, 2),           # bidirectional over live keys
-    (128, [130, 20], False, True, False, 3),                # few causal queries per sequence
+@pytest.mark.parametrize("hd,lens,decode,causal,live,H,frac", [
+    (128, [1000, 999, 513, 64, 1], True, True, False, 4, 1.0),   # decode, ragged, 1-key sequence
+    (64, [700, 255, 256, 257], True, True, False, 6, 1.0),       # decode, chunk-boundary lengths
+    (64, [512, 300, 77], False, False, True, 2, 0.01),          # few bidirectional live queries
+    (128, [130, 20], False, True, False, 3, 0.02),               # few causal queries per sequence
 ])
-def test_attend_split_matches_oracle(hd, lens, decode, causal, live, H):
-    """bf16 key-chunked kernel (one or few queries per sequence, bidirectional)."""
+def test_attend_split_matches_oracle(hd, lens, decode, causal, live, H, frac):
+    """bf16 key-chunked kernel (fewer than 4 queries per sequence on average)."""
     say(f"attend split hd={hd} lens={lens} decode={decode} causal={causal} live={live}")
     n_seq, s_max = len(lens), max(lens)
-    got, ref = _attend_case("bf16", H, hd, n_seq, s_max, lens, 0.02 if causal and not decode
-                            else 0.5, 23 + hd, causal=causal, live=live, decode=decode)
+    got, ref = _attend_case("bf16", H, hd, n_seq, s_max, lens, frac, 23 + hd, causal=causal,
+                            live=live, decode=decode)
+    assert np.max(np.abs(got - ref)) <= 2e-2, np.max(np.abs(got - ref))
+
+
+@pytest.mark.parametrize("hd,lens,live,frac", [(64, [512, 512, 300], True, 0.7),
+                                               (64, [100, 512], True, 1.0),
+                                               (128, [250, 129, 64], False, 0.5)])
+def test_attend_tiles_bidirectional_matches_oracle(hd, lens, live, frac):
+    """bf16 query-tile MFMA kernel, bidirectional (classification): every
+    query sees all keys of its sequence below key_len, minus the dead ones."""
+    say(f"attend tiles bidirectional hd={hd} lens={lens} live={live} frac={frac}")
+    n_seq, s_max = len(lens), max(lens)
+    got, ref = _attend_case("bf16", 12 if hd == 64 else 4, hd, n_seq, s_max, lens, frac, 31 + hd,
+                            causal=False, live=live)
     assert np.max(np.abs(got - ref)) <= 2e-2, np.max(np.abs(got - ref))
 
 
