@@ -251,16 +251,18 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   auto no_dma = [](int) {};
 
   // K loop over a 5-slot ring.  At the top of iteration kt stage kt (A_kt,
-  // B_kt) has landed and is visible to every wave, A_kt+1 is in flight, and
-  // the fragments of stage kt's first k step (f) were read just before.  The
-  // slots of stage kt-1, retired by the previous barrier, take B_kt+1 (during
-  // k step 0) and A_kt+2 (during k step 1): A gets two iterations of lead, B
-  // one.  Before each k step, the reads issued during the previous one are
-  // waited for; at most 8 LDS reads are ever outstanding (the 4-bit lgkm
-  // counter cannot express more).  The last k step is split around the wait
-  // for stage kt+1 (only A_kt+2 may stay outstanding) and the barrier, which
-  // publishes stage kt+1 and retires every read of stage kt; its last two
-  // MFMA rows carry the reads of stage kt+1's first fragments.
+  // B_kt) has landed and is visible to every wave, A_kt+1 and B_kt+1 are in
+  // flight, and the fragments of stage kt's first k step (f) were read just
+  // before.  A slot is refilled as soon as a barrier retires its last reads:
+  // A_kt+2 goes into the slot of B_kt-1 during k step 0, and B_kt+2 into the
+  // slot of A_kt right after this iteration's barrier, so each stage has
+  // about two iterations of MFMA work to land.  Before each k step, the
+  // reads issued during the previous one are waited for; at most 8 LDS reads
+  // are ever outstanding (the 4-bit lgkm counter cannot express more).  The
+  // last k step is split around the wait for stage kt+1 (only A_kt+2 may
+  // stay outstanding) and the barrier, which publishes stage kt+1 and
+  // retires every read of stage kt; its last two MFMA rows carry the reads
+  // of stage kt+1's first fragments and the DMA of B_kt+2.
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     issue_a(0, j);
@@ -268,8 +270,11 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   }
   if (KT > 1) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) issue_a(1, j);
-    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    for (int j = 0; j < 8; ++j) {
+      issue_a(1, j);
+      issue_b(1, j);
+    }
+    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
   } else {
     wait_dma();
   }
@@ -279,13 +284,13 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   for (int kt = 0; kt < KT; ++kt) {
     const char* cA = slot(2 * kt);
     const char* cB = slot(2 * kt + 1);
-    const bool nb = kt + 1 < KT, na = kt + 2 < KT;
+    const bool n2 = kt + 2 < KT;
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_sched_barrier(0);
-    kstep(fa, fb, ga, gb, cA, cB, 1, [&](int j) { issue_b(kt + 1, j); }, nb);
+    kstep(fa, fb, ga, gb, cA, cB, 1, [&](int j) { issue_a(kt + 2, j); }, n2);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_sched_barrier(0);
-    kstep(ga, gb, fa, fb, cA, cB, 2, [&](int j) { issue_a(kt + 2, j); }, na);
+    kstep(ga, gb, fa, fb, cA, cB, 2, no_dma, false);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_sched_barrier(0);
     kstep(fa, fb, ga, gb, cA, cB, 3, no_dma, false);
@@ -294,7 +299,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     mma_row(ga, gb, 0);
     mma_row(ga, gb, 1);
     __builtin_amdgcn_sched_barrier(0);
-    if (na) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    if (n2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
     else wait_dma();
     stage_barrier();
     // unconditional: after the last stage this reads stale but valid LDS
@@ -305,6 +310,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
       const int i = 2 + (n >> 2), j = n & 3;
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[i], gb[j], acc[i][j], 0, 0, 0);
       frag1(nA, nB, 0, n, fa, fb);
+      if (n2) issue_b(kt + 2, n);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
