@@ -94,7 +94,10 @@ adept_status adept_rope_table(int max_pos, int head_dim, double theta,
  *
  * The three sums <h,h>, <r,r>, <h,r> are reduced in double precision from
  * the stored values (each product is exact in double), the decision is
- * taken in double.  One wavefront per row; HBM-bound.
+ * taken in double.  One wavefront per row; HBM-bound.  d_model must be a
+ * multiple of 4 (GLOBAL, and LOCAL f32) or 8 (LOCAL bf16) and at most 8192
+ * (GLOBAL; 8192 f32 / 16384 bf16 for LOCAL), else ADEPT_E_INVALID /
+ * ADEPT_E_UNSUPPORTED; h_cur, h_prev and the inertia 16-byte aligned.
  * ------------------------------------------------------------------------- */
 adept_status adept_exit_test(adept_dtype dt, int d_model, int layer, const adept_exit_cfg* cfg,
                              const int32_t* active_rows, const int32_t* n_active, int max_active,

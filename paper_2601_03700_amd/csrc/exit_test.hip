@@ -1,88 +1,93 @@
 // Token-level exit test (Section 4.1, Eq. 7-8; local metric of Appendix H.3).
 //
-// One wavefront per active row.  Each lane reads 16-byte vectors of the row
-// (8 bf16 or 4 f32 values) at vector index c*64 + lane, keeps them in
-// registers, and accumulates the three sums <h,h>, <r,r>, <h,r> in double
-// (every product of two float values is exact in double).  A xor butterfly
-// reduces across the wave; the decision is taken in double.  For the global
-// metric the inertia row is then updated from the registers, so each byte
-// of h and of the inertia crosses HBM once (read h, read + write inertia).
+// One wavefront per active row.  Per chunk c each lane holds E consecutive
+// elements of h starting at element (c*64 + lane)*E, with E = 4 for the
+// global metric (8 bytes of bf16 h beside one contiguous 16-byte vector of
+// the f32 inertia) and E = 16/sizeof(T) for the local one, so that every
+// load and store instruction of the wave covers one contiguous span.  The
+// values stay in registers in their stored form between the reduction and
+// the inertia update; the three sums <h,h>, <r,r>, <h,r> are accumulated in
+// double (every product of two float values is exact in double), a xor
+// butterfly reduces across the wave and the decision is taken in double.
+// For the global metric the inertia row is then updated from the registers,
+// so each byte of h and of the inertia crosses HBM once (read h, read +
+// write inertia).  Every access is streaming (non-temporal): nothing the
+// kernel touches is read again before it has left the caches.
 #include "common.h"
 
 namespace adept {
 namespace {
 
 constexpr int kWavesPerBlock = 4;
+constexpr int kMaxChunks = 32;
 
 struct ExitParams {
   double delta;
   int min_exit_layer, n_layers, layer, d;
 };
 
-template <typename T> struct Vec16;
-template <> struct Vec16<float> { static constexpr int n = 4; };
-template <> struct Vec16<bf16> { static constexpr int n = 8; };
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <int BYTES> struct Raw;
+template <> struct Raw<8> { using type = u32x2; };
+template <> struct Raw<16> { using type = u32x4; };
 
-// Element i of a 16-byte vector of T, as float.
-template <typename T> __device__ __forceinline__ float elem(const uint4& r, int i);
-template <> __device__ __forceinline__ float elem<float>(const uint4& r, int i) {
-  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
-  return __uint_as_float(w[i]);
-}
-template <> __device__ __forceinline__ float elem<bf16>(const uint4& r, int i) {
-  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
-  return __uint_as_float((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16));
+// Element i of a raw vector of T, as float.
+template <typename T, typename R> __device__ __forceinline__ float elem(const R& r, int i) {
+  if constexpr (sizeof(T) == 4) {
+    return __uint_as_float(r[i]);
+  } else {
+    const uint32_t w = r[i >> 1];
+    return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
 }
 
-// Values stay in registers in their stored form (16-byte vectors, bf16
-// packed) between the reduction and the inertia update, which keeps the
-// register count low enough for several rows in flight per SIMD.
 template <typename T, int CH, bool GLOBAL>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void exit_test_kernel(
+__global__ __launch_bounds__(64 * kWavesPerBlock)
+void exit_test_kernel(
     ExitParams p, int max_active, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_active,
     const T* __restrict__ h_cur, const T* __restrict__ h_prev, float* __restrict__ inertia,
     const int32_t* __restrict__ force_layer, uint8_t* __restrict__ exit_flag,
     double* __restrict__ sim_out) {
-  constexpr int V = Vec16<T>::n;
-  constexpr int RV = GLOBAL ? V / 4 : 1;   // 16-byte vectors of the reference per chunk
+  constexpr int E = GLOBAL ? 4 : 16 / (int)sizeof(T);
+  using HRaw = typename Raw<E * sizeof(T)>::type;
+  using RRaw = u32x4;   // 4 f32 of the inertia, or E values of h_prev
   const int lane = threadIdx.x & 63;
   const int k = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   if (k >= min(*n_active, max_active)) return;
   const int row = rows[k];
-  const int nvec = p.d / V;
+  const int nvec = p.d / E;
   const T* hr = h_cur + (int64_t)row * p.d;
+  const uint32_t* rr = GLOBAL ? reinterpret_cast<const uint32_t*>(inertia + (int64_t)row * p.d)
+                              : reinterpret_cast<const uint32_t*>(h_prev + (int64_t)row * p.d);
 
-  uint4 hv[CH];
-  uint4 rv[CH][RV];
+  HRaw hv[CH];
+  RRaw rv[CH];
+  // Loads are not predicated: a lane past the end of the row re-reads the
+  // row's last vector and contributes zeros (predicated loads leave the
+  // register allocator with partially defined values and cost spills).
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
-    const int vi = c * 64 + lane;
-    if (vi < nvec) {
-      hv[c] = *reinterpret_cast<const uint4*>(hr + vi * V);
-      if (GLOBAL) {
-        const float* ir = inertia + (int64_t)row * p.d + vi * V;
-#pragma unroll
-        for (int q = 0; q < RV; ++q) rv[c][q] = *reinterpret_cast<const uint4*>(ir + 4 * q);
-      } else {
-        rv[c][0] = *reinterpret_cast<const uint4*>(h_prev + (int64_t)row * p.d + vi * V);
-      }
-    }
+    const int vi = min(c * 64 + lane, nvec - 1);
+    hv[c] = __builtin_nontemporal_load(reinterpret_cast<const HRaw*>(hr + vi * E));
+    rv[c] = __builtin_nontemporal_load(reinterpret_cast<const RRaw*>(rr) + vi);
   }
   double s_hh = 0.0, s_rr = 0.0, s_hr = 0.0;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
-    const int vi = c * 64 + lane;
-    if (vi < nvec) {
+    const bool live = c * 64 + lane < nvec;
 #pragma unroll
-      for (int v = 0; v < V; ++v) {
-        const double a = elem<T>(hv[c], v);
-        const double b = GLOBAL ? elem<float>(rv[c][v >> 2], v & 3) : elem<T>(rv[c][0], v);
-        s_hh = fma(a, a, s_hh);
-        s_rr = fma(b, b, s_rr);
-        s_hr = fma(a, b, s_hr);
-      }
+    for (int v = 0; v < E; ++v) {
+      const double a = live ? elem<T>(hv[c], v) : 0.0f;
+      const double b = live ? (GLOBAL ? elem<float>(rv[c], v) : elem<T>(rv[c], v)) : 0.0f;
+      s_hh = fma(a, a, s_hh);
+      s_rr = fma(b, b, s_rr);
+      s_hr = fma(a, b, s_hr);
     }
+    // chunk by chunk: the conversions to double are not hoisted (and held
+    // in registers) ahead of the chunk that needs them
+    __builtin_amdgcn_sched_barrier(0);
   }
   s_hh = wave_sum_f64(s_hh);
   s_rr = wave_sum_f64(s_rr);
@@ -102,20 +107,20 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void exit_test_kernel(
   }
   if (GLOBAL && nh > 0.0) {
     const double inv = 1.0 / nh;
+    float* iw = inertia + (int64_t)row * p.d;
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
+      // opaque to the optimiser: the values are converted again here rather
+      // than kept in double registers since the reduction
+      asm volatile("" : "+v"(hv[c]), "+v"(rv[c]));
       const int vi = c * 64 + lane;
       if (vi < nvec) {
-        float* ir = inertia + (int64_t)row * p.d + vi * V;
+        u32x4 o;
 #pragma unroll
-        for (int q = 0; q < RV; ++q) {
-          float4 o;
-          o.x = (float)((double)elem<float>(rv[c][q], 0) + (double)elem<T>(hv[c], 4 * q + 0) * inv);
-          o.y = (float)((double)elem<float>(rv[c][q], 1) + (double)elem<T>(hv[c], 4 * q + 1) * inv);
-          o.z = (float)((double)elem<float>(rv[c][q], 2) + (double)elem<T>(hv[c], 4 * q + 2) * inv);
-          o.w = (float)((double)elem<float>(rv[c][q], 3) + (double)elem<T>(hv[c], 4 * q + 3) * inv);
-          *reinterpret_cast<float4*>(ir + 4 * q) = o;
-        }
+        for (int e = 0; e < 4; ++e)
+          o[e] = __float_as_uint(
+              (float)((double)elem<float>(rv[c], e) + (double)elem<T>(hv[c], e) * inv));
+        __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(iw) + vi);
       }
     }
   }
@@ -139,6 +144,8 @@ adept_status launch_exit(int ch, const ExitParams& p, int max_active, const int3
     ADEPT_EXIT_CASE(2)
     ADEPT_EXIT_CASE(4)
     ADEPT_EXIT_CASE(8)
+    ADEPT_EXIT_CASE(16)
+    ADEPT_EXIT_CASE(32)
     default:
       set_error("exit_test: unsupported chunk count %d", ch);
       return ADEPT_E_UNSUPPORTED;
@@ -166,10 +173,11 @@ extern "C" adept_status adept_exit_test(adept_dtype dt, int d_model, int layer,
                 "exit_test: layer %d outside 1..%d", layer, cfg->n_layers);
   ADEPT_REQUIRE(max_active >= 0, "exit_test: max_active < 0");
   ADEPT_REQUIRE(!std::isnan(cfg->delta), "exit_test: delta is NaN");
-  const int V = dt == ADEPT_BF16 ? 8 : 4;
+  const bool global = cfg->metric == ADEPT_SIM_GLOBAL;
+  // elements per lane and chunk (kernel's E)
+  const int V = global ? 4 : (dt == ADEPT_BF16 ? 8 : 4);
   ADEPT_REQUIRE(d_model > 0 && d_model % V == 0, "exit_test: d_model %d not a multiple of %d",
                 d_model, V);
-  const bool global = cfg->metric == ADEPT_SIM_GLOBAL;
   ADEPT_REQUIRE(active_rows && n_active && h_cur && exit_flag, "exit_test: NULL tensor");
   ADEPT_REQUIRE(global ? inertia != nullptr : h_prev != nullptr,
                 "exit_test: %s needs %s", global ? "GLOBAL" : "LOCAL",
@@ -182,8 +190,8 @@ extern "C" adept_status adept_exit_test(adept_dtype dt, int d_model, int layer,
   int ch = (nvec + 63) / 64;
   int chp = 1;
   while (chp < ch) chp <<= 1;
-  if (chp > 8) {
-    set_error("exit_test: d_model %d too large (max %d)", d_model, 8 * 64 * V);
+  if (chp > kMaxChunks) {
+    set_error("exit_test: d_model %d too large (max %d)", d_model, kMaxChunks * 64 * V);
     return ADEPT_E_UNSUPPORTED;
   }
   ExitParams p{cfg->delta, cfg->min_exit_layer, cfg->n_layers, layer, d_model};

@@ -68,6 +68,10 @@ def test_host_validation_rejects_bad_arguments():
                                       16, None, None))
     _expect_invalid(L.adept_exit_test(1, 250, 1, ctypes.byref(cfg), 16, 16, 4, 16, 16, 16, None,
                                       16, None, None))
+    # d_model beyond the largest row one wavefront holds (8192 for GLOBAL)
+    assert L.adept_exit_test(1, 8196, 1, ctypes.byref(cfg), 16, 16, 4, 16, 16, 16, None, 16,
+                             None, None) == -2
+    assert L.adept_last_error()
     # GLOBAL without inertia
     _expect_invalid(L.adept_exit_test(1, 256, 1, ctypes.byref(cfg), 16, 16, 4, 16, 16, None, None,
                                       16, None, None))

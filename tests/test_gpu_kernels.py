@@ -49,7 +49,8 @@ def count(n):
 
 EXIT_CASES = [("bf16", 4096, "global"), ("bf16", 4096, "local"), ("bf16", 768, "global"),
               ("bf16", 1000, "local"), ("f32", 256, "global"), ("f32", 256, "local"),
-              ("f32", 1028, "global")]
+              ("f32", 1028, "global"), ("bf16", 8192, "global"), ("f32", 4100, "global"),
+              ("bf16", 16384, "local")]
 
 
 @pytest.mark.parametrize("dt,D,metric", EXIT_CASES)
