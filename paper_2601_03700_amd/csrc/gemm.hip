@@ -145,7 +145,10 @@ __device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "
 template <int EPI, bool GROUPED, int HD>
 __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, int mt, int nt,
                                           int M, const bf16* Bm) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index in a scalar register: LDS destinations of the direct
+  // loads (M0) then need no read-back from a vector register
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = mt * BM;
 
@@ -216,10 +219,6 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     for (int j = 0; j < 4; ++j)
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   };
-  auto mma = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) mma_row(a, b, i);
-  };
 
   // One fragment (A block i or B block i) of k step ks, for the
   // interleaved schedule below: read n = 0..7 is A_{n/2} for even n, B_{n/2}
@@ -233,22 +232,25 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   };
   // One k step: 16 MFMAs on (a, b); the 8 reads of the next step's fragments
   // (k step nks of cA/cB into na/nb) go out one after each of the first 8
-  // MFMAs, and up to 8 DMA instructions dma(0..7) one after each of the last
-  // 8, so that every non-MFMA instruction issues while the matrix core has
-  // work queued.
+  // MFMAs, and 8 DMA instructions dma(0..7), when DMA is set, one after each
+  // of the last 8, so that every non-MFMA instruction issues while the
+  // matrix core has work queued.  DMA is a compile-time constant: a branch
+  // between MFMAs costs an instruction-fetch bubble.
   auto kstep = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], bf16x8_t (&na)[4],
                    bf16x8_t (&nb)[4], const char* cA, const char* cB, int nks, auto&& dma,
-                   bool do_dma) {
+                   auto with_dma) {
 #pragma unroll
     for (int n = 0; n < 16; ++n) {
       const int i = n >> 2, j = n & 3;
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
       if (n < 8) frag1(cA, cB, nks, n, na, nb);
-      else if (do_dma) dma(n - 8);
+      else if constexpr (decltype(with_dma)::value) dma(n - 8);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
   auto no_dma = [](int) {};
+  using True = std::true_type;
+  using False = std::false_type;
 
   // K loop over a 5-slot ring.  At the top of iteration kt stage kt (A_kt,
   // B_kt) has landed and is visible to every wave, A_kt+1 and B_kt+1 are in
@@ -262,7 +264,8 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   // last k step is split around the wait for stage kt+1 (only A_kt+2 may
   // stay outstanding) and the barrier, which publishes stage kt+1 and
   // retires every read of stage kt; its last two MFMA rows carry the reads
-  // of stage kt+1's first fragments and the DMA of B_kt+2.
+  // of stage kt+1's first fragments and the DMA of B_kt+2.  The last two
+  // iterations, which load nothing, are a separate copy of the body.
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     issue_a(0, j);
@@ -281,25 +284,25 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   stage_barrier();
   bf16x8_t fa[4], fb[4], ga[4], gb[4];
   frags(slot(0), slot(1), 0, fa, fb);
-  for (int kt = 0; kt < KT; ++kt) {
+  auto iteration = [&](int kt, auto with_dma) {
+    constexpr bool kDma = decltype(with_dma)::value;
     const char* cA = slot(2 * kt);
     const char* cB = slot(2 * kt + 1);
-    const bool n2 = kt + 2 < KT;
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_sched_barrier(0);
-    kstep(fa, fb, ga, gb, cA, cB, 1, [&](int j) { issue_a(kt + 2, j); }, n2);
+    kstep(fa, fb, ga, gb, cA, cB, 1, [&](int j) { issue_a(kt + 2, j); }, with_dma);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_sched_barrier(0);
-    kstep(ga, gb, fa, fb, cA, cB, 2, no_dma, false);
+    kstep(ga, gb, fa, fb, cA, cB, 2, no_dma, False{});
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_sched_barrier(0);
-    kstep(fa, fb, ga, gb, cA, cB, 3, no_dma, false);
+    kstep(fa, fb, ga, gb, cA, cB, 3, no_dma, False{});
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_sched_barrier(0);
     mma_row(ga, gb, 0);
     mma_row(ga, gb, 1);
     __builtin_amdgcn_sched_barrier(0);
-    if (n2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    if constexpr (kDma) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
     else wait_dma();
     stage_barrier();
     // unconditional: after the last stage this reads stale but valid LDS
@@ -310,10 +313,13 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
       const int i = 2 + (n >> 2), j = n & 3;
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[i], gb[j], acc[i][j], 0, 0, 0);
       frag1(nA, nB, 0, n, fa, fb);
-      if (n2) issue_b(kt + 2, n);
+      if constexpr (kDma) issue_b(kt + 2, n);
       __builtin_amdgcn_sched_barrier(0);
     }
-  }
+  };
+  int kt = 0;
+  for (; kt + 2 < KT; ++kt) iteration(kt, True{});
+  for (; kt < KT; ++kt) iteration(kt, False{});
   __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
   stage_barrier();   // every wave is done with the ring; LDS is reused below
 
