@@ -65,6 +65,8 @@ static_assert(4 * (kEpiWaveBytes + kEpiMetaBytes) <= (int)kLdsBytes,
 constexpr int kPersistentBlocks = 256;                          // one workgroup per CU
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) char lds_char_t;
+typedef __attribute__((address_space(3))) const bf16x8_t lds_bf16x8_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
 struct GP {
@@ -129,6 +131,28 @@ __device__ __forceinline__ void dma16(const bf16* g, char* l) {
 // lgkmcnt 0.
 constexpr int kWaitLgkm0 = 0xC07F;
 
+// s_waitcnt for at most N outstanding vector-memory operations (6-bit
+// vmcnt: low bits 3:0, high bits 15:14), leaving the export and LDS
+// counters free.
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// K-loop issue plan, as 16-bit masks over the 16 MFMAs of a k step (bit n:
+// after MFMA n): the 8 fragment reads of the next k step, the 8 direct loads
+// of A two stages ahead over k steps 0..2, and the 8 of B two stages ahead in
+// k step 3 (after the stage barrier, which frees its slot).  A wave stalls
+// when the load path's queue is full and the four waves issue in step, so
+// the loads of A are spread out.
+constexpr int kReadMask = 0x00FF;
+constexpr int kDmaA0 = 0x8800, kDmaA1 = 0x8888, kDmaA2 = 0x8800;
+constexpr int kDmaB3 = 0xFF00;
+static_assert(__builtin_popcount(kDmaA0) + __builtin_popcount(kDmaA1) +
+                      __builtin_popcount(kDmaA2) == 8 &&
+                  __builtin_popcount(kDmaB3) == 8 && __builtin_popcount(kReadMask) == 8,
+              "eight loads of each operand and eight reads per k step");
+
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Workgroup barrier of the K loop.  __syncthreads() would also wait for every
@@ -182,11 +206,11 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   // Ring of kSlots one-operand slots: A of stage k in slot 2k mod 5, B of
   // stage k in slot 2k+1 mod 5.  DMA instruction j (0..7) of an operand.
   auto slot = [&](int u) { return smem + (u % kSlots) * kStageBytes; };
-  auto issue_a = [&](int k, int j) {
-    dma16(a_src[j] + k * BK, slot(2 * k) + (wave * 8 + j) * 1024);
+  auto issue_a = [&](int k, int u, int j) {
+    dma16(a_src[j] + k * BK, slot(u) + (wave * 8 + j) * 1024);
   };
-  auto issue_b = [&](int k, int j) {
-    dma16(b_src[j] + k * BK, slot(2 * k + 1) + (wave * 8 + j) * 1024);
+  auto issue_b = [&](int k, int u, int j) {
+    dma16(b_src[j] + k * BK, slot(u) + (wave * 8 + j) * 1024);
   };
 
   f32x16_t acc[4][4];
@@ -205,121 +229,164 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   const int rB = wn * 128 + (lane & 31);
   const int swz = (lane >> 1) & 7;
   const int KT = p.K / BK;
-  // operand fragments of one 16-wide k step (4 A blocks, 4 B blocks)
-  auto frags = [&](const char* cA, const char* cB, int ks, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
-    const int ch = (2 * ks + (lane >> 5)) ^ swz;
+  // Fragment reads from a slot known at compile time: win[o][w][ks] + a
+  // constant, with window w (64 KiB of the ring) plus the lane's offset of k
+  // step ks in block 0 of operand o (0 = A, 1 = B); the slot within the
+  // window and the block (i * 4 KiB) fit the 16-bit offset of ds_read, so a
+  // read takes no address arithmetic.
+  lds_char_t* win[2][3][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      a[i] = *reinterpret_cast<const bf16x8_t*>(cA + ((rA + i * 32) * 8 + ch) * 16);
-      b[i] = *reinterpret_cast<const bf16x8_t*>(cB + ((rB + i * 32) * 8 + ch) * 16);
-    }
-  };
-  auto mma_row = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], int i) {
+  for (int o = 0; o < 2; ++o)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    for (int w = 0; w < 3; ++w)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        win[o][w][ks] = (lds_char_t*)smem + w * 65536 +
+                        ((o ? rB : rA) * 8 + ((2 * ks + (lane >> 5)) ^ swz)) * 16;
+  // Re-defines the bases (no instruction): otherwise the compiler hoists
+  // the addresses derived for every slot, operand and k step out of the
+  // loop, into registers of their own.
+  auto refresh = [&]() {
+#pragma unroll
+    for (int o = 0; o < 2; ++o)
+#pragma unroll
+      for (int w = 0; w < 3; ++w)
+        asm volatile("" : "+v"(win[o][w][0]), "+v"(win[o][w][1]), "+v"(win[o][w][2]),
+                     "+v"(win[o][w][3]));
   };
-
-  // One fragment (A block i or B block i) of k step ks, for the
-  // interleaved schedule below: read n = 0..7 is A_{n/2} for even n, B_{n/2}
-  // for odd n.
-  auto frag1 = [&](const char* cA, const char* cB, int ks, int n, bf16x8_t (&a)[4],
-                   bf16x8_t (&b)[4]) {
+  // Fragment n (0..7: A block n/2 for even n, B block n/2 for odd n) of k
+  // step ks from slots uA / uB, compile-time slots (fixed) or any slot
+  // (run-time address arithmetic).
+  auto frag_fixed = [&](int uA, int uB, int ks, int n, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
+    const int i = n >> 1;
+    uA %= kSlots;
+    uB %= kSlots;
+    if (n & 1)
+      b[i] = *reinterpret_cast<const lds_bf16x8_t*>(win[1][uB >> 1][ks] + (uB & 1) * kStageBytes +
+                                                    i * 4096);
+    else
+      a[i] = *reinterpret_cast<const lds_bf16x8_t*>(win[0][uA >> 1][ks] + (uA & 1) * kStageBytes +
+                                                    i * 4096);
+  };
+  auto frag_any = [&](int uA, int uB, int ks, int n, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
     const int ch = (2 * ks + (lane >> 5)) ^ swz;
     const int i = n >> 1;
-    if (n & 1) b[i] = *reinterpret_cast<const bf16x8_t*>(cB + ((rB + i * 32) * 8 + ch) * 16);
-    else a[i] = *reinterpret_cast<const bf16x8_t*>(cA + ((rA + i * 32) * 8 + ch) * 16);
+    if (n & 1)
+      b[i] = *reinterpret_cast<const lds_bf16x8_t*>((lds_char_t*)slot(uB) +
+                                                    ((rB + i * 32) * 8 + ch) * 16);
+    else
+      a[i] = *reinterpret_cast<const lds_bf16x8_t*>((lds_char_t*)slot(uA) +
+                                                    ((rA + i * 32) * 8 + ch) * 16);
   };
-  // One k step: 16 MFMAs on (a, b); the 8 reads of the next step's fragments
-  // (k step nks of cA/cB into na/nb) go out one after each of the first 8
-  // MFMAs, and 8 DMA instructions dma(0..7), when DMA is set, one after each
-  // of the last 8, so that every non-MFMA instruction issues while the
-  // matrix core has work queued.  DMA is a compile-time constant: a branch
-  // between MFMAs costs an instruction-fetch bubble.
-  auto kstep = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], bf16x8_t (&na)[4],
-                   bf16x8_t (&nb)[4], const char* cA, const char* cB, int nks, auto&& dma,
-                   auto with_dma) {
+  // One k step: 16 MFMAs on (a, b).  After MFMA n, read(r) issues fragment
+  // r of the next k step when bit n of RMASK is set, and dma(d) issues DMA
+  // instruction d0 + (number of DMAs already issued in this step) when bit
+  // n of DMASK is set, so that every non-MFMA instruction issues while the
+  // matrix core has work queued.  The masks are compile-time constants: a
+  // branch between MFMAs costs an instruction-fetch bubble.
+  auto kstep = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], auto&& read, auto&& dma,
+                   auto rmask, auto dmask, int d0) {
+    constexpr int RM = decltype(rmask)::value, DM = decltype(dmask)::value;
 #pragma unroll
     for (int n = 0; n < 16; ++n) {
       const int i = n >> 2, j = n & 3;
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-      if (n < 8) frag1(cA, cB, nks, n, na, nb);
-      else if constexpr (decltype(with_dma)::value) dma(n - 8);
+      if ((RM >> n) & 1) read(__builtin_popcount(RM & ((1 << n) - 1)));
+      if ((DM >> n) & 1) dma(d0 + __builtin_popcount(DM & ((1 << n) - 1)));
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto no_dma = [](int) {};
-  using True = std::true_type;
-  using False = std::false_type;
+  using Reads = std::integral_constant<int, kReadMask>;
+  using A0 = std::integral_constant<int, kDmaA0>;
+  using A1 = std::integral_constant<int, kDmaA1>;
+  using A2 = std::integral_constant<int, kDmaA2>;
+  using B3 = std::integral_constant<int, kDmaB3>;
+  constexpr int kA01 = __builtin_popcount(kDmaA0) + __builtin_popcount(kDmaA1);
 
-  // K loop over a 5-slot ring.  At the top of iteration kt stage kt (A_kt,
-  // B_kt) has landed and is visible to every wave, A_kt+1 and B_kt+1 are in
-  // flight, and the fragments of stage kt's first k step (f) were read just
-  // before.  A slot is refilled as soon as a barrier retires its last reads:
-  // A_kt+2 goes into the slot of B_kt-1 during k step 0, and B_kt+2 into the
-  // slot of A_kt right after this iteration's barrier, so each stage has
-  // about two iterations of MFMA work to land.  Before each k step, the
-  // reads issued during the previous one are waited for; at most 8 LDS reads
-  // are ever outstanding (the 4-bit lgkm counter cannot express more).  The
-  // last k step is split around the wait for stage kt+1 (only A_kt+2 may
-  // stay outstanding) and the barrier, which publishes stage kt+1 and
-  // retires every read of stage kt; its last two MFMA rows carry the reads
-  // of stage kt+1's first fragments and the DMA of B_kt+2.  The last two
-  // iterations, which load nothing, are a separate copy of the body.
+  // K loop over a 5-slot ring (A of stage k in slot 2k mod 5, B in 2k+1
+  // mod 5).  At the top of iteration kt stage kt has landed and is visible
+  // to every wave, A_kt+1 and B_kt+1 are in flight, and the fragments of
+  // stage kt's first k step were read just before.  A slot is refilled as
+  // soon as a barrier retires its last reads: A_kt+2 goes into the slot of
+  // B_kt-1 during k steps 0..2, and B_kt+2 into the slot of A_kt right after
+  // this iteration's barrier, so each stage has one to two iterations of
+  // MFMA work to land.  Before each k step, the reads issued during the
+  // previous one are waited for; at most 8 LDS reads are ever outstanding
+  // (the 4-bit lgkm counter cannot express more).  The wait for stage kt+1
+  // (only A_kt+2, issued last, may stay outstanding) and the barrier, which
+  // publishes stage kt+1 and retires every read of stage kt, come before the
+  // last k step, whose 16 MFMAs then cover the reads of stage kt+1's first
+  // fragments.
+  //
+  // Every iteration issues the same loads: past the last stage the stage
+  // index is clamped, so the last two iterations refill free slots with
+  // data that is never read (two stages of extra L2 traffic per tile) and
+  // the body has no conditional code.  The loop runs in groups of five, the
+  // ring's period, in which every slot is a compile-time constant; the
+  // KT mod 5 iterations before them take the same body with run-time slots.
+  const int kLast = KT - 1;
+  // stage k's slots are shifted by sh so that the groups of five, which
+  // follow the KT mod 5 iterations with run-time slots, start at phase 0
+  const int sh = (kSlots - KT % kSlots) % kSlots;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    issue_a(0, j);
-    issue_b(0, j);
+    issue_a(0, 2 * sh, j);
+    issue_b(0, 2 * sh + 1, j);
   }
-  if (KT > 1) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      issue_a(1, j);
-      issue_b(1, j);
-    }
-    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-  } else {
-    wait_dma();
+  for (int j = 0; j < 8; ++j) {
+    issue_a(min(1, kLast), 2 * sh + 2, j);
+    issue_b(min(1, kLast), 2 * sh + 3, j);
   }
+  wait_vm<16>();
   stage_barrier();
   bf16x8_t fa[4], fb[4], ga[4], gb[4];
-  frags(slot(0), slot(1), 0, fa, fb);
-  auto iteration = [&](int kt, auto with_dma) {
-    constexpr bool kDma = decltype(with_dma)::value;
-    const char* cA = slot(2 * kt);
-    const char* cB = slot(2 * kt + 1);
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    __builtin_amdgcn_sched_barrier(0);
-    kstep(fa, fb, ga, gb, cA, cB, 1, [&](int j) { issue_a(kt + 2, j); }, with_dma);
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    __builtin_amdgcn_sched_barrier(0);
-    kstep(ga, gb, fa, fb, cA, cB, 2, no_dma, False{});
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    __builtin_amdgcn_sched_barrier(0);
-    kstep(fa, fb, ga, gb, cA, cB, 3, no_dma, False{});
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    __builtin_amdgcn_sched_barrier(0);
-    mma_row(ga, gb, 0);
-    mma_row(ga, gb, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    if constexpr (kDma) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else wait_dma();
-    stage_barrier();
-    // unconditional: after the last stage this reads stale but valid LDS
-    const char* nA = slot(2 * kt + 2);
-    const char* nB = slot(2 * kt + 3);
 #pragma unroll
-    for (int n = 0; n < 8; ++n) {
-      const int i = 2 + (n >> 2), j = n & 3;
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[i], gb[j], acc[i][j], 0, 0, 0);
-      frag1(nA, nB, 0, n, fa, fb);
-      if constexpr (kDma) issue_b(kt + 2, n);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+  for (int n = 0; n < 8; ++n) frag_any(2 * sh, 2 * sh + 1, 0, n, fa, fb);
+  // iteration kt, with P = (kt + sh) mod 5 (a compile-time constant when FIXED)
+  auto iteration = [&](int kt, int P, auto fixed) {
+    constexpr bool kFixed = decltype(fixed)::value;
+    auto frag = [&](int uA, int uB, int ks, int n, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
+      if constexpr (kFixed) frag_fixed(uA, uB, ks, n, a, b);
+      else frag_any(uA, uB, ks, n, a, b);
+    };
+    const int kd = min(kt + 2, kLast);
+    const int uA = 2 * P, uB = 2 * P + 1;
+    auto dma_a = [&](int j) { issue_a(kd, 2 * P + 4, j); };
+    if constexpr (kFixed) refresh();
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_sched_barrier(0);
+    kstep(fa, fb, [&](int n) { frag(uA, uB, 1, n, ga, gb); }, dma_a, Reads{}, A0{}, 0);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_sched_barrier(0);
+    kstep(ga, gb, [&](int n) { frag(uA, uB, 2, n, fa, fb); }, dma_a, Reads{}, A1{},
+          __builtin_popcount(kDmaA0));
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_sched_barrier(0);
+    kstep(fa, fb, [&](int n) { frag(uA, uB, 3, n, ga, gb); }, dma_a, Reads{}, A2{}, kA01);
+    // every read of stage kt has completed: wait for stage kt+1 (A_kt+2,
+    // issued last, may stay outstanding), publish it, retire stage kt's slots
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm<8>();
+    stage_barrier();
+    // after the last stage this reads stale but valid LDS
+    kstep(ga, gb, [&](int n) { frag(uA + 2, uB + 2, 0, n, fa, fb); },
+          [&](int j) { issue_b(kd, 2 * P, j); }, Reads{}, B3{}, 0);
   };
+  using Fixed = std::true_type;
+  using Any = std::false_type;
+  const int r = KT % kSlots;
   int kt = 0;
-  for (; kt + 2 < KT; ++kt) iteration(kt, True{});
-  for (; kt < KT; ++kt) iteration(kt, False{});
+  for (; kt < r; ++kt) iteration(kt, (kt + sh) % kSlots, Any{});
+  for (; kt < KT; kt += kSlots) {
+    iteration(kt, 0, Fixed{});
+    iteration(kt + 1, 1, Fixed{});
+    iteration(kt + 2, 2, Fixed{});
+    iteration(kt + 3, 3, Fixed{});
+    iteration(kt + 4, 4, Fixed{});
+  }
+  wait_dma();   // the clamped loads of the last iterations land before LDS is reused
   __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
   stage_barrier();   // every wave is done with the ring; LDS is reused below
 

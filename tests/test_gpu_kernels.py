@@ -243,6 +243,12 @@ def test_kv_generate_matches_oracle(dt, hd, fold):
     pos = rng.integers(0, 2000, n_tok).astype(np.int32)
     slot = rng.permutation(n_tok + 11)[:n_tok].astype(np.int32)
     kc, vc = _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_tok + 11, 2048, fold)
+    _check_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_tok + 11, kc, vc)
+
+
+def _check_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_slots, kc, vc):
+    N, Dq = shape.n_layers, shape.n_heads * shape.head_dim
+    n_tok = n_slots - 11
     gen = O.kv_generate({"layers": _layers_for_oracle(wkv, gain, Dq)}, shape, s[rows], el[rows],
                         pos[rows])
     K, V = host64(kc), host64(vc)
@@ -262,6 +268,22 @@ def test_kv_generate_matches_oracle(dt, hd, fold):
     # exactly the (layer, slot) pairs of skipped layers were written
     np.testing.assert_array_equal(~np.isnan(K).any(axis=(2, 3)), written)
     np.testing.assert_array_equal(~np.isnan(V).any(axis=(2, 3)), written)
+
+
+@pytest.mark.parametrize("D", [64, 128, 192, 320, 448, 512, 576, 704, 1024])
+def test_kv_generate_k_depths(D):
+    """The GEMM K loop at 1..16 stages of 64: fewer stages than the
+    five-slot ring, every remainder of KT mod 5 before the groups of five,
+    and the clamped loads past the last stage."""
+    say(f"kv_generate K depth D={D}")
+    dt, N, H, hd, n_tok = "bf16", 3, 2, 128, 300
+    shape, s, wkv, gain, el = _kv_case(dt, N, D, H, hd, n_tok, 500 + D, std=D ** -0.5)
+    rng = np.random.default_rng(D)
+    rows = np.sort(rng.choice(n_tok, 257, replace=False)).astype(np.int32)
+    pos = rng.integers(0, 2000, n_tok).astype(np.int32)
+    slot = rng.permutation(n_tok + 11)[:n_tok].astype(np.int32)
+    kc, vc = _run_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_tok + 11, 2048)
+    _check_kv(dt, shape, s, wkv, gain, el, rows, pos, slot, n_tok + 11, kc, vc)
 
 
 def test_kv_generate_equals_layer_by_layer():
