@@ -31,12 +31,25 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "llama7b_prefill_8x2048_hbm_traffic.json")
 
 
-def sources_sha256():
-    """Hash of the HIP sources, the same way the traffic summary records it."""
+# HIP sources each kernel family is built from (its traffic figure is void
+# once any of them changes)
+FAMILY_SOURCES = {
+    "gemm": ("gemm.hip", "common.h"), "kv_generate": ("gemm.hip", "kvgen.hip", "common.h"),
+    "attention": ("attention.hip", "common.h"), "exit_test": ("exit_test.hip", "common.h"),
+    "compact_single": ("compact.hip", "common.h"),
+}
+
+
+def family_sources(fam):
+    return FAMILY_SOURCES["gemm" if fam.startswith("gemm_") else fam]
+
+
+def sources_sha256(files):
+    """Hash of the given HIP sources, the same way the traffic summary records it."""
     import hashlib
     h = hashlib.sha256()
     d = os.path.join(HERE, "paper_2601_03700_amd", "csrc")
-    for f in sorted(os.listdir(d)):
+    for f in sorted(files):
         with open(os.path.join(d, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -45,17 +58,19 @@ def sources_sha256():
 def measured_traffic(fam):
     """HBM bytes per launch of a kernel family from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary (each scaled by what it reads for a
-    device copy of known size), or None when the HIP sources changed after
-    the counters were taken."""
+    device copy of known size), or None when the sources of that kernel
+    changed after the counters were taken."""
     try:
         with open(TRAFFIC_FILE) as fh:
             d = json.load(fh)
     except OSError:
         return None
-    if d.get("source_sha256") != sources_sha256():
-        return None
     k = d.get("kernels", {}).get(fam)
-    return None if k is None else k["traffic_bytes"]
+    if k is None or fam not in FAMILY_SOURCES and not fam.startswith("gemm_"):
+        return None
+    if k.get("source_sha256") != sources_sha256(family_sources(fam)):
+        return None
+    return k["traffic_bytes"]
 
 
 def log(*a):
