@@ -95,7 +95,7 @@ __global__ __launch_bounds__(kGenThreads) void attend_generic_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// prefill plan: tiles of <= 64 consecutive query entries of one sequence
+// prefill plan: tiles of <= QT consecutive query entries of one sequence
 // ---------------------------------------------------------------------------
 constexpr int QT = 128;  // queries per tile (4 waves x 2 groups of 16)
 constexpr int KB = 64;   // keys per LDS block
@@ -144,6 +144,15 @@ __global__ __launch_bounds__(1024) void attend_plan_kernel(const int32_t* __rest
 // causal: keys 0..pos of each query; else keys 0..key_len[b]-1 of the
 // sequence, all of them for every query (bidirectional).  key_live
 // (nullable) drops keys whose byte is 0.
+//
+// One workgroup per (tile of <= 128 queries of one sequence, head); each of
+// the four waves holds two groups of 16 queries, so every K and V fragment
+// read from LDS serves two MFMAs, and two workgroups share a CU, so one
+// wave's softmax overlaps the other's MFMAs on each SIMD.  K and V advance in blocks
+// of 64 keys through two LDS buffers: the global loads of block kb+1 are
+// issued into registers before block kb is computed and written to the
+// other buffer after it, so their latency hides behind the block's MFMAs,
+// and one barrier per block orders the buffers.
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     int H, float scale_log2, int causal, const bf16* __restrict__ q,
@@ -156,9 +165,12 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
   constexpr int DS = HD / 32;     // 32-wide dim steps for S
   constexpr int DB = HD / 16;     // 16-row dim blocks of O^T
   constexpr int QG = QT / 64;     // 16-query groups per wave
-  __shared__ __attribute__((aligned(16))) bf16 sK[KB * KLD];
-  __shared__ __attribute__((aligned(16))) bf16 sVt[HD * VLD];
-  __shared__ uint8_t sLive[KB];
+  constexpr int CH = HD / 8;      // 16-byte chunks per row
+  constexpr int KPT = (KB * CH + 255) / 256;          // K chunks per thread
+  constexpr int VPT = ((KB / 4) * CH + 255) / 256;    // V 4-key groups per thread
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][KB * KLD];
+  __shared__ __attribute__((aligned(16))) bf16 sVt[2][HD * VLD];
+  __shared__ uint8_t sLive[2][KB];
   const int nt = *n_tiles;
   if ((int)blockIdx.x >= nt) return;
   const int2 tile = tiles[nt - 1 - blockIdx.x];   // longest (latest) tiles first
@@ -196,43 +208,79 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     l_run[qg] = 0.0f;
   }
 
-  const int nkb = (tend + KB - 1) / KB;
-  for (int kb = 0; kb < nkb; ++kb) {
+  // ---- block staging: fetch() loads block kb into registers (keys past
+  // the range as zeros), stash() writes them to LDS buffer u: K [64][HD]
+  // row-major, V^T [HD][64] (a thread takes 4 keys x 8 dims and writes eight
+  // 8-byte runs of 4 keys of one dim)
+  uint4 kr[KPT], vr[VPT][4];
+  uint8_t live = 0;
+  auto fetch = [&](int kb) {
     const int t0 = kb * KB;
-    if (tid < KB) sLive[tid] = (t0 + tid < tend && (!key_live || key_live[kbase + t0 + tid])) ? 1 : 0;
-    // ---- stage K [64][HD] row-major; keys past the range are zero
-    constexpr int CH = HD / 8;  // 16-byte chunks per row
 #pragma unroll
-    for (int e = tid; e < KB * CH; e += 256) {
+    for (int i = 0; i < KPT; ++i) {
+      const int e = tid + 256 * i;
       const int r = e / CH, c = (e % CH) * 8;
       const int t = t0 + r;
-      uint4 kv = make_uint4(0, 0, 0, 0);
-      if (t < tend) kv = *reinterpret_cast<const uint4*>(kc + (kbase + t) * rs + h * HD + c);
-      *reinterpret_cast<uint4*>(sK + r * KLD + c) = kv;
+      kr[i] = make_uint4(0, 0, 0, 0);
+      if (e < KB * CH && t < tend)
+        kr[i] = *reinterpret_cast<const uint4*>(kc + (kbase + t) * rs + h * HD + c);
     }
-    // ---- stage V^T [HD][64]: a thread takes 4 keys x 8 dims and writes eight
-    // 8-byte runs (4 keys of one dim)
 #pragma unroll
-    for (int e = tid; e < (KB / 4) * CH; e += 256) {
+    for (int i = 0; i < VPT; ++i) {
+      const int e = tid + 256 * i;
       const int kg = e % (KB / 4), dc = e / (KB / 4);
-      uint32_t w[4][4];
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int t = t0 + 4 * kg + kk;
-        uint4 vv = make_uint4(0, 0, 0, 0);
-        if (t < tend) vv = *reinterpret_cast<const uint4*>(vc + (kbase + t) * rs + h * HD + dc * 8);
-        w[kk][0] = vv.x; w[kk][1] = vv.y; w[kk][2] = vv.z; w[kk][3] = vv.w;
-      }
-#pragma unroll
-      for (int d = 0; d < 8; ++d) {
-        const int sh = (d & 1) * 16;
-        const uint32_t e0 = (w[0][d >> 1] >> sh) & 0xffff, e1 = (w[1][d >> 1] >> sh) & 0xffff;
-        const uint32_t e2 = (w[2][d >> 1] >> sh) & 0xffff, e3 = (w[3][d >> 1] >> sh) & 0xffff;
-        *reinterpret_cast<uint2*>(sVt + (dc * 8 + d) * VLD + 4 * kg) =
-            make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+        vr[i][kk] = make_uint4(0, 0, 0, 0);
+        if (e < (KB / 4) * CH && t < tend)
+          vr[i][kk] = *reinterpret_cast<const uint4*>(vc + (kbase + t) * rs + h * HD + dc * 8);
       }
     }
-    __syncthreads();
+    if (tid < KB) live = (t0 + tid < tend && (!key_live || key_live[kbase + t0 + tid])) ? 1 : 0;
+  };
+  auto stash = [&](int u) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int e = tid + 256 * i;
+      if (e < KB * CH) {
+        const int r = e / CH, c = (e % CH) * 8;
+        *reinterpret_cast<uint4*>(&sK[u][r * KLD + c]) = kr[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int e = tid + 256 * i;
+      if (e < (KB / 4) * CH) {
+        const int kg = e % (KB / 4), dc = e / (KB / 4);
+        const uint32_t w[4][4] = {{vr[i][0].x, vr[i][0].y, vr[i][0].z, vr[i][0].w},
+                                  {vr[i][1].x, vr[i][1].y, vr[i][1].z, vr[i][1].w},
+                                  {vr[i][2].x, vr[i][2].y, vr[i][2].z, vr[i][2].w},
+                                  {vr[i][3].x, vr[i][3].y, vr[i][3].z, vr[i][3].w}};
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+          const int sh = (d & 1) * 16;
+          const uint32_t e0 = (w[0][d >> 1] >> sh) & 0xffff, e1 = (w[1][d >> 1] >> sh) & 0xffff;
+          const uint32_t e2 = (w[2][d >> 1] >> sh) & 0xffff, e3 = (w[3][d >> 1] >> sh) & 0xffff;
+          *reinterpret_cast<uint2*>(&sVt[u][(dc * 8 + d) * VLD + 4 * kg]) =
+              make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+        }
+      }
+    }
+    if (tid < KB) sLive[u][tid] = live;
+  };
+
+  const int nkb = (tend + KB - 1) / KB;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int u = kb & 1;
+    const int t0 = kb * KB;
+    if (kb + 1 < nkb) fetch(kb + 1);   // in flight during this block's MFMAs
+    const bf16* cK = sK[u];
+    const bf16* cV = sVt[u];
+    const uint8_t* cL = sLive[u];
 
     // ---- S^T = K Q^T: 4 key sub-blocks of 16; each K fragment serves QG groups
     f32x4_t s[QG][4];
@@ -243,7 +291,7 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
         const bf16x8_t a =
-            *reinterpret_cast<const bf16x8_t*>(sK + (sb * 16 + c16) * KLD + ds * 32 + g * 8);
+            *reinterpret_cast<const bf16x8_t*>(cK + (sb * 16 + c16) * KLD + ds * 32 + g * 8);
 #pragma unroll
         for (int qg = 0; qg < QG; ++qg)
           s[qg][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qg][ds], s[qg][sb], 0, 0, 0);
@@ -260,7 +308,7 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
         for (int v = 0; v < 4; ++v) {
           const int kl = sb * 16 + g * 4 + v;
           float x = s[qg][sb][v] * scale_log2;
-          x = (t0 + kl <= qpos[qg] && sLive[kl]) ? x : -INFINITY;
+          x = (t0 + kl <= qpos[qg] && cL[kl]) ? x : -INFINITY;
           s[qg][sb][v] = x;
           mloc = fmaxf(mloc, x);
         }
@@ -296,14 +344,17 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp) {
-        const bf16* vr = sVt + (db * 16 + c16) * VLD + kp * 32 + g * 4;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+        const bf16* vp = cV + (db * 16 + c16) * VLD + kp * 32 + g * 4;
+        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 16);
         const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
 #pragma unroll
         for (int qg = 0; qg < QG; ++qg)
           o[qg][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qg][kp], o[qg][db], 0, 0, 0);
       }
+    // the other buffer was last read in block kb-1, which every wave finished
+    // before the previous barrier
+    if (kb + 1 < nkb) stash(u ^ 1);
     __syncthreads();
   }
 #pragma unroll
