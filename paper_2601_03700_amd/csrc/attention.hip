@@ -98,6 +98,7 @@ __global__ __launch_bounds__(kGenThreads) void attend_generic_kernel(
 // prefill plan: tiles of <= QT consecutive query entries of one sequence
 // ---------------------------------------------------------------------------
 constexpr int QT = 128;  // queries per tile (4 waves x 2 groups of 16)
+constexpr int kPrefillThreads = 256;
 constexpr int KB = 64;   // keys per LDS block
 
 __global__ __launch_bounds__(1024) void attend_plan_kernel(const int32_t* __restrict__ rows,
@@ -148,34 +149,54 @@ __global__ __launch_bounds__(1024) void attend_plan_kernel(const int32_t* __rest
 // One workgroup per (tile of <= 128 queries of one sequence, head); each of
 // the four waves holds two groups of 16 queries, so every K and V fragment
 // read from LDS serves two MFMAs, and two workgroups share a CU, so one
-// wave's softmax overlaps the other's MFMAs on each SIMD.  K and V advance in blocks
-// of 64 keys through two LDS buffers: the global loads of block kb+1 are
-// issued into registers before block kb is computed and written to the
-// other buffer after it, so their latency hides behind the block's MFMAs,
-// and one barrier per block orders the buffers.
+// wave's softmax overlaps the other's MFMAs on each SIMD.  K and V advance
+// in blocks of 64 keys through two LDS stages filled by direct
+// global->LDS loads: the loads of block kb+1 are issued before block kb is
+// computed, and one barrier per block publishes the next stage and retires
+// the current one.  V stays row-major in LDS; the A operand of O^T = V^T P^T
+// is read with the LDS transpose read.
 template <int HD>
-__global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
+__global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
     int H, float scale_log2, int causal, const bf16* __restrict__ q,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ pos,
     const int32_t* __restrict__ seq, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
     int s_max, const int32_t* __restrict__ key_len, const uint8_t* __restrict__ key_live,
-    const int2* __restrict__ tiles, const int32_t* __restrict__ n_tiles, bf16* __restrict__ out) {
-  constexpr int KLD = HD + 8;     // sK row stride (elements)
-  constexpr int VLD = KB + 8;     // sVt row stride
-  constexpr int DS = HD / 32;     // 32-wide dim steps for S
-  constexpr int DB = HD / 16;     // 16-row dim blocks of O^T
-  constexpr int QG = QT / 64;     // 16-query groups per wave
-  constexpr int CH = HD / 8;      // 16-byte chunks per row
-  constexpr int KPT = (KB * CH + 255) / 256;          // K chunks per thread
-  constexpr int VPT = ((KB / 4) * CH + 255) / 256;    // V 4-key groups per thread
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][KB * KLD];
-  __shared__ __attribute__((aligned(16))) bf16 sVt[2][HD * VLD];
-  __shared__ uint8_t sLive[2][KB];
+    const int2* __restrict__ tiles, const int32_t* __restrict__ n_tiles, int max_tiles,
+    bf16* __restrict__ out) {
+  constexpr int NT = kPrefillThreads;
+  constexpr int DS = HD / 32;               // 32-wide dim steps for S
+  constexpr int DB = HD / 16;               // 16-row dim blocks of O^T
+  constexpr int QG = QT / (16 * (NT / 64)); // 16-query groups per wave
+  constexpr int ROWB = HD * 2;              // bytes per K or V row
+  constexpr int NCH = ROWB / 16;            // 16-byte chunks per row
+  constexpr int RPI = 1024 / ROWB;          // rows per direct-load instruction
+  constexpr int BLK = KB * ROWB;            // bytes of one block of K (or V)
+  constexpr int DPW = (KB / RPI) / (NT / 64);   // direct loads per wave and operand
+  static_assert(DPW >= 1 && (KB / RPI) % (NT / 64) == 0, "block splits over the waves");
+  // [stage][K = 0, V = 1][block]
+  __shared__ __attribute__((aligned(1024))) char sKV[2][2][BLK];
+  __shared__ uint64_t sLive[2];
+
+  // Work item of this workgroup.  The hardware deals consecutive workgroup
+  // ids round-robin to the 8 XCDs; when the heads split evenly over them
+  // (1-D grid), XCD x takes heads x, x+8, ... one after another, each head's
+  // tiles longest first, so the tiles in flight on an XCD share a few
+  // sequences' K/V in its L2.  Otherwise blockIdx = (tile, head).
   const int nt = *n_tiles;
-  if ((int)blockIdx.x >= nt) return;
-  const int2 tile = tiles[nt - 1 - blockIdx.x];   // longest (latest) tiles first
-  const int h = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int ti, h;
+  if (gridDim.y == 1 && H > 1) {
+    const int k = blockIdx.x >> 3;
+    ti = k % max_tiles;
+    h = (blockIdx.x & 7) + 8 * (k / max_tiles);
+    if (h >= H) return;
+  } else {
+    ti = blockIdx.x;
+    h = blockIdx.y;
+  }
+  if (ti >= nt) return;
+  const int2 tile = tiles[nt - 1 - ti];   // longest (latest) tiles first
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
   const int64_t rs = (int64_t)H * HD;
 
@@ -207,80 +228,61 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     m_run[qg] = -INFINITY;
     l_run[qg] = 0.0f;
   }
+  // smallest position among the wave's valid queries: blocks of keys at or
+  // below it (and inside the range, without a live-key mask) need no mask
+  int wmin = INT_MAX;
+#pragma unroll
+  for (int qg = 0; qg < QG; ++qg) wmin = min(wmin, qvalid[qg] ? qpos[qg] : INT_MAX);
+  wmin = min(wmin, __shfl_xor(wmin, 1, 64));
+  wmin = min(wmin, __shfl_xor(wmin, 2, 64));
+  wmin = min(wmin, __shfl_xor(wmin, 4, 64));
+  wmin = min(wmin, __shfl_xor(wmin, 8, 64));
 
-  // ---- block staging: fetch() loads block kb into registers (keys past
-  // the range as zeros), stash() writes them to LDS buffer u: K [64][HD]
-  // row-major, V^T [HD][64] (a thread takes 4 keys x 8 dims and writes eight
-  // 8-byte runs of 4 keys of one dim)
-  uint4 kr[KPT], vr[VPT][4];
-  uint8_t live = 0;
-  auto fetch = [&](int kb) {
+  // ---- K and V blocks reach LDS by direct global->LDS loads (lane l of an
+  // instruction writes 16 bytes at base + 16 l, i.e. RPI whole rows), two
+  // stages deep.  The 16-byte chunk c of row r is stored at position
+  // c ^ fK(r) (K) or c ^ fV(r) (V): the K fragment reads (16 rows, one
+  // chunk) and the V transpose reads (4 rows x 2 chunks per 16 lanes) then
+  // fall on distinct banks.  Keys past the range re-read the range's last
+  // key: finite values the mask gives weight 0.
+  auto fK = [](int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); };
+  auto fV = [](int r) { return HD == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); };
+  auto issue = [&](int kb, int u) {
     const int t0 = kb * KB;
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int e = tid + 256 * i;
-      const int r = e / CH, c = (e % CH) * 8;
-      const int t = t0 + r;
-      kr[i] = make_uint4(0, 0, 0, 0);
-      if (e < KB * CH && t < tend)
-        kr[i] = *reinterpret_cast<const uint4*>(kc + (kbase + t) * rs + h * HD + c);
-    }
+    for (int op = 0; op < 2; ++op) {
+      const bf16* src = op ? vc : kc;
 #pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int e = tid + 256 * i;
-      const int kg = e % (KB / 4), dc = e / (KB / 4);
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int t = t0 + 4 * kg + kk;
-        vr[i][kk] = make_uint4(0, 0, 0, 0);
-        if (e < (KB / 4) * CH && t < tend)
-          vr[i][kk] = *reinterpret_cast<const uint4*>(vc + (kbase + t) * rs + h * HD + dc * 8);
+      for (int j = 0; j < DPW; ++j) {
+        const int qd = wave * DPW + j;
+        const int r = qd * RPI + lane / NCH;
+        const int c = (lane % NCH) ^ (op ? fV(r) : fK(r));
+        const int t = min(t0 + r, tend - 1);
+        __builtin_amdgcn_global_load_lds(
+            (__attribute__((address_space(1))) void*)(src + (kbase + t) * rs + h * HD + c * 8),
+            (__attribute__((address_space(3))) void*)(&sKV[u][op][qd * 1024]), 16, 0, 0);
       }
     }
-    if (tid < KB) live = (t0 + tid < tend && (!key_live || key_live[kbase + t0 + tid])) ? 1 : 0;
+    if (key_live && wave == 0) {
+      const bool lv = t0 + lane < tend && key_live[kbase + min(t0 + lane, tend - 1)] != 0;
+      const uint64_t m = __ballot(lv);
+      if (lane == 0) sLive[u] = m;
+    }
   };
-  auto stash = [&](int u) {
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int e = tid + 256 * i;
-      if (e < KB * CH) {
-        const int r = e / CH, c = (e % CH) * 8;
-        *reinterpret_cast<uint4*>(&sK[u][r * KLD + c]) = kr[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int e = tid + 256 * i;
-      if (e < (KB / 4) * CH) {
-        const int kg = e % (KB / 4), dc = e / (KB / 4);
-        const uint32_t w[4][4] = {{vr[i][0].x, vr[i][0].y, vr[i][0].z, vr[i][0].w},
-                                  {vr[i][1].x, vr[i][1].y, vr[i][1].z, vr[i][1].w},
-                                  {vr[i][2].x, vr[i][2].y, vr[i][2].z, vr[i][2].w},
-                                  {vr[i][3].x, vr[i][3].y, vr[i][3].z, vr[i][3].w}};
-#pragma unroll
-        for (int d = 0; d < 8; ++d) {
-          const int sh = (d & 1) * 16;
-          const uint32_t e0 = (w[0][d >> 1] >> sh) & 0xffff, e1 = (w[1][d >> 1] >> sh) & 0xffff;
-          const uint32_t e2 = (w[2][d >> 1] >> sh) & 0xffff, e3 = (w[3][d >> 1] >> sh) & 0xffff;
-          *reinterpret_cast<uint2*>(&sVt[u][(dc * 8 + d) * VLD + 4 * kg]) =
-              make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
-        }
-      }
-    }
-    if (tid < KB) sLive[u][tid] = live;
-  };
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
   const int nkb = (tend + KB - 1) / KB;
-  fetch(0);
-  stash(0);
-  __syncthreads();
+  if (nkb > 0) issue(0, 0);
+  __syncthreads();   // waits for every wave's loads, then publishes stage 0
   for (int kb = 0; kb < nkb; ++kb) {
     const int u = kb & 1;
     const int t0 = kb * KB;
-    if (kb + 1 < nkb) fetch(kb + 1);   // in flight during this block's MFMAs
-    const bf16* cK = sK[u];
-    const bf16* cV = sVt[u];
-    const uint8_t* cL = sLive[u];
+    // the other stage was last read in block kb-1, which every wave
+    // finished before the previous barrier
+    if (kb + 1 < nkb) issue(kb + 1, u ^ 1);
+    const char* cK = sKV[u][0];
+    const char* cV = sKV[u][1];
 
     // ---- S^T = K Q^T: 4 key sub-blocks of 16; each K fragment serves QG groups
     f32x4_t s[QG][4];
@@ -288,74 +290,107 @@ __global__ __launch_bounds__(256, 2) void attend_prefill_kernel(
     for (int sb = 0; sb < 4; ++sb) {
 #pragma unroll
       for (int qg = 0; qg < QG; ++qg) s[qg][sb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      const int r = sb * 16 + c16;
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
-        const bf16x8_t a =
-            *reinterpret_cast<const bf16x8_t*>(cK + (sb * 16 + c16) * KLD + ds * 32 + g * 8);
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
+            cK + r * ROWB + ((4 * ds + g) ^ fK(r)) * 16);
 #pragma unroll
         for (int qg = 0; qg < QG; ++qg)
           s[qg][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qg][ds], s[qg][sb], 0, 0, 0);
       }
     }
+    // ---- mask (only blocks that reach past a query's position, past the
+    // range, or under a live-key mask), in the exp2 domain
+    const bool full = !key_live && t0 + KB <= tend && t0 + KB - 1 <= wmin;
+    if (!full) {
+      const uint64_t lm = key_live ? sLive[u] : ~0ull;
+#pragma unroll
+      for (int qg = 0; qg < QG; ++qg)
+#pragma unroll
+        for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int kl = sb * 16 + g * 4 + v;
+            const bool keep = t0 + kl <= qpos[qg] && ((lm >> kl) & 1);
+            s[qg][sb][v] = keep ? s[qg][sb][v] : -INFINITY;
+          }
+    }
     bf16x8_t pb[QG][2];
+    bool grew = false;
+    float alpha[QG];
 #pragma unroll
     for (int qg = 0; qg < QG; ++qg) {
-      // ---- mask, running max
+      // ---- running max (scale > 0: the max of the raw scores is taken
+      // first and scaled once)
       float mloc = -INFINITY;
 #pragma unroll
       for (int sb = 0; sb < 4; ++sb)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int kl = sb * 16 + g * 4 + v;
-          float x = s[qg][sb][v] * scale_log2;
-          x = (t0 + kl <= qpos[qg] && cL[kl]) ? x : -INFINITY;
-          s[qg][sb][v] = x;
-          mloc = fmaxf(mloc, x);
-        }
+        mloc = fmaxf(fmaxf(mloc, fmaxf(s[qg][sb][0], s[qg][sb][1])),
+                     fmaxf(s[qg][sb][2], s[qg][sb][3]));
       mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run[qg], mloc);
-      const float alpha = (m_new == -INFINITY) ? 1.0f : exp2f(m_run[qg] - m_new);
+      const float m_new = fmaxf(m_run[qg], mloc * scale_log2);
+      grew |= m_new > m_run[qg];
+      alpha[qg] = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run[qg] - m_new);
       m_run[qg] = m_new;
-      l_run[qg] *= alpha;
-#pragma unroll
-      for (int i = 0; i < DB; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) o[qg][i][v] *= alpha;
-      // ---- P = exp2(S - m) packed as the B operand (key order: sub-block pairs)
+      l_run[qg] *= alpha[qg];
+      // ---- P = exp2(S * scale - m) packed as the B operand (key order:
+      // sub-block pairs); a masked score (-inf) gives exp2(-inf) = 0
+      const float msub = (m_new == -INFINITY) ? 0.0f : m_new;
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp) {
-        uint16_t pv[8];
+        uint32_t pw[4];
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const float x = s[qg][2 * kp + hh][v];
-            const float ev = (x == -INFINITY) ? 0.0f : exp2f(x - m_new);
-            const bf16 eb = f2bf(ev);
-            l_run[qg] += bf2f(eb);
-            pv[hh * 4 + v] = eb;
+          for (int v = 0; v < 4; v += 2) {
+            const float e0 =
+                __builtin_amdgcn_exp2f(fmaf(s[qg][2 * kp + hh][v], scale_log2, -msub));
+            const float e1 =
+                __builtin_amdgcn_exp2f(fmaf(s[qg][2 * kp + hh][v + 1], scale_log2, -msub));
+            const uint32_t w = pack_bf16x2(e0, e1);
+            // the normaliser sums the rounded weights the MFMA multiplies
+            l_run[qg] += __uint_as_float(w << 16) + __uint_as_float(w & 0xffff0000u);
+            pw[hh * 2 + v / 2] = w;
           }
-        pb[qg][kp] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(pv));
+        pb[qg][kp] = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
       }
     }
-    // ---- O^T += V^T P^T; each V^T fragment serves QG groups
+    // ---- rescale O only when some query's running max grew in this block
+    // (alpha = 1 otherwise: skipping the multiply changes nothing)
+    if (__any(grew)) {
+#pragma unroll
+      for (int qg = 0; qg < QG; ++qg)
+#pragma unroll
+        for (int i = 0; i < DB; ++i)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[qg][i][v] *= alpha[qg];
+    }
+    // ---- O^T += V^T P^T; each V^T fragment serves QG groups.  The A operand
+    // (16 dims x 32 keys) comes from row-major V by two transpose reads: in
+    // each 16-lane group, source lane L reads 4 dims of key k0 + L/4 and
+    // lane i receives dim n0 + i of keys k0..k0+3, k0 = 32 kp + 16 hh + 4 g,
+    // which is the key order of P.
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp) {
-        const bf16* vp = cV + (db * 16 + c16) * VLD + kp * 32 + g * 4;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 16);
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        s16x4 half[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int r = 32 * kp + 16 * hh + 4 * g + (c16 >> 2);
+          const int c = 2 * db + ((c16 & 3) >> 1);
+          const char* pa = cV + r * ROWB + ((c ^ fV(r)) * 16) + 8 * (c16 & 1);
+          half[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)pa);
+        }
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
         for (int qg = 0; qg < QG; ++qg)
           o[qg][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qg][kp], o[qg][db], 0, 0, 0);
       }
-    // the other buffer was last read in block kb-1, which every wave finished
-    // before the previous barrier
-    if (kb + 1 < nkb) stash(u ^ 1);
-    __syncthreads();
+    __syncthreads();   // stage kb+1 landed (every wave waited for its loads); stage u retired
   }
 #pragma unroll
   for (int qg = 0; qg < QG; ++qg) {
@@ -599,15 +634,16 @@ adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float sc
     ADEPT_LAUNCH(attend_plan_kernel, dim3(1), dim3(1024), 2 * (n_seq + 1) * sizeof(int), s,
                  rows, n_active, max_active, seq, n_seq, tiles, n_tiles);
     ADEPT_CHECK_LAUNCH("attend_plan");
-    dim3 grid(max_tiles, n_heads);
+    // heads that split evenly over the 8 XCDs: 1-D grid, XCD-major order
+    const dim3 grid = n_heads % 8 == 0 ? dim3(max_tiles * n_heads) : dim3(max_tiles, n_heads);
     if (head_dim == 128)
-      ADEPT_LAUNCH(attend_prefill_kernel<128>, grid, dim3(256), 0, s, n_heads, sl, causal,
+      ADEPT_LAUNCH(attend_prefill_kernel<128>, grid, dim3(kPrefillThreads), 0, s, n_heads, sl, causal,
                    (const bf16*)q, rows, pos, seq, (const bf16*)k_layer, (const bf16*)v_layer,
-                   s_max, key_len, key_live, tiles, n_tiles, (bf16*)out);
+                   s_max, key_len, key_live, tiles, n_tiles, max_tiles, (bf16*)out);
     else
-      ADEPT_LAUNCH(attend_prefill_kernel<64>, grid, dim3(256), 0, s, n_heads, sl, causal,
+      ADEPT_LAUNCH(attend_prefill_kernel<64>, grid, dim3(kPrefillThreads), 0, s, n_heads, sl, causal,
                    (const bf16*)q, rows, pos, seq, (const bf16*)k_layer, (const bf16*)v_layer,
-                   s_max, key_len, key_live, tiles, n_tiles, (bf16*)out);
+                   s_max, key_len, key_live, tiles, n_tiles, max_tiles, (bf16*)out);
     return launch_status("attend_prefill");
   }
   if (fast) {

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <climits>
 #include <stdint.h>
 
 #include <cmath>
@@ -22,6 +23,12 @@ __device__ __forceinline__ float bf2f(bf16 x) { return __uint_as_float(((uint32_
 // float -> bf16 bits: round to nearest, ties to even; NaN stays a quiet NaN
 // (v_cvt_pk_bf16_f32 on gfx950)
 __device__ __forceinline__ bf16 f2bf(float f) { return __builtin_bit_cast(bf16, (__bf16)f); }
+// two floats to a packed pair of bf16 (round to nearest even), a in the low half
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 nbf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, nbf16x2));
+}
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {

@@ -441,10 +441,12 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
       }
     }
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  // one 32-row block; the block index is a compile-time constant (an
+  // accumulator indexed at run time would move the whole tile to scratch)
+  auto block = [&](auto ic) {
+    constexpr int i = decltype(ic)::value;
     const int mb = m0 + wm * 128 + i * 32;   // first row of the block
-    if (mb >= M) break;                       // the wave's remaining rows are past M
+    if (mb >= M) return;                      // the wave's remaining rows are past M
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int lr = 8 * (v >> 2) + row_q + (v & 3);
@@ -578,7 +580,11 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     else emit(std::true_type{});
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);   // block reads done before the next block's writes
     __builtin_amdgcn_wave_barrier();
-  }
+  };
+  block(std::integral_constant<int, 0>{});
+  block(std::integral_constant<int, 1>{});
+  block(std::integral_constant<int, 2>{});
+  block(std::integral_constant<int, 3>{});
 }
 
 // XCD-aware tile order (see the header comment).
