@@ -774,68 +774,81 @@ adept_status launch_bf16(const GP& p, hipStream_t s, const char* name) {
 // in slice order (deterministic) and applies the same epilogues as the tiled
 // path.
 // ---------------------------------------------------------------------------
-constexpr int kSkinnyM = 64;
-constexpr int kSkinnyBN = 32;
-constexpr int kSkinnyU = 8;
+constexpr int kSkinnyM = 64;      // rows of a skinny pass (decode: one per sequence)
+constexpr int kSkinnyBN = 64;     // output columns per workgroup
+constexpr int kSkStages = 4;      // LDS ring depth
+constexpr int kSkStage = 2 * 64 * 128;   // A and B, 64 rows x 64 k each: 16 KiB
 
-__global__ __launch_bounds__(256) void gemm_skinny_kernel(GP p, int Nt, int nb, int k_slice,
-                                                          float* __restrict__ part) {
-  __shared__ float red[4][kSkinnyM][kSkinnyBN + 1];
+// Skinny GEMM (M <= 64): C[m][n] over a K slice into fp32 partials
+// part[slice][m][n].  The pass streams B (the weights) once, so it is
+// HBM-bound: A and B reach LDS by direct loads of whole 128-byte rows
+// (eight lanes per row, one cache line), four stages deep, and the four
+// waves each take a 32x32 block of the 64x64 output tile.  Every iteration
+// issues the same loads (the stage index clamped past the slice's last
+// stage), so the vmcnt accounting is uniform.
+__global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int Nt, int nb, int k_slice,
+                                                             float* __restrict__ part) {
+  __shared__ __attribute__((aligned(1024))) char sm[kSkStages * kSkStage];
   const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
   if (M <= 0) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
   const int n0 = blockIdx.x * kSkinnyBN, slice = blockIdx.y;
-  const int k0 = slice * k_slice, k1 = min(p.K, k0 + k_slice);
-  const int steps = (k1 - k0) / 16;
-  const int w0 = k0 + 16 * ((steps * wave) / 4), w1 = k0 + 16 * ((steps * (wave + 1)) / 4);
-  const int n = n0 + (lane & 31);
-  const int koff = 8 * (lane >> 5);
-  const bf16* brow = (n >= nb ? p.B2 + (int64_t)(n - nb) * p.ldb : p.B + (int64_t)n * p.ldb) + koff;
-  const bf16* arow[2];
+  const int k0 = slice * k_slice;
+  const int KT = (min(p.K, k0 + k_slice) - k0) / BK;
+  // direct-load instruction j (0..3) of wave w: operand (A for waves 0-1, B
+  // for 2-3), rows 8q .. 8q+7 with q = (4w + j) mod 8; lane l -> row
+  // 8q + l/8, stored position l%8, logical chunk (l%8) ^ ((row >> 1) & 7)
+  const bf16* src[4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int m = min(i * 32 + (lane & 31), M - 1);   // clamped: loaded, never stored
-    const int r = p.a_rows ? p.a_rows[m] : m;
-    arow[i] = p.A + (int64_t)r * p.lda + koff;
-  }
-  f32x16_t acc[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[i][v] = 0.0f;
-  int k = w0;
-  for (; k + 16 * kSkinnyU <= w1; k += 16 * kSkinnyU) {
-    bf16x8_t a0[kSkinnyU], a1[kSkinnyU], b[kSkinnyU];
-#pragma unroll
-    for (int u = 0; u < kSkinnyU; ++u) {
-      b[u] = *reinterpret_cast<const bf16x8_t*>(brow + k + 16 * u);
-      a0[u] = *reinterpret_cast<const bf16x8_t*>(arow[0] + k + 16 * u);
-      a1[u] = *reinterpret_cast<const bf16x8_t*>(arow[1] + k + 16 * u);
-    }
-#pragma unroll
-    for (int u = 0; u < kSkinnyU; ++u) {
-      acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[u], b[u], acc[0], 0, 0, 0);
-      acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[u], b[u], acc[1], 0, 0, 0);
+  for (int j = 0; j < 4; ++j) {
+    const int q = (4 * wave + j) & 7;
+    const int r = 8 * q + (lane >> 3);
+    const int ch = (lane & 7) ^ ((r >> 1) & 7);
+    if (wave < 2) {
+      const int m = min(r, M - 1);   // clamped: loaded, never stored
+      const int row = p.a_rows ? p.a_rows[m] : m;
+      src[j] = p.A + (int64_t)row * p.lda + ch * 8 + k0;
+    } else {
+      const int n = n0 + r;
+      src[j] = (n >= nb ? p.B2 + (int64_t)(n - nb) * p.ldb : p.B + (int64_t)n * p.ldb) + ch * 8 +
+               k0;
     }
   }
-  for (; k < w1; k += 16) {
-    const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(brow + k);
-    const bf16x8_t x0 = *reinterpret_cast<const bf16x8_t*>(arow[0] + k);
-    const bf16x8_t x1 = *reinterpret_cast<const bf16x8_t*>(arow[1] + k);
-    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x0, b0, acc[0], 0, 0, 0);
-    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x1, b0, acc[1], 0, 0, 0);
+  auto issue = [&](int kt) {
+    const int k = min(kt, KT - 1) * BK;
+    char* slot = sm + (kt % kSkStages) * kSkStage + (wave >> 1) * 8192;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dma16(src[j] + k, slot + ((4 * wave + j) & 7) * 1024);
+  };
+  f32x16_t acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+  const int rA = wm * 32 + (lane & 31), rB = wn * 32 + (lane & 31);
+  const int swz = (lane >> 1) & 7;
+#pragma unroll
+  for (int s = 0; s < kSkStages - 1; ++s) issue(s);
+  for (int kt = 0; kt < KT; ++kt) {
+    // stage kt has landed once at most the later stages' loads are in flight
+    wait_vm<4 * (kSkStages - 2)>();
+    stage_barrier();   // publishes stage kt; every wave is done with stage kt-1
+    issue(kt + kSkStages - 1);   // into stage kt-1's slot
+    const char* st = sm + (kt % kSkStages) * kSkStage;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int ch = (2 * ks + (lane >> 5)) ^ swz;
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(st + (rA * 8 + ch) * 16);
+      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(st + 8192 + (rB * 8 + ch) * 16);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+    }
   }
-  // C layout: value v of block i is row i*32 + 8*(v/4) + 4*(lane/32) + v%4, column lane%32
+  wait_dma();   // the clamped loads land before the workgroup's LDS is released
+  // C layout: value v is row 8*(v/4) + 4*(lane/32) + v%4 of the block, column lane%32
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int v = 0; v < 16; ++v)
-      red[wave][i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)][lane & 31] = acc[i][v];
-  __syncthreads();
-  for (int e = tid; e < kSkinnyM * kSkinnyBN; e += 256) {
-    const int r = e / kSkinnyBN, c = e % kSkinnyBN;
-    part[((int64_t)slice * kSkinnyM + r) * Nt + n0 + c] =
-        red[0][r][c] + red[1][r][c] + red[2][r][c] + red[3][r][c];
+  for (int v = 0; v < 16; ++v) {
+    const int r = wm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+    part[((int64_t)slice * kSkinnyM + r) * Nt + n0 + wn * 32 + (lane & 31)] = acc[v];
   }
 }
 
@@ -922,9 +935,10 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
 
 // K slices of the skinny path: about 512 workgroups in all, slices of a
 // multiple of 64 (four waves x 16).
+// K slices: enough workgroups for two per CU (the pass is bandwidth-bound).
 void skinny_split(int Nt, int K, int* S, int* k_slice) {
   const int tiles = Nt / kSkinnyBN;
-  int want = std::max(1, std::min(8, (512 + tiles - 1) / tiles));
+  int want = std::max(1, std::min(16, (512 + tiles - 1) / tiles));
   int ks = ((K + want - 1) / want + 63) / 64 * 64;
   *k_slice = ks;
   *S = (K + ks - 1) / ks;
