@@ -203,6 +203,32 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     }
     b_src[j] = bbase + brow * p.ldb + lchunk * 8;
   }
+  // Per-row inputs of the epilogue (row scale, residual row or cache slot,
+  // rotary position) for the wave's 128 rows, two per lane: loaded here so
+  // that their latency (two dependent loads for a cache slot) passes during
+  // the K loop.
+  float pre_sc[2];
+  int pre_row[2], pre_pos[2];
+  {
+    constexpr bool kC = EPI == EPI_QKV || EPI == EPI_KV;
+    const int secp = kC ? (nt * BN + wn * 128) / p.d_q : 0;
+    const bool q_sec = EPI == EPI_QKV && secp == 0;
+    const bool v_sec = EPI == EPI_QKV ? secp == 2 : (EPI == EPI_KV && secp == 1);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int mc = min(m0 + wm * 128 + lane + 64 * h, M - 1);   // clamped: never stored
+      pre_sc[h] = p.row_scale ? p.row_scale[mc] : 1.0f;
+      pre_row[h] = 0;
+      pre_pos[h] = 0;
+      if (EPI == EPI_RESID) {
+        pre_row[h] = p.rows[mc];
+      } else if (kC) {
+        const int row = GROUPED ? p.srows[mc] : p.rows[mc];
+        pre_row[h] = q_sec ? 0 : (p.slot ? p.slot[row] : row);
+        pre_pos[h] = (v_sec || !p.rope_cos) ? 0 : p.pos[row];
+      }
+    }
+  }
   // Ring of kSlots one-operand slots: A of stage k in slot 2k mod 5, B of
   // stage k in slot 2k+1 mod 5.  DMA instruction j (0..7) of an operand.
   auto slot = [&](int u) { return smem + (u % kSlots) * kStageBytes; };
@@ -426,20 +452,12 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     }
     sec_dst += cbase;
   }
-  {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int lr = lane + 64 * h;
-      const int mc = min(m0 + wm * 128 + lr, M - 1);   // clamped: rows past M are never stored
-      msc[lr] = p.row_scale ? p.row_scale[mc] : 1.0f;
-      if (EPI == EPI_RESID) {
-        mrow[lr] = p.rows[mc];
-      } else if (kCache) {
-        const int row = GROUPED ? p.srows[mc] : p.rows[mc];
-        mrow[lr] = is_q ? 0 : (p.slot ? p.slot[row] : row);
-        mpos[lr] = (is_v || !p.rope_cos) ? 0 : p.pos[row];
-      }
-    }
+  for (int h = 0; h < 2; ++h) {
+    const int lr = lane + 64 * h;
+    msc[lr] = pre_sc[h];
+    if (EPI == EPI_RESID || kCache) mrow[lr] = pre_row[h];
+    if (kCache) mpos[lr] = pre_pos[h];
   }
   // one 32-row block; the block index is a compile-time constant (an
   // accumulator indexed at run time would move the whole tile to scratch)
