@@ -465,6 +465,53 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     constexpr int i = decltype(ic)::value;
     const int mb = m0 + wm * 128 + i * 32;   // first row of the block
     if (mb >= M) return;                      // the wave's remaining rows are past M
+    if constexpr (EPI == EPI_SWIGLU) {
+      // Gate (blocks j = 0, 1) and up (j = 2, 3) of an output column sit in
+      // the same lane, so h = silu(g) * u is formed in registers; lanes 2k
+      // and 2k+1 hold adjacent columns and swap one value (DPP), so the even
+      // lane holds row v and the odd lane row v+1 of a pair of columns as
+      // one 4-byte bf16 pair.  The pairs go to LDS (32 rows x 128 bytes; two
+      // rows fill the 64 banks) and come back as 16-byte row segments: four
+      // full-row stores per block instead of 32 narrow ones.
+      float sc[16];
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 t = *reinterpret_cast<const float4*>(msc + i * 32 + 8 * g4 + row_q);
+        sc[4 * g4 + 0] = t.x; sc[4 * g4 + 1] = t.y; sc[4 * g4 + 2] = t.z; sc[4 * g4 + 3] = t.w;
+      }
+      const bool odd = lane & 1;
+      char* sb = reinterpret_cast<char*>(stg);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int v0 = 2 * t, v1 = 2 * t + 1;
+          const float h0 = silu(acc[i][j][v0] * sc[v0]) * (acc[i][j + 2][v0] * sc[v0]);
+          const float h1 = silu(acc[i][j][v1] * sc[v1]) * (acc[i][j + 2][v1] * sc[v1]);
+          // quad_perm [1,0,3,2]: exchange with the neighbouring lane
+          const float y = __int_as_float(__builtin_amdgcn_mov_dpp(
+              __float_as_int(odd ? h0 : h1), 0xB1, 0xF, 0xF, false));
+          const uint32_t w = odd ? pack_bf16x2(y, h1) : pack_bf16x2(h0, y);
+          const int lr = 8 * (v0 >> 2) + row_q + (v0 & 3) + (odd ? 1 : 0);
+          *reinterpret_cast<uint32_t*>(sb + lr * 128 + j * 64 + (col_l & ~1) * 2) = w;
+        }
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+      __builtin_amdgcn_wave_barrier();
+      const bool full = mb + 32 <= M;
+      bf16* cb = reinterpret_cast<bf16*>(p.C) + nt * 128 + wn * 64 + (lane & 7) * 8;
+      uint4 seg[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        seg[q] = *reinterpret_cast<const uint4*>(sb + (8 * q + (lane >> 3)) * 128 + (lane & 7) * 16);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m = mb + 8 * q + (lane >> 3);
+        if (full || m < M) *reinterpret_cast<uint4*>(cb + (int64_t)m * p.ldc) = seg[q];
+      }
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);   // reads done before the next block's writes
+      __builtin_amdgcn_wave_barrier();
+      return;
+    }
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int lr = 8 * (v >> 2) + row_q + (v & 3);
