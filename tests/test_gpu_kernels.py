@@ -137,6 +137,7 @@ def test_exit_test_window_and_special_thresholds():
 @pytest.mark.parametrize("n_tok,n_act,p_exit,slack", [
     (16, 16, 0.5, 0), (5000, 4097, 0.3, 0), (16384, 16384, 0.1, 0), (16384, 9000, 0.0, 0),
     (16384, 9000, 1.0, 0), (300000, 200003, 0.4, 0),
+    (300000, 300000, 0.0, 0), (300000, 299999, 1.0, 0),   # multi-pass, no / all exits
     (70000, 65536, 0.5, 0),          # largest single-workgroup list
     (70000, 65537, 0.5, 0),          # smallest multi-pass list
     (1000, 0, 0.5, 64),              # empty list
