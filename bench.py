@@ -260,6 +260,7 @@ def main():
             "kernels": kernel_table(kern_f, work_f, ms_f, steps_f),
         }
         log(f"no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
+        out["delta_sweep"] = delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf)
         out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
         out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
 
@@ -273,9 +274,55 @@ def main():
         torch.cuda.empty_cache()
         out["classification"] = classification(args, ai, B, torch, np)
 
+    if not args.no_extras:
+        out["tiny_f32"] = tiny_decoder(ai, B, torch, np)
+
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args, shape, ai, np)
     print(json.dumps(out), flush=True)
+
+
+def skipped_fraction(exit_layer, n_layers):
+    """Fraction of (token, layer) pairs a run skipped: layers after each exit."""
+    el = exit_layer.to("cpu").long()
+    return float((n_layers - el).clamp(min=0).sum()) / (n_layers * el.numel())
+
+
+def exit_histogram(exit_layer, n_layers):
+    import torch
+    return torch.bincount(exit_layer.to("cpu").long(), minlength=n_layers + 1)[1:].tolist()
+
+
+def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf):
+    """The policy's own decisions: the threshold set {0.90, 0.95, 0.99} of
+    the prefill configuration, then thresholds calibrated (bisection on
+    delta, the skipped fraction falls as delta rises) so that 10 / 20 / 25 %
+    of the (token, layer) pairs are skipped by the exit test itself."""
+    res_out = {"thresholds": {}, "calibrated": {}}
+    for d in (0.90, 0.95, 0.99):
+        ms, res, _ = run(B.exit_cfg(d, N, args.metric), steps=2, warmup=1)
+        res_out["thresholds"][f"{d:.2f}"] = {
+            "tokens_per_s": n_tok / (ms / 1e3), "ms_per_step": ms,
+            "skipped_fraction": skipped_fraction(res.exit_layer, N),
+            "exit_layer_histogram": exit_histogram(res.exit_layer, N)}
+    for target in (0.10, 0.20, 0.25):
+        lo, hi = -1.0, 1.0          # skipped(lo) >= target > skipped(hi)
+        for _ in range(12):
+            mid = 0.5 * (lo + hi)
+            _, res, _ = run(B.exit_cfg(mid, N, args.metric), steps=1, warmup=0)
+            if skipped_fraction(res.exit_layer, N) >= target:
+                lo = mid
+            else:
+                hi = mid
+        ms, res, _ = run(B.exit_cfg(lo, N, args.metric), steps=2, warmup=1)
+        frac = skipped_fraction(res.exit_layer, N)
+        res_out["calibrated"][f"{int(round(target * 100))}%"] = {
+            "delta": lo, "tokens_per_s": n_tok / (ms / 1e3), "ms_per_step": ms,
+            "skipped_fraction": frac, "speedup_vs_no_exit": ms_inf / ms,
+            "exit_layer_histogram": exit_histogram(res.exit_layer, N)}
+        log(f"calibrated delta {lo:.4f}: {frac:.1%} of token-layers skipped, "
+            f"{ms:.1f} ms/step ({ms_inf / ms:.2f}x vs no exit)")
+    return res_out
 
 
 def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
@@ -288,8 +335,9 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
     el = torch.from_numpy(ai.forced_exit_layers(12, n, 8, 31)).cuda()
     rows = torch.arange(n, dtype=torch.int32, device="cuda")
     cnt = torch.tensor([n], dtype=torch.int32, device="cuda")
-    kc = torch.empty((N, n, H, hd), dtype=torch.bfloat16, device="cuda")
-    vc = torch.empty_like(kc)
+    # NaN sentinel: exactly layers i*+1..N of each slot must be written
+    kc = torch.full((N, n, H, hd), float("nan"), dtype=torch.bfloat16, device="cuda")
+    vc = torch.full_like(kc, float("nan"))
     ws = torch.empty(B.kv_generate_workspace_bytes(N, n), dtype=torch.uint8, device="cuda")
     w_kv = model.w_qkv[:, Dq:]          # K and V rows of each layer's stacked QKV weight
     # positions 0..4095 (token t at position t and slot t)
@@ -302,6 +350,11 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
                       3 * Dq * D, None, cos, sin, kc, vc, n, ws)
     call()
     torch.cuda.synchronize()
+    layer = torch.arange(1, N + 1, device="cuda").view(N, 1)
+    want = layer > el.view(1, n).long()                      # [N][n]: layer r > i*
+    written_k = ~torch.isnan(kc).any(dim=(2, 3))
+    written_v = ~torch.isnan(vc).any(dim=(2, 3))
+    sentinel_ok = bool(torch.equal(written_k, want) and torch.equal(written_v, want))
     B.timing_reset()
     B.timing_enable(True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -318,6 +371,7 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
     g_launch, g_ms = k.get("gemm_kv_grouped_kernel", (reps, call_ms * reps))
     gemm_ms = g_ms / g_launch
     return {"tokens": n, "pairs": pairs, "tflop": flops / 1e12, "call_ms": call_ms,
+            "sentinel_ok": sentinel_ok,
             "gemm_ms": gemm_ms, "mfma_util": flops / (gemm_ms / 1e3) / PEAK_BF16,
             "mfma_util_whole_call": flops / (call_ms / 1e3) / PEAK_BF16,
             "kernels": {kk: {"launches": v[0], "avg_us": 1e3 * v[1] / max(v[0], 1)}
@@ -567,6 +621,46 @@ def classification(args, ai, B, torch, np, reps=5):
     return res
 
 
+def tiny_decoder(ai, B, torch, np, prompt=128, steps=32, reps=5):
+    """The tiny f32 decoder (4 layers, width 256, 4 x 64 heads, FFN 1024,
+    vocab 1024): one 128-token prompt, then 32 greedy steps, local metric
+    delta 0.95, against delta = +inf.  Launch-latency-bound at this size."""
+    from paper_2601_03700_amd.model import DecoderModel
+    shape = ai.TINY
+    model = DecoderModel(shape, ai.decoder_weights(shape, seed=21, dtype="f32"), dtype="f32",
+                         rope_max_pos=prompt + steps)
+    ids = ai.token_ids(22, shape.vocab, 1, prompt)
+    out = {"workload": f"tiny f32 decoder, 1 x {prompt}-token prompt + {steps} greedy steps, "
+                       "local metric"}
+    for name, delta in (("delta_0.95", 0.95), ("no_exit", math.inf)):
+        cfg = B.exit_cfg(delta, shape.n_layers, "local")
+        model.generate(ids, steps, cfg)      # warm-up
+        torch.cuda.synchronize()
+        tp = td = 0.0
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            res, cache = model.prefill(ids, cfg, s_max=prompt + steps, logits="last")
+            nxt = model.greedy(res.logits)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            for k in range(steps):
+                pos = torch.full((1,), prompt + k, dtype=torch.int32, device="cuda")
+                st = model.decode_step(cache, nxt, pos, cfg)
+                nxt = model.greedy(st.logits)
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            tp += t1 - t0
+            td += t2 - t1
+        tp, td = tp / reps, td / reps
+        out[name] = {"prefill_tokens_per_s": prompt / tp, "decode_tokens_per_s": steps / td,
+                     "combined_tokens_per_s": (prompt + steps) / (tp + td),
+                     "prefill_ms": 1e3 * tp, "decode_ms_per_step": 1e3 * td / steps,
+                     "prefill_skipped_fraction": skipped_fraction(res.exit_layer, shape.n_layers)}
+    log(f"tiny f32: prefill {out['delta_0.95']['prefill_ms']:.2f} ms, decode "
+        f"{out['delta_0.95']['decode_ms_per_step']:.2f} ms/step")
+    return out
+
+
 def cpu_baseline(args, shape, ai, np):
     """The oracle (numpy fp64) on a bounded sample of the same workload: one
     sequence of --cpu-tokens tokens through --cpu-layers of the 32 layers at
@@ -586,12 +680,35 @@ def cpu_baseline(args, shape, ai, np):
     scaled = dt * shape.n_layers / L
     cores = len(os.sched_getaffinity(0))
     log(f"cpu baseline: {dt:.1f}s for the sample")
+    # one thread, a smaller sample (256 tokens through 2 layers)
+    from threadpoolctl import threadpool_limits
+    sub1 = dataclasses.replace(shape, n_layers=2)
+    w1 = O.as64(ai.decoder_weights(sub1, seed=7, dtype="bf16"))
+    ids1 = ai.token_ids(8, shape.vocab, 1, 256)
+    with threadpool_limits(limits=1):
+        t1 = time.perf_counter()
+        O.prefill(w1, sub1, ids1, cfg)
+        dt1 = time.perf_counter() - t1
+    one_thread = 256 / (dt1 * shape.n_layers / 2)
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    log(f"cpu baseline (1 thread): {dt1:.1f}s for 256 tokens x 2 layers")
     return {"value": args.cpu_tokens / scaled, "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
             "sample": (f"1 x {args.cpu_tokens} tokens through {L} of 32 layers at full width "
                        f"(numpy fp64, BLAS on {cores} threads), {dt:.1f}s, extrapolated x{shape.n_layers / L:g} "
                        f"to the 32-layer step; includes the oracle's LM head over all rows"),
-            "sample_seconds": dt}
+            "sample_seconds": dt, "cpu_model": cpu_model,
+            "one_thread": {"value": one_thread, "unit": "tokens/s",
+                           "sample": "1 x 256 tokens through 2 of 32 layers, extrapolated x16",
+                           "sample_seconds": dt1}}
 
 
 if __name__ == "__main__":
