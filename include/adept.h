@@ -115,6 +115,10 @@ adept_status adept_exit_test(adept_dtype dt, int d_model, int layer, const adept
  *  exit_layer [n_tok] int32: exit_layer[row] = layer for every exited row.
  *  Counts are exact; with an ascending active list both outputs are ascending.
  *  next_rows / exited_rows must not alias active_rows.
+ *  workspace: adept_compact_workspace_bytes(max_active) bytes, 8-byte aligned
+ *  (0 bytes, workspace may be NULL, for max_active <= 65536); larger lists
+ *  keep per-16K-entry exit counts and one 64-bit exit mask per 64 entries
+ *  there.  ADEPT_E_WORKSPACE if it is missing or too small.
  * ------------------------------------------------------------------------- */
 size_t adept_compact_workspace_bytes(int max_active);
 adept_status adept_compact(int layer, const uint8_t* exit_flag, const int32_t* active_rows,

@@ -11,8 +11,10 @@
 // wave land on consecutive addresses.  Lists up to 64K entries (the
 // per-layer case) use one workgroup over the whole list; longer lists use
 // three passes over 16K-entry tiles: a count of exits per tile (16 flags per
-// thread, one 16-byte load), a scan of the tile counts, and the split of
-// each tile from its offsets.  Input order is kept in both outputs.
+// thread, one 16-byte load) that also stores the 64-bit exit mask of every
+// 64 entries, a scan of the tile counts, and the split of each tile from its
+// offsets, which reads the masks (one bit per entry) instead of the flags.
+// Input order is kept in both outputs.
 #include "common.h"
 
 namespace adept {
@@ -146,37 +148,63 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int* total) 
   return excl;
 }
 
-// pass 1: exits per tile
-__global__ __launch_bounds__(kThreads) void compact_count(const uint8_t* __restrict__ flags,
-                                                          const int32_t* __restrict__ n_active,
-                                                          int32_t* __restrict__ tile_ex,
-                                                          int max_n) {
-  __shared__ int sh[kWaves + 1];
+// pass 1: exits per tile.  256 threads per 16K-entry tile; thread t reads
+// the 16 flags at 16 * (j * 256 + t) for j < 4 (four 16-byte loads in
+// flight, each instruction of a wave on 1 KB of consecutive flags).  The four
+// threads of a quad then hold 64 consecutive entries, whose exit bits the
+// quad's first thread stores as one 64-bit mask.
+constexpr int kCountThreads = 256;
+constexpr int kCountLoads = kTile / (kCountThreads * 16);   // 4
+__global__ __launch_bounds__(kCountThreads) void compact_count(
+    const uint8_t* __restrict__ flags, const int32_t* __restrict__ n_active,
+    int32_t* __restrict__ tile_ex, uint64_t* __restrict__ masks, int max_n) {
+  __shared__ int sh[kCountThreads / 64];
   const int n = min(*n_active, max_n);
   const int start = blockIdx.x * kTile;
   if (start >= n) return;
   const int end = min(n, start + kTile);
-  // kTileItems flags per thread: one 16-byte load, nonzero bytes counted
-  static_assert(kTileItems == 16, "one uint4 of flags per thread");
-  const int e0 = start + threadIdx.x * kTileItems;
-  int cnt = 0;
-  if (e0 + kTileItems <= end) {
-    const uint4 v = *reinterpret_cast<const uint4*>(flags + e0);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 v[kCountLoads];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint32_t x = w[q];
-      x |= x >> 4;
-      x |= x >> 2;
-      x |= x >> 1;
-      cnt += __popc(x & 0x01010101u);
-    }
-  } else {
-    for (int e = e0; e < end && e < e0 + kTileItems; ++e) cnt += flags[e] ? 1 : 0;
+  for (int j = 0; j < kCountLoads; ++j) {
+    const int e0 = start + (j * kCountThreads + (int)threadIdx.x) * 16;
+    // the load is clamped to the array's last whole 16 bytes and its value
+    // used only when all 16 flags lie before `end`
+    const int ec = min(e0, (max_n - 16) & ~15);
+    v[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(flags + ec));
+    if (e0 + 16 > end) v[j] = u32x4{0u, 0u, 0u, 0u};
   }
-  int tot;
-  block_exclusive_scan(cnt, sh, &tot);
-  if (threadIdx.x == 0) tile_ex[blockIdx.x] = tot;
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < kCountLoads; ++j) {
+    const int e0 = start + (j * kCountThreads + (int)threadIdx.x) * 16;
+    uint32_t m16 = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+        if ((v[j][q] >> (8 * bb)) & 0xffu) m16 |= 1u << (4 * q + bb);
+    if (e0 < end && e0 + 16 > end) {   // the row's ragged end: byte loads
+      for (int e = e0; e < end; ++e)
+        if (flags[e]) m16 |= 1u << (e - e0);
+    }
+    cnt += __popc(m16);
+    const uint32_t m1 = __shfl_down(m16, 1, 64), m2 = __shfl_down(m16, 2, 64),
+                   m3 = __shfl_down(m16, 3, 64);
+    if ((lane & 3) == 0 && e0 < end)
+      masks[e0 >> 6] = (uint64_t)m16 | ((uint64_t)m1 << 16) | ((uint64_t)m2 << 32) |
+                       ((uint64_t)m3 << 48);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+  if (lane == 0) sh[wave] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int t = 0;
+    for (int w = 0; w < kCountThreads / 64; ++w) t += sh[w];
+    tile_ex[blockIdx.x] = t;
+  }
 }
 
 // pass 2: exclusive scan of the tile counts (one workgroup), totals
@@ -203,21 +231,73 @@ __global__ __launch_bounds__(kThreads) void compact_scan(const int32_t* __restri
   }
 }
 
-// pass 3: split each tile from its offsets
+// pass 3: split each tile from its offsets.  The waves own consecutive
+// chunks of 1024 entries; a wave reads its 16 exit masks (128 consecutive
+// bytes, one bit per entry) instead of the flags, so a lane's output slot is
+// a popcount of the lower lanes' bits, and the row loads of all 16 of its
+// 64-entry steps are in flight together.  Each step is one store per lane,
+// to the exit list or to the kept list, and the exit layer of the exits.
 __global__ __launch_bounds__(kThreads) void compact_scatter(
-    int layer, const uint8_t* __restrict__ flags, const int32_t* __restrict__ active,
+    int layer, const uint64_t* __restrict__ masks, const int32_t* __restrict__ active,
     const int32_t* __restrict__ n_active, const int32_t* __restrict__ tile_ex,
     int32_t* __restrict__ next, int32_t* __restrict__ exited, int32_t* __restrict__ exit_layer,
     int max_n) {
-  __shared__ uint64_t masks[kTile / 64];
+  constexpr int kChunk = kTile / kWaves;      // 1024 entries, 16 steps
+  constexpr int kSteps = kChunk / 64;
   __shared__ int sh[2 * kWaves];
   const int n = min(*n_active, max_n);
   const int start = blockIdx.x * kTile;
   if (start >= n) return;
   const int end = min(n, start + kTile);
-  const int ex = tile_ex[blockIdx.x];
-  split_block(start, end, kTile / kWaves, ex, start - ex, layer, flags, active, next, exited,
-              exit_layer, masks, sh);
+  const int tex = tile_ex[blockIdx.x];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lo = start + wave * kChunk;
+  const int hi = min(end, lo + kChunk);
+  // the mask array holds whole tiles (kTile / 64 masks each), so all 16
+  // loads stay inside it; masks of steps at or past `hi` are not used
+  const uint64_t* wm = masks + (lo >> 6);
+  uint64_t m[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) m[st] = wm[st];
+  int32_t r[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int e = min(lo + st * 64 + lane, n - 1);   // clamped: in bounds, unused past hi
+    r[st] = __builtin_nontemporal_load(active + e);
+  }
+  int ex = 0;
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    m[st] = lo + st * 64 < hi ? m[st] : 0ull;
+    ex += __popcll(m[st]);
+  }
+  if (lane == 0) {
+    sh[wave] = ex;
+    sh[kWaves + wave] = max(0, hi - lo) - ex;
+  }
+  __syncthreads();
+  int ex_off = tex, keep_off = start - tex;
+  for (int w = 0; w < wave; ++w) {
+    ex_off += sh[w];
+    keep_off += sh[kWaves + w];
+  }
+  const uint64_t lt = (1ull << lane) - 1ull;   // lanes below this one
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int base = lo + st * 64;
+    const uint64_t mm = m[st];
+    const int below = __popcll(mm & lt);
+    const bool gone = (mm >> lane) & 1ull;
+    int32_t* dst = gone ? exited + (ex_off + below) : next + (keep_off + lane - below);
+    if (base + lane < hi) {
+      __builtin_nontemporal_store(r[st], dst);
+      if (gone) exit_layer[r[st]] = layer;
+    }
+    const int me = __popcll(mm);
+    ex_off += me;
+    keep_off += max(0, min(64, hi - base)) - me;
+  }
 }
 
 }  // namespace
@@ -226,7 +306,10 @@ using namespace adept;
 
 extern "C" size_t adept_compact_workspace_bytes(int max_active) {
   if (max_active <= kSingleMax) return 0;
-  return (size_t)ceil_div(max_active, kTile) * sizeof(int32_t);
+  // tile offsets, then one 64-bit exit mask per 64 entries of every tile
+  // (whole tiles, 256-byte aligned)
+  const size_t tiles = (size_t)ceil_div(max_active, kTile);
+  return ((tiles * sizeof(int32_t) + 255) & ~size_t(255)) + tiles * (kTile / 64) * sizeof(uint64_t);
 }
 
 extern "C" adept_status adept_compact(int layer, const uint8_t* exit_flag,
@@ -253,19 +336,22 @@ extern "C" adept_status adept_compact(int layer, const uint8_t* exit_flag,
   ADEPT_REQUIRE(aligned16(exit_flag),
                 "compact: exit_flag must be 16-byte aligned above %d entries", kSingleMax);
   const size_t need = adept_compact_workspace_bytes(max_active);
+  ADEPT_REQUIRE(((uintptr_t)workspace & 7) == 0, "compact: workspace must be 8-byte aligned");
   if (!workspace || workspace_bytes < need) {
     set_error("compact: workspace of %zu bytes needed", need);
     return ADEPT_E_WORKSPACE;
   }
   const int tiles = ceil_div(max_active, kTile);
   int32_t* tile_ex = (int32_t*)workspace;
-  ADEPT_LAUNCH(compact_count, dim3(tiles), dim3(kThreads), 0, s, exit_flag, n_active,
-                     tile_ex, max_active);
+  uint64_t* masks =
+      (uint64_t*)((char*)workspace + (((size_t)tiles * sizeof(int32_t) + 255) & ~size_t(255)));
+  ADEPT_LAUNCH(compact_count, dim3(tiles), dim3(kCountThreads), 0, s, exit_flag, n_active,
+                     tile_ex, masks, max_active);
   ADEPT_CHECK_LAUNCH("compact_count");
   ADEPT_LAUNCH(compact_scan, dim3(1), dim3(kThreads), 0, s, n_active, tile_ex, n_next,
                      n_exited, max_active);
   ADEPT_CHECK_LAUNCH("compact_scan");
-  ADEPT_LAUNCH(compact_scatter, dim3(tiles), dim3(kThreads), 0, s, layer, exit_flag,
+  ADEPT_LAUNCH(compact_scatter, dim3(tiles), dim3(kThreads), 0, s, layer, masks,
                      active_rows, n_active, tile_ex, next_rows, exited_rows, exit_layer,
                      max_active);
   return launch_status("compact_scatter");
