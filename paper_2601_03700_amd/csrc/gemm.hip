@@ -98,6 +98,7 @@ struct GP {
   // grouped (KV generation)
   const int32_t* work;      // packed (layer << 16) | m_tile
   const int32_t* n_work;
+  int32_t* queue;           // [8] item counters, zero at launch
   const int32_t* grp_m;     // [N+2]: rows with exit layer < r
   const int32_t* srows;     // exited rows sorted by exit layer
   int64_t b_layer_stride;
@@ -679,35 +680,46 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GP p) {
   gemm_tile<EPI, false, HD>(p, smem, 0, mt, nt, M, p.B);
 }
 
-// Persistent grouped GEMM: workgroups stride over the device-built list of
-// (layer, row tile) items times the column tiles; an empty list costs one
-// read per workgroup.  The items, rastered in groups of 8 row tiles, are cut
-// into 8 contiguous chunks, one per XCD, walked by that XCD's workgroups.
+// Persistent grouped GEMM over the device-built list of (layer, row tile)
+// items times the column tiles.  The items, rastered in groups of 8 row tiles,
+// are cut into 8 contiguous chunks with one work counter each; a workgroup
+// takes items from the chunk of its own XCD (workgroups are dispatched to the
+// XCDs round-robin), in order, so that the tiles running together on an XCD
+// share operand slices in its L2, and then helps drain the other chunks.
+// Taking items from counters rather than a fixed stride keeps the
+// workgroups busy until the last items: item times vary with the clock and
+// with how much of a layer's weights come from HBM.
 template <int HD>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kv_grouped_kernel(GP p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int n_work = *p.n_work;
   const int total = n_work * p.tiles_n;
-  int lo = 0, hi = total, t0 = blockIdx.x, step = gridDim.x;
-  if ((gridDim.x & 7) == 0 && total >= (int)gridDim.x) {
-    const int chunk = (total + 7) >> 3;
-    lo = (blockIdx.x & 7) * chunk;
-    hi = min(total, lo + chunk);
-    t0 = lo + (blockIdx.x >> 3);
-    step = gridDim.x >> 3;
-  }
-  for (int t = t0; t < hi; t += step) {
-    constexpr int G = 8;
-    const int gsz = G * p.tiles_n;
-    const int g = t / gsz, r = t - g * gsz;
-    const int rows_in_g = min(G, n_work - g * G);
-    const int w = g * G + r % rows_in_g, nt = r / rows_in_g;
-    const int packed = p.work[w];
-    const int layer = packed >> 16, mt = packed & 0xffff;
-    const int M = p.grp_m[layer];
-    gemm_tile<EPI_KV, true, HD>(p, smem, layer, mt, nt, M,
-                            p.B + (int64_t)(layer - 1) * p.b_layer_stride);
-    __syncthreads();  // LDS is reused by the next item
+  const int chunk = (total + 7) >> 3;
+  const int home = blockIdx.x & 7;
+  // the item index is passed to all waves through the first word of the
+  // LDS ring, which no tile uses between items
+  int* const s_item = reinterpret_cast<int*>(smem);
+  for (int q = 0; q < 8; ++q) {
+    const int qi = (home + q) & 7;
+    const int lo = qi * chunk, hi = min(total, lo + chunk);
+    for (;;) {
+      if (threadIdx.x == 0) *s_item = lo + atomicAdd(&p.queue[qi], 1);
+      __syncthreads();
+      const int t = __builtin_amdgcn_readfirstlane(*s_item);
+      __syncthreads();  // every wave has the index before the ring is refilled
+      if (t >= hi) break;
+      constexpr int G = 8;
+      const int gsz = G * p.tiles_n;
+      const int g = t / gsz, r = t - g * gsz;
+      const int rows_in_g = min(G, n_work - g * G);
+      const int w = g * G + r % rows_in_g, nt = r / rows_in_g;
+      const int packed = p.work[w];
+      const int layer = packed >> 16, mt = packed & 0xffff;
+      const int M = p.grp_m[layer];
+      gemm_tile<EPI_KV, true, HD>(p, smem, layer, mt, nt, M,
+                              p.B + (int64_t)(layer - 1) * p.b_layer_stride);
+      __syncthreads();  // LDS is reused by the next item
+    }
   }
 }
 
@@ -1144,7 +1156,8 @@ adept_status gemm_f32_direct(const GemmArgs& g, hipStream_t s) {
 // Grouped bf16 GEMM of the KV generation (see the header comment).  g.row_scale
 // is indexed by the sorted position.
 adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32_t* n_work,
-                             int max_work, const int32_t* grp_m, const int32_t* srows,
+                             int32_t* queue, int max_work, const int32_t* grp_m,
+                             const int32_t* srows,
                              int64_t b_layer_stride, int64_t cache_layer_stride, hipStream_t s) {
   if (max_work <= 0) return ADEPT_OK;
   if (!aligned_operands(g)) {
@@ -1152,7 +1165,7 @@ adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32
     return ADEPT_E_INVALID;
   }
   GP p = to_gp(g);
-  p.work = work; p.n_work = n_work; p.grp_m = grp_m; p.srows = srows;
+  p.work = work; p.n_work = n_work; p.queue = queue; p.grp_m = grp_m; p.srows = srows;
   p.b_layer_stride = b_layer_stride;
   p.cache_layer_stride = cache_layer_stride;
   p.tiles_n = g.N / BN;
