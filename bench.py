@@ -238,6 +238,7 @@ def main():
                    "global_batch": Bn, "seq_len": T, "parallelism": "none (one GPU)"},
         "roofline": roofline,
         "exit_fraction": exit_frac,
+        "rdc": reduction(res.exit_layer, shape),
         "active_rows_per_layer": cnt,
         "kernels": per_kernel,
     }
@@ -256,6 +257,7 @@ def main():
             "schedule": "exit layer uniform in 8..31 per token (seeded)",
             "tokens_per_s": n_tok / (ms_f / 1e3), "ms_per_step": ms_f,
             "speedup_vs_no_exit": ms_inf / ms_f,
+            "rdc": reduction(res_f.exit_layer, shape),
             "active_rows_per_layer": cnt_f,
             "kernels": kernel_table(kern_f, work_f, ms_f, steps_f),
         }
@@ -288,6 +290,15 @@ def skipped_fraction(exit_layer, n_layers):
     return float((n_layers - el).clamp(min=0).sum()) / (n_layers * el.numel())
 
 
+def reduction(exit_layer, shape):
+    """Compute reduction (RDC) of a run's exit layers, three K/V charges
+    (none / the paper's / algorithmic); dense projections of a SwiGLU layer
+    plus the LM head once per token."""
+    from paper_2601_03700_amd.accounting import rdc
+    return rdc(exit_layer.to("cpu").numpy(), shape.n_layers, shape.d_model, shape.d_q,
+               shape.d_ff, shape.vocab, ffn_mats=3)
+
+
 def exit_histogram(exit_layer, n_layers):
     import torch
     return torch.bincount(exit_layer.to("cpu").long(), minlength=n_layers + 1)[1:].tolist()
@@ -304,6 +315,7 @@ def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf):
         res_out["thresholds"][f"{d:.2f}"] = {
             "tokens_per_s": n_tok / (ms / 1e3), "ms_per_step": ms,
             "skipped_fraction": skipped_fraction(res.exit_layer, N),
+            "rdc": reduction(res.exit_layer, shape),
             "exit_layer_histogram": exit_histogram(res.exit_layer, N)}
     for target in (0.10, 0.20, 0.25):
         lo, hi = -1.0, 1.0          # skipped(lo) >= target > skipped(hi)
@@ -319,6 +331,7 @@ def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf):
         res_out["calibrated"][f"{int(round(target * 100))}%"] = {
             "delta": lo, "tokens_per_s": n_tok / (ms / 1e3), "ms_per_step": ms,
             "skipped_fraction": frac, "speedup_vs_no_exit": ms_inf / ms,
+            "rdc": reduction(res.exit_layer, shape),
             "exit_layer_histogram": exit_histogram(res.exit_layer, N)}
         log(f"calibrated delta {lo:.4f}: {frac:.1%} of token-layers skipped, "
             f"{ms:.1f} ms/step ({ms_inf / ms:.2f}x vs no exit)")
