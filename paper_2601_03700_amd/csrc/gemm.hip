@@ -513,6 +513,103 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
       __builtin_amdgcn_wave_barrier();
       return;
     }
+    if constexpr (kCache) {
+      if (!p.bias) {   // wave-uniform: the decoder's QKV and the KV generation
+        // The wave's 128 columns are whole heads, so the rotary partner of a
+        // column (c ^ hd/2) sits in the same lane, hd/64 blocks away: RoPE
+        // runs on the accumulators.  Positions come from the gathered
+        // per-row inputs and the cos/sin values of the block's 16 rows per
+        // lane are loaded at once (one memory latency per block).  Results
+        // leave as in the SwiGLU path: bf16 pairs (DPP lane swap) to LDS,
+        // 32 rows x 256 bytes, each row's four 64-byte segments permuted by
+        // (row & 1) | ((row >> 2) & 1) << 1 so the four row groups of a
+        // write fall on distinct banks, read back as 16-byte row segments
+        // and stored as whole 256-byte rows of the destination.
+        constexpr int kPair = hd / 64;          // block distance of rotary partners
+        constexpr int kTab = hd == 128 ? 2 : 1; // table columns per lane and row
+        const bool rope = !is_v && p.rope_cos;  // wave-uniform
+        float sc[16];
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const float4 t = *reinterpret_cast<const float4*>(msc + i * 32 + 8 * g4 + row_q);
+          sc[4 * g4 + 0] = t.x; sc[4 * g4 + 1] = t.y; sc[4 * g4 + 2] = t.z; sc[4 * g4 + 3] = t.w;
+        }
+        float cv[16][kTab], sv[16][kTab];
+        if (rope) {
+          int ps[16];
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int4 t = *reinterpret_cast<const int4*>(mpos + i * 32 + 8 * g4 + row_q);
+            ps[4 * g4 + 0] = t.x; ps[4 * g4 + 1] = t.y; ps[4 * g4 + 2] = t.z; ps[4 * g4 + 3] = t.w;
+          }
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+#pragma unroll
+            for (int u = 0; u < kTab; ++u) {
+              const int64_t t = (int64_t)ps[v] * half + u * 32 + col_l;
+              cv[v][u] = p.rope_cos[t];
+              sv[v][u] = p.rope_sin[t];
+            }
+        }
+        // output of column block j, row v of the lane
+        auto out = [&](int j, int v) {
+          const float x = acc[i][j][v] * sc[v];
+          if (!rope) return x;
+          const float y = acc[i][j ^ kPair][v] * sc[v];
+          const int u = hd == 128 ? (j & 1) : 0;
+          const bool first = hd == 128 ? j < 2 : (j & 1) == 0;   // column < hd/2
+          return first ? x * cv[v][u] - y * sv[v][u] : x * cv[v][u] + y * sv[v][u];
+        };
+        // Lanes 2k, 2k+1 hold adjacent columns.  Each packs its rows v0, v1
+        // as one bf16 pair, the pairs are swapped (DPP quad_perm [1,0,3,2])
+        // and one byte permute forms row v0 (even lane) or row v1 (odd
+        // lane) of the two columns.
+        const bool odd = lane & 1;
+        const uint32_t psel = odd ? 0x03020706u : 0x05040100u;
+        char* sb = reinterpret_cast<char*>(stg);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {
+            const int v0 = 2 * t, v1 = 2 * t + 1;
+            const uint32_t own = pack_bf16x2(out(j, v0), out(j, v1));
+            const uint32_t nbr = (uint32_t)__builtin_amdgcn_mov_dpp((int)own, 0xB1, 0xF, 0xF, false);
+            const uint32_t w = __builtin_amdgcn_perm(nbr, own, psel);
+            const int lr = 8 * (v0 >> 2) + row_q + (v0 & 3) + (odd ? 1 : 0);
+            const int g = (lr & 1) | (((lr >> 2) & 1) << 1);
+            *reinterpret_cast<uint32_t*>(sb + lr * 256 + ((j ^ g) << 6) + (col_l & ~1) * 2) = w;
+          }
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        __builtin_amdgcn_wave_barrier();
+        const bool full = mb + 32 <= M;
+        const int sg = lane & 15;
+        typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+        u32x4_t seg[8];
+        int drow[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int R = 4 * q + (lane >> 4);
+          const int g = (R & 1) | (((R >> 2) & 1) << 1);
+          seg[q] = *reinterpret_cast<const u32x4_t*>(sb + R * 256 + (((sg >> 2) ^ g) << 6) +
+                                                     (sg & 3) * 16);
+          drow[q] = is_q ? mb + R : mrow[i * 32 + R];
+        }
+        // cache rows are streamed out (not read again while cached); Q rows
+        // are read by the attention that follows
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int m = mb + 4 * q + (lane >> 4);
+          u32x4_t* dst = reinterpret_cast<u32x4_t*>(sec_dst + (int64_t)drow[q] * p.d_q + sg * 8);
+          if (full || m < M) {
+            if (is_q) *dst = seg[q];
+            else __builtin_nontemporal_store(seg[q], dst);
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);   // reads done before the next block's writes
+        __builtin_amdgcn_wave_barrier();
+        return;
+      }
+    }
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int lr = 8 * (v >> 2) + row_q + (v & 3);
