@@ -49,8 +49,11 @@ typedef enum {
 typedef enum { ADEPT_F32 = 0, ADEPT_BF16 = 1 } adept_dtype;
 
 /* Exit metric: GLOBAL compares h_i with the inertia of Section 4.1 (Eq. 7-8);
- * LOCAL compares h_i with h_{i-1} (the "local" metric of Appendix H.3). */
-typedef enum { ADEPT_SIM_GLOBAL = 0, ADEPT_SIM_LOCAL = 1 } adept_metric;
+ * LOCAL compares h_i with h_{i-1} (the "local" metric of Appendix H.3);
+ * BOTH is the combination Appendix H.3 compares the two against, which it
+ * does not define: taken here as exit iff both cosines reach delta (the
+ * inertia is kept and updated as for GLOBAL). */
+typedef enum { ADEPT_SIM_GLOBAL = 0, ADEPT_SIM_LOCAL = 1, ADEPT_SIM_BOTH = 2 } adept_metric;
 
 /* (host) Exit policy of Section 4.1, Eq. 8: token j exits at layer i iff
  * min_exit_layer <= i <= n_layers-1 and cos >= delta.  An undefined cosine
@@ -81,23 +84,25 @@ adept_status adept_rope_table(int max_pos, int head_dim, double theta,
  *  active_rows[k], k < *n_active (device count, <= max_active): rows tested.
  *  h_cur  [n_tok][d_model] (dtype): h_i, the residual stream after layer i.
  *  h_prev [n_tok][d_model] (dtype): h_{i-1}; read only for ADEPT_SIM_LOCAL
- *         (may be NULL otherwise).
+ *         and ADEPT_SIM_BOTH (may be NULL otherwise).
  *  inertia [n_tok][d_model] float: Eq. 7's running sum of unit states of the
- *         layers before i.  For ADEPT_SIM_GLOBAL it is read for the test and
- *         then updated in place, inertia += h_i/|h_i| (after the test).  For
- *         LOCAL it is not touched (may be NULL).
+ *         layers before i.  For ADEPT_SIM_GLOBAL and ADEPT_SIM_BOTH it is read
+ *         for the test and then updated in place, inertia += h_i/|h_i| (after
+ *         the test).  For LOCAL it is not touched (may be NULL).
  *  force_layer [n_tok] int32, nullable: f = force_layer[row] > 0 replaces the
  *         policy for that row by "exit iff layer == f and layer <= N-1"; 0
  *         keeps the policy (teacher forcing and fixed exit schedules).
  *  exit_flag [max_active] uint8 out: 1 = exit, aligned with active_rows.
- *  sim_out [max_active] double out, nullable: the cosine (NaN if undefined).
+ *  sim_out [max_active] double out, nullable: the cosine (NaN if undefined);
+ *         for BOTH the smaller of the two cosines (NaN if either is).
  *
  * The three sums <h,h>, <r,r>, <h,r> are reduced in double precision from
  * the stored values (each product is exact in double), the decision is
  * taken in double.  One wavefront per row; HBM-bound.  d_model must be a
- * multiple of 4 (GLOBAL, and LOCAL f32) or 8 (LOCAL bf16) and at most 8192
- * (GLOBAL; 8192 f32 / 16384 bf16 for LOCAL), else ADEPT_E_INVALID /
- * ADEPT_E_UNSUPPORTED; h_cur, h_prev and the inertia 16-byte aligned.
+ * multiple of 4 (GLOBAL, BOTH, and LOCAL f32) or 8 (LOCAL bf16) and at most
+ * 8192 (GLOBAL; 8192 f32 / 16384 bf16 for LOCAL; 4096 for BOTH), else
+ * ADEPT_E_INVALID / ADEPT_E_UNSUPPORTED; h_cur, h_prev and the inertia
+ * 16-byte aligned.
  * ------------------------------------------------------------------------- */
 adept_status adept_exit_test(adept_dtype dt, int d_model, int layer, const adept_exit_cfg* cfg,
                              const int32_t* active_rows, const int32_t* n_active, int max_active,
@@ -233,7 +238,7 @@ typedef struct {
                             K/V of all exited rows generated after layer N (no row of
                             the pass reads them); the pass must then run all N layers */
   void* h[2];            /* [n_tok][D] residual stream ping-pong */
-  float* inertia;        /* [n_tok][D] (GLOBAL metric) */
+  float* inertia;        /* [n_tok][D] (GLOBAL and BOTH metrics) */
   const int32_t* pos;    /* [n_tok] */
   const int32_t* seq;    /* [n_tok] */
   const int32_t* slot;   /* [n_tok] */
@@ -335,7 +340,7 @@ typedef struct {
   int32_t n_tok, n_seq, seq_len;   /* n_tok = n_seq * seq_len */
   int32_t reserved;
   void* h[2];            /* [n_tok][D] residual stream ping-pong */
-  float* inertia;        /* [n_tok][D] (GLOBAL metric) */
+  float* inertia;        /* [n_tok][D] (GLOBAL and BOTH metrics) */
   const int32_t* pos;    /* [n_tok] position of row j (j mod seq_len) */
   const int32_t* seq;    /* [n_tok] sequence of row j */
   int32_t* active[2];    /* [n_tok] ping-pong active lists */

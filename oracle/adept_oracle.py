@@ -34,6 +34,9 @@ Readings of the paper taken here (where it is silent or ambiguous):
     its logits use h_{i*}.
   * compaction keeps both lists in ascending row order (Appendix I update).
   * the "local" metric of Appendix H.3 is cos(h_i, h_{i-1}).
+  * the "both" metric of Appendix H.3 (not defined there) exits only when
+    the global and the local cosine both reach delta; its similarity is
+    the smaller of the two, and the inertia is kept as for the global one.
 """
 from __future__ import annotations
 
@@ -46,6 +49,7 @@ F64 = np.float64
 
 GLOBAL = "global"   # inertia metric, Section 4.1 Eq. 7-8
 LOCAL = "local"     # consecutive-layer metric, Appendix H.3
+BOTH = "both"       # both of them (Appendix H.3 names the combination, not its rule)
 
 
 # ---------------------------------------------------------------------------
@@ -135,6 +139,20 @@ def cosine(h, ref):
     ok = den > 0
     out[ok] = s_hr[ok] / den[ok]
     return out
+
+
+def similarity(metric, h, inertia, h_prev):
+    """The similarity the exit test compares with delta: the global cosine
+    (with the inertia), the local one (with h_{i-1}), or for "both" the
+    smaller of the two, so that sim >= delta exactly when both pass (NaN if
+    either is undefined)."""
+    if metric == GLOBAL:
+        return cosine(h, inertia)
+    if metric == LOCAL:
+        return cosine(h, h_prev)
+    if metric == BOTH:
+        return np.minimum(cosine(h, inertia), cosine(h, h_prev))   # NaN propagates
+    raise ValueError(metric)
 
 
 def exit_decision(sim, layer, n_layers, delta, min_exit_layer):
@@ -323,15 +341,15 @@ def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None):
         if active.size:
             h[active] = decoder_layer(weights["layers"][i - 1], shape, h_prev[active],
                                       pos[active], seq[active], cache, i)
-        ref = inertia[active] if cfg.metric == GLOBAL else h_prev[active]
-        sim = cosine(h[active], ref) if active.size else np.zeros(0)
+        sim = (similarity(cfg.metric, h[active], inertia[active], h_prev[active])
+               if active.size else np.zeros(0))
         sims[i - 1, active] = sim
         flags = exit_decision(sim, i, N, cfg.delta, cfg.min_exit_layer)
         if force_layer is not None:
             f = np.asarray(force_layer)[active]
             forced = f > 0
             flags = np.where(forced, (f == i) & (i <= N - 1), flags)
-        if cfg.metric == GLOBAL and active.size:
+        if cfg.metric != LOCAL and active.size:
             inertia[active] = inertia_update(inertia[active], h[active])
         active, exited = compact(flags, active)
         exit_layer[exited] = i
@@ -456,15 +474,15 @@ def classify(weights, shape, ids, cfg, force_layer=None):
                             lw["ln1_g"], lw["ln1_b"], shape.ln_eps)
             ff = gelu_erf(h1 @ lw["w_in"].T + lw["b_in"]) @ lw["w_out"].T + lw["b_out"]
             h[active] = layer_norm(h1 + ff, lw["ln2_g"], lw["ln2_b"], shape.ln_eps)
-        ref = inertia[active] if cfg.metric == GLOBAL else h_prev[active]
-        sim = cosine(h[active], ref) if active.size else np.zeros(0)
+        sim = (similarity(cfg.metric, h[active], inertia[active], h_prev[active])
+               if active.size else np.zeros(0))
         sims[i - 1, active] = sim
         flags = exit_decision(sim, i, N, cfg.delta, cfg.min_exit_layer)
         if force_layer is not None:
             f = np.asarray(force_layer).reshape(-1)[active]
             forced = f > 0
             flags = np.where(forced, (f == i) & (i <= N - 1), flags)
-        if cfg.metric == GLOBAL and active.size:
+        if cfg.metric != LOCAL and active.size:
             inertia[active] = inertia_update(inertia[active], h[active])
         active, exited = compact(flags, active)
         exit_layer[exited] = i

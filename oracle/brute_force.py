@@ -25,7 +25,7 @@ import math
 
 import numpy as np
 
-from .adept_oracle import (F64, GLOBAL, apply_rope, cosine, exit_decision, inertia_update,
+from .adept_oracle import (BOTH, F64, GLOBAL, apply_rope, cosine, exit_decision, inertia_update,
                            rms_norm, silu)
 
 
@@ -74,12 +74,19 @@ def brute_force_sequence(weights, shape, ids_row, cfg, force_row=None, prior=Non
             x1 = x + lw["wo"] @ o.reshape(-1)
             u2 = rms_norm(x1[None, :], lw["ffn_norm"], shape.rms_eps)[0]
             x_new = x1 + lw["w_down"] @ (silu(lw["w_gate"] @ u2) * (lw["w_up"] @ u2))
-            ref = inertia if cfg.metric == GLOBAL else x
-            sim = cosine(x_new[None, :], ref[None, :])
-            flag = bool(exit_decision(sim, i, N, cfg.delta, cfg.min_exit_layer)[0])
+            if cfg.metric == BOTH:
+                # both cosines must pass: two separate decisions, and-ed
+                flag = bool(exit_decision(cosine(x_new[None, :], inertia[None, :]), i, N,
+                                          cfg.delta, cfg.min_exit_layer)[0]) and \
+                    bool(exit_decision(cosine(x_new[None, :], x[None, :]), i, N, cfg.delta,
+                                       cfg.min_exit_layer)[0])
+            else:
+                ref = inertia if cfg.metric == GLOBAL else x
+                sim = cosine(x_new[None, :], ref[None, :])
+                flag = bool(exit_decision(sim, i, N, cfg.delta, cfg.min_exit_layer)[0])
             if force_row is not None and force_row[t] > 0:
                 flag = (force_row[t] == i) and i <= N - 1
-            if cfg.metric == GLOBAL:
+            if cfg.metric in (GLOBAL, BOTH):
                 inertia = inertia_update(inertia[None, :], x_new[None, :])[0]
             x = x_new
             if flag:

@@ -16,8 +16,8 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadept.so")
 
 F32, BF16 = 0, 1
-SIM_GLOBAL, SIM_LOCAL = 0, 1
-METRICS = {"global": SIM_GLOBAL, "local": SIM_LOCAL}
+SIM_GLOBAL, SIM_LOCAL, SIM_BOTH = 0, 1, 2
+METRICS = {"global": SIM_GLOBAL, "local": SIM_LOCAL, "both": SIM_BOTH}
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32

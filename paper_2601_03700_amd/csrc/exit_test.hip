@@ -12,7 +12,10 @@
 // For the global metric the inertia row is then updated from the registers,
 // so each byte of h and of the inertia crosses HBM once (read h, read +
 // write inertia).  Every access is streaming (non-temporal): nothing the
-// kernel touches is read again before it has left the caches.
+// kernel touches is read again before it has left the caches.  The combined
+// metric (both cosines must reach the threshold) reads h, h_prev and the
+// inertia with the global metric's grouping (4 elements per lane and chunk)
+// and keeps five sums.
 #include "common.h"
 
 namespace adept {
@@ -20,6 +23,9 @@ namespace {
 
 constexpr int kWavesPerBlock = 4;
 constexpr int kMaxChunks = 32;
+constexpr int kMaxChunksBoth = 16;   // three row streams in registers
+
+enum Mode { kLocal = 0, kGlobal = 1, kBoth = 2 };
 
 struct ExitParams {
   double delta;
@@ -42,7 +48,7 @@ template <typename T, typename R> __device__ __forceinline__ float elem(const R&
   }
 }
 
-template <typename T, int CH, bool GLOBAL>
+template <typename T, int CH, int MODE>
 __global__ __launch_bounds__(64 * kWavesPerBlock)
 void exit_test_kernel(
     ExitParams p, int max_active, const int32_t* __restrict__ rows,
@@ -50,6 +56,8 @@ void exit_test_kernel(
     const T* __restrict__ h_cur, const T* __restrict__ h_prev, float* __restrict__ inertia,
     const int32_t* __restrict__ force_layer, uint8_t* __restrict__ exit_flag,
     double* __restrict__ sim_out) {
+  constexpr bool GLOBAL = MODE != kLocal;   // reads and updates the inertia
+  constexpr bool BOTH = MODE == kBoth;      // also reads h_prev
   constexpr int E = GLOBAL ? 4 : 16 / (int)sizeof(T);
   using HRaw = typename Raw<E * sizeof(T)>::type;
   using RRaw = u32x4;   // 4 f32 of the inertia, or E values of h_prev
@@ -62,8 +70,11 @@ void exit_test_kernel(
   const uint32_t* rr = GLOBAL ? reinterpret_cast<const uint32_t*>(inertia + (int64_t)row * p.d)
                               : reinterpret_cast<const uint32_t*>(h_prev + (int64_t)row * p.d);
 
+  const T* pr = BOTH ? h_prev + (int64_t)row * p.d : nullptr;   // combined metric only
+
   HRaw hv[CH];
   RRaw rv[CH];
+  HRaw pv[BOTH ? CH : 1];
   // Loads are not predicated: a lane past the end of the row re-reads the
   // row's last vector and contributes zeros (predicated loads leave the
   // register allocator with partially defined values and cost spills).
@@ -72,8 +83,9 @@ void exit_test_kernel(
     const int vi = min(c * 64 + lane, nvec - 1);
     hv[c] = __builtin_nontemporal_load(reinterpret_cast<const HRaw*>(hr + vi * E));
     rv[c] = __builtin_nontemporal_load(reinterpret_cast<const RRaw*>(rr) + vi);
+    if constexpr (BOTH) pv[c] = __builtin_nontemporal_load(reinterpret_cast<const HRaw*>(pr + vi * E));
   }
-  double s_hh = 0.0, s_rr = 0.0, s_hr = 0.0;
+  double s_hh = 0.0, s_rr = 0.0, s_hr = 0.0, s_pp = 0.0, s_hp = 0.0;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const bool live = c * 64 + lane < nvec;
@@ -84,6 +96,11 @@ void exit_test_kernel(
       s_hh = fma(a, a, s_hh);
       s_rr = fma(b, b, s_rr);
       s_hr = fma(a, b, s_hr);
+      if constexpr (BOTH) {
+        const double q = live ? elem<T>(pv[c], v) : 0.0f;
+        s_pp = fma(q, q, s_pp);
+        s_hp = fma(a, q, s_hp);
+      }
     }
     // chunk by chunk: the conversions to double are not hoisted (and held
     // in registers) ahead of the chunk that needs them
@@ -92,11 +109,25 @@ void exit_test_kernel(
   s_hh = wave_sum_f64(s_hh);
   s_rr = wave_sum_f64(s_rr);
   s_hr = wave_sum_f64(s_hr);
+  if constexpr (BOTH) {
+    s_pp = wave_sum_f64(s_pp);
+    s_hp = wave_sum_f64(s_hp);
+  }
 
+  const double kNaN = __longlong_as_double(0x7ff8000000000000ll);
   const double nh = sqrt(s_hh), nr = sqrt(s_rr);
   const double den = nh * nr;
-  const double sim = den > 0.0 ? s_hr / den : __longlong_as_double(0x7ff8000000000000ll);
-  bool ex = (p.layer >= p.min_exit_layer) && (p.layer <= p.n_layers - 1) && (sim >= p.delta);
+  double sim = den > 0.0 ? s_hr / den : kNaN;
+  bool pass = sim >= p.delta;
+  if constexpr (BOTH) {
+    // the local cosine must pass too; the reported similarity is the
+    // smaller of the two (NaN if either is undefined)
+    const double den_l = nh * sqrt(s_pp);
+    const double sim_l = den_l > 0.0 ? s_hp / den_l : kNaN;
+    pass = pass && sim_l >= p.delta;
+    sim = (sim != sim || sim_l != sim_l) ? kNaN : fmin(sim, sim_l);
+  }
+  bool ex = (p.layer >= p.min_exit_layer) && (p.layer <= p.n_layers - 1) && pass;
   if (force_layer) {
     const int f = force_layer[row];
     if (f > 0) ex = (p.layer == f) && (p.layer <= p.n_layers - 1);
@@ -126,7 +157,7 @@ void exit_test_kernel(
   }
 }
 
-template <typename T, bool GLOBAL>
+template <typename T, int MODE>
 adept_status launch_exit(int ch, const ExitParams& p, int max_active, const int32_t* rows,
                          const int32_t* n_active, const void* h_cur, const void* h_prev,
                          float* inertia, const int32_t* force, uint8_t* flag, double* sim,
@@ -136,16 +167,22 @@ adept_status launch_exit(int ch, const ExitParams& p, int max_active, const int3
   const T* hp = (const T*)h_prev;
 #define ADEPT_EXIT_CASE(C)                                                                     \
   case C:                                                                                      \
-    ADEPT_LAUNCH((exit_test_kernel<T, C, GLOBAL>), grid, block, 0, s, p, max_active, rows, n_active, \
+    ADEPT_LAUNCH((exit_test_kernel<T, C, MODE>), grid, block, 0, s, p, max_active, rows, n_active, \
                        hc, hp, inertia, force, flag, sim);                                     \
     break;
-  switch (ch) {
+  switch (MODE == kBoth && ch > kMaxChunksBoth ? 0 : ch) {
     ADEPT_EXIT_CASE(1)
     ADEPT_EXIT_CASE(2)
     ADEPT_EXIT_CASE(4)
     ADEPT_EXIT_CASE(8)
     ADEPT_EXIT_CASE(16)
-    ADEPT_EXIT_CASE(32)
+    case 32:
+      if constexpr (MODE != kBoth) {
+        ADEPT_LAUNCH((exit_test_kernel<T, 32, MODE>), grid, block, 0, s, p, max_active, rows,
+                     n_active, hc, hp, inertia, force, flag, sim);
+        break;
+      }
+      [[fallthrough]];
     default:
       set_error("exit_test: unsupported chunk count %d", ch);
       return ADEPT_E_UNSUPPORTED;
@@ -167,21 +204,22 @@ extern "C" adept_status adept_exit_test(adept_dtype dt, int d_model, int layer,
                                         double* sim_out, void* stream) {
   ADEPT_REQUIRE(cfg != nullptr, "exit_test: cfg is NULL");
   ADEPT_REQUIRE(dt == ADEPT_F32 || dt == ADEPT_BF16, "exit_test: bad dtype %d", (int)dt);
-  ADEPT_REQUIRE(cfg->metric == ADEPT_SIM_GLOBAL || cfg->metric == ADEPT_SIM_LOCAL,
+  ADEPT_REQUIRE(cfg->metric == ADEPT_SIM_GLOBAL || cfg->metric == ADEPT_SIM_LOCAL ||
+                    cfg->metric == ADEPT_SIM_BOTH,
                 "exit_test: bad metric %d", cfg->metric);
   ADEPT_REQUIRE(cfg->n_layers >= 1 && layer >= 1 && layer <= cfg->n_layers,
                 "exit_test: layer %d outside 1..%d", layer, cfg->n_layers);
   ADEPT_REQUIRE(max_active >= 0, "exit_test: max_active < 0");
   ADEPT_REQUIRE(!std::isnan(cfg->delta), "exit_test: delta is NaN");
-  const bool global = cfg->metric == ADEPT_SIM_GLOBAL;
+  const bool global = cfg->metric != ADEPT_SIM_LOCAL;   // GLOBAL or BOTH: inertia
+  const bool both = cfg->metric == ADEPT_SIM_BOTH;
   // elements per lane and chunk (kernel's E)
   const int V = global ? 4 : (dt == ADEPT_BF16 ? 8 : 4);
   ADEPT_REQUIRE(d_model > 0 && d_model % V == 0, "exit_test: d_model %d not a multiple of %d",
                 d_model, V);
   ADEPT_REQUIRE(active_rows && n_active && h_cur && exit_flag, "exit_test: NULL tensor");
-  ADEPT_REQUIRE(global ? inertia != nullptr : h_prev != nullptr,
-                "exit_test: %s needs %s", global ? "GLOBAL" : "LOCAL",
-                global ? "inertia" : "h_prev");
+  ADEPT_REQUIRE(!global || inertia != nullptr, "exit_test: GLOBAL/BOTH need inertia");
+  ADEPT_REQUIRE((global && !both) || h_prev != nullptr, "exit_test: LOCAL/BOTH need h_prev");
   ADEPT_REQUIRE(aligned16(h_cur) && (!h_prev || aligned16(h_prev)) &&
                     (!inertia || aligned16(inertia)),
                 "exit_test: tensors must be 16-byte aligned");
@@ -190,20 +228,28 @@ extern "C" adept_status adept_exit_test(adept_dtype dt, int d_model, int layer,
   int ch = (nvec + 63) / 64;
   int chp = 1;
   while (chp < ch) chp <<= 1;
-  if (chp > kMaxChunks) {
-    set_error("exit_test: d_model %d too large (max %d)", d_model, kMaxChunks * 64 * V);
+  const int max_ch = both ? kMaxChunksBoth : kMaxChunks;
+  if (chp > max_ch) {
+    set_error("exit_test: d_model %d too large (max %d)", d_model, max_ch * 64 * V);
     return ADEPT_E_UNSUPPORTED;
   }
   ExitParams p{cfg->delta, cfg->min_exit_layer, cfg->n_layers, layer, d_model};
   hipStream_t s = as_stream(stream);
-  if (dt == ADEPT_BF16) {
-    return global ? launch_exit<bf16, true>(chp, p, max_active, active_rows, n_active, h_cur,
-                                            h_prev, inertia, force_layer, exit_flag, sim_out, s)
-                  : launch_exit<bf16, false>(chp, p, max_active, active_rows, n_active, h_cur,
-                                             h_prev, inertia, force_layer, exit_flag, sim_out, s);
+#define ADEPT_EXIT_MODE(T)                                                                   \
+  switch (cfg->metric) {                                                                     \
+    case ADEPT_SIM_GLOBAL:                                                                   \
+      return launch_exit<T, kGlobal>(chp, p, max_active, active_rows, n_active, h_cur, h_prev, \
+                                     inertia, force_layer, exit_flag, sim_out, s);           \
+    case ADEPT_SIM_LOCAL:                                                                    \
+      return launch_exit<T, kLocal>(chp, p, max_active, active_rows, n_active, h_cur, h_prev,  \
+                                    inertia, force_layer, exit_flag, sim_out, s);            \
+    default:                                                                                 \
+      return launch_exit<T, kBoth>(chp, p, max_active, active_rows, n_active, h_cur, h_prev,   \
+                                   inertia, force_layer, exit_flag, sim_out, s);             \
   }
-  return global ? launch_exit<float, true>(chp, p, max_active, active_rows, n_active, h_cur,
-                                           h_prev, inertia, force_layer, exit_flag, sim_out, s)
-                : launch_exit<float, false>(chp, p, max_active, active_rows, n_active, h_cur,
-                                            h_prev, inertia, force_layer, exit_flag, sim_out, s);
+  if (dt == ADEPT_BF16) {
+    ADEPT_EXIT_MODE(bf16)
+  }
+  ADEPT_EXIT_MODE(float)
+#undef ADEPT_EXIT_MODE
 }

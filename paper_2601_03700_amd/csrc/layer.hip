@@ -111,8 +111,8 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
                     a->exited && a->n_exited && a->exit_layer && a->exit_flag && a->k_cache &&
                     a->v_cache && a->q_buf && a->attn_out && a->ffn_act,
                 "layer_step: NULL pointer in args");
-  ADEPT_REQUIRE(a->exit.metric != ADEPT_SIM_GLOBAL || a->inertia,
-                "layer_step: GLOBAL metric needs inertia");
+  ADEPT_REQUIRE(a->exit.metric == ADEPT_SIM_LOCAL || a->inertia,
+                "layer_step: GLOBAL/BOTH metrics need inertia");
   const size_t need = adept_layer_workspace_bytes(a);
   if (!a->workspace || a->workspace_bytes < need) {
     set_error("layer_step: workspace of %zu bytes needed", need);

@@ -75,6 +75,18 @@ def test_host_validation_rejects_bad_arguments():
     # GLOBAL without inertia
     _expect_invalid(L.adept_exit_test(1, 256, 1, ctypes.byref(cfg), 16, 16, 4, 16, 16, None, None,
                                       16, None, None))
+    # BOTH needs h_prev and the inertia, and holds rows up to 4096 wide; unknown metric
+    both = B.exit_cfg(0.9, 4, "both")
+    _expect_invalid(L.adept_exit_test(1, 256, 1, ctypes.byref(both), 16, 16, 4, 16, None, 16,
+                                      None, 16, None, None))
+    _expect_invalid(L.adept_exit_test(1, 256, 1, ctypes.byref(both), 16, 16, 4, 16, 16, None,
+                                      None, 16, None, None))
+    assert L.adept_exit_test(1, 4100, 1, ctypes.byref(both), 16, 16, 4, 16, 16, 16, None, 16,
+                             None, None) == -2
+    bad = B.exit_cfg(0.9, 4)
+    bad.metric = 3
+    _expect_invalid(L.adept_exit_test(1, 256, 1, ctypes.byref(bad), 16, 16, 4, 16, 16, 16, None,
+                                      16, None, None))
     # compaction output aliasing its input
     _expect_invalid(L.adept_compact(1, 16, 32, 16, 8, 32, 16, 48, 16, 64, None, 0, None))
     # KV generation: layer stride smaller than one [2*H*hd][D] block

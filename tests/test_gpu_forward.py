@@ -58,7 +58,7 @@ def tiny_f32():
     return O.as64(w), ids, model
 
 
-@pytest.mark.parametrize("metric", ["local", "global"])
+@pytest.mark.parametrize("metric", ["local", "global", "both"])
 def test_tiny_f32_prefill_and_decode(tiny_f32, metric):
     """The tiny configuration (4 layers, width 256, 128-token prompt, 32
     greedy steps, local metric at delta 0.95) and thresholds that fire."""

@@ -109,6 +109,59 @@ def test_exit_test_matches_oracle(dt, D, metric):
         np.testing.assert_array_equal(new_g[untouched], ref.astype(np.float32)[untouched])
 
 
+@pytest.mark.parametrize("dt,D", [("bf16", 4096), ("bf16", 1000), ("f32", 256), ("f32", 4096)])
+def test_exit_test_both_metric_matches_oracle(dt, D):
+    """Combined metric: exit iff the global and the local cosine both reach
+    delta; sim_out is the smaller cosine; the inertia is updated as for the
+    global metric."""
+    say(f"exit_test both dt={dt} D={D}")
+    n_tok, N, layer = 500, 8, 3
+    seed = 300 + D
+    h = ai.normal(seed, "h", (n_tok, D), dtype=dt)
+    # per-row weights of h in both references, so that the two cosines spread
+    # independently and each one alone decides for some rows
+    rng = np.random.default_rng(seed)
+    wg = rng.uniform(0.3, 3.0, (n_tok, 1))
+    wl = rng.uniform(0.3, 3.0, (n_tok, 1))
+    inertia = (ai.normal(seed, "ref", (n_tok, D), dtype="f32") + wg * h).astype(np.float32)
+    prev = ai.normal(seed, "prev", (n_tok, D), dtype="f32") + wl * h
+    prev = ai.to_bf16_values(prev) if dt == "bf16" else prev.astype(np.float32)
+    h[5] = 0.0
+    inertia[9] = 0.0
+    prev[13] = 0.0
+    active = np.sort(rng.choice(n_tok, 401, replace=False)).astype(np.int32)
+    active[:3] = [5, 9, 13]
+    active = np.sort(active)
+    sims_o = O.similarity(O.BOTH, h[active], inertia[active], prev[active])
+    g_o = O.cosine(h[active], inertia[active])
+    l_o = O.cosine(h[active], prev[active])
+    srt = np.sort(sims_o[np.isfinite(sims_o)])
+    delta = float(0.5 * (srt[len(srt) // 2] + srt[len(srt) // 2 + 1]))
+    # the threshold splits the tokens so that each cosine alone decides some
+    assert np.sum((g_o >= delta) & ~(l_o >= delta)) > 0 and np.sum((l_o >= delta) & ~(g_o >= delta)) > 0
+    cfg = B.exit_cfg(delta, N, "both")
+    h_d, in_d, pv_d = dev(h, TDT[dt]), dev(inertia), dev(prev, TDT[dt])
+    flag_d = torch.full((len(active) + 8,), 7, dtype=torch.uint8, device=DEV)
+    sim_d = torch.full((len(active),), -5.0, dtype=torch.float64, device=DEV)
+    B.exit_test(D, layer, cfg, i32(active), count(len(active)), len(active), h_d, pv_d, in_d,
+                None, flag_d, sim_d)
+    torch.cuda.synchronize()
+    flags_o = O.exit_decision(sims_o, layer, N, delta, 1)
+    sims_g = sim_d.cpu().numpy()
+    ok = np.isfinite(sims_o)
+    np.testing.assert_array_equal(np.isfinite(sims_g), ok)
+    np.testing.assert_allclose(sims_g[ok], sims_o[ok], rtol=0, atol=1e-13)
+    assert np.min(np.abs(g_o[np.isfinite(g_o)] - delta)) > 1e-12
+    assert np.min(np.abs(l_o[np.isfinite(l_o)] - delta)) > 1e-12
+    np.testing.assert_array_equal(flag_d[:len(active)].cpu().numpy().astype(bool), flags_o)
+    assert (flag_d[len(active):].cpu().numpy() == 7).all()
+    new_o = O.inertia_update(inertia[active], h[active])
+    new_g = in_d.cpu().numpy()
+    np.testing.assert_allclose(new_g[active], new_o, rtol=2 ** -23, atol=2 ** -40)
+    untouched = np.setdiff1d(np.arange(n_tok), active)
+    np.testing.assert_array_equal(new_g[untouched], inertia[untouched])
+
+
 def test_exit_test_window_and_special_thresholds():
     say("exit_test window")
     D, n, N = 512, 64, 6

@@ -124,6 +124,29 @@ def test_cosine_closed_forms():
     assert np.isnan(s[4]) and np.isnan(s[5])
 
 
+def test_both_metric_is_and_of_global_and_local():
+    """The combined metric (a reading: Appendix H.3 does not define it) exits
+    only where both cosines pass; built from rows with known cosines."""
+    rng = np.random.default_rng(11)
+    a = rng.standard_normal(32)
+    b = rng.standard_normal(32)
+    b_perp = b - a * (a @ b) / (a @ a)
+    z = np.zeros(32)
+    #              global passes, local fails | local passes, global fails | both | none | NaN
+    h = np.stack([a, a, a, a, a])
+    inertia = np.stack([2 * a, b_perp, 5 * a, -a, z])
+    prev = np.stack([b_perp, 0.5 * a, 3 * a, b_perp, a])
+    sim = O.similarity(O.BOTH, h, inertia, prev)
+    np.testing.assert_allclose(sim[:4], [0.0, 0.0, 1.0, -1.0], atol=1e-15)
+    assert np.isnan(sim[4])
+    assert O.exit_decision(sim, 2, 4, 0.5, 1).tolist() == [False, False, True, False, False]
+    # the single metrics on the same rows
+    assert O.exit_decision(O.similarity(O.GLOBAL, h, inertia, prev), 2, 4, 0.5, 1).tolist() == \
+        [True, False, True, False, False]
+    assert O.exit_decision(O.similarity(O.LOCAL, h, inertia, prev), 2, 4, 0.5, 1).tolist() == \
+        [False, True, True, False, True]
+
+
 def test_exit_decision_window_and_special_thresholds():
     s = np.array([0.5, 0.97, np.nan, 1.0])
     assert O.exit_decision(s, 2, 4, 0.95, 1).tolist() == [False, True, False, True]
@@ -264,7 +287,8 @@ def test_exit_everything_at_k_is_truncated_model(small, k):
 
 
 CASES = [("global", 2, 0.5, False), ("global", 3, 0.3, False), ("local", 1, 0.6, False),
-         ("local", 2, 0.5, False), ("global", 2, 0.5, True)]
+         ("local", 2, 0.5, False), ("global", 2, 0.5, True), ("both", 2, 0.4, False),
+         ("both", 3, 0.3, False)]
 
 
 @pytest.mark.parametrize("metric,layer,q,forced", CASES)
@@ -313,7 +337,7 @@ def test_generation_matches_transformers_greedy(small):
             nxt = o.logits[:, 0].argmax(-1)
 
 
-@pytest.mark.parametrize("metric", ["global", "local"])
+@pytest.mark.parametrize("metric", ["global", "local", "both"])
 def test_generation_with_exits_equals_token_at_a_time(small, metric):
     """Generation steps with token-level exits (Appendix I, generation phase)
     equal the token-at-a-time recomputation over prompt + generated tokens."""
