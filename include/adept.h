@@ -58,13 +58,17 @@ typedef enum { ADEPT_SIM_GLOBAL = 0, ADEPT_SIM_LOCAL = 1, ADEPT_SIM_BOTH = 2 } a
 /* (host) Exit policy of Section 4.1, Eq. 8: token j exits at layer i iff
  * min_exit_layer <= i <= n_layers-1 and cos >= delta.  An undefined cosine
  * (a zero-norm vector, e.g. the empty inertia at layer 1) never exits, and
- * delta = +INFINITY never fires. */
+ * delta = +INFINITY never fires.  prompt_level = 1 selects the all-at-once
+ * variant of Appendix H.2 for prefill passes (adept_exit_prompt_level): the
+ * last prompt token of each sequence decides for all of its tokens; it is
+ * honoured by adept_layer_step with attn_tiles = 1 and rejected by the
+ * encoder step.  0 is the token-level method. */
 typedef struct {
   double delta;
   int32_t min_exit_layer;
   int32_t n_layers;
   int32_t metric; /* adept_metric */
-  int32_t reserved;
+  int32_t prompt_level;
 } adept_exit_cfg;
 
 int adept_abi_version(void);
@@ -109,6 +113,26 @@ adept_status adept_exit_test(adept_dtype dt, int d_model, int layer, const adept
                              const void* h_cur, const void* h_prev, float* inertia,
                              const int32_t* force_layer, uint8_t* exit_flag, double* sim_out,
                              void* stream);
+
+/* ---------------------------------------------------------------------------
+ * adept_exit_prompt_level -- the all-at-once variant of Appendix H.2: after
+ * adept_exit_test, every active row takes the decision of its sequence's
+ * last prompt token, i.e. the active row of that sequence with the largest
+ * position, so a sequence's tokens exit together.
+ *
+ *  active_rows[k], k < *n_active (<= max_active); exit_flag[k] in/out.
+ *  seq [n_tok] int32: sequence of each row, 0 <= seq < n_seq (rows outside
+ *  that range keep their flag); pos [n_tok] int32 >= 0.
+ *  workspace: adept_exit_prompt_level_workspace_bytes(n_seq) bytes, 8-byte
+ *  aligned (one 64-bit key per sequence), else ADEPT_E_WORKSPACE.
+ *  Three small kernels: clear the keys, per sequence the largest
+ *  (position, index) key, then the broadcast.
+ * ------------------------------------------------------------------------- */
+size_t adept_exit_prompt_level_workspace_bytes(int n_seq);
+adept_status adept_exit_prompt_level(const int32_t* active_rows, const int32_t* n_active,
+                                     int max_active, const int32_t* seq, const int32_t* pos,
+                                     int n_seq, uint8_t* exit_flag, void* workspace,
+                                     size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * adept_compact -- the active-index update of Appendix I: split the active

@@ -264,6 +264,7 @@ class ExitConfig:
     delta: float = math.inf        # Eq. 8 threshold; +inf never fires
     min_exit_layer: int = 1
     metric: str = GLOBAL
+    prompt_level: bool = False     # all-at-once variant (Appendix H.2)
 
 
 @dataclasses.dataclass
@@ -349,6 +350,13 @@ def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None):
             f = np.asarray(force_layer)[active]
             forced = f > 0
             flags = np.where(forced, (f == i) & (i <= N - 1), flags)
+        if cfg.prompt_level and active.size:
+            # Appendix H.2: each prompt's last token (its active row of
+            # largest position) decides for all of the prompt's tokens
+            sa, pa = seq[active], pos[active]
+            for b in np.unique(sa):
+                members = np.nonzero(sa == b)[0]
+                flags[members] = flags[members[np.argmax(pa[members])]]
         if cfg.metric != LOCAL and active.size:
             inertia[active] = inertia_update(inertia[active], h[active])
         active, exited = compact(flags, active)

@@ -31,7 +31,7 @@ class AdeptError(RuntimeError):
 
 class ExitCfg(ctypes.Structure):
     _fields_ = [("delta", ctypes.c_double), ("min_exit_layer", _i32), ("n_layers", _i32),
-                ("metric", _i32), ("reserved", _i32)]
+                ("metric", _i32), ("prompt_level", _i32)]
 
 
 class LayerArgs(ctypes.Structure):
@@ -76,6 +76,8 @@ _SIGS = {
     "adept_exit_test": (_i32, [_i32, _i32, _i32, ctypes.POINTER(ExitCfg), _vp, _vp, _i32, _vp,
                                _vp, _vp, _vp, _vp, _vp, _vp]),
     "adept_compact_workspace_bytes": (_sz, [_i32]),
+    "adept_exit_prompt_level_workspace_bytes": (_sz, [_i32]),
+    "adept_exit_prompt_level": (_i32, [_vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
     "adept_compact": (_i32, [_i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "adept_kv_generate_workspace_bytes": (_sz, [_i32, _i32]),
     "adept_kv_generate": (_i32, [_i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp, _vp,
@@ -149,8 +151,9 @@ def dtype_code(t_or_str):
     return {torch.float32: F32, torch.bfloat16: BF16}[t_or_str.dtype]
 
 
-def exit_cfg(delta, n_layers, metric="global", min_exit_layer=1):
-    return ExitCfg(float(delta), int(min_exit_layer), int(n_layers), METRICS[metric], 0)
+def exit_cfg(delta, n_layers, metric="global", min_exit_layer=1, prompt_level=False):
+    return ExitCfg(float(delta), int(min_exit_layer), int(n_layers), METRICS[metric],
+                   int(bool(prompt_level)))
 
 
 # ----------------------------------------------------------------------------
@@ -168,6 +171,19 @@ def exit_test(d_model, layer, cfg, active_rows, n_active, max_active, h_cur, h_p
                                  ptr(active_rows), ptr(n_active), max_active, ptr(h_cur),
                                  ptr(h_prev), ptr(inertia), ptr(force_layer), ptr(exit_flag),
                                  ptr(sim_out), stream_handle(stream)), "adept_exit_test")
+
+
+def exit_prompt_level_workspace_bytes(n_seq):
+    return lib().adept_exit_prompt_level_workspace_bytes(n_seq)
+
+
+def exit_prompt_level(active_rows, n_active, max_active, seq, pos, n_seq, exit_flag,
+                      workspace=None, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().adept_exit_prompt_level(ptr(active_rows), ptr(n_active), max_active, ptr(seq),
+                                         ptr(pos), n_seq, ptr(exit_flag), ptr(workspace),
+                                         ws_bytes, stream_handle(stream)),
+           "adept_exit_prompt_level")
 
 
 def compact_workspace_bytes(max_active):

@@ -196,6 +196,8 @@ extern "C" adept_status adept_encoder_layer_step(const adept_encoder_args* a, in
                     a->exit_layer && a->exit_flag && a->key_live && a->key_len && a->k_buf &&
                     a->v_buf && a->q_buf && a->attn_out && a->y_buf && a->ffn_act,
                 "encoder_layer_step: NULL tensor");
+  ADEPT_REQUIRE(a->exit.prompt_level == 0,
+                "encoder_layer_step: the all-at-once variant is defined for prefill only");
   ADEPT_REQUIRE(a->exit.metric == ADEPT_SIM_LOCAL || a->inertia,
                 "encoder_layer_step: GLOBAL/BOTH metrics need inertia");
   const size_t need = adept_encoder_workspace_bytes(a);

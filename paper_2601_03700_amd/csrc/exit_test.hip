@@ -191,10 +191,73 @@ adept_status launch_exit(int ch, const ExitParams& p, int max_active, const int3
   return launch_status("exit_test");
 }
 
+// All-at-once variant (Appendix H.2).  Key of an active row: (position + 1)
+// in the high word, its list index in the low word; the largest key of a
+// sequence names its last prompt token.
+__global__ __launch_bounds__(256) void prompt_level_clear(unsigned long long* __restrict__ key,
+                                                          int n_seq) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b < n_seq) key[b] = 0ull;
+}
+
+__global__ __launch_bounds__(256) void prompt_level_pick(
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ n_active, int max_active,
+    const int32_t* __restrict__ seq, const int32_t* __restrict__ pos, int n_seq,
+    unsigned long long* __restrict__ key) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= min(*n_active, max_active)) return;
+  const int row = rows[k];
+  const int b = seq[row];
+  if (b < 0 || b >= n_seq) return;
+  atomicMax(&key[b], ((unsigned long long)(uint32_t)(pos[row] + 1) << 32) | (uint32_t)k);
+}
+
+__global__ __launch_bounds__(256) void prompt_level_apply(
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ n_active, int max_active,
+    const int32_t* __restrict__ seq, int n_seq, const unsigned long long* __restrict__ key,
+    uint8_t* flag) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= min(*n_active, max_active)) return;
+  const int b = seq[rows[k]];
+  if (b < 0 || b >= n_seq) return;
+  // the deciding row rewrites its own flag with the value it already holds
+  flag[k] = flag[(uint32_t)key[b]];
+}
+
 }  // namespace
 }  // namespace adept
 
 using namespace adept;
+
+extern "C" size_t adept_exit_prompt_level_workspace_bytes(int n_seq) {
+  return n_seq > 0 ? (size_t)n_seq * sizeof(unsigned long long) : 0;
+}
+
+extern "C" adept_status adept_exit_prompt_level(const int32_t* active_rows,
+                                                const int32_t* n_active, int max_active,
+                                                const int32_t* seq, const int32_t* pos, int n_seq,
+                                                uint8_t* exit_flag, void* workspace,
+                                                size_t workspace_bytes, void* stream) {
+  ADEPT_REQUIRE(max_active >= 0 && n_seq >= 0, "exit_prompt_level: negative size");
+  ADEPT_REQUIRE(active_rows && n_active && seq && pos && exit_flag,
+                "exit_prompt_level: NULL tensor");
+  if (max_active == 0 || n_seq == 0) return ADEPT_OK;
+  const size_t need = adept_exit_prompt_level_workspace_bytes(n_seq);
+  if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 7)) {
+    set_error("exit_prompt_level: workspace of %zu bytes (8-byte aligned) needed", need);
+    return ADEPT_E_WORKSPACE;
+  }
+  hipStream_t s = as_stream(stream);
+  auto* key = (unsigned long long*)workspace;
+  ADEPT_LAUNCH(prompt_level_clear, dim3(ceil_div(n_seq, 256)), dim3(256), 0, s, key, n_seq);
+  ADEPT_CHECK_LAUNCH("prompt_level_clear");
+  ADEPT_LAUNCH(prompt_level_pick, dim3(ceil_div(max_active, 256)), dim3(256), 0, s, active_rows,
+               n_active, max_active, seq, pos, n_seq, key);
+  ADEPT_CHECK_LAUNCH("prompt_level_pick");
+  ADEPT_LAUNCH(prompt_level_apply, dim3(ceil_div(max_active, 256)), dim3(256), 0, s, active_rows,
+               n_active, max_active, seq, n_seq, key, exit_flag);
+  return launch_status("prompt_level_apply");
+}
 
 extern "C" adept_status adept_exit_test(adept_dtype dt, int d_model, int layer,
                                         const adept_exit_cfg* cfg, const int32_t* active_rows,
@@ -211,6 +274,8 @@ extern "C" adept_status adept_exit_test(adept_dtype dt, int d_model, int layer,
                 "exit_test: layer %d outside 1..%d", layer, cfg->n_layers);
   ADEPT_REQUIRE(max_active >= 0, "exit_test: max_active < 0");
   ADEPT_REQUIRE(!std::isnan(cfg->delta), "exit_test: delta is NaN");
+  ADEPT_REQUIRE(cfg->prompt_level == 0 || cfg->prompt_level == 1,
+                "exit_test: prompt_level %d is not 0 or 1", cfg->prompt_level);
   const bool global = cfg->metric != ADEPT_SIM_LOCAL;   // GLOBAL or BOTH: inertia
   const bool both = cfg->metric == ADEPT_SIM_BOTH;
   // elements per lane and chunk (kernel's E)

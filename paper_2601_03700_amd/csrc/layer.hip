@@ -23,6 +23,7 @@ struct LayerWs {
   void* attend;   size_t attend_bytes;
   void* kvgen;    size_t kvgen_bytes;
   int32_t* all_rows;  // [n_tok + 64]: rows 0..n_tok-1 and their count (deferred KV generation)
+  void* prompt;   size_t prompt_bytes;   // per-sequence keys of the all-at-once variant
   float* skinny;  size_t skinny_bytes;   // GEMM partial sums when n_tok <= 64 (decode)
   float* gemm_tmp;  // f32 path only
   size_t total;
@@ -41,6 +42,8 @@ LayerWs carve(const adept_layer_args* a, void* base) {
   w.kvgen_bytes = adept_kv_generate_workspace_bytes(a->n_layers, a->n_tok);
   w.kvgen = p + off; off += align256(w.kvgen_bytes);
   w.all_rows = (int32_t*)(p + off); off += align256(((size_t)a->n_tok + 64) * sizeof(int32_t));
+  w.prompt_bytes = adept_exit_prompt_level_workspace_bytes(a->n_seq);
+  w.prompt = p + off; off += align256(w.prompt_bytes);
   if (a->dtype == ADEPT_BF16 && a->n_tok <= 64) {
     w.skinny_bytes = std::max({skinny_ws_bytes(3 * dq, a->d_model), skinny_ws_bytes(a->d_model, dq),
                                skinny_ws_bytes(2 * a->d_ff, a->d_model),
@@ -184,6 +187,10 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   // 8. exit test (Eq. 7-8)
   ADEPT_TRY(adept_exit_test(dt, D, layer, &a->exit, act, nact, maxn, a->h[out], a->h[in],
                             a->inertia, a->force_layer, a->exit_flag, a->sim_out, stream));
+  // all-at-once variant (Appendix H.2): a prompt's last token decides for all of it
+  if (a->exit.prompt_level && a->attn_tiles)
+    ADEPT_TRY(adept_exit_prompt_level(act, nact, maxn, a->seq, a->pos, a->n_seq, a->exit_flag,
+                                      ws.prompt, ws.prompt_bytes, stream));
   // 9. active-list update
   ADEPT_TRY(adept_compact(layer, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
                           a->exited, a->n_exited, a->exit_layer, ws.compact, ws.compact_bytes,

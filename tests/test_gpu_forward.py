@@ -93,6 +93,39 @@ def test_tiny_f32_prefill_and_decode(tiny_f32, metric):
         assert rel_err(kg, cache_o.k) <= 1e-5 and rel_err(vg, cache_o.v) <= 1e-5
 
 
+@pytest.mark.parametrize("metric", ["global", "local"])
+def test_tiny_f32_all_at_once_prefill(metric):
+    """All-at-once variant (Appendix H.2) on the GPU: every prompt's tokens
+    take the decision of its last token; exit layers exact, logits and the
+    K/V cache within the f32 bound."""
+    w32 = ai.decoder_weights(TINY, seed=4, dtype="f32")
+    w = O.as64(w32)
+    ids = ai.token_ids(6, TINY.vocab, 4, 40)
+    B_, T = ids.shape
+    model = DecoderModel(TINY, w32, dtype="f32", rope_max_pos=64)
+    full, _ = O.prefill(w, TINY, ids, O.ExitConfig(delta=math.inf, metric=metric))
+    s_last = full.sims[: TINY.n_layers - 1, np.arange(B_) * T + T - 1]
+    s = np.sort(s_last[np.isfinite(s_last)])
+    for q in (0.4, 0.7):
+        j = int(q * (len(s) - 1))
+        delta = float(0.5 * (s[j] + s[j + 1]))
+        say(f"all-at-once metric={metric} delta={delta:.6f}")
+        cfg_o = O.ExitConfig(delta=delta, metric=metric, prompt_level=True)
+        res_o, cache_o = O.prefill(w, TINY, ids, cfg_o, s_max=T)
+        res_g, cache_g = model.prefill(ids, B.exit_cfg(delta, TINY.n_layers, metric,
+                                                       prompt_level=True), s_max=T, logits="all")
+        torch.cuda.synchronize()
+        tested = res_o.sims[: TINY.n_layers - 1]
+        assert np.nanmin(np.abs(tested - delta)) > 1e-6
+        el = res_g.exit_layer.cpu().numpy()
+        np.testing.assert_array_equal(el, res_o.exit_layer)
+        for b in range(B_):      # one exit layer per prompt
+            assert len(set(el[b * T:(b + 1) * T].tolist())) == 1
+        assert rel_err(res_g.logits.cpu().numpy(), res_o.logits) <= 1e-5
+        kg, vg = cache_host(cache_g, B_, T)
+        assert rel_err(kg, cache_o.k) <= 1e-5 and rel_err(vg, cache_o.v) <= 1e-5
+
+
 SMALL_BF16 = ai.DecoderShape(n_layers=6, d_model=512, n_heads=4, head_dim=128, d_ff=1024,
                              vocab=512)
 

@@ -317,6 +317,40 @@ def test_batched_prefill_equals_token_at_a_time(small, metric, layer, q, forced)
                                        np.stack(bf[b]["values"][r]), rtol=0, atol=1e-12)
 
 
+@pytest.mark.parametrize("metric", ["global", "local"])
+def test_all_at_once_follows_last_prompt_token(small, metric):
+    """All-at-once variant (Appendix H.2): a prompt's tokens all run until the
+    first layer at which the prompt's last token passes the test, and that
+    token's path equals the no-exit run's up to there (every key it attends
+    to is then still computed), so the exit layer of each prompt can be read
+    off the no-exit similarities of its last token; each token's final state
+    is its state after that layer in the no-exit run."""
+    w, ids = small
+    B, T = ids.shape
+    N = SMALL.n_layers
+    full, _ = O.prefill(w, SMALL, ids, O.ExitConfig(delta=math.inf, metric=metric))
+    last = np.arange(B) * T + T - 1
+    s_last = full.sims[:, last]                       # [N, B]
+    tested = s_last[: N - 1]
+    distinct = 0
+    for delta in np.quantile(tested[np.isfinite(tested)], [0.3, 0.5, 0.7, 0.9]):
+        res, _ = O.prefill(w, SMALL, ids, O.ExitConfig(delta=float(delta), metric=metric,
+                                                       prompt_level=True))
+        for b in range(B):
+            fire = [i for i in range(1, N) if s_last[i - 1, b] >= delta]
+            want = fire[0] if fire else N
+            rows = np.arange(b * T, (b + 1) * T)
+            assert (res.exit_layer[rows] == want).all(), (b, want, res.exit_layer[rows])
+            np.testing.assert_allclose(res.h_final[rows], full.hidden[want - 1][rows], rtol=0,
+                                       atol=1e-12)
+        distinct += len(set(res.exit_layer.tolist())) > 1
+    assert distinct > 0          # some threshold gives the prompts different exit layers
+    # token-level exits differ: the variant is not the method
+    tok, _ = O.prefill(w, SMALL, ids, O.ExitConfig(delta=float(np.median(s_last[1:N - 1])),
+                                                   metric=metric))
+    assert len(set(tok.exit_layer[:T].tolist())) > 1
+
+
 def test_generation_matches_transformers_greedy(small):
     """Full depth: prefill then greedy steps equal transformers' cached decoding."""
     w, ids = small
