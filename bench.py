@@ -328,11 +328,18 @@ def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf):
                 hi = mid
         ms, res, _ = run(B.exit_cfg(lo, N, args.metric), steps=2, warmup=1)
         frac = skipped_fraction(res.exit_layer, N)
+        # the all-at-once variant (Appendix H.2) at the same threshold: each
+        # prompt's last token decides for the whole prompt
+        ms_a, res_a, _ = run(B.exit_cfg(lo, N, args.metric, prompt_level=True), steps=2, warmup=1)
         res_out["calibrated"][f"{int(round(target * 100))}%"] = {
             "delta": lo, "tokens_per_s": n_tok / (ms / 1e3), "ms_per_step": ms,
             "skipped_fraction": frac, "speedup_vs_no_exit": ms_inf / ms,
             "rdc": reduction(res.exit_layer, shape),
-            "exit_layer_histogram": exit_histogram(res.exit_layer, N)}
+            "exit_layer_histogram": exit_histogram(res.exit_layer, N),
+            "all_at_once": {"tokens_per_s": n_tok / (ms_a / 1e3), "ms_per_step": ms_a,
+                            "skipped_fraction": skipped_fraction(res_a.exit_layer, N),
+                            "rdc": reduction(res_a.exit_layer, shape),
+                            "exit_layer_histogram": exit_histogram(res_a.exit_layer, N)}}
         log(f"calibrated delta {lo:.4f}: {frac:.1%} of token-layers skipped, "
             f"{ms:.1f} ms/step ({ms_inf / ms:.2f}x vs no exit)")
     return res_out
@@ -426,7 +433,22 @@ def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
     bytes_comp = n_tok * (1 + 4 + 4)
     et_s = et_ms / et_launch / 1e3
     comp_s = comp_ms / comp_launch / 1e3
-    del h, inertia
+    # the combined metric (global and local cosine) also reads h_prev: 12 D + 5 bytes per row
+    h_prev = torch.randn((n_tok, D), generator=g, device="cuda").to(torch.bfloat16)
+    cfg_b = B.exit_cfg(0.95, N, "both")
+    B.exit_test(D, 5, cfg_b, rows, cnt, n_tok, h, h_prev, inertia, None, flag)
+    torch.cuda.synchronize()
+    B.timing_reset()
+    B.timing_enable(True)
+    for _ in range(reps):
+        B.exit_test(D, 5, cfg_b, rows, cnt, n_tok, h, h_prev, inertia, None, flag)
+    torch.cuda.synchronize()
+    B.timing_enable(False)
+    kb = B.timing_read()
+    both_launch, both_ms = kb[[x for x in kb if x.startswith("(exit_test_kernel")][0]]
+    both_s = both_ms / both_launch / 1e3
+    bytes_both = n_tok * (2 * D + 2 * D + 8 * D) + n_tok * (4 + 1)
+    del h, inertia, h_prev
     # compaction of a 2^26-entry list (multi-pass path): reads flags (1 B) and
     # rows (4 B), writes each row once (4 B) -> 9 B per entry, plus the exit
     # layer (4 B) of each exiting row.  Exit fraction 0.3 is the headline;
@@ -477,6 +499,8 @@ def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
     del src, dst
     return {"rows": n_tok, "d_model": D, "exit_test_us": et_s * 1e6,
             "exit_test_gbs": bytes_et / et_s / 1e9, "exit_test_hbm_frac": bytes_et / et_s / PEAK_HBM,
+            "exit_test_both_metric_us": both_s * 1e6, "exit_test_both_metric_gbs": bytes_both / both_s / 1e9,
+            "exit_test_both_metric_hbm_frac": bytes_both / both_s / PEAK_HBM,
             "compact_us": comp_s * 1e6, "compact_gbs": bytes_comp / comp_s / 1e9,
             "compact_2p26_us": big_s * 1e6, "compact_2p26_gbs": bytes_big / big_s / 1e9,
             "compact_2p26_hbm_frac": bytes_big / big_s / PEAK_HBM,
