@@ -222,6 +222,29 @@ def decoder_weights_torch(shape: DecoderShape, seed: int, device, dtype=None, st
     }
 
 
+def hsm_weights(d_model: int, seed: int, dtype: str = "f32", std: float = 0.02) -> dict:
+    """Random-init weights of a hidden state mapper of width D (the layer list
+    of Table S1): fully connected weights N(0, std^2) in [out, in] order,
+    biases N(0, std^2), the three norm gains 1 + 0.1 N(0,1), a 3 x 3
+    convolution kernel N(0, 0.25) and its scalar bias N(0, 0.01) (f32)."""
+    D = d_model
+    return {
+        "g0": gains(seed, "hsm.g0", (D,), dtype),
+        "conv": normal(seed, "hsm.conv", (3, 3), 0.5, dtype="f32"),
+        "conv_b": float(normal(seed, "hsm.conv_b", (1,), 0.1, dtype="f32")[0]),
+        "w1": normal(seed, "hsm.w1", (4 * D, D), std, dtype=dtype),
+        "b1": normal(seed, "hsm.b1", (4 * D,), std, dtype=dtype),
+        "w2": normal(seed, "hsm.w2", (8 * D, 4 * D), std, dtype=dtype),
+        "b2": normal(seed, "hsm.b2", (8 * D,), std, dtype=dtype),
+        "w3": normal(seed, "hsm.w3", (4 * D, 8 * D), std, dtype=dtype),
+        "b3": normal(seed, "hsm.b3", (4 * D,), std, dtype=dtype),
+        "g1": gains(seed, "hsm.g1", (4 * D,), dtype),
+        "w4": normal(seed, "hsm.w4", (D, 4 * D), std, dtype=dtype),
+        "b4": normal(seed, "hsm.b4", (D,), std, dtype=dtype),
+        "g2": gains(seed, "hsm.g2", (D,), dtype),
+    }
+
+
 def forced_exit_layers(seed: int, n: int, lo: int, hi: int) -> np.ndarray:
     """Seeded exit schedule: exit layer of each of n tokens uniform in [lo, hi]."""
     return rng(seed, "forced_exit").integers(lo, hi + 1, size=n).astype(np.int32)
