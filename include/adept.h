@@ -135,6 +135,50 @@ adept_status adept_exit_prompt_level(const int32_t* active_rows, const int32_t* 
                                      size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * adept_hsm_forward -- the Hidden State Mapper of Section 4.2 (Appendix B,
+ * Table S1, Fig. S1): the mapped state s~ of each exiting token from its
+ * current state s_i, its previous state s_{i-1} and the inertia of Eq. 7
+ * (as the exit test of layer i saw it).  Per row (D = d_model):
+ *   x_r = RMSNorm(z_r) * g0 for z = (s_i, s_{i-1}, inertia), r = 0, 1, 2
+ *   u   = conv_bias + sum_{r,t} conv[r][t] * x_r[d + t - 1]  (zero outside 0..D-1)
+ *   a   = W1 u + b1                  [4D]
+ *   c   = W3 gelu(W2 gelu(a) + b2) + b3   (gelu: exact erf form)
+ *   e   = W4 (RMSNorm(c) * g1 + a) + b4   [D]
+ *   s~  = RMSNorm(e) * g2 + u
+ * (The paper leaves the activations, the skip sources and the biases open;
+ * this is the reading implemented.)  The four layers run as MFMA GEMMs.
+ *
+ *  rows[k], k < *n_rows (<= max_rows): token rows of the inputs.
+ *  h_cur, h_prev [n_tok][D] bf16; inertia [n_tok][D] float.
+ *  inertia_updated: 1 when the inertia already holds layer i's update
+ *  (inertia += s_i/|s_i|, the exit test's order), which is then taken back;
+ *  0 when it is the inertia before layer i.
+ *  out [n_tok][D] bf16: out[rows[k]] = s~_k; may be h_cur itself.
+ *  Weights (bf16, device, 16-byte aligned matrices in [out][in] order):
+ *  W1 [4D][D], W2 [8D][4D], W3 [4D][8D], W4 [D][4D], biases b1..b4, gains
+ *  g0 [D], g1 [4D], g2 [D]; the convolution (host floats) by value.
+ *  d_model a multiple of 256; workspace adept_hsm_workspace_bytes(D,
+ *  max_rows) bytes (44 * D bytes per row), 16-byte aligned.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  const void* g0;
+  float conv[3][3];      /* (host) row: state (current, previous, inertia); column: offset -1..1 */
+  float conv_bias;       /* (host) */
+  const void* w1; const void* b1;
+  const void* w2; const void* b2;
+  const void* w3; const void* b3;
+  const void* g1;
+  const void* w4; const void* b4;
+  const void* g2;
+} adept_hsm_weights;
+size_t adept_hsm_workspace_bytes(int d_model, int max_rows);
+adept_status adept_hsm_forward(adept_dtype dt, int d_model, float eps, const adept_hsm_weights* w,
+                               const int32_t* rows, const int32_t* n_rows, int max_rows,
+                               const void* h_cur, const void* h_prev, const float* inertia,
+                               int inertia_updated, void* out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * adept_compact -- the active-index update of Appendix I: split the active
  * list by the exit flags into the rows that continue and the rows that exit.
  *

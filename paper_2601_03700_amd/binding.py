@@ -34,6 +34,12 @@ class ExitCfg(ctypes.Structure):
                 ("metric", _i32), ("prompt_level", _i32)]
 
 
+class HsmWeights(ctypes.Structure):
+    _fields_ = [("g0", _vp), ("conv", (ctypes.c_float * 3) * 3), ("conv_bias", ctypes.c_float),
+                ("w1", _vp), ("b1", _vp), ("w2", _vp), ("b2", _vp), ("w3", _vp), ("b3", _vp),
+                ("g1", _vp), ("w4", _vp), ("b4", _vp), ("g2", _vp)]
+
+
 class LayerArgs(ctypes.Structure):
     _fields_ = [
         ("dtype", _i32), ("n_layers", _i32), ("d_model", _i32), ("n_heads", _i32),
@@ -76,6 +82,9 @@ _SIGS = {
     "adept_exit_test": (_i32, [_i32, _i32, _i32, ctypes.POINTER(ExitCfg), _vp, _vp, _i32, _vp,
                                _vp, _vp, _vp, _vp, _vp, _vp]),
     "adept_compact_workspace_bytes": (_sz, [_i32]),
+    "adept_hsm_workspace_bytes": (_sz, [_i32, _i32]),
+    "adept_hsm_forward": (_i32, [_i32, _i32, ctypes.c_float, ctypes.POINTER(HsmWeights), _vp, _vp,
+                                 _i32, _vp, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
     "adept_exit_prompt_level_workspace_bytes": (_sz, [_i32]),
     "adept_exit_prompt_level": (_i32, [_vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
     "adept_compact": (_i32, [_i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -184,6 +193,34 @@ def exit_prompt_level(active_rows, n_active, max_active, seq, pos, n_seq, exit_f
                                          ptr(pos), n_seq, ptr(exit_flag), ptr(workspace),
                                          ws_bytes, stream_handle(stream)),
            "adept_exit_prompt_level")
+
+
+def hsm_weights(w):
+    """HsmWeights from a dict of device tensors (bf16 matrices, biases and
+    gains) plus the host 3x3 "conv" values and the "conv_b" scalar.  Keep the
+    dict alive while the struct is used."""
+    hw = HsmWeights()
+    for k in ("g0", "w1", "b1", "w2", "b2", "w3", "b3", "g1", "w4", "b4", "g2"):
+        setattr(hw, k, ptr(w[k]))
+    for r in range(3):
+        for t in range(3):
+            hw.conv[r][t] = float(w["conv"][r][t])
+    hw.conv_bias = float(w["conv_b"])
+    return hw
+
+
+def hsm_workspace_bytes(d_model, max_rows):
+    return lib().adept_hsm_workspace_bytes(d_model, max_rows)
+
+
+def hsm_forward(d_model, eps, hw, rows, n_rows, max_rows, h_cur, h_prev, inertia,
+                inertia_updated, out, workspace=None, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().adept_hsm_forward(dtype_code(h_cur), d_model, eps, ctypes.byref(hw), ptr(rows),
+                                   ptr(n_rows), max_rows, ptr(h_cur), ptr(h_prev), ptr(inertia),
+                                   int(inertia_updated), ptr(out), ptr(workspace), ws_bytes,
+                                   stream_handle(stream)),
+           "adept_hsm_forward")
 
 
 def compact_workspace_bytes(max_active):
