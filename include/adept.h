@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define ADEPT_ABI_VERSION 2
+#define ADEPT_ABI_VERSION 3
 
 typedef enum {
   ADEPT_OK = 0,
@@ -271,6 +271,7 @@ adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale
  *   O GEMM (+residual: h[i&1] = h[(i-1)&1] + o Wo^T) -> RMSNorm ->
  *   gate/up GEMM (+SwiGLU) -> down GEMM (+residual) -> adept_exit_test ->
  *   adept_compact (next list into active[i&1], exited rows into `exited`) ->
+ *   [adept_hsm_forward on the exited rows, when `hsm` is set] ->
  *   adept_kv_generate for the rows exited at i (layers i+1..N); with
  *   attn_tiles = 0 (decode) the generation of every exited row is enqueued
  *   once, by the step of layer N, after copying the exit states into h[N&1].
@@ -327,6 +328,11 @@ typedef struct {
   void* ffn_act;         /* [n_tok][F] */
   void* workspace;
   size_t workspace_bytes;
+  /* mapper of the exiting rows (Section 4.2): NULL = identity (s~ = h_i);
+   * else adept_hsm_forward maps the rows exited at layer i in place in
+   * h[i&1] before their K/V are generated (bf16, GLOBAL or BOTH metric: it
+   * reads the inertia) */
+  const adept_hsm_weights* hsm;
 } adept_layer_args;
 
 size_t adept_layer_workspace_bytes(const adept_layer_args* a);

@@ -23,7 +23,9 @@ Readings of the paper taken here (where it is silent or ambiguous):
     is 0/0 = NaN and the token continues.
   * the test runs only for i_min <= i <= N-1 (exiting at N skips nothing).
   * the mapped state s~ fed to the KV generation is the identity map of the
-    exit state, s~ = h_{i*} (the trained mapper is not available).
+    exit state, s~ = h_{i*}, unless a mapper is given (the paper's trained
+    mapper is not available; oracle/hsm.py holds its architecture, which
+    takes the inertia as the exit test of layer i* saw it).
   * generated K/V of layer r apply layer r's own pre-attention RMSNorm, its
     own K/V projection and, for K, the rotary embedding at the token's
     position -- i.e. s~ is treated as layer r's input (Eq. 9).
@@ -311,7 +313,7 @@ def decoder_layer(layer_w, shape, h_in, pos, seq, cache, layer):
     return h1 + ff
 
 
-def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None):
+def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None, mapper=None):
     """Run a set of token rows through the N layers with token-level exit.
 
     This is the prefill of Appendix I when the rows are a whole prompt batch,
@@ -324,6 +326,10 @@ def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None):
       4. the exited rows' K/V for every layer r > i are generated (Eq. 9).
     force_layer (optional int [n]): a value f > 0 replaces the policy for that
     row by "exit exactly at layer f" (f >= N: never); 0 keeps the policy.
+    mapper (optional): s~ = mapper(h_i, h_{i-1}, inertia before layer i's
+    update) for the rows exiting at layer i (Section 4.2); s~ replaces h_i as
+    the exited row's state, so its generated K/V and its final state use it.
+    None is the identity mapper.
     """
     N, D = shape.n_layers, shape.d_model
     h0 = np.asarray(h0, F64)
@@ -357,10 +363,13 @@ def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None):
             for b in np.unique(sa):
                 members = np.nonzero(sa == b)[0]
                 flags[members] = flags[members[np.argmax(pa[members])]]
+        inertia_pre = inertia.copy() if mapper is not None else None
         if cfg.metric != LOCAL and active.size:
             inertia[active] = inertia_update(inertia[active], h[active])
         active, exited = compact(flags, active)
         exit_layer[exited] = i
+        if mapper is not None and exited.size and i < N:
+            h[exited] = mapper(h[exited], h_prev[exited], inertia_pre[exited])
         if exited.size and i < N:
             gen = kv_generate(weights, shape, h[exited], exit_layer[exited], pos[exited])
             for r, (idx, k, v) in gen.items():
@@ -372,7 +381,7 @@ def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None):
     return TokenPassResult(h, exit_layer, logits, sims, counts, hidden, inertia)
 
 
-def prefill(weights, shape, ids, cfg, s_max=None, force_layer=None):
+def prefill(weights, shape, ids, cfg, s_max=None, force_layer=None, mapper=None):
     """Prefill of a [B, T] prompt batch; rows are j = b*T + p (Appendix I's
     [4N, D_h] flattening).  Returns (TokenPassResult, KVCache)."""
     ids = np.asarray(ids)
@@ -383,7 +392,8 @@ def prefill(weights, shape, ids, cfg, s_max=None, force_layer=None):
     seq = np.repeat(np.arange(B), T)
     h0 = np.asarray(weights["embed"], F64)[ids.reshape(-1)]
     res = token_pass(weights, shape, h0, pos, seq, cache, cfg,
-                     None if force_layer is None else np.asarray(force_layer).reshape(-1))
+                     None if force_layer is None else np.asarray(force_layer).reshape(-1),
+                     mapper=mapper)
     return res, cache
 
 
@@ -392,26 +402,28 @@ def greedy(logits):
     return np.argmax(np.asarray(logits), axis=-1)
 
 
-def decode_step(weights, shape, cache, ids, pos, cfg, force_layer=None):
+def decode_step(weights, shape, cache, ids, pos, cfg, force_layer=None, mapper=None):
     """One generation step (Appendix I, generation phase): token ids[b] sits
     at position pos[b] of sequence b; inertia starts empty for the new token."""
     ids = np.asarray(ids)
     B = ids.shape[0]
     h0 = np.asarray(weights["embed"], F64)[ids]
-    return token_pass(weights, shape, h0, np.asarray(pos), np.arange(B), cache, cfg, force_layer)
+    return token_pass(weights, shape, h0, np.asarray(pos), np.arange(B), cache, cfg, force_layer,
+                      mapper=mapper)
 
 
-def generate(weights, shape, ids, n_steps, cfg, force_layer=None):
+def generate(weights, shape, ids, n_steps, cfg, force_layer=None, mapper=None):
     """Prefill of ids [B, T] then n_steps greedy generation steps.
     Returns (prefill result, list of step results, generated ids [B, n_steps], cache)."""
     B, T = np.asarray(ids).shape
-    res, cache = prefill(weights, shape, ids, cfg, s_max=T + n_steps, force_layer=force_layer)
+    res, cache = prefill(weights, shape, ids, cfg, s_max=T + n_steps, force_layer=force_layer,
+                         mapper=mapper)
     last = res.logits.reshape(B, T, -1)[:, -1]
     nxt = greedy(last)
     steps, out = [], []
     for s in range(n_steps):
         out.append(nxt)
-        st = decode_step(weights, shape, cache, nxt, np.full(B, T + s), cfg)
+        st = decode_step(weights, shape, cache, nxt, np.full(B, T + s), cfg, mapper=mapper)
         steps.append(st)
         nxt = greedy(st.logits)
     return res, steps, np.stack(out, axis=1) if out else np.zeros((B, 0), np.int64), cache

@@ -36,7 +36,7 @@ def _proj_kv(lw, shape, x, p):
     return apply_rope(k, np.array([p]), shape.rope_theta)[0], v
 
 
-def brute_force_sequence(weights, shape, ids_row, cfg, force_row=None, prior=None):
+def brute_force_sequence(weights, shape, ids_row, cfg, force_row=None, prior=None, mapper=None):
     """Process one sequence token by token.
 
     ids_row: [T] token ids.  prior: optional (keys, values) lists per layer
@@ -86,11 +86,14 @@ def brute_force_sequence(weights, shape, ids_row, cfg, force_row=None, prior=Non
                 flag = bool(exit_decision(sim, i, N, cfg.delta, cfg.min_exit_layer)[0])
             if force_row is not None and force_row[t] > 0:
                 flag = (force_row[t] == i) and i <= N - 1
+            inertia_seen = inertia
             if cfg.metric in (GLOBAL, BOTH):
                 inertia = inertia_update(inertia[None, :], x_new[None, :])[0]
-            x = x_new
+            x_prev, x = x, x_new
             if flag:
                 exit_at = i
+                if mapper is not None and i < N:
+                    x = mapper(x[None, :], x_prev[None, :], inertia_seen[None, :])[0]
                 for r in range(i + 1, N + 1):
                     kr, vr = _proj_kv(W[r - 1], shape, x, p)
                     keys[r - 1].append(kr)
@@ -104,11 +107,11 @@ def brute_force_sequence(weights, shape, ids_row, cfg, force_row=None, prior=Non
             "values": vals, "h_final": np.stack(finals)}
 
 
-def brute_force_prefill(weights, shape, ids, cfg, force_layer=None):
+def brute_force_prefill(weights, shape, ids, cfg, force_layer=None, mapper=None):
     """Brute force over a [B, T] batch: sequences are independent."""
     ids = np.asarray(ids)
     outs = []
     for b in range(ids.shape[0]):
         fr = None if force_layer is None else np.asarray(force_layer)[b]
-        outs.append(brute_force_sequence(weights, shape, ids[b], cfg, fr))
+        outs.append(brute_force_sequence(weights, shape, ids[b], cfg, fr, mapper=mapper))
     return outs

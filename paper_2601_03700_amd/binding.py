@@ -54,7 +54,7 @@ class LayerArgs(ctypes.Structure):
         ("exit_layer", _vp), ("exit_flag", _vp), ("sim_out", _vp), ("force_layer", _vp),
         ("k_cache", _vp), ("v_cache", _vp), ("n_slots", _i64),
         ("q_buf", _vp), ("attn_out", _vp), ("ffn_act", _vp),
-        ("workspace", _vp), ("workspace_bytes", _sz),
+        ("workspace", _vp), ("workspace_bytes", _sz), ("hsm", _vp),
     ]
 
 

@@ -24,6 +24,7 @@ struct LayerWs {
   void* kvgen;    size_t kvgen_bytes;
   int32_t* all_rows;  // [n_tok + 64]: rows 0..n_tok-1 and their count (deferred KV generation)
   void* prompt;   size_t prompt_bytes;   // per-sequence keys of the all-at-once variant
+  void* hsm;      size_t hsm_bytes;      // mapper activations (when a mapper is given)
   float* skinny;  size_t skinny_bytes;   // GEMM partial sums when n_tok <= 64 (decode)
   float* gemm_tmp;  // f32 path only
   size_t total;
@@ -44,6 +45,8 @@ LayerWs carve(const adept_layer_args* a, void* base) {
   w.all_rows = (int32_t*)(p + off); off += align256(((size_t)a->n_tok + 64) * sizeof(int32_t));
   w.prompt_bytes = adept_exit_prompt_level_workspace_bytes(a->n_seq);
   w.prompt = p + off; off += align256(w.prompt_bytes);
+  w.hsm_bytes = a->hsm ? adept_hsm_workspace_bytes(a->d_model, a->n_tok) : 0;
+  w.hsm = p + off; off += align256(w.hsm_bytes);
   if (a->dtype == ADEPT_BF16 && a->n_tok <= 64) {
     w.skinny_bytes = std::max({skinny_ws_bytes(3 * dq, a->d_model), skinny_ws_bytes(a->d_model, dq),
                                skinny_ws_bytes(2 * a->d_ff, a->d_model),
@@ -116,6 +119,8 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
                 "layer_step: NULL pointer in args");
   ADEPT_REQUIRE(a->exit.metric == ADEPT_SIM_LOCAL || a->inertia,
                 "layer_step: GLOBAL/BOTH metrics need inertia");
+  ADEPT_REQUIRE(!a->hsm || (dt == ADEPT_BF16 && a->exit.metric != ADEPT_SIM_LOCAL && a->inertia),
+                "layer_step: the mapper needs bf16 and the inertia (GLOBAL or BOTH metric)");
   const size_t need = adept_layer_workspace_bytes(a);
   if (!a->workspace || a->workspace_bytes < need) {
     set_error("layer_step: workspace of %zu bytes needed", need);
@@ -195,6 +200,12 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   ADEPT_TRY(adept_compact(layer, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
                           a->exited, a->n_exited, a->exit_layer, ws.compact, ws.compact_bytes,
                           stream));
+  // 9b. mapper (Section 4.2) of the rows that exited here: s~ replaces h_i
+  //     in place, so the K/V generation and the final state use it
+  if (a->hsm && layer < N && maxn > 0)
+    ADEPT_TRY(adept_hsm_forward(dt, D, a->rms_eps, a->hsm, a->exited, a->n_exited, maxn,
+                                a->h[out], a->h[in], a->inertia, 1, a->h[out], ws.hsm,
+                                ws.hsm_bytes, stream));
   // 10. K/V of the skipped layers of the rows that exited here (Eq. 9); in
   //     decode, of every row that exited in the pass, after layer N
   const bool defer = a->attn_tiles == 0;

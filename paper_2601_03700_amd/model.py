@@ -13,6 +13,7 @@ earlier steps) filled, with generated entries for every skipped layer.
 """
 from __future__ import annotations
 
+import ctypes
 import dataclasses
 import math
 
@@ -78,7 +79,8 @@ class DecoderModel:
     adept_inputs.decoder_weights_torch() (stacked torch tensors on device).
     """
 
-    def __init__(self, shape, weights, dtype="bf16", device="cuda", rope_max_pos=4096):
+    def __init__(self, shape, weights, dtype="bf16", device="cuda", rope_max_pos=4096,
+                 hsm_weights=None):
         self.shape = shape
         self.dtype = dtype
         self.tdt = _TORCH_DT[dtype]
@@ -116,6 +118,12 @@ class DecoderModel:
         B.fold_gain(self.w_qkv, self.attn_norm)
         B.fold_gain(self.w_gate, self.ffn_norm)
         B.fold_gain(self.w_up, self.ffn_norm)
+        # optional hidden state mapper (Section 4.2) of the exiting rows: a dict
+        # like adept_inputs.hsm_weights(); None keeps the identity mapper
+        self.hsm, self._hsm_struct = None, None
+        if hsm_weights is not None:
+            self.hsm = {k: (v if k in ("conv", "conv_b") else up(v)) for k, v in hsm_weights.items()}
+            self._hsm_struct = B.hsm_weights(self.hsm)
         self.rope_max_pos = rope_max_pos
         half = shape.head_dim // 2
         self.rope_cos = torch.empty((rope_max_pos, half), dtype=torch.float32, device=dev)
@@ -177,6 +185,7 @@ class DecoderModel:
         a.force_layer = B.ptr(st.force_layer)
         a.k_cache, a.v_cache, a.n_slots = B.ptr(cache.k), B.ptr(cache.v), cache.n_slots
         a.q_buf, a.attn_out, a.ffn_act = B.ptr(st.q_buf), B.ptr(st.attn_out), B.ptr(st.ffn_act)
+        a.hsm = ctypes.addressof(self._hsm_struct) if self._hsm_struct is not None else None
         need = B.layer_workspace_bytes(a)
         if st.workspace is None or st.workspace.numel() < need:
             st.workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)

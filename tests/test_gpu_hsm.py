@@ -97,3 +97,42 @@ def test_hsm_forward_empty_and_errors():
         B.hsm_forward(D, 1e-6, hw, rows, zero, 8, h, h, inertia, 0, out, ws[:100])
     with pytest.raises(B.AdeptError):
         B.hsm_forward(200, 1e-6, hw, rows, zero, 8, h, h, inertia, 0, out, ws)
+
+
+SMALL_BF16 = ai.DecoderShape(n_layers=6, d_model=512, n_heads=4, head_dim=128, d_ff=1024,
+                             vocab=512)
+
+
+@pytest.mark.parametrize("metric", ["global", "both"])
+def test_prefill_with_mapper_matches_oracle(metric):
+    """The layer step maps the rows exiting at each layer in place before
+    their K/V are generated; with a seeded exit schedule on both sides the
+    exit layers are exact and logits and caches are within the bf16 bound."""
+    import math
+    from oracle import adept_oracle as O
+    from paper_2601_03700_amd.model import DecoderModel
+    say(f"prefill with mapper, metric={metric}")
+    shape = SMALL_BF16
+    D = shape.d_model
+    w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
+    w = O.as64(w32)
+    hn = ai.hsm_weights(D, seed=2, dtype="bf16", std=1.0 / np.sqrt(4 * D))
+    h64 = H.HSMWeights(**{k: (np.asarray(v, np.float64) if k != "conv_b" else float(v))
+                          for k, v in hn.items()})
+    ids = ai.token_ids(10, shape.vocab, 3, 200)
+    force = np.random.default_rng(5).integers(0, shape.n_layers + 1, size=ids.shape)
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512, hsm_weights=hn)
+    res_g, cache_g = model.prefill(ids, B.exit_cfg(math.inf, shape.n_layers, metric),
+                                   force_layer=force, logits="all")
+    torch.cuda.synchronize()
+    mapper = lambda s, p, i: H.hsm_forward(h64, s, p, i, shape.rms_eps)
+    res_o, cache_o = O.prefill(w, shape, ids, O.ExitConfig(delta=math.inf, metric=metric),
+                               force_layer=force, mapper=mapper)
+    np.testing.assert_array_equal(res_g.exit_layer.cpu().numpy(), res_o.exit_layer)
+    bf16_close(cache_g.k.float().cpu().numpy().astype(np.float64), cache_o.k, "K cache")
+    bf16_close(cache_g.v.float().cpu().numpy().astype(np.float64), cache_o.v, "V cache")
+    bf16_close(res_g.logits.cpu().numpy(), res_o.logits, "logits")
+    # the identity mapper gives other logits: the mapper ran
+    ident, _ = O.prefill(w, shape, ids, O.ExitConfig(delta=math.inf, metric=metric),
+                         force_layer=force)
+    assert np.max(np.abs(ident.logits - res_o.logits)) > 0.1

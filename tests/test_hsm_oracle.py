@@ -85,3 +85,39 @@ def test_special_weights():
     x = O.rms_norm(s, w.g0, eps)
     np.testing.assert_allclose(out[:, 1:], x[:, :-1], rtol=0, atol=1e-13)
     np.testing.assert_allclose(out[:, 0], 0.0, atol=1e-15)
+
+
+SMALL = ai.DecoderShape(n_layers=4, d_model=64, n_heads=4, head_dim=16, d_ff=128, vocab=97)
+
+
+@pytest.mark.parametrize("metric,forced", [("global", False), ("both", False), ("global", True)])
+def test_prefill_with_mapper_equals_token_at_a_time(metric, forced):
+    """With the mapper in place of the identity, the batched prefill
+    (compaction, decoupled K/V from the mapped state) still equals the
+    token-at-a-time recomputation in which each token is mapped at its exit."""
+    from oracle import brute_force as BF
+    import math
+    w = O.as64(ai.decoder_weights(SMALL, seed=11))
+    ids = ai.token_ids(12, SMALL.vocab, 2, 12)
+    hw = _weights(SMALL.d_model, seed=5, std=0.08)
+    mapper = lambda s, p, i: H.hsm_forward(hw, s, p, i, SMALL.rms_eps)
+    full, _ = O.prefill(w, SMALL, ids, O.ExitConfig(delta=math.inf, metric=metric))
+    sims = full.sims[1:SMALL.n_layers - 1]
+    delta = float(np.quantile(sims[np.isfinite(sims)], 0.5))
+    cfg = O.ExitConfig(delta=delta, metric=metric)
+    force = (np.random.default_rng(4).integers(0, SMALL.n_layers + 1, size=ids.shape)
+             if forced else None)
+    res, cache = O.prefill(w, SMALL, ids, cfg, force_layer=force, mapper=mapper)
+    assert np.sum(res.exit_layer < SMALL.n_layers) > 0
+    bf = BF.brute_force_prefill(w, SMALL, ids, cfg, force_layer=force, mapper=mapper)
+    B_, T = ids.shape
+    for b in range(B_):
+        rows = slice(b * T, (b + 1) * T)
+        np.testing.assert_array_equal(res.exit_layer[rows], bf[b]["exit_layer"])
+        np.testing.assert_allclose(res.logits[rows], bf[b]["logits"], rtol=0, atol=1e-12)
+        for r in range(SMALL.n_layers):
+            np.testing.assert_allclose(cache.k[r][rows], np.stack(bf[b]["keys"][r]), rtol=0,
+                                       atol=1e-12)
+    # the mapper changes the result (it is not silently skipped)
+    ident, _ = O.prefill(w, SMALL, ids, cfg, force_layer=force)
+    assert np.max(np.abs(ident.logits - res.logits)) > 1e-3
