@@ -264,6 +264,9 @@ def main():
         log(f"no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
         out["delta_sweep"] = delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf)
         out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
+        out["hsm_standalone"] = hsm_standalone(shape, ai, B, torch, np)
+        log(f"hsm (mapper) 4096 rows: {out['hsm_standalone']['call_ms']:.2f} ms, "
+            f"{out['hsm_standalone']['tflops']:.0f} TFLOP/s")
         out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
 
     if not args.no_generation:
@@ -394,6 +397,56 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
             "sentinel_ok": sentinel_ok,
             "gemm_ms": gemm_ms, "mfma_util": flops / (gemm_ms / 1e3) / PEAK_BF16,
             "mfma_util_whole_call": flops / (call_ms / 1e3) / PEAK_BF16,
+            "kernels": {kk: {"launches": v[0], "avg_us": 1e3 * v[1] / max(v[0], 1)}
+                        for kk, v in k.items()}}
+
+
+def hsm_standalone(shape, ai, B, torch, np, n_rows=4096, reps=5):
+    """Hidden state mapper (Section 4.2, Table S1) at the decoder's width for
+    n_rows exiting tokens: 144 D^2 FLOPs per row in the four fully connected
+    layers (MFMA GEMMs), plus the input and norm row kernels."""
+    D = shape.d_model
+    g = torch.Generator(device="cuda").manual_seed(21)
+    std = 1.0 / math.sqrt(4 * D)
+
+    def rnd(*dims, mean=0.0, sd=std):
+        return (torch.randn(dims, generator=g, device="cuda") * sd + mean).to(torch.bfloat16)
+    # random-init weights of the Table S1 layer list, drawn on the device
+    wd = {"g0": rnd(D, mean=1.0, sd=0.1), "w1": rnd(4 * D, D), "b1": rnd(4 * D),
+          "w2": rnd(8 * D, 4 * D), "b2": rnd(8 * D), "w3": rnd(4 * D, 8 * D), "b3": rnd(4 * D),
+          "g1": rnd(4 * D, mean=1.0, sd=0.1), "w4": rnd(D, 4 * D), "b4": rnd(D),
+          "g2": rnd(D, mean=1.0, sd=0.1),
+          "conv": np.random.default_rng(21).normal(0.0, 0.5, (3, 3)), "conv_b": 0.05}
+    hw = B.hsm_weights(wd)
+    h = torch.randn((n_rows, D), generator=g, device="cuda").to(torch.bfloat16)
+    hp = torch.randn((n_rows, D), generator=g, device="cuda").to(torch.bfloat16)
+    inertia = torch.randn((n_rows, D), generator=g, device="cuda")
+    rows = torch.arange(n_rows, dtype=torch.int32, device="cuda")
+    cnt = torch.tensor([n_rows], dtype=torch.int32, device="cuda")
+    out = torch.empty_like(h)
+    ws = torch.empty(B.hsm_workspace_bytes(D, n_rows), dtype=torch.uint8, device="cuda")
+
+    def call():
+        B.hsm_forward(D, shape.rms_eps, hw, rows, cnt, n_rows, h, hp, inertia, 0, out, ws)
+    call()
+    torch.cuda.synchronize()
+    B.timing_reset()
+    B.timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    B.timing_enable(False)
+    k = B.timing_read()
+    ms = e0.elapsed_time(e1) / reps
+    flops = 144.0 * D * D * n_rows
+    fc_ms = sum(v[1] for kk, v in k.items() if kk.startswith("hsm_fc")) / reps
+    del wd, h, hp, inertia, out, ws
+    return {"d_model": D, "rows": n_rows, "gflop_per_row": 144.0 * D * D / 1e9, "call_ms": ms,
+            "tflops": flops / (ms / 1e3) / 1e12, "mfma_util": flops / (ms / 1e3) / PEAK_BF16,
+            "fc_gemm_ms": fc_ms, "fc_mfma_util": flops / (fc_ms / 1e3) / PEAK_BF16 if fc_ms else None,
             "kernels": {kk: {"launches": v[0], "avg_us": 1e3 * v[1] / max(v[0], 1)}
                         for kk, v in k.items()}}
 
