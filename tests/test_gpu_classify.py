@@ -75,20 +75,21 @@ def test_classify_full_depth(enc):
     bf16_close(out.logits.cpu().numpy(), ref.logits, "logits")
 
 
-def test_classify_policy_decisions(enc):
-    """Global metric, a threshold between the oracle's similarities: every
-    token whose margin exceeds 5e-3 at every tested layer exits at the same
-    layer on both sides."""
+@pytest.mark.parametrize("metric", ["global", "both"])
+def test_classify_policy_decisions(enc, metric):
+    """A threshold between the oracle's similarities (global or combined
+    metric): every token whose margin exceeds 5e-3 at every tested layer exits
+    at the same layer on both sides."""
     w32, w, model = enc
-    say("classify policy")
+    say(f"classify policy metric={metric}")
     ids = ai.token_ids(41, ENC.vocab, 2, 96)
-    full = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf))
+    full = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf, metric=metric))
     sims = full.sims[:ENC.n_layers - 1]
     fin = np.sort(sims[np.isfinite(sims)])
     q = np.searchsorted(fin, np.quantile(fin, 0.6))
     delta = float(0.5 * (fin[q - 1] + fin[q]))
-    ref = O.classify(w, ENC, ids, O.ExitConfig(delta=delta))
-    out = model.classify(ids, B.exit_cfg(delta, ENC.n_layers, "global"))
+    ref = O.classify(w, ENC, ids, O.ExitConfig(delta=delta, metric=metric))
+    out = model.classify(ids, B.exit_cfg(delta, ENC.n_layers, metric))
     torch.cuda.synchronize()
     m = np.abs(ref.sims - delta)
     safe = np.nanmin(np.where(np.isfinite(m), m, np.inf), axis=0) > 5e-3
