@@ -618,6 +618,69 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     }
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_wave_barrier();
+    if constexpr (EPI == EPI_RESID || EPI == EPI_STORE || EPI == EPI_GELU) {
+      if (EPI != EPI_STORE || !p.c_f32) {   // wave-uniform
+        // Row-segment form: 16 lanes per row, 8 consecutive columns per lane
+        // (two 16-byte LDS reads of the staged f32 row), so the residual
+        // segment is one 16-byte load and the result one 16-byte store; the
+        // 8 residual loads of a block are issued together (one memory
+        // latency per block).  The sum is rounded to bf16 once.
+        const bool full = mb + 32 <= M;
+        const int sg = lane & 15;
+        const int col = nw + 8 * sg;
+        int drow[8];
+        float scv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int R = 4 * q + (lane >> 4);
+          drow[q] = EPI == EPI_RESID ? mrow[i * 32 + R] : mb + R;
+          scv[q] = msc[i * 32 + R];
+        }
+        uint4 rres[8];
+        if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const int m = mb + 4 * q + (lane >> 4);
+            rres[q] = (full || m < M) ? *reinterpret_cast<const uint4*>(
+                                            reinterpret_cast<const bf16*>(p.resid) +
+                                            (int64_t)drow[q] * p.ldc + col)
+                                      : make_uint4(0, 0, 0, 0);
+          }
+        }
+        const float4 b0 = bias4(p.bias, col), b1 = bias4(p.bias, col + 4);
+        const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int R = 4 * q + (lane >> 4);
+          const int m = mb + R;
+          const float4 f0 = *reinterpret_cast<const float4*>(stg + R * kEpiStride + 8 * sg);
+          const float4 f1 = *reinterpret_cast<const float4*>(stg + R * kEpiStride + 8 * sg + 4);
+          const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+          float x[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            x[e] = f[e] * scv[q] + bv[e];
+            if constexpr (EPI == EPI_GELU) x[e] = gelu_erf(x[e]);
+          }
+          if constexpr (EPI == EPI_RESID) {
+            const uint32_t rw[4] = {rres[q].x, rres[q].y, rres[q].z, rres[q].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              x[2 * e] += __uint_as_float(rw[e] << 16);
+              x[2 * e + 1] += __uint_as_float(rw[e] & 0xffff0000u);
+            }
+          }
+          const uint4 o = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
+                                     pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7]));
+          if (full || m < M)
+            *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + (int64_t)drow[q] * p.ldc +
+                                      col) = o;
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);   // reads done before the next block's writes
+        __builtin_amdgcn_wave_barrier();
+        return;
+      }
+    }
     // Each block is emitted in phases: all LDS reads of a group of rounds
     // into registers, then the global loads they index, then arithmetic and
     // stores (the stores go through generic pointers, which the compiler
