@@ -264,7 +264,7 @@ def main():
         log(f"no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
         out["delta_sweep"] = delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf)
         out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
-        out["hsm_standalone"] = hsm_standalone(shape, ai, B, torch, np)
+        out["hsm_standalone"] = hsm_standalone(shape, B, torch, np)
         log(f"hsm (mapper) 4096 rows: {out['hsm_standalone']['call_ms']:.2f} ms, "
             f"{out['hsm_standalone']['tflops']:.0f} TFLOP/s")
         out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
@@ -401,7 +401,7 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
                         for kk, v in k.items()}}
 
 
-def hsm_standalone(shape, ai, B, torch, np, n_rows=4096, reps=5):
+def hsm_standalone(shape, B, torch, np, n_rows=4096, reps=5):
     """Hidden state mapper (Section 4.2, Table S1) at the decoder's width for
     n_rows exiting tokens: 144 D^2 FLOPs per row in the four fully connected
     layers (MFMA GEMMs), plus the input and norm row kernels."""

@@ -11,8 +11,8 @@
 // wave land on consecutive addresses.  Lists up to 64K entries (the
 // per-layer case) use one workgroup over the whole list; longer lists use
 // three passes over 16K-entry tiles: a count of exits per tile (16 flags per
-// thread, one 16-byte load) that also stores the 64-bit exit mask of every
-// 64 entries, a scan of the tile counts, and the split of each tile from its
+// 16-byte load, four loads per thread) that also stores the 64-bit exit mask
+// of every 64 entries, a scan of the tile counts, and the split of each tile from its
 // offsets, which reads the masks (one bit per entry) instead of the flags.
 // Input order is kept in both outputs.
 #include "common.h"
@@ -22,8 +22,7 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
-constexpr int kTileItems = 16;                 // flags per thread in the count pass
-constexpr int kTile = kThreads * kTileItems;   // multi-pass tile = 16K entries
+constexpr int kTile = 1 << 14;                 // multi-pass tile = 16K entries
 constexpr int kSingleMax = 1 << 16;            // lists up to this use one workgroup
 constexpr int kMaxSteps = kSingleMax / kThreads;   // 64-entry steps per wave, at most
 constexpr int kBatch = 16;                     // steps whose loads are issued together
