@@ -846,6 +846,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GP p) {
 // takes items from the chunk of its own XCD (workgroups are dispatched to the
 // XCDs round-robin), in order, so that the tiles running together on an XCD
 // share operand slices in its L2, and then helps drain the other chunks.
+// A chunk's counter only grows; values past the chunk's end are discarded.
 // Taking items from counters rather than a fixed stride keeps the
 // workgroups busy until the last items: item times vary with the clock and
 // with how much of a layer's weights come from HBM.
@@ -856,30 +857,38 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kv_grouped_kernel(GP p) {
   const int total = n_work * p.tiles_n;
   const int chunk = (total + 7) >> 3;
   const int home = blockIdx.x & 7;
-  // the item index is passed to all waves through the first word of the
-  // LDS ring, which no tile uses between items
+  // The item index is passed to all waves through the first word of the LDS
+  // ring, which no tile uses between items.  Thread 0 takes each counter
+  // value one item ahead, so the atomic's round trip passes during a tile;
+  // a value past its chunk moves it on to the next chunk (-1: all drained).
   int* const s_item = reinterpret_cast<int*>(smem);
-  for (int q = 0; q < 8; ++q) {
-    const int qi = (home + q) & 7;
-    const int lo = qi * chunk, hi = min(total, lo + chunk);
-    for (;;) {
-      if (threadIdx.x == 0) *s_item = lo + atomicAdd(&p.queue[qi], 1);
-      __syncthreads();
-      const int t = __builtin_amdgcn_readfirstlane(*s_item);
-      __syncthreads();  // every wave has the index before the ring is refilled
-      if (t >= hi) break;
-      constexpr int G = 8;
-      const int gsz = G * p.tiles_n;
-      const int g = t / gsz, r = t - g * gsz;
-      const int rows_in_g = min(G, n_work - g * G);
-      const int w = g * G + r % rows_in_g, nt = r / rows_in_g;
-      const int packed = p.work[w];
-      const int layer = packed >> 16, mt = packed & 0xffff;
-      const int M = p.grp_m[layer];
-      gemm_tile<EPI_KV, true, HD>(p, smem, layer, mt, nt, M,
-                              p.B + (int64_t)(layer - 1) * p.b_layer_stride);
-      __syncthreads();  // LDS is reused by the next item
+  int qn = 0, qi = home, pre = 0;
+  if (threadIdx.x == 0) pre = atomicAdd(&p.queue[qi], 1);
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int t = qi * chunk + pre;
+      while (t >= min(total, qi * chunk + chunk) && ++qn < 8) {
+        qi = (home + qn) & 7;
+        t = qi * chunk + atomicAdd(&p.queue[qi], 1);
+      }
+      *s_item = qn < 8 ? t : -1;
+      if (qn < 8) pre = atomicAdd(&p.queue[qi], 1);
     }
+    __syncthreads();
+    const int t = __builtin_amdgcn_readfirstlane(*s_item);
+    __syncthreads();  // every wave has the index before the ring is refilled
+    if (t < 0) break;
+    constexpr int G = 8;
+    const int gsz = G * p.tiles_n;
+    const int g = t / gsz, r = t - g * gsz;
+    const int rows_in_g = min(G, n_work - g * G);
+    const int w = g * G + r % rows_in_g, nt = r / rows_in_g;
+    const int packed = p.work[w];
+    const int layer = packed >> 16, mt = packed & 0xffff;
+    const int M = p.grp_m[layer];
+    gemm_tile<EPI_KV, true, HD>(p, smem, layer, mt, nt, M,
+                                p.B + (int64_t)(layer - 1) * p.b_layer_stride);
+    __syncthreads();  // LDS is reused by the next item
   }
 }
 
