@@ -1,18 +1,23 @@
 #!/usr/bin/env python3
 """Throughput of the early-exit hot path on one MI355X.
 
-One step = one prefill pass of a Llama-7B-shaped decoder (32 layers, width
-4096, 32 heads x 128, SwiGLU 11008, vocab 32000; bf16, random-init weights)
-over a batch of 8 x 2048 uniform-random tokens with token-level exit: per
-layer the regular layer for the active rows, the exit test (Eq. 7-8),
-compaction of the active list, and the decoupled KV generation (Eq. 9) for
-the rows that exit; then the final norm and LM head for the last position of
-each sequence.  Inputs and weights are resident in HBM before timing.
+One step = one generation pass of a Llama-7B-shaped decoder (32 layers,
+width 4096, 32 heads x 128, SwiGLU 11008, vocab 32000; bf16, random-init
+weights): prefill of 64 prompts of 4096 uniform-random tokens, then 256
+greedy decode steps, with token-level exit throughout -- per layer the
+regular layer for the active rows, the exit test (Eq. 7-8), compaction of
+the active list and the decoupled KV generation (Eq. 9) of the rows that
+exit; attention runs over the cache of computed and generated entries.
+Inputs, weights and the cache are resident in HBM before timing.  The value
+is (prefill + decode) tokens/s of the whole pass.
 
-Printed: one JSON line with tokens/s, the roofline of the dominant kernel
-(timed live with HIP events inside the timed steps), the standalone KV
-generation's MFMA utilisation and the exit test's HBM bandwidth, the no-exit
-and fixed-schedule variants, and the CPU oracle on a bounded sample.
+Printed: one JSON line with that value, the roofline of the pass's dominant
+kernel (timed live with HIP events inside the timed passes), the 8 x 2048
+prefill section (threshold sweep, calibrated thresholds, the no-exit and
+fixed-schedule variants, per-kernel MFMA figures), the standalone KV
+generation, mapper, exit test and compaction, the fixed-schedule generation,
+the BERT-base classification, the tiny f32 decoder, and the CPU oracle on a
+bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--delta 0.95] [--metric global]
 """
@@ -28,14 +33,18 @@ import time
 PEAK_BF16 = 2.5e15      # dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12       # HBM3E, B/s
 HERE = os.path.dirname(os.path.abspath(__file__))
-TRAFFIC_FILE = os.path.join(HERE, "profiles", "llama7b_prefill_8x2048_hbm_traffic.json")
+# rocprofv3 traffic summaries: the generation headline (decode attention) and
+# the 8 x 2048 prefill section (GEMMs, prefill attention, exit test, compaction)
+TRAFFIC_FILES = (os.path.join(HERE, "profiles", "llama7b_generation_64x4096_hbm_traffic.json"),
+                 os.path.join(HERE, "profiles", "llama7b_prefill_8x2048_hbm_traffic.json"))
 
 
 # HIP sources each kernel family is built from (its traffic figure is void
 # once any of them changes)
 FAMILY_SOURCES = {
     "gemm": ("gemm.hip", "common.h"), "kv_generate": ("gemm.hip", "kvgen.hip", "common.h"),
-    "attention": ("attention.hip", "common.h"), "exit_test": ("exit_test.hip", "common.h"),
+    "attention": ("attention.hip", "common.h"), "attention_decode": ("attention.hip", "common.h"),
+    "exit_test": ("exit_test.hip", "common.h"),
     "compact_single": ("compact.hip", "common.h"),
 }
 
@@ -60,17 +69,39 @@ def measured_traffic(fam):
     FETCH_SIZE / WRITE_SIZE summary (each scaled by what it reads for a
     device copy of known size), or None when the sources of that kernel
     changed after the counters were taken."""
-    try:
-        with open(TRAFFIC_FILE) as fh:
-            d = json.load(fh)
-    except OSError:
+    if fam not in FAMILY_SOURCES and not fam.startswith("gemm_"):
         return None
-    k = d.get("kernels", {}).get(fam)
-    if k is None or fam not in FAMILY_SOURCES and not fam.startswith("gemm_"):
-        return None
-    if k.get("source_sha256") != sources_sha256(family_sources(fam)):
-        return None
-    return k["traffic_bytes"]
+    for path in TRAFFIC_FILES:
+        try:
+            with open(path) as fh:
+                d = json.load(fh)
+        except OSError:
+            continue
+        k = d.get("kernels", {}).get(fam)
+        if k is None:
+            continue
+        if k.get("source_sha256") != sources_sha256(family_sources(fam)):
+            return None
+        return k["traffic_bytes"]
+    return None
+
+
+def measured_traffic_ratio(fam):
+    """HBM bytes per algorithmic byte of a kernel family from the committed
+    summaries (for a kernel whose bytes per launch vary with the workload,
+    such as the decode attention with the context length), or None."""
+    for path in TRAFFIC_FILES:
+        try:
+            with open(path) as fh:
+                k = json.load(fh).get("kernels", {}).get(fam)
+        except OSError:
+            continue
+        if k is None:
+            continue
+        if k.get("source_sha256") != sources_sha256(family_sources(fam)):
+            return None
+        return k.get("traffic_per_algorithmic_byte")
+    return None
 
 
 def log(*a):
@@ -80,8 +111,11 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=2,
+                    help="timed generation passes (prefill + decode steps) of the headline")
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--prefill-steps", type=int, default=5,
+                    help="timed steps of the 8 x 2048 prefill section")
     ap.add_argument("--delta", type=float, default=0.95)
     ap.add_argument("--metric", choices=("global", "local"), default="global")
     ap.add_argument("--batch", type=int, default=8)
@@ -177,18 +211,41 @@ def main():
     model = DecoderModel(shape, weights, dtype="bf16", rope_max_pos=rope_pos)
     del weights
     torch.cuda.empty_cache()
-    ids = torch.from_numpy(ai.token_ids(8, shape.vocab, Bn, T)).cuda()
-    cache = model.new_cache(Bn, T)
     if args.copy_calibration:
         src = torch.ones(1 << 27, dtype=torch.int16, device="cuda")   # 256 MiB
         dst = torch.empty_like(src)
         dst.copy_(src)
         del src, dst
     torch.cuda.synchronize()
-    log(f"weights + cache ready in {time.time() - t0:.1f}s; "
+    log(f"weights ready in {time.time() - t0:.1f}s; "
         f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated")
 
-    def run(cfg, force=None, steps=args.steps, warmup=args.warmup, timing=False):
+    # ---- headline: generation (prefill + decode) with the policy's decisions
+    log(f"headline: generation, batch {args.gen_batch}, {args.gen_context}-token prompts, "
+        f"{args.gen_steps} decode steps, delta={args.delta} metric={args.metric}; "
+        f"{args.warmup} warmup + {args.steps} timed passes")
+    head = generation_policy(args, model, shape, ai, B, torch, np)
+    out = {
+        "metric": "tokens/s (prefill+decode) at Llama-7B shape; KV-gen MFMA util %",
+        "value": head["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": head["ms_per_pass"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded uniform token ids, random-init N(0,0.02) weights)",
+        "config": {"workload": (f"Llama-7B-shaped decoder generation: batch {args.gen_batch}, "
+                                f"{args.gen_context}-token prompts prefilled, then "
+                                f"{args.gen_steps} greedy decode steps; token-level exit "
+                                f"({args.metric} metric, delta {args.delta})"),
+                   "global_batch": args.gen_batch, "seq_len": args.gen_context + args.gen_steps,
+                   "parallelism": "none (one GPU)"},
+        "roofline": head.pop("roofline"),
+        "generation_policy": head,
+    }
+
+    # ---- prefill 8 x 2048 with the threshold sweep and the per-kernel figures
+    ids = torch.from_numpy(ai.token_ids(8, shape.vocab, Bn, T)).cuda()
+    cache = model.new_cache(Bn, T)
+
+    def run(cfg, force=None, steps=args.prefill_steps, warmup=2, timing=False):
         for _ in range(warmup):
             res, _ = model.prefill(ids, cfg, cache=cache, logits="last", force_layer=force)
         torch.cuda.synchronize()
@@ -208,52 +265,47 @@ def main():
         return e0.elapsed_time(e1) / steps, res, kern
 
     cfg = B.exit_cfg(args.delta, N, args.metric)
-    log(f"timed run: delta={args.delta} metric={args.metric}, {args.warmup} warmup + {args.steps} steps")
-    ms, res, kern = run(cfg, timing=True)
+    psteps = args.prefill_steps
+    ms, res, kern = run(cfg, timing=True, warmup=0 if psteps <= 1 else 2)
     tok_s = n_tok / (ms / 1e3)
     pos = torch.arange(T, dtype=torch.int32).repeat(Bn)
     work, cnt = step_work(shape, res.exit_layer, pos)
     exit_frac = 1.0 - cnt[-1] / n_tok
-    log(f"{ms:.1f} ms/step, {tok_s:.0f} tokens/s, exited {exit_frac:.3%}")
-
-    per_kernel = kernel_table(kern, work, ms, args.steps)
+    log(f"prefill {Bn}x{T}: {ms:.1f} ms/step, {tok_s:.0f} tokens/s, exited {exit_frac:.3%}")
+    per_kernel = kernel_table(kern, work, ms, psteps)
     dom = max((k for k in kern if family(k)), key=lambda k: kern[k][1])
     d_launch, d_ms = kern[dom]
-    d_flops_launch = work[family(dom)] * args.steps / d_launch
+    d_flops_launch = work[family(dom)] * psteps / d_launch
     d_avg_s = d_ms / d_launch / 1e3
     achieved = d_flops_launch / d_avg_s
-    roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16, "traffic": measured_traffic(family(dom)),
-                "flops_per_launch": d_flops_launch, "avg_launch_us": d_avg_s * 1e6,
-                "launches": d_launch}
-
-    out = {
-        "metric": "tokens/s (prefill+decode) at Llama-7B shape; KV-gen MFMA util %",
-        "value": tok_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic (seeded uniform token ids, random-init N(0,0.02) weights)",
-        "config": {"workload": (f"Llama-7B-shaped decoder prefill, batch {Bn} x {T}, token-level "
-                                f"exit ({args.metric} metric, delta {args.delta})"),
-                   "global_batch": Bn, "seq_len": T, "parallelism": "none (one GPU)"},
-        "roofline": roofline,
+    pre = {
+        "workload": (f"Llama-7B-shaped decoder prefill, batch {Bn} x {T}, token-level exit "
+                     f"({args.metric} metric, delta {args.delta})"),
+        "tokens_per_s": tok_s, "ms_per_step": ms, "steps": psteps,
+        "dominant_kernel": {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12,
+                            "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+                            "frac": achieved / PEAK_BF16,
+                            "traffic": measured_traffic(family(dom)),
+                            "flops_per_launch": d_flops_launch, "avg_launch_us": d_avg_s * 1e6,
+                            "launches": d_launch},
         "exit_fraction": exit_frac,
         "rdc": reduction(res.exit_layer, shape),
         "active_rows_per_layer": cnt,
         "kernels": per_kernel,
     }
+    out["prefill_8x2048"] = pre
 
     if not args.no_extras:
         # no-exit reference (delta = +inf) and a fixed exit schedule (i* ~ U{8..31})
-        ms_inf, _, _ = run(B.exit_cfg(math.inf, N, args.metric), steps=max(2, args.steps // 2),
+        ms_inf, _, _ = run(B.exit_cfg(math.inf, N, args.metric), steps=max(2, psteps // 2),
                            warmup=1)
         sched = torch.from_numpy(ai.forced_exit_layers(3, n_tok, 8, 31)).cuda()
-        ms_f, res_f, kern_f = run(cfg, force=sched, steps=max(2, args.steps // 2), warmup=1,
+        ms_f, res_f, kern_f = run(cfg, force=sched, steps=max(2, psteps // 2), warmup=1,
                                   timing=True)
         work_f, cnt_f = step_work(shape, res_f.exit_layer, pos)
-        out["no_exit"] = {"tokens_per_s": n_tok / (ms_inf / 1e3), "ms_per_step": ms_inf}
-        steps_f = max(2, args.steps // 2)
-        out["fixed_schedule"] = {
+        pre["no_exit"] = {"tokens_per_s": n_tok / (ms_inf / 1e3), "ms_per_step": ms_inf}
+        steps_f = max(2, psteps // 2)
+        pre["fixed_schedule"] = {
             "schedule": "exit layer uniform in 8..31 per token (seeded)",
             "tokens_per_s": n_tok / (ms_f / 1e3), "ms_per_step": ms_f,
             "speedup_vs_no_exit": ms_inf / ms_f,
@@ -261,18 +313,18 @@ def main():
             "active_rows_per_layer": cnt_f,
             "kernels": kernel_table(kern_f, work_f, ms_f, steps_f),
         }
-        log(f"no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
-        out["delta_sweep"] = delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf)
+        log(f"prefill no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
+        pre["delta_sweep"] = delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf)
         out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
         out["hsm_standalone"] = hsm_standalone(shape, B, torch, np)
         log(f"hsm (mapper) 4096 rows: {out['hsm_standalone']['call_ms']:.2f} ms, "
             f"{out['hsm_standalone']['tflops']:.0f} TFLOP/s")
         out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
 
+    del cache, ids
+    torch.cuda.empty_cache()
     if not args.no_generation:
-        del cache, ids
-        torch.cuda.empty_cache()
-        out["generation"] = generation(args, model, shape, ai, B, torch, np)
+        out["generation_fixed_schedule"] = generation(args, model, shape, ai, B, torch, np)
 
     if not args.no_classification:
         del model
@@ -563,6 +615,112 @@ def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
                     "(16K entries) is latency-bound, the 2^26 list measures bandwidth"}
 
 
+def decode_attention_bytes(shape, el_steps, T):
+    """Algorithmic bytes of the decode attention over a pass: each active
+    (query, layer) streams the K and V rows (bf16) of its whole context.
+    el_steps: [S][B] exit layers of the decode steps' tokens."""
+    import torch
+    N, H, hd = shape.n_layers, shape.n_heads, shape.head_dim
+    el = el_steps.to(torch.int64).cpu()
+    total = 0.0
+    for k in range(el.shape[0]):
+        active = sum(int((el[k] >= i).sum()) for i in range(1, N + 1))
+        total += active * (T + k + 1) * H * hd * 2 * 2
+    return total
+
+
+def generation_policy(args, model, shape, ai, B, torch, np):
+    """The headline: generation at the 7B shape with the policy's own exit
+    decisions.  One step = one pass: prefill of gen_batch prompts of
+    gen_context uniform-random tokens, then gen_steps greedy decode steps
+    (each new token through the layers with token-level exit, attention over
+    the mixed computed / generated cache).  Timed: `steps` passes after
+    `warmup` untimed ones, each launch also timed on its stream."""
+    N = shape.n_layers
+    Bn, T, S = args.gen_batch, args.gen_context, args.gen_steps
+    cache = model.new_cache(Bn, T + S)
+    ids = torch.from_numpy(ai.token_ids(9, shape.vocab, Bn, T)).cuda()
+    cfg = B.exit_cfg(args.delta, N, args.metric)
+    pos_dec = [torch.full((Bn,), T + k, dtype=torch.int32, device="cuda") for k in range(S)]
+
+    def one_pass(ev=None):
+        if ev is not None:
+            ev[0].record()
+        res, _ = model.prefill(ids, cfg, cache=cache, logits="last")
+        nxt = model.greedy(res.logits)
+        if ev is not None:
+            ev[1].record()
+        els = []
+        for k in range(S):
+            st = model.decode_step(cache, nxt, pos_dec[k], cfg, pos_max=T + k)
+            nxt = model.greedy(st.logits)
+            els.append(st.exit_layer)
+        if ev is not None:
+            ev[2].record()
+        return res.exit_layer, torch.stack(els) if els else torch.zeros((0, Bn), dtype=torch.int32)
+
+    t0 = time.time()
+    for _ in range(args.warmup):
+        one_pass()
+    torch.cuda.synchronize()
+    log(f"headline: cache {2 * cache.k.numel() * 2 / 2**30:.0f} GiB, {args.warmup} warmup "
+        f"pass(es) in {time.time() - t0:.1f}s")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    B.timing_reset()
+    B.timing_enable(True)
+    torch.cuda.synchronize()
+    e0.record()
+    passes = [one_pass(evs[k]) for k in range(args.steps)]
+    e1.record()
+    torch.cuda.synchronize()
+    B.timing_enable(False)
+    kern = B.timing_read()
+    ms_pass = e0.elapsed_time(e1) / args.steps
+    prefill_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    decode_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    el_prompt, el_dec = passes[-1]
+    # the dominant kernel over the timed passes and its roofline
+    dom = max(kern, key=lambda k: kern[k][1])
+    d_launch, d_ms = kern[dom]
+    d_avg_s = d_ms / d_launch / 1e3
+    if dom.startswith("attend_split"):
+        bytes_launch = sum(decode_attention_bytes(shape, p[1], T) for p in passes) / d_launch
+        achieved = bytes_launch / d_avg_s
+        ratio = measured_traffic_ratio("attention_decode")
+        roofline = {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9,
+                    "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": achieved / PEAK_HBM,
+                    "traffic": ratio * bytes_launch if ratio else None,
+                    "bytes_per_launch": bytes_launch, "avg_launch_us": d_avg_s * 1e6,
+                    "launches": d_launch}
+    else:
+        roofline = {"bound": None, "kernel": dom, "achieved": None, "peak": None, "unit": None,
+                    "frac": None, "traffic": None, "avg_launch_us": d_avg_s * 1e6,
+                    "launches": d_launch}
+    tokens = Bn * (T + S)
+    out = {
+        "tokens_per_s": tokens / (ms_pass / 1e3), "ms_per_pass": ms_pass,
+        "prefill_ms": prefill_ms, "decode_ms": decode_ms,
+        "prefill_tokens_per_s": Bn * T / (prefill_ms / 1e3),
+        "decode_tokens_per_s": Bn * S / (decode_ms / 1e3) if S else None,
+        "decode_ms_per_step": decode_ms / S if S else None,
+        "prompt_exit_fraction": float((el_prompt < N).to(torch.float64).mean()),
+        "prompt_rdc": reduction(el_prompt, shape),
+        "decode_exit_fraction": float((el_dec < N).to(torch.float64).mean()) if S else None,
+        "exited_fraction_by_layer": [float((el_dec <= i).to(torch.float64).mean())
+                                     for i in range(1, N + 1)] if S else None,
+        "roofline": roofline,
+        "kernels": {k: {"launches": n, "avg_us": ms * 1e3 / n, "share": ms / (ms_pass * args.steps)}
+                    for k, (n, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1])[:16]},
+    }
+    log(f"headline: {ms_pass:.0f} ms per pass = {out['tokens_per_s']:.0f} tokens/s "
+        f"(prefill {prefill_ms:.0f} ms, decode {decode_ms / max(S, 1):.1f} ms/step); "
+        f"{dom} {roofline.get('frac') or 0:.3f} of its roofline")
+    del cache, ids
+    torch.cuda.empty_cache()
+    return out
+
+
 def generation(args, model, shape, ai, B, torch, np):
     """Generation at the 7B shape: a batch of gen_context-token prompts is
     prefilled with exits (exit layer uniform in 8..31 per token, seeded), so
@@ -595,7 +753,8 @@ def generation(args, model, shape, ai, B, torch, np):
         el = []
         for k in range(2):      # warmup at the first two positions (rewritten below)
             pos = torch.full((Bn,), T + k, dtype=torch.int32, device="cuda")
-            model.decode_step(cache, nxt, pos, cfg_, force_layer=None if force is None else force[k])
+            model.decode_step(cache, nxt, pos, cfg_, force_layer=None if force is None else force[k],
+                              pos_max=T + k)
         torch.cuda.synchronize()
         if timing:
             B.timing_reset()
@@ -605,7 +764,7 @@ def generation(args, model, shape, ai, B, torch, np):
         for k in range(n_steps):
             pos = torch.full((Bn,), T + k, dtype=torch.int32, device="cuda")
             st = model.decode_step(cache, nxt, pos, cfg_,
-                                   force_layer=None if force is None else force[k])
+                                   force_layer=None if force is None else force[k], pos_max=T + k)
             nxt = model.greedy(st.logits)
             el.append(st.exit_layer)
         e1.record()

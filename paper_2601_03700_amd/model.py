@@ -193,8 +193,10 @@ class DecoderModel:
         return a
 
     # ------------------------------------------------------------------ passes
-    def _check_positions(self, pos, s_max):
-        pmax = int(pos.max()) if pos.numel() else 0
+    def _check_positions(self, pos, s_max, pos_max=None):
+        """Positions must lie inside the rotary table and the cache; pos_max
+        (a host int, when the caller knows it) avoids reading pos back."""
+        pmax = pos_max if pos_max is not None else (int(pos.max()) if pos.numel() else 0)
         if pmax >= self.rope_max_pos or pmax >= s_max:
             raise ValueError(f"position {pmax} outside rotary table / cache")
 
@@ -234,7 +236,7 @@ class DecoderModel:
             cache = self.new_cache(Bn, s_max)
         pos = torch.arange(T, dtype=torch.int32, device=dev).repeat(Bn)
         seq = torch.arange(Bn, dtype=torch.int32, device=dev).repeat_interleave(T)
-        self._check_positions(pos, s_max)
+        self._check_positions(pos, s_max, pos_max=T - 1)
         fl = None
         if isinstance(force_layer, torch.Tensor):
             fl = force_layer.reshape(-1).to(dev, torch.int32)
@@ -249,12 +251,13 @@ class DecoderModel:
                               True, rows, on_layer)
         return res, cache
 
-    def decode_step(self, cache, ids, pos, cfg, force_layer=None, on_layer=None):
-        """One new token per sequence: ids, pos int32 device tensors [n_seq]."""
+    def decode_step(self, cache, ids, pos, cfg, force_layer=None, on_layer=None, pos_max=None):
+        """One new token per sequence: ids, pos int32 device tensors [n_seq];
+        pos_max: the largest position, when known on the host (no read-back)."""
         dev = self.device
         n = int(ids.shape[0])
         seq = torch.arange(n, dtype=torch.int32, device=dev)
-        self._check_positions(pos, cache.s_max)
+        self._check_positions(pos, cache.s_max, pos_max)
         rows = torch.arange(n, dtype=torch.int32, device=dev)
         return self.token_pass(ids.to(torch.int32), pos.to(torch.int32), seq, cache, cfg,
                                force_layer, False, rows, on_layer)
@@ -276,7 +279,7 @@ class DecoderModel:
         for k in range(n_steps):
             out.append(nxt)
             pos = torch.full((Bn,), T + k, dtype=torch.int32, device=self.device)
-            st = self.decode_step(cache, nxt, pos, cfg)
+            st = self.decode_step(cache, nxt, pos, cfg, pos_max=T + k)
             steps.append(st)
             nxt = self.greedy(st.logits)
         gen = torch.stack(out, dim=1) if out else torch.zeros((Bn, 0), dtype=torch.int32)
