@@ -420,13 +420,15 @@ constexpr int kSplitThreads = 256;
 
 // Workgroup (k, c, h): keys [c*CK, min(L, (c+1)*CK)) of query entry k, head
 // h, CK = ceil(L / nc).  A key's row of head h (HD bf16 = HD*2 bytes) is read
-// by LPK = HD/8 lanes, 16 bytes each, so every load instruction covers whole
-// rows; the wave's GPW lane groups take different keys, four per group in
+// by LPK = HD/8 lanes, 16 bytes each (non-temporal: nothing reads it again
+// while cached), so every load instruction covers whole rows; the wave's GPW lane groups take different keys, four per group in
 // flight.  Scores are q.k over the group (xor shuffles), and each group keeps
 // an online softmax in the exp2 domain (q is pre-scaled by scale*log2(e)).
 // The workgroup's groups are merged in LDS; with one chunk the output is
 // written directly, else (max, sum, unnormalised o) go to the workspace for
 // attend_combine_kernel.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 template <int HD>
 __global__ __launch_bounds__(kSplitThreads) void attend_split_kernel(
     int H, float scale_log2, int causal, int nc, const bf16* __restrict__ q,
@@ -476,8 +478,11 @@ __global__ __launch_bounds__(kSplitThreads) void attend_split_kernel(
       const int t = tb + u * G;
       ok[u] = t < t1;
       const int tt = ok[u] ? t : t0;            // clamped: loaded, never used
-      kv[u] = *reinterpret_cast<const uint4*>(kb + (int64_t)tt * rs);
-      vv[u] = *reinterpret_cast<const uint4*>(vb + (int64_t)tt * rs);
+      // streaming: a key row is read once per (query, head)
+      const u32x4_t kn = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(kb + (int64_t)tt * rs));
+      const u32x4_t vn = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(vb + (int64_t)tt * rs));
+      kv[u] = make_uint4(kn.x, kn.y, kn.z, kn.w);
+      vv[u] = make_uint4(vn.x, vn.y, vn.z, vn.w);
     }
     float sc[4];
 #pragma unroll
