@@ -564,10 +564,13 @@ __global__ __launch_bounds__(HD) void attend_combine_kernel(int H, int nc,
   if (k >= min(*n_active, max_active)) return;
   const int64_t pq = (int64_t)k * H + h;
   const float* pp = part + pq * nc * (HD + 2);
+  // the chunks' loads are independent: unrolled so that they are in flight together
   float M = -INFINITY;
+#pragma unroll 8
   for (int c = 0; c < nc; ++c) M = fmaxf(M, pp[c * (HD + 2)]);
   float Ls = 0.0f, O = 0.0f;
   if (M != -INFINITY) {
+#pragma unroll 8
     for (int c = 0; c < nc; ++c) {
       const float* pc = pp + c * (HD + 2);
       const float w = exp2f(pc[0] - M);
