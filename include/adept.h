@@ -464,6 +464,9 @@ adept_status adept_classify_head(int n_seq, int seq_len, int d_model, int n_clas
  * Names are sorted; index 0..adept_timing_count()-1.  No device memory is
  * used.  Disabled by default; reset clears the totals. */
 adept_status adept_timing_enable(int on);
+/* Restricts the bracketing to launches whose kernel name starts with `prefix`
+ * (host string, copied); NULL or "" times every launch again (the default). */
+adept_status adept_timing_select(const char* prefix);
 void adept_timing_reset(void);
 int adept_timing_count(void);
 adept_status adept_timing_get(int idx, char* name, int name_len, int64_t* launches,

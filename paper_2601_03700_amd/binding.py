@@ -109,6 +109,7 @@ _SIGS = {
                                    _vp, _vp, _vp, _vp, _vp]),
     "adept_classify_head": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "adept_timing_enable": (_i32, [_i32]),
+    "adept_timing_select": (_i32, [ctypes.c_char_p]),
     "adept_timing_reset": (None, []),
     "adept_timing_count": (_i32, []),
     "adept_timing_get": (_i32, [_i32, ctypes.c_char_p, _i32, ctypes.POINTER(_i64),
@@ -304,6 +305,12 @@ def token_init(n_tok, n_layers, d_model, active, n_active, exit_layer, inertia=N
 
 def timing_enable(on=True):
     _check(lib().adept_timing_enable(1 if on else 0), "adept_timing_enable")
+
+
+def timing_select(prefix=None):
+    """Time only the launches whose kernel name starts with `prefix` (None: all)."""
+    _check(lib().adept_timing_select(prefix.encode() if prefix else None),
+           "adept_timing_select")
 
 
 def timing_reset():

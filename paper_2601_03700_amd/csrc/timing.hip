@@ -3,9 +3,14 @@
 // When enabled, every kernel launch of the library is bracketed by two
 // events recorded on the launch stream; adept_timing_get() waits for the
 // pending events and accumulates elapsed time and launch count per kernel
-// name.  Events come from a pool and are reused; nothing is allocated on the
-// device.  Disabled (the default), a launch costs one relaxed atomic load.
+// name.  A name prefix can restrict the bracketing to one kernel family, so
+// that a measurement run adds events (and their gaps) only around the kernel
+// it measures.  Events come from a pool and are reused; nothing is allocated
+// on the device.  Disabled (the default), a launch costs one relaxed atomic
+// load.
+#include <algorithm>
 #include <atomic>
+#include <cstring>
 #include <map>
 #include <mutex>
 #include <vector>
@@ -29,6 +34,7 @@ std::mutex g_mu;
 std::vector<hipEvent_t> g_pool;
 std::vector<Pending> g_pending;
 std::map<std::string, Total> g_totals;
+std::string g_prefix;   // empty: every launch is timed
 
 hipEvent_t take_event() {
   if (!g_pool.empty()) {
@@ -41,9 +47,11 @@ hipEvent_t take_event() {
   return e;
 }
 
-// Resolve all pending pairs (blocks until they completed).
-void drain() {
-  for (auto& p : g_pending) {
+// Resolve the oldest `n` pending pairs (blocks until they completed).
+void drain(size_t n) {
+  n = std::min(n, g_pending.size());
+  for (size_t i = 0; i < n; ++i) {
+    const Pending& p = g_pending[i];
     float ms = 0.0f;
     if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
       Total& t = g_totals[p.name];
@@ -53,14 +61,17 @@ void drain() {
     g_pool.push_back(p.a);
     g_pool.push_back(p.b);
   }
-  g_pending.clear();
+  g_pending.erase(g_pending.begin(), g_pending.begin() + n);
 }
+
+void drain() { drain(g_pending.size()); }
 
 }  // namespace
 
 TimedLaunch::TimedLaunch(const char* name, hipStream_t s) : name_(name), s_(s) {
   if (!g_on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_prefix.empty() && strncmp(name, g_prefix.c_str(), g_prefix.size()) != 0) return;
   a_ = take_event();
   b_ = take_event();
   if (a_ && b_) hipEventRecord((hipEvent_t)a_, s_);
@@ -71,7 +82,9 @@ TimedLaunch::~TimedLaunch() {
   std::lock_guard<std::mutex> lk(g_mu);
   if (hipEventRecord((hipEvent_t)b_, s_) == hipSuccess) {
     g_pending.push_back({name_, (hipEvent_t)a_, (hipEvent_t)b_});
-    if (g_pending.size() > 8192) drain();
+    // the oldest half finished long ago: resolving it does not wait for
+    // the queue to run dry
+    if (g_pending.size() > 8192) drain(4096);
   } else {
     g_pool.push_back((hipEvent_t)a_);
     g_pool.push_back((hipEvent_t)b_);
@@ -85,6 +98,12 @@ using namespace adept;
 extern "C" adept_status adept_timing_enable(int on) {
   std::lock_guard<std::mutex> lk(g_mu);
   g_on.store(on ? 1 : 0);
+  return ADEPT_OK;
+}
+
+extern "C" adept_status adept_timing_select(const char* prefix) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_prefix = prefix ? prefix : "";
   return ADEPT_OK;
 }
 
