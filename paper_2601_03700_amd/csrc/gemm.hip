@@ -1010,29 +1010,50 @@ adept_status launch_bf16(const GP& p, hipStream_t s, const char* name) {
 // ---------------------------------------------------------------------------
 // Skinny path (at most 64 rows: decode).  The weights are streamed from HBM
 // once; M is too small for the 256x256 tile to give the chip enough
-// workgroups.  A workgroup owns 32 columns of the partial space (N columns,
-// or the F gate columns followed by the F up columns for SWIGLU) and one
-// slice of K; its four waves take contiguous quarters of the slice, keep
-// eight 16-wide k steps of loads in flight (operands straight from global
-// memory in the MFMA layout: 32 rows x 32 bytes per instruction, whole
-// 128-byte lines over four consecutive steps), and add up in LDS.  The
-// slices' partial tiles go to a workspace; skinny_epilogue_kernel sums them
-// in slice order (deterministic) and applies the same epilogues as the tiled
-// path.
+// workgroups.  The work is a flattened space of units: a unit is one
+// 64-column tile of the partial space (N columns, or the
+// F gate columns followed by the F up columns for SWIGLU) times one 64-deep
+// k step.  The units are cut into G equal contiguous ranges, one per
+// workgroup (stream-K), so that every workgroup streams the same number of
+// weight bytes and the grid is one even wave of about two workgroups per CU;
+// a range is never longer than a tile's k extent, so it covers at most two
+// tiles (two segments).  Each (workgroup, segment) writes one 64x64 fp32
+// partial tile; skinny_epilogue_kernel sums a tile's partials in workgroup
+// order (deterministic) and applies the same epilogues as the tiled path.
 // ---------------------------------------------------------------------------
 constexpr int kSkinnyM = 64;      // rows of a skinny pass (decode: one per sequence)
-constexpr int kSkinnyBN = 64;     // output columns per workgroup
+constexpr int kSkinnyBN = 64;     // output columns per tile
 constexpr int kSkStages = 4;      // LDS ring depth
 constexpr int kSkStage = 2 * 64 * 128;   // A and B, 64 rows x 64 k each: 16 KiB
+constexpr int kSkPart = kSkinnyM * kSkinnyBN;   // floats of one partial tile
+constexpr int kSkGroups = 512;    // target grid: two workgroups per CU
 
-// Skinny GEMM (M <= 64): C[m][n] over a K slice into fp32 partials
-// part[slice][m][n].  The pass streams B (the weights) once, so it is
-// HBM-bound: A and B reach LDS by direct loads of whole 128-byte rows
-// (eight lanes per row, one cache line), four stages deep, and the four
-// waves each take a 32x32 block of the 64x64 output tile.  Every iteration
-// issues the same loads (the stage index clamped past the slice's last
-// stage), so the vmcnt accounting is uniform.
-__global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int Nt, int nb, int k_slice,
+struct SkSplit {
+  int G;        // workgroups
+  int U;        // units per workgroup (the last one may hold fewer)
+  int KT;       // k steps per tile
+  int64_t total;
+};
+
+SkSplit skinny_split(int Nt, int K) {
+  SkSplit sp;
+  sp.KT = K / BK;
+  sp.total = (int64_t)(Nt / kSkinnyBN) * sp.KT;
+  const int64_t g = std::max<int64_t>(1, std::min<int64_t>(kSkGroups, sp.total));
+  // at least four k steps (32 KiB of weights) against each 16 KiB partial tile
+  sp.U = (int)std::min<int64_t>(std::max<int64_t>((sp.total + g - 1) / g, 4), sp.KT);
+  sp.G = (int)((sp.total + sp.U - 1) / sp.U);
+  return sp;
+}
+
+// Skinny GEMM (M <= 64): workgroup w multiplies the units [w*U, w*U + U) and
+// writes the partial tile of each segment to part[w][segment][m][c].  The
+// pass streams B (the weights) once, so it is HBM-bound: A and B reach LDS by
+// direct loads of whole 128-byte rows (eight lanes per row, one cache line),
+// four stages deep, and the four waves each take a 32x32 block of the 64x64
+// tile.  Every iteration issues the same loads (the stage index clamped past
+// the segment's last stage), so the vmcnt accounting is uniform.
+__global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int nb, SkSplit sp,
                                                              float* __restrict__ part) {
   __shared__ __attribute__((aligned(1024))) char sm[kSkStages * kSkStage];
   const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
@@ -1040,71 +1061,85 @@ __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int Nt, int n
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int n0 = blockIdx.x * kSkinnyBN, slice = blockIdx.y;
-  const int k0 = slice * k_slice;
-  const int KT = (min(p.K, k0 + k_slice) - k0) / BK;
-  // direct-load instruction j (0..3) of wave w: operand (A for waves 0-1, B
-  // for 2-3), rows 8q .. 8q+7 with q = (4w + j) mod 8; lane l -> row
-  // 8q + l/8, stored position l%8, logical chunk (l%8) ^ ((row >> 1) & 7)
-  const bf16* src[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int q = (4 * wave + j) & 7;
-    const int r = 8 * q + (lane >> 3);
-    const int ch = (lane & 7) ^ ((r >> 1) & 7);
-    if (wave < 2) {
-      const int m = min(r, M - 1);   // clamped: loaded, never stored
-      const int row = p.a_rows ? p.a_rows[m] : m;
-      src[j] = p.A + (int64_t)row * p.lda + ch * 8 + k0;
-    } else {
-      const int n = n0 + r;
-      src[j] = (n >= nb ? p.B2 + (int64_t)(n - nb) * p.ldb : p.B + (int64_t)n * p.ldb) + ch * 8 +
-               k0;
-    }
-  }
-  auto issue = [&](int kt) {
-    const int k = min(kt, KT - 1) * BK;
-    char* slot = sm + (kt % kSkStages) * kSkStage + (wave >> 1) * 8192;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) dma16(src[j] + k, slot + ((4 * wave + j) & 7) * 1024);
-  };
-  f32x16_t acc;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+  const int64_t u_end = min(sp.total, (int64_t)(blockIdx.x + 1) * sp.U);
+  int64_t u = (int64_t)blockIdx.x * sp.U;
   const int rA = wm * 32 + (lane & 31), rB = wn * 32 + (lane & 31);
   const int swz = (lane >> 1) & 7;
+  for (int seg = 0; seg < 2 && u < u_end; ++seg) {
+    const int tile = (int)(u / sp.KT), kb = (int)(u - (int64_t)tile * sp.KT);
+    const int KT = (int)min<int64_t>(sp.KT - kb, u_end - u);
+    u += KT;
+    const int n0 = tile * kSkinnyBN, k0 = kb * BK;
+    // direct-load instruction j (0..3) of wave w: operand (A for waves 0-1,
+    // B for 2-3), rows 8q .. 8q+7 with q = (4w + j) mod 8; lane l -> row
+    // 8q + l/8, stored position l%8, logical chunk (l%8) ^ ((row >> 1) & 7)
+    const bf16* src[4];
 #pragma unroll
-  for (int s = 0; s < kSkStages - 1; ++s) issue(s);
-  for (int kt = 0; kt < KT; ++kt) {
-    // stage kt has landed once at most the later stages' loads are in flight
-    wait_vm<4 * (kSkStages - 2)>();
-    stage_barrier();   // publishes stage kt; every wave is done with stage kt-1
-    issue(kt + kSkStages - 1);   // into stage kt-1's slot
-    const char* st = sm + (kt % kSkStages) * kSkStage;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = (2 * ks + (lane >> 5)) ^ swz;
-      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(st + (rA * 8 + ch) * 16);
-      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(st + 8192 + (rB * 8 + ch) * 16);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+    for (int j = 0; j < 4; ++j) {
+      const int q = (4 * wave + j) & 7;
+      const int r = 8 * q + (lane >> 3);
+      const int ch = (lane & 7) ^ ((r >> 1) & 7);
+      if (wave < 2) {
+        const int m = min(r, M - 1);   // clamped: loaded, never stored
+        const int row = p.a_rows ? p.a_rows[m] : m;
+        src[j] = p.A + (int64_t)row * p.lda + ch * 8 + k0;
+      } else {
+        const int n = n0 + r;
+        src[j] = (n >= nb ? p.B2 + (int64_t)(n - nb) * p.ldb : p.B + (int64_t)n * p.ldb) +
+                 ch * 8 + k0;
+      }
     }
-  }
-  wait_dma();   // the clamped loads land before the workgroup's LDS is released
-  // C layout: value v is row 8*(v/4) + 4*(lane/32) + v%4 of the block, column lane%32
+    auto issue = [&](int kt) {
+      const int k = min(kt, KT - 1) * BK;
+      char* slot = sm + (kt % kSkStages) * kSkStage + (wave >> 1) * 8192;
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int r = wm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-    part[((int64_t)slice * kSkinnyM + r) * Nt + n0 + wn * 32 + (lane & 31)] = acc[v];
+      for (int j = 0; j < 4; ++j) dma16(src[j] + k, slot + ((4 * wave + j) & 7) * 1024);
+    };
+    f32x16_t acc;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+#pragma unroll
+    for (int s = 0; s < kSkStages - 1; ++s) issue(s);
+    for (int kt = 0; kt < KT; ++kt) {
+      // stage kt has landed once at most the later stages' loads are in flight
+      wait_vm<4 * (kSkStages - 2)>();
+      stage_barrier();   // publishes stage kt; every wave is done with stage kt-1
+      issue(kt + kSkStages - 1);   // into stage kt-1's slot
+      const char* st = sm + (kt % kSkStages) * kSkStage;
+#pragma unroll
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        const int ch = (2 * ks + (lane >> 5)) ^ swz;
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(st + (rA * 8 + ch) * 16);
+        const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(st + 8192 + (rB * 8 + ch) * 16);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+      }
+    }
+    wait_dma();        // the clamped loads land before the ring is reused
+    stage_barrier();   // every wave is done reading the ring
+    // C layout: value v is row 8*(v/4) + 4*(lane/32) + v%4 of the block, column lane%32
+    float* dst = part + ((int64_t)blockIdx.x * 2 + seg) * kSkPart;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int r = wm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+      dst[r * kSkinnyBN + wn * 32 + (lane & 31)] = acc[v];
+    }
   }
 }
 
-// Sum of the S slices for row m, columns c..c+3.
-__device__ __forceinline__ float4 skinny_sum(const float* __restrict__ part, int S, int Nt, int m,
-                                             int c) {
+// Sum of the partials of row m, partial-space columns c..c+3: the
+// workgroups whose ranges meet c's tile, in ascending order; a workgroup
+// whose range starts in that tile holds it as segment 0, one that starts in
+// the tile before as segment 1.
+__device__ __forceinline__ float4 skinny_sum(const float* __restrict__ part, const SkSplit& sp,
+                                             int m, int c) {
+  const int t = c / kSkinnyBN, col = c - t * kSkinnyBN;
+  const int64_t u0 = (int64_t)t * sp.KT;
+  const int w0 = (int)(u0 / sp.U), w1 = (int)((u0 + sp.KT - 1) / sp.U);
   float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int sl = 0; sl < S; ++sl) {
-    const float4 y =
-        *reinterpret_cast<const float4*>(part + ((int64_t)sl * kSkinnyM + m) * Nt + c);
+  for (int w = w0; w <= w1; ++w) {
+    const int seg = (int64_t)w * sp.U >= u0 ? 0 : 1;
+    const float4 y = *reinterpret_cast<const float4*>(part + ((int64_t)w * 2 + seg) * kSkPart +
+                                                      m * kSkinnyBN + col);
     x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
   }
   return x;
@@ -1112,7 +1147,7 @@ __device__ __forceinline__ float4 skinny_sum(const float* __restrict__ part, int
 
 // One thread per (row, 4 output columns).
 template <int EPI>
-__global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int nout, int S,
+__global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int nout, SkSplit sp,
                                                               const float* __restrict__ part) {
   const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
   const int g4 = nout / 4;
@@ -1120,7 +1155,7 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
   const int m = (int)(idx / g4), n = (int)(idx % g4) * 4;
   if (m >= M) return;
   const float sc = p.row_scale ? p.row_scale[m] : 1.0f;
-  const float4 x4 = skinny_sum(part, S, Nt, m, n);
+  const float4 x4 = skinny_sum(part, sp, m, n);
   const float4 bx = bias4(p.bias, n);
   const float x[4] = {x4.x * sc + bx.x, x4.y * sc + bx.y, x4.z * sc + bx.z, x4.w * sc + bx.w};
   bf16x4_t o;
@@ -1145,7 +1180,7 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
     for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e] + bf2f(r[e]));
     *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
   } else if (EPI == EPI_SWIGLU) {
-    const float4 u4 = skinny_sum(part, S, Nt, m, nout + n);
+    const float4 u4 = skinny_sum(part, sp, m, nout + n);
     const float u[4] = {u4.x * sc, u4.y * sc, u4.z * sc, u4.w * sc};
 #pragma unroll
     for (int e = 0; e < 4; ++e) o[e] = f2bf(silu(x[e]) * u[e]);
@@ -1164,7 +1199,7 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
       // rotate-half RoPE: column c pairs with c +- hd/2 of the same head
       const int hd = p.head_dim, half = hd >> 1;
       const int c = cin & (hd - 1);
-      const float4 y4 = skinny_sum(part, S, Nt, m, n ^ half);
+      const float4 y4 = skinny_sum(part, sp, m, n ^ half);
       const float4 by = bias4(p.bias, n ^ half);
       const float y[4] = {y4.x * sc + by.x, y4.y * sc + by.y, y4.z * sc + by.z, y4.w * sc + by.w};
       const int64_t t = (int64_t)p.pos[row] * half + (c & (half - 1));
@@ -1179,31 +1214,19 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int Nt, int 
   }
 }
 
-// K slices of the skinny path: about 512 workgroups in all, slices of a
-// multiple of 64 (four waves x 16).
-// K slices: enough workgroups for two per CU (the pass is bandwidth-bound).
-void skinny_split(int Nt, int K, int* S, int* k_slice) {
-  const int tiles = Nt / kSkinnyBN;
-  int want = std::max(1, std::min(16, (512 + tiles - 1) / tiles));
-  int ks = ((K + want - 1) / want + 63) / 64 * 64;
-  *k_slice = ks;
-  *S = (K + ks - 1) / ks;
-}
-
 template <int EPI>
 adept_status launch_skinny(const GP& p, int Nt, int nout, hipStream_t s, const char* name,
                            float* part) {
-  int S, ks;
-  skinny_split(Nt, p.K, &S, &ks);
+  const SkSplit sp = skinny_split(Nt, p.K);
   {
     TimedLaunch tl(name ? name : "gemm_skinny", s);
-    hipLaunchKernelGGL(gemm_skinny_kernel, dim3(Nt / kSkinnyBN, S), dim3(256), 0, s, p, Nt,
-                       EPI == EPI_SWIGLU ? nout : Nt, ks, part);
+    hipLaunchKernelGGL(gemm_skinny_kernel, dim3(sp.G), dim3(256), 0, s, p,
+                       EPI == EPI_SWIGLU ? nout : Nt, sp, part);
   }
   ADEPT_CHECK_LAUNCH("gemm_skinny");
   const int64_t total = (int64_t)p.M_max * (nout / 4);
   ADEPT_LAUNCH(skinny_epilogue_kernel<EPI>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
-               s, p, Nt, nout, S, part);
+               s, p, nout, sp, part);
   return launch_status("skinny_epilogue");
 }
 
@@ -1230,9 +1253,7 @@ bool aligned_operands(const GemmArgs& g) {
 }  // namespace
 
 size_t skinny_ws_bytes(int Nt, int K) {
-  int S, ks;
-  skinny_split(Nt, K, &S, &ks);
-  return (size_t)S * kSkinnyM * Nt * sizeof(float);
+  return (size_t)skinny_split(Nt, K).G * 2 * kSkPart * sizeof(float);
 }
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
