@@ -221,3 +221,73 @@ def test_small_bf16_decode_forced_schedule():
     kg, vg = cache_host(cache_g, Bn, T + S)
     bf16_close(kg, cache_o.k, "K cache")
     bf16_close(vg, cache_o.v, "V cache")
+
+
+def test_7b_width_decode_forced_schedule():
+    """Decode at the 7B layer width (d_model 4096, 32 x 128 heads, d_ff
+    11008; two layers, small vocabulary): a 64-sequence decode pass takes
+    the skinny GEMMs at their real shapes, whose stream-K ranges straddle
+    column tiles (QKV, gate/up, down).  Seeded exit schedule on both sides;
+    exit layers exact, logits and the cache within the bf16 bound."""
+    say("7B-width decode forced schedule")
+    shape = ai.DecoderShape(n_layers=2, d_model=4096, n_heads=32, head_dim=128, d_ff=11008,
+                            vocab=512)
+    N = shape.n_layers
+    w32 = ai.decoder_weights(shape, seed=21, dtype="bf16")
+    Bn, T = 64, 2
+    ids = ai.token_ids(22, shape.vocab, Bn, T)
+    step = ai.token_ids(23, shape.vocab, 1, Bn)[0]
+    rng = np.random.default_rng(24)
+    force_p = rng.integers(0, N + 1, size=ids.shape)
+    force_s = rng.integers(1, N + 1, size=Bn)
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=64)
+    cfg_g = B.exit_cfg(math.inf, N, "global")
+    res_g, cache_g = model.prefill(ids, cfg_g, s_max=T + 1, force_layer=force_p, logits="last")
+    st_g = model.decode_step(cache_g, torch.from_numpy(step).to("cuda", torch.int32),
+                             torch.full((Bn,), T, dtype=torch.int32, device="cuda"), cfg_g,
+                             force_layer=torch.from_numpy(force_s).to("cuda", torch.int32))
+    torch.cuda.synchronize()
+    say("  GPU done; oracle")
+    w = O.as64(w32)
+    del w32
+    cfg_o = O.ExitConfig(delta=math.inf)
+    res_o, cache_o = O.prefill(w, shape, ids, cfg_o, s_max=T + 1, force_layer=force_p)
+    st_o = O.decode_step(w, shape, cache_o, step, np.full(Bn, T), cfg_o, force_layer=force_s)
+    np.testing.assert_array_equal(res_g.exit_layer.cpu().numpy(), res_o.exit_layer)
+    np.testing.assert_array_equal(st_g.exit_layer.cpu().numpy(), st_o.exit_layer)
+    assert 0 < int(np.sum(st_o.exit_layer < N)) < Bn
+    bf16_close(st_g.logits.cpu().numpy(), st_o.logits, "decode logits")
+    kg, vg = cache_host(cache_g, Bn, T + 1)
+    bf16_close(kg, cache_o.k, "K cache")
+    bf16_close(vg, cache_o.v, "V cache")
+
+
+def test_timing_select_prefix():
+    """adept_timing_select: with a prefix only the matching launches are
+    bracketed by events; with none, every launch is again."""
+    shape = SMALL_BF16
+    w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512)
+    ids = ai.token_ids(14, shape.vocab, 2, 16)
+    cfg = B.exit_cfg(math.inf, shape.n_layers, "global")
+    res, cache = model.prefill(ids, cfg, s_max=20, logits="last")
+    nxt = torch.from_numpy(ids[:, -1].copy()).to("cuda", torch.int32)
+
+    def timed(prefix):
+        B.timing_reset()
+        B.timing_select(prefix)
+        B.timing_enable(True)
+        try:
+            model.decode_step(cache, nxt, torch.full((2,), 16, dtype=torch.int32, device="cuda"),
+                              cfg)
+            torch.cuda.synchronize()
+        finally:
+            B.timing_enable(False)
+            B.timing_select(None)
+        return B.timing_read()
+
+    only = timed("attend_split")
+    assert only and all(k.startswith("attend_split") for k in only), only
+    assert only[next(iter(only))][0] == shape.n_layers
+    every = timed(None)
+    assert set(only) < set(every) and any(k.startswith("gemm_") for k in every), every
