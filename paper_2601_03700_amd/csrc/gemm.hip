@@ -1039,6 +1039,11 @@ SkSplit skinny_split(int Nt, int K) {
   SkSplit sp;
   sp.KT = K / BK;
   sp.total = (int64_t)(Nt / kSkinnyBN) * sp.KT;
+  if (sp.total <= 0) {   // no work (the entry rejects K or N below one tile)
+    sp.G = 0;
+    sp.U = 1;
+    return sp;
+  }
   const int64_t g = std::max<int64_t>(1, std::min<int64_t>(kSkGroups, sp.total));
   // at least four k steps (32 KiB of weights) against each 16 KiB partial tile
   sp.U = (int)std::min<int64_t>(std::max<int64_t>((sp.total + g - 1) / g, 4), sp.KT);
@@ -1262,13 +1267,13 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
     set_error("gemm: bf16 entry called with another dtype");
     return ADEPT_E_INVALID;
   }
-  if (g.K % BK != 0) {
-    set_error("gemm: K=%d not a multiple of %d", g.K, BK);
+  if (g.K <= 0 || g.K % BK != 0) {
+    set_error("gemm: K=%d not a positive multiple of %d", g.K, BK);
     return ADEPT_E_UNSUPPORTED;
   }
   const int ncols = g.epi == EPI_SWIGLU ? 128 : BN;
-  if (g.N % ncols != 0) {
-    set_error("gemm: N=%d not a multiple of %d", g.N, ncols);
+  if (g.N <= 0 || g.N % ncols != 0) {
+    set_error("gemm: N=%d not a positive multiple of %d", g.N, ncols);
     return ADEPT_E_UNSUPPORTED;
   }
   if ((g.epi == EPI_QKV) &&
