@@ -293,24 +293,43 @@ class TokenPassResult:
     inertia: np.ndarray        # [n, D] inertia after the last test (global metric)
 
 
+def layer_q(layer_w, shape, h_in, pos):
+    """Layer i's queries of input states h_in[n, D]: RoPE(RMSNorm_i(h_in) Wq_i^T), [n, H, hd]."""
+    n = h_in.shape[0]
+    u = rms_norm(h_in, layer_w["attn_norm"], shape.rms_eps)
+    return apply_rope((u @ layer_w["wq"].T).reshape(n, shape.n_heads, shape.head_dim), pos,
+                      shape.rope_theta)
+
+
+def layer_out(layer_w, shape, h_in, o):
+    """The rest of a regular layer after attention: output projection and
+    residual, then the SwiGLU FFN on its RMS-normalised input and the second
+    residual.  h_in [n, D] = h_{i-1}, o [n, H, hd] = attention output."""
+    n = h_in.shape[0]
+    h1 = np.asarray(h_in, F64) + np.asarray(o, F64).reshape(n, -1) @ layer_w["wo"].T
+    u2 = rms_norm(h1, layer_w["ffn_norm"], shape.rms_eps)
+    ff = (silu(u2 @ layer_w["w_gate"].T) * (u2 @ layer_w["w_up"].T)) @ layer_w["w_down"].T
+    return h1 + ff
+
+
 def decoder_layer(layer_w, shape, h_in, pos, seq, cache, layer):
     """One regular decoder layer for the active rows (Appendix I, "Process 1").
 
     h_in [n, D] are the rows' states h_{i-1}; their own K/V are written to
     the cache first, then every row attends causally over its sequence."""
-    n = h_in.shape[0]
-    H, hd = shape.n_heads, shape.head_dim
-    u = rms_norm(h_in, layer_w["attn_norm"], shape.rms_eps)
-    q = apply_rope((u @ layer_w["wq"].T).reshape(n, H, hd), pos, shape.rope_theta)
+    q = layer_q(layer_w, shape, h_in, pos)
     k, v = layer_kv(layer_w, h_in, pos, shape)
     slots = seq * cache.s_max + pos
     cache.k[layer - 1][slots] = k
     cache.v[layer - 1][slots] = v
     o = attend(q, cache.k[layer - 1], cache.v[layer - 1], seq * cache.s_max, pos)
-    h1 = h_in + o.reshape(n, H * hd) @ layer_w["wo"].T
-    u2 = rms_norm(h1, layer_w["ffn_norm"], shape.rms_eps)
-    ff = (silu(u2 @ layer_w["w_gate"].T) * (u2 @ layer_w["w_up"].T)) @ layer_w["w_down"].T
-    return h1 + ff
+    return layer_out(layer_w, shape, h_in, o)
+
+
+def lm_logits(weights, shape, h_final):
+    """Final RMSNorm and LM head of final states h_final[n, D] (an exited
+    token's final state is its mapped state, Fig. 1 caption)."""
+    return rms_norm(h_final, weights["final_norm"], shape.rms_eps) @ weights["lm_head"].T
 
 
 def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None, mapper=None):
@@ -377,8 +396,8 @@ def token_pass(weights, shape, h0, pos, seq, cache, cfg, force_layer=None, mappe
                 cache.k[r - 1][slots] = k
                 cache.v[r - 1][slots] = v
         hidden.append(h.copy())
-    logits = rms_norm(h, weights["final_norm"], shape.rms_eps) @ weights["lm_head"].T
-    return TokenPassResult(h, exit_layer, logits, sims, counts, hidden, inertia)
+    return TokenPassResult(h, exit_layer, lm_logits(weights, shape, h), sims, counts, hidden,
+                           inertia)
 
 
 def prefill(weights, shape, ids, cfg, s_max=None, force_layer=None, mapper=None):
@@ -451,6 +470,34 @@ class ClassifyResult:
     active_counts: list
 
 
+def encoder_layer(lw, shape, x, seq):
+    """One post-norm encoder layer over the live (still active) tokens x[m, D]
+    of their sequences seq[m]: bidirectional attention of each token over the
+    live tokens of its own sequence, LayerNorm after each residual, GELU FFN."""
+    x = np.asarray(x, F64)
+    m, H, hd = x.shape[0], shape.n_heads, shape.head_dim
+    scale = 1.0 / math.sqrt(hd)
+    q = (x @ lw["wq"].T + lw["bq"]).reshape(m, H, hd)
+    kk = (x @ lw["wk"].T + lw["bk"]).reshape(m, H, hd)
+    vv = (x @ lw["wv"].T + lw["bv"]).reshape(m, H, hd)
+    o = np.empty((m, H, hd))
+    seq = np.asarray(seq)
+    for b in np.unique(seq):
+        rows = np.nonzero(seq == b)[0]           # live tokens of sequence b
+        s = np.einsum("qhd,khd->hqk", q[rows], kk[rows]) * scale
+        o[rows] = np.einsum("hqk,khd->qhd", softmax_rows(s), vv[rows])
+    h1 = layer_norm(x + o.reshape(m, H * hd) @ lw["wo"].T + lw["bo"],
+                    lw["ln1_g"], lw["ln1_b"], shape.ln_eps)
+    ff = gelu_erf(h1 @ lw["w_in"].T + lw["b_in"]) @ lw["w_out"].T + lw["b_out"]
+    return layer_norm(h1 + ff, lw["ln2_g"], lw["ln2_b"], shape.ln_eps)
+
+
+def classify_logits(weights, cls_states):
+    """The linear head on [CLS] states (Section 4.3: the mapped state feeds the classifier)."""
+    return (np.asarray(cls_states, F64) @ np.asarray(weights["cls_w"], F64).T
+            + np.asarray(weights["cls_b"], F64))
+
+
 def classify(weights, shape, ids, cfg, force_layer=None):
     """Token-level exit in an encoder classifier.
 
@@ -473,27 +520,12 @@ def classify(weights, shape, ids, cfg, force_layer=None):
     active = np.arange(n)
     sims = np.full((N, n), np.nan)
     counts = []
-    scale = 1.0 / math.sqrt(hd)
     for i in range(1, N + 1):
         counts.append(int(active.size))
         lw = weights["layers"][i - 1]
         h_prev = h.copy()
         if active.size:
-            xa = h_prev[active]
-            m = active.size
-            q = (xa @ lw["wq"].T + lw["bq"]).reshape(m, H, hd)
-            kk = (xa @ lw["wk"].T + lw["bk"]).reshape(m, H, hd)
-            vv = (xa @ lw["wv"].T + lw["bv"]).reshape(m, H, hd)
-            o = np.empty((m, H, hd))
-            sa = seq[active]
-            for b in np.unique(sa):
-                rows = np.nonzero(sa == b)[0]           # live tokens of sequence b
-                s = np.einsum("qhd,khd->hqk", q[rows], kk[rows]) * scale
-                o[rows] = np.einsum("hqk,khd->qhd", softmax_rows(s), vv[rows])
-            h1 = layer_norm(xa + o.reshape(m, H * hd) @ lw["wo"].T + lw["bo"],
-                            lw["ln1_g"], lw["ln1_b"], shape.ln_eps)
-            ff = gelu_erf(h1 @ lw["w_in"].T + lw["b_in"]) @ lw["w_out"].T + lw["b_out"]
-            h[active] = layer_norm(h1 + ff, lw["ln2_g"], lw["ln2_b"], shape.ln_eps)
+            h[active] = encoder_layer(lw, shape, h_prev[active], seq[active])
         sim = (similarity(cfg.metric, h[active], inertia[active], h_prev[active])
                if active.size else np.zeros(0))
         sims[i - 1, active] = sim
@@ -508,5 +540,5 @@ def classify(weights, shape, ids, cfg, force_layer=None):
         exit_layer[exited] = i
         live[exited] = False
     cls_rows = np.arange(B) * T
-    logits = h[cls_rows] @ np.asarray(weights["cls_w"], F64).T + np.asarray(weights["cls_b"], F64)
-    return ClassifyResult(logits, exit_layer, exit_layer[cls_rows], h, sims, counts)
+    return ClassifyResult(classify_logits(weights, h[cls_rows]), exit_layer, exit_layer[cls_rows],
+                          h, sims, counts)
