@@ -4,7 +4,8 @@
  *
  * Conventions (apply to every entry point)
  *  - Pointers are DEVICE pointers unless marked (host).  The caller owns all
- *    memory; the library never allocates or frees device memory.  Scratch
+ *    memory; the library never allocates or frees device memory (the one
+ *    fixed scratch array of adept_kv_generate_noalloc is static).  Scratch
  *    space is passed in as `workspace` of at least the size returned by the
  *    matching *_workspace_bytes() query.
  *  - Calls only enqueue work on `stream` (a hipStream_t; NULL = the null
@@ -233,6 +234,31 @@ adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_model, int n_
                                const float* rope_cos, const float* rope_sin, int rope_max_pos,
                                void* k_cache, void* v_cache, int64_t n_slots, void* workspace,
                                size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * adept_kv_generate_noalloc -- adept_kv_generate for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc): same arguments and results, minus the
+ * workspace.  Its scratch (exit-layer plan, work list and counters, sorted
+ * rows, row scales) is a fixed 4 MiB device array inside the library, one
+ * copy per GPU, held until the process ends; the call allocates nothing.
+ * adept_kv_generate_workspace_bytes(n_layers, max_rows) must not exceed
+ * 4 MiB (32 layers: up to about 480K rows), else ADEPT_E_UNSUPPORTED and
+ * nothing is enqueued.  Every call on a GPU uses that GPU's one array and
+ * re-initialises what it reads, so calls that overlap on one GPU (other
+ * streams, other host threads) race: serialise them.  The device current
+ * at the call selects the array; the first call on a device looks up its
+ * address (ADEPT_E_HIP if that fails).
+ * ------------------------------------------------------------------------- */
+adept_status adept_kv_generate_noalloc(adept_dtype dt, int n_layers, int d_model, int n_heads,
+                                       int head_dim, float eps, const void* s_map,
+                                       const int32_t* rows, const int32_t* n_rows, int max_rows,
+                                       const int32_t* exit_layer, const int32_t* cache_slot,
+                                       const int32_t* pos, const void* w_kv,
+                                       int64_t w_kv_layer_stride, const void* attn_gain,
+                                       const float* rope_cos, const float* rope_sin,
+                                       int rope_max_pos, void* k_cache, void* v_cache,
+                                       int64_t n_slots, void* stream);
 
 /* ---------------------------------------------------------------------------
  * adept_attend -- attention of the active tokens over one layer's cache,

@@ -92,6 +92,9 @@ _SIGS = {
     "adept_kv_generate": (_i32, [_i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp, _vp,
                                  _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _vp,
                                  _i64, _vp, _sz, _vp]),
+    "adept_kv_generate_noalloc": (_i32, [_i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp,
+                                         _vp, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i32,
+                                         _vp, _vp, _i64, _vp]),
     "adept_attend_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32]),
     "adept_attend": (_i32, [_i32, _i32, _i32, ctypes.c_float, _i32, _vp, _vp, _vp, _i32, _vp,
                             _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -252,6 +255,19 @@ def kv_generate(n_layers, d_model, n_heads, head_dim, eps, s_map, rows, n_rows, 
                                    rope_cos.shape[0], ptr(k_cache), ptr(v_cache), n_slots,
                                    ptr(workspace), ws_bytes, stream_handle(stream)),
            "adept_kv_generate")
+
+
+def kv_generate_noalloc(n_layers, d_model, n_heads, head_dim, eps, s_map, rows, n_rows, max_rows,
+                        exit_layer, cache_slot, pos, w_kv, w_kv_layer_stride, attn_gain,
+                        rope_cos, rope_sin, k_cache, v_cache, n_slots, stream=None):
+    _check(lib().adept_kv_generate_noalloc(dtype_code(s_map), n_layers, d_model, n_heads,
+                                           head_dim, eps, ptr(s_map), ptr(rows), ptr(n_rows),
+                                           max_rows, ptr(exit_layer), ptr(cache_slot), ptr(pos),
+                                           ptr(w_kv), w_kv_layer_stride, ptr(attn_gain),
+                                           ptr(rope_cos), ptr(rope_sin), rope_cos.shape[0],
+                                           ptr(k_cache), ptr(v_cache), n_slots,
+                                           stream_handle(stream)),
+           "adept_kv_generate_noalloc")
 
 
 def attend_workspace_bytes(max_active, n_seq, n_heads, head_dim, s_max):

@@ -12,6 +12,11 @@
 //
 // f32 (small configurations): one workgroup per (row, layer) pair computes
 // the normalised state in LDS and the 2*H*hd dot products directly.
+//
+// adept_kv_generate_noalloc runs the same kernels with their scratch in a
+// file-scope device array instead of a caller workspace.
+#include <mutex>
+
 #include "common.h"
 
 namespace adept {
@@ -234,4 +239,71 @@ extern "C" adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_mo
   const int max_work = n_layers * ceil_div(max_rows, kTileM);
   return gemm_kv_grouped(g, w.work, w.n_work, w.queue, max_work, w.grp_m, w.srows,
                          w_kv_layer_stride, layer_stride, s);
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free variant: the plan / work-list / row-scale scratch lives in
+// a file-scope device array (one copy per GPU, kept until the process ends).
+// Host code never passes the array's name to a kernel: its device address is
+// looked up once per device with hipGetSymbolAddress and kept per device.
+// ---------------------------------------------------------------------------
+namespace adept {
+namespace {
+
+constexpr size_t kNoallocScratchBytes = (size_t)4 << 20;
+__device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch array's device address on the current device (looked up on
+// the first call made with that device current); nullptr with the error set.
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    set_error("kv_generate_noalloc: no usable current device (%d)", dev);
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      set_error("kv_generate_noalloc: hipGetSymbolAddress failed on device %d: %s", dev,
+                hipGetErrorString(e));
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+}  // namespace adept
+
+extern "C" adept_status adept_kv_generate_noalloc(
+    adept_dtype dt, int n_layers, int d_model, int n_heads, int head_dim, float eps,
+    const void* s_map, const int32_t* rows, const int32_t* n_rows, int max_rows,
+    const int32_t* exit_layer, const int32_t* cache_slot, const int32_t* pos, const void* w_kv,
+    int64_t w_kv_layer_stride, const void* attn_gain, const float* rope_cos,
+    const float* rope_sin, int rope_max_pos, void* k_cache, void* v_cache, int64_t n_slots,
+    void* stream) {
+  ADEPT_REQUIRE(n_layers >= 1 && n_layers <= kMaxLayers && max_rows >= 0 &&
+                    max_rows < (1 << 24),
+                "kv_generate_noalloc: bad sizes");
+  size_t need = 0;
+  carve(nullptr, n_layers, max_rows, &need);
+  if (need > kNoallocScratchBytes) {
+    set_error("kv_generate_noalloc: %d layers x %d rows need %zu bytes of scratch, above the "
+              "fixed %zu; use adept_kv_generate with a workspace",
+              n_layers, max_rows, need, kNoallocScratchBytes);
+    return ADEPT_E_UNSUPPORTED;
+  }
+  void* ws = scratch_on_current_device();
+  if (!ws) return ADEPT_E_HIP;
+  return adept_kv_generate(dt, n_layers, d_model, n_heads, head_dim, eps, s_map, rows, n_rows,
+                           max_rows, exit_layer, cache_slot, pos, w_kv, w_kv_layer_stride,
+                           attn_gain, rope_cos, rope_sin, rope_max_pos, k_cache, v_cache, n_slots,
+                           ws, kNoallocScratchBytes, stream);
 }
