@@ -474,20 +474,50 @@ def encoder_layer(lw, shape, x, seq):
     """One post-norm encoder layer over the live (still active) tokens x[m, D]
     of their sequences seq[m]: bidirectional attention of each token over the
     live tokens of its own sequence, LayerNorm after each residual, GELU FFN."""
+    return encoder_ffn_block(lw, shape, encoder_attention_block(lw, shape, x, seq))
+
+
+def encoder_qkv(lw, shape, x):
+    """Queries, keys and values (with biases) of encoder states x[m, D], [m, H, hd] each."""
     x = np.asarray(x, F64)
     m, H, hd = x.shape[0], shape.n_heads, shape.head_dim
-    scale = 1.0 / math.sqrt(hd)
-    q = (x @ lw["wq"].T + lw["bq"]).reshape(m, H, hd)
-    kk = (x @ lw["wk"].T + lw["bk"]).reshape(m, H, hd)
-    vv = (x @ lw["wv"].T + lw["bv"]).reshape(m, H, hd)
-    o = np.empty((m, H, hd))
+    return tuple((x @ lw[w].T + lw[b]).reshape(m, H, hd)
+                 for w, b in (("wq", "bq"), ("wk", "bk"), ("wv", "bv")))
+
+
+def encoder_attend(q, kk, vv, seq):
+    """Bidirectional attention of each live token over the live tokens of its
+    own sequence (rows with the same seq), per head."""
+    q, kk, vv = (np.asarray(t, F64) for t in (q, kk, vv))
+    scale = 1.0 / math.sqrt(q.shape[-1])
+    o = np.empty(q.shape)
     seq = np.asarray(seq)
     for b in np.unique(seq):
         rows = np.nonzero(seq == b)[0]           # live tokens of sequence b
         s = np.einsum("qhd,khd->hqk", q[rows], kk[rows]) * scale
         o[rows] = np.einsum("hqk,khd->qhd", softmax_rows(s), vv[rows])
-    h1 = layer_norm(x + o.reshape(m, H * hd) @ lw["wo"].T + lw["bo"],
-                    lw["ln1_g"], lw["ln1_b"], shape.ln_eps)
+    return o
+
+
+def encoder_attention_out(lw, shape, x, o):
+    """LayerNorm_1(x + o Wo^T + bo): the attention sub-layer's output from its
+    input x[m, D] and the attention output o[m, H, hd]."""
+    x = np.asarray(x, F64)
+    return layer_norm(x + np.asarray(o, F64).reshape(x.shape[0], -1) @ lw["wo"].T + lw["bo"],
+                      lw["ln1_g"], lw["ln1_b"], shape.ln_eps)
+
+
+def encoder_attention_block(lw, shape, x, seq):
+    """The attention sub-layer of a post-norm encoder layer:
+    LayerNorm_1(x + Attention(x) Wo^T + bo) for the live tokens x[m, D]."""
+    q, kk, vv = encoder_qkv(lw, shape, x)
+    return encoder_attention_out(lw, shape, x, encoder_attend(q, kk, vv, seq))
+
+
+def encoder_ffn_block(lw, shape, h1):
+    """The FFN sub-layer of a post-norm encoder layer:
+    LayerNorm_2(h1 + GELU(h1 W_in^T + b_in) W_out^T + b_out)."""
+    h1 = np.asarray(h1, F64)
     ff = gelu_erf(h1 @ lw["w_in"].T + lw["b_in"]) @ lw["w_out"].T + lw["b_out"]
     return layer_norm(h1 + ff, lw["ln2_g"], lw["ln2_b"], shape.ln_eps)
 
