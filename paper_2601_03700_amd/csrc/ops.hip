@@ -289,14 +289,15 @@ namespace {
 __global__ void token_init_kernel(int n_tok, int n_layers, int d, int32_t* active, int32_t* n_active,
                                   int32_t* exit_layer, float* inertia) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx < n_tok) {
-    active[idx] = (int32_t)idx;
-    exit_layer[idx] = n_layers;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  // grid-stride: the grid is capped, the row count is not
+  for (int64_t j = idx; j < n_tok; j += stride) {
+    active[j] = (int32_t)j;
+    exit_layer[j] = n_layers;
   }
   if (idx == 0) *n_active = n_tok;
   if (inertia) {
-    for (int64_t e = idx; e < (int64_t)n_tok * d; e += (int64_t)gridDim.x * blockDim.x)
-      inertia[e] = 0.0f;
+    for (int64_t e = idx; e < (int64_t)n_tok * d; e += stride) inertia[e] = 0.0f;
   }
 }
 }  // namespace

@@ -335,9 +335,10 @@ class EncoderModel:
         self.eln_g, self.eln_b = up(weights["embed_ln_g"]), up(weights["embed_ln_b"])
         self.cls_w, self.cls_b = up(weights["cls_w"]), up(weights["cls_b"])
 
-    def classify(self, ids, cfg, force_layer=None, state=None):
+    def classify(self, ids, cfg, force_layer=None, state=None, on_layer=None):
         """ids [B, T] (numpy or tensor); cfg from binding.exit_cfg.  A state
-        dict from an earlier call of the same shape is reused (no allocation)."""
+        dict from an earlier call of the same shape is reused (no allocation).
+        on_layer(i, state) is called after each layer step (read-back hook)."""
         s, dev = self.shape, self.device
         ids = torch.as_tensor(np.asarray(ids) if not isinstance(ids, torch.Tensor) else ids)
         Bn, T = ids.shape
@@ -401,6 +402,8 @@ class EncoderModel:
         st["key_live"].fill_(1)
         for i in range(1, N + 1):
             B.encoder_layer_step(a, i)
+            if on_layer is not None:
+                on_layer(i, st)
         B.classify_head(Bn, T, D, s.n_classes, st["h"][0], st["h"][1], st["exit_layer"],
                         self.cls_w, self.cls_b, st["logits"])
         return ClassifyOutput(st["logits"], st["exit_layer"], st["exit_layer"][::T], st)

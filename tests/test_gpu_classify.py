@@ -1,9 +1,11 @@
 """Classification mode (Section 4.3) on the GPU against the oracle: a
 BERT-style post-norm encoder with token-level exit, where exited tokens
 leave the key set and each sequence's [CLS] row at its exit feeds the linear
-head.  bf16 throughout: a seeded exit schedule imposed on both sides gives
-exact exit layers and logits within the bf16 bound; policy-driven decisions
-are compared where the oracle's margin exceeds the bf16 error."""
+head.  bf16 throughout, teacher-forced per layer (tests/layer_check.py):
+each layer's GPU input goes to the oracle's encoder layer, h within
+max(2e-2, one bf16 ulp) per element, decisions / lists / exit layers
+bit-exact on identical inputs; free-running decisions end to end are compared
+where the oracle's margin exceeds the bf16 error."""
 import math
 import sys
 
@@ -15,6 +17,7 @@ import adept_inputs as ai
 from oracle import adept_oracle as O
 from paper_2601_03700_amd import binding as B
 from paper_2601_03700_amd.model import EncoderModel
+from tests import layer_check as LC
 
 pytestmark = pytest.mark.gpu
 
@@ -27,21 +30,26 @@ def say(*a):
     sys.stdout.flush()
 
 
-def bf16_close(a, b, what):
-    """2e-2 on unit-scale values, scaled by the reference's largest magnitude
-    above 1, plus an RMS bound of 1e-2 relative (each layer stores its
-    activations and residual stream in bf16)."""
-    m = max(1.0, float(np.max(np.abs(b))))
-    err = np.abs(a - b)
-    rms = float(np.sqrt(np.mean(err ** 2)) / max(np.sqrt(np.mean(b ** 2)), 1e-30))
-    say(f"  {what}: max err {err.max():.4g} (bound {2e-2 * m:.4g}), rms rel {rms:.3g}")
-    assert err.max() <= 2e-2 * m and rms <= 1e-2, what
-
-
 @pytest.fixture(scope="module")
 def enc():
     w32 = ai.encoder_weights(ENC, seed=21, dtype="bf16", std=0.05)
     return w32, O.as64(w32), EncoderModel(ENC, w32)
+
+
+def _tf_classify(model, w, ids, delta, metric="global", force=None):
+    """Classification with the teacher-forced per-layer check: each layer's
+    GPU input (the live rows) goes to the oracle's encoder layer; h within
+    max(2e-2, one bf16 ulp) per element, exit flags / lists / exit layers
+    bit-exact on identical inputs, logits of the GPU's [CLS] states within
+    2e-2."""
+    rep = LC.Report(say)
+    chk = LC.EncoderLayerCheck(w, ENC, O.ExitConfig(delta=delta, metric=metric),
+                               force_layer=force, report=rep)
+    out = model.classify(ids, B.exit_cfg(delta, ENC.n_layers, metric), force_layer=force,
+                         on_layer=chk)
+    chk.finish(out, ids.shape[1])
+    rep.summary()
+    return out, chk
 
 
 @pytest.mark.parametrize("Bn,T", [(3, 100), (2, 24)])   # tiled GEMMs; skinny GEMMs (48 rows)
@@ -51,28 +59,30 @@ def test_classify_forced_schedule(enc, Bn, T):
     ids = ai.token_ids(30 + T, ENC.vocab, Bn, T)
     force = np.random.default_rng(T).integers(0, ENC.n_layers + 1, size=ids.shape)
     force[0, 0] = 2                       # a [CLS] row that exits early
-    out = model.classify(ids, B.exit_cfg(math.inf, ENC.n_layers, "global"), force_layer=force)
-    torch.cuda.synchronize()
-    ref = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf), force_layer=force)
-    np.testing.assert_array_equal(out.exit_layer.cpu().numpy(), ref.exit_layer)
-    np.testing.assert_array_equal(out.cls_exit_layer.cpu().numpy(), ref.cls_exit_layer)
-    bf16_close(out.logits.cpu().numpy(), ref.logits, "logits")
-    # the final states the head reads (each row's state at its exit)
-    h = [t.float().cpu().numpy().astype(np.float64) for t in out.state["h"]]
-    el = out.exit_layer.cpu().numpy()
-    hf = np.where((el & 1)[:, None] == 1, h[1], h[0])
-    bf16_close(hf, ref.h_final, "final states")
+    out, chk = _tf_classify(model, w, ids, math.inf, force=force)
+    assert int(out.cls_exit_layer[0]) == 2
 
 
 def test_classify_full_depth(enc):
     w32, w, model = enc
     say("classify full depth")
     ids = ai.token_ids(40, ENC.vocab, 2, 128)
-    out = model.classify(ids, B.exit_cfg(math.inf, ENC.n_layers, "global"))
-    torch.cuda.synchronize()
-    ref = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf))
+    out, _ = _tf_classify(model, w, ids, math.inf)
     assert (out.exit_layer.cpu().numpy() == ENC.n_layers).all()
-    bf16_close(out.logits.cpu().numpy(), ref.logits, "logits")
+
+
+def test_classify_policy_teacher_forced(enc):
+    """The policy at a threshold that fires (global metric), every layer on
+    the GPU's own inputs."""
+    w32, w, model = enc
+    say("classify policy teacher-forced")
+    ids = ai.token_ids(42, ENC.vocab, 3, 80)
+    full = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf))
+    fin = np.sort(full.sims[:ENC.n_layers - 1][np.isfinite(full.sims[:ENC.n_layers - 1])])
+    q = np.searchsorted(fin, np.quantile(fin, 0.5))
+    delta = float(0.5 * (fin[q - 1] + fin[q]))
+    out, chk = _tf_classify(model, w, ids, delta)
+    assert 0 < np.sum(chk.exit_layer < ENC.n_layers) < chk.exit_layer.size
 
 
 @pytest.mark.parametrize("metric", ["global", "both"])

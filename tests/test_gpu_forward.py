@@ -2,10 +2,12 @@
 GPU against the oracle, through adept_layer_step and the support calls.
 
 fp32 (the tiny 4-layer configuration): free-running; exit layers must match
-exactly and logits / caches within 1e-5 relative (max-norm).  bf16: the
-same exit schedule is imposed on both sides (force_layer, a seeded input),
-and the outputs compared within bf16 tolerances; free-running bf16 decisions
-are compared where the oracle's margin |sim - delta| exceeds the bf16 error.
+exactly and logits / caches within 1e-5 relative (max-norm).  bf16: teacher-
+forced per layer (tests/layer_check.py): each layer's GPU input goes to the
+oracle's layer and its outputs are compared per element within max(2e-2,
+one bf16 ulp); exit flags, lists and exit layers bit-exactly on identical
+inputs; free-running bf16 decisions end to end are compared where the
+oracle's margin |sim - delta| exceeds the bf16 error.
 """
 import math
 import sys
@@ -18,6 +20,7 @@ import adept_inputs as ai
 from oracle import adept_oracle as O
 from paper_2601_03700_amd import binding as B
 from paper_2601_03700_amd.model import DecoderModel
+from tests import layer_check as LC
 
 pytestmark = pytest.mark.gpu
 
@@ -130,43 +133,95 @@ SMALL_BF16 = ai.DecoderShape(n_layers=6, d_model=512, n_heads=4, head_dim=128, d
                              vocab=512)
 
 
-def bf16_close(a, b, what):
-    """bf16 end-to-end bound: 2e-2 on unit-scale values, scaled by the largest
-    magnitude M of the reference when M > 1 (the bf16 spacing grows with
-    magnitude), plus an RMS bound of 1e-2 relative against systematic error
-    (each bf16 rounding is up to 2^-9 relative, and a 6-layer pass stores the
-    residual stream and five activations per layer in bf16)."""
-    m = max(1.0, float(np.max(np.abs(b))))
-    err = np.abs(a - b)
-    rms = float(np.sqrt(np.mean(err ** 2)) / max(np.sqrt(np.mean(b ** 2)), 1e-30))
-    say(f"  {what}: max err {err.max():.4g} (bound {2e-2 * m:.4g}), rms rel {rms:.3g}")
-    assert err.max() <= 2e-2 * m and rms <= 1e-2, what
+def _tf_prefill(model, w, shape, ids, cfg_o, cfg_g, force=None, s_max=None, logits="all",
+                n_sample=256, rep=None):
+    """Prefill on the GPU with the teacher-forced per-layer check, then the
+    generated K/V and the logits of the GPU's final states."""
+    chk = LC.DecoderLayerCheck(w, shape, None, cfg_o, model.dtype, force_layer=force,
+                               n_sample=n_sample, report=rep)
+    cache = model.new_cache(ids.shape[0], ids.shape[1] if s_max is None else s_max)
+    chk.cache = cache
+    res, cache = model.prefill(ids, cfg_g, s_max=s_max, force_layer=force, logits=logits,
+                               cache=cache, on_layer=chk)
+    chk.finish(res.state, res.logits, res.rows)
+    return res, cache, chk
 
 
-def test_small_bf16_prefill_forced_schedule():
-    """bf16 prefill with a seeded exit schedule imposed on both sides: exit
-    layers exact, logits and the K/V cache within the bf16 bound."""
-    say("small bf16 forced schedule")
+def _tf_decode(model, w, shape, cache, ids, pos, cfg_o, cfg_g, force=None, rep=None):
+    chk = LC.DecoderLayerCheck(w, shape, cache, cfg_o, model.dtype, force_layer=force,
+                               report=rep)
+    dev = model.device
+    res = model.decode_step(cache, torch.from_numpy(np.asarray(ids)).to(dev, torch.int32),
+                            torch.from_numpy(np.asarray(pos)).to(dev, torch.int32), cfg_g,
+                            force_layer=None if force is None else
+                            torch.from_numpy(np.asarray(force)).to(dev, torch.int32),
+                            on_layer=chk)
+    chk.finish(res.state, res.logits, res.rows)
+    return res, chk
+
+
+def _half_forced(seed, shape_ids, n_layers):
+    """Teacher-forced exit layers for about half of the rows (1..N, N = never),
+    the policy's own decision (0) for the others."""
+    rng = np.random.default_rng(seed)
+    f = rng.integers(1, n_layers + 1, size=shape_ids)
+    return np.where(rng.random(shape_ids) < 0.5, 0, f).astype(np.int32)
+
+
+@pytest.mark.parametrize("metric", ["global", "local", "both"])
+def test_small_bf16_prefill_teacher_forced(metric):
+    """bf16 prefill (6 layers, width 512, 3 x 200 rows), half of the rows on a
+    seeded exit schedule and half on the policy at a threshold that fires:
+    every layer checked on the GPU's own inputs at the per-element bound."""
+    say(f"small bf16 prefill teacher-forced metric={metric}")
     shape = SMALL_BF16
     w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
     w = O.as64(w32)
     ids = ai.token_ids(10, shape.vocab, 3, 200)
-    force = np.random.default_rng(5).integers(0, shape.n_layers + 1, size=ids.shape)
+    force = _half_forced(5, ids.shape, shape.n_layers)
+    delta = oracle_deltas(w, shape, ids, metric)[0]
     model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512)
-    cfg_g = B.exit_cfg(math.inf, shape.n_layers, "global")
-    res_g, cache_g = model.prefill(ids, cfg_g, force_layer=force, logits="all")
-    torch.cuda.synchronize()
-    res_o, cache_o = O.prefill(w, shape, ids, O.ExitConfig(delta=math.inf), force_layer=force)
-    np.testing.assert_array_equal(res_g.exit_layer.cpu().numpy(), res_o.exit_layer)
-    kg, vg = cache_host(cache_g, 3, 200)
-    bf16_close(kg, cache_o.k, "K cache")
-    bf16_close(vg, cache_o.v, "V cache")
-    bf16_close(res_g.logits.cpu().numpy(), res_o.logits, "logits")
+    rep = LC.Report(say)
+    res, cache, chk = _tf_prefill(model, w, shape, ids, O.ExitConfig(delta=delta, metric=metric),
+                                  B.exit_cfg(delta, shape.n_layers, metric), force=force, rep=rep)
+    rep.summary()
+    el = chk.exit_layer
+    policy_exits = int(np.sum((force.reshape(-1) == 0) & (el < shape.n_layers)))
+    say(f"  exits {int(np.sum(el < shape.n_layers))} (policy {policy_exits})")
+    assert policy_exits > 0 and np.sum(el < shape.n_layers) < el.size
+
+
+def test_small_bf16_decode_teacher_forced():
+    """bf16 generation: a prompt with a seeded schedule, then six decode
+    passes (one row per sequence: key-chunked attention, skinny GEMMs, KV
+    generation deferred to the end of the pass), each pass checked layer by
+    layer on the GPU's own inputs, generated K/V included."""
+    say("small bf16 decode teacher-forced")
+    shape = SMALL_BF16
+    N = shape.n_layers
+    w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
+    w = O.as64(w32)
+    Bn, T, S = 3, 40, 6
+    ids = ai.token_ids(12, shape.vocab, Bn, T)
+    step_ids = ai.token_ids(13, shape.vocab, S, Bn)
+    rng = np.random.default_rng(6)
+    force_p = rng.integers(0, N + 1, size=ids.shape).astype(np.int32)
+    force_s = rng.integers(1, N + 1, size=(S, Bn)).astype(np.int32)   # every step token exits
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512)
+    cfg_g = B.exit_cfg(math.inf, N, "global")
+    cfg_o = O.ExitConfig(delta=math.inf)
+    rep = LC.Report(say)
+    _, cache, _ = _tf_prefill(model, w, shape, ids, cfg_o, cfg_g, force=force_p, s_max=T + S,
+                              logits="last", rep=rep)
+    for s in range(S):
+        _tf_decode(model, w, shape, cache, step_ids[s], np.full(Bn, T + s), cfg_o, cfg_g,
+                   force=force_s[s], rep=rep)
+    rep.summary()
 
 
 def test_small_bf16_free_running_decisions():
-    """bf16, policy-driven (global metric): every exit decision the oracle
-    takes with a margin above the bf16 error of the similarity matches."""
+    """bf16, policy-driven (global metric) end to end: every exit decision the
+    oracle takes with a margin above the bf16 error of the similarity matches."""
     say("small bf16 free running")
     shape = SMALL_BF16
     w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
@@ -186,80 +241,72 @@ def test_small_bf16_free_running_decisions():
     assert 0 < np.sum(el_o < shape.n_layers) < el_o.size
 
 
-def test_small_bf16_decode_forced_schedule():
-    """bf16 generation with a seeded exit schedule on both sides, for the
-    prompt and every step: the decode passes (one row per sequence) take the
-    key-chunked attention, the skinny GEMMs and the KV generation deferred to
-    the end of the pass.  Step tokens are seeded (not greedy) so both sides
-    see the same ids; exit layers exact, logits and the whole cache (computed
-    and generated entries) within the bf16 bound."""
-    say("small bf16 decode forced schedule")
-    shape = SMALL_BF16
-    N = shape.n_layers
-    w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
-    w = O.as64(w32)
-    Bn, T, S = 3, 40, 6
-    ids = ai.token_ids(12, shape.vocab, Bn, T)
-    step_ids = ai.token_ids(13, shape.vocab, S, Bn)
-    rng = np.random.default_rng(6)
-    force_p = rng.integers(0, N + 1, size=ids.shape)
-    force_s = rng.integers(1, N + 1, size=(S, Bn))     # every step token exits somewhere
-    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512)
-    cfg_g = B.exit_cfg(math.inf, N, "global")
-    cfg_o = O.ExitConfig(delta=math.inf)
-    res_g, cache_g = model.prefill(ids, cfg_g, s_max=T + S, force_layer=force_p, logits="last")
-    res_o, cache_o = O.prefill(w, shape, ids, cfg_o, s_max=T + S, force_layer=force_p)
-    for s in range(S):
-        pos = np.full(Bn, T + s)
-        st_g = model.decode_step(cache_g, torch.from_numpy(step_ids[s]).to("cuda", torch.int32),
-                                 torch.from_numpy(pos).to("cuda", torch.int32), cfg_g,
-                                 force_layer=torch.from_numpy(force_s[s]).to("cuda", torch.int32))
-        st_o = O.decode_step(w, shape, cache_o, step_ids[s], pos, cfg_o, force_layer=force_s[s])
-        torch.cuda.synchronize()
-        np.testing.assert_array_equal(st_g.exit_layer.cpu().numpy(), st_o.exit_layer)
-        bf16_close(st_g.logits.cpu().numpy(), st_o.logits, f"step {s} logits")
-    kg, vg = cache_host(cache_g, Bn, T + S)
-    bf16_close(kg, cache_o.k, "K cache")
-    bf16_close(vg, cache_o.v, "V cache")
+SHAPE_7B_4L = ai.DecoderShape(n_layers=4, d_model=4096, n_heads=32, head_dim=128, d_ff=11008,
+                              vocab=512)
 
 
-def test_7b_width_decode_forced_schedule():
-    """Decode at the 7B layer width (d_model 4096, 32 x 128 heads, d_ff
-    11008; two layers, small vocabulary): a 64-sequence decode pass takes
-    the skinny GEMMs at their real shapes, whose stream-K ranges straddle
-    column tiles (QKV, gate/up, down).  Seeded exit schedule on both sides;
-    exit layers exact, logits and the cache within the bf16 bound."""
-    say("7B-width decode forced schedule")
-    shape = ai.DecoderShape(n_layers=2, d_model=4096, n_heads=32, head_dim=128, d_ff=11008,
-                            vocab=512)
+@pytest.fixture(scope="module")
+def w7b():
+    """Four layers of the 7B-class decoder (width 4096, 32 x 128 heads, FFN
+    11008; a 512-entry vocabulary) as bf16 values, and their float64 copy."""
+    w32 = ai.decoder_weights(SHAPE_7B_4L, seed=21, dtype="bf16")
+    return w32, O.as64(w32)
+
+
+def test_7b_prefill_teacher_forced(w7b):
+    """Prefill at the 7B layer shapes: 4 sequences x 600 rows (2400 rows: ten
+    256-row GEMM tiles, the last ragged, at K = 4096 and K = 11008; 32 heads,
+    so the query-tile attention takes its XCD-major one-dimensional grid, with
+    a ragged last query tile per sequence).  Half of the rows follow a seeded
+    schedule, half the policy; every layer is checked on the GPU's own
+    inputs (>= 256 sampled rows for q, attention and h; all rows for K/V,
+    exit flags, lists and exit layers), then the generated K/V of up to 256
+    exited rows at all their skipped layers, and the logits."""
+    shape = SHAPE_7B_4L
+    say("7B-shape prefill teacher-forced (4 x 600 rows)")
+    w32, w = w7b
+    ids = ai.token_ids(31, shape.vocab, 4, 600)
+    force = _half_forced(32, ids.shape, shape.n_layers)
+    delta = 0.70
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=640)
+    rep = LC.Report(say)
+    res, cache, chk = _tf_prefill(model, w, shape, ids, O.ExitConfig(delta=delta),
+                                  B.exit_cfg(delta, shape.n_layers, "global"), force=force,
+                                  rep=rep)
+    rep.summary()
+    el = chk.exit_layer
+    say(f"  exits {int(np.sum(el < shape.n_layers))} of {el.size} "
+        f"(policy {int(np.sum((force.reshape(-1) == 0) & (el < shape.n_layers)))})")
+    assert 0 < np.sum(el < shape.n_layers) < el.size
+    del model, cache, res
+    torch.cuda.empty_cache()
+
+
+def test_7b_width_decode_teacher_forced(w7b):
+    """Decode at the 7B layer shapes (64 sequences): the skinny stream-K GEMMs
+    at their real shapes (ranges straddling column tiles for QKV, gate/up and
+    down), key-chunked attention, the deferred KV generation; prompt and
+    decode pass checked layer by layer on the GPU's own inputs."""
+    shape = SHAPE_7B_4L
+    say("7B-width decode teacher-forced")
+    w32, w = w7b
     N = shape.n_layers
-    w32 = ai.decoder_weights(shape, seed=21, dtype="bf16")
     Bn, T = 64, 2
     ids = ai.token_ids(22, shape.vocab, Bn, T)
     step = ai.token_ids(23, shape.vocab, 1, Bn)[0]
     rng = np.random.default_rng(24)
-    force_p = rng.integers(0, N + 1, size=ids.shape)
-    force_s = rng.integers(1, N + 1, size=Bn)
+    force_p = rng.integers(0, N + 1, size=ids.shape).astype(np.int32)
+    force_s = rng.integers(1, N + 1, size=Bn).astype(np.int32)
     model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=64)
     cfg_g = B.exit_cfg(math.inf, N, "global")
-    res_g, cache_g = model.prefill(ids, cfg_g, s_max=T + 1, force_layer=force_p, logits="last")
-    st_g = model.decode_step(cache_g, torch.from_numpy(step).to("cuda", torch.int32),
-                             torch.full((Bn,), T, dtype=torch.int32, device="cuda"), cfg_g,
-                             force_layer=torch.from_numpy(force_s).to("cuda", torch.int32))
-    torch.cuda.synchronize()
-    say("  GPU done; oracle")
-    w = O.as64(w32)
-    del w32
     cfg_o = O.ExitConfig(delta=math.inf)
-    res_o, cache_o = O.prefill(w, shape, ids, cfg_o, s_max=T + 1, force_layer=force_p)
-    st_o = O.decode_step(w, shape, cache_o, step, np.full(Bn, T), cfg_o, force_layer=force_s)
-    np.testing.assert_array_equal(res_g.exit_layer.cpu().numpy(), res_o.exit_layer)
-    np.testing.assert_array_equal(st_g.exit_layer.cpu().numpy(), st_o.exit_layer)
-    assert 0 < int(np.sum(st_o.exit_layer < N)) < Bn
-    bf16_close(st_g.logits.cpu().numpy(), st_o.logits, "decode logits")
-    kg, vg = cache_host(cache_g, Bn, T + 1)
-    bf16_close(kg, cache_o.k, "K cache")
-    bf16_close(vg, cache_o.v, "V cache")
+    rep = LC.Report(say)
+    _, cache, _ = _tf_prefill(model, w, shape, ids, cfg_o, cfg_g, force=force_p, s_max=T + 1,
+                              logits="last", rep=rep)
+    _, chk = _tf_decode(model, w, shape, cache, step, np.full(Bn, T), cfg_o, cfg_g,
+                        force=force_s, rep=rep)
+    rep.summary()
+    assert 0 < int(np.sum(chk.exit_layer < N)) < Bn
 
 
 def test_timing_select_prefix():
