@@ -19,7 +19,7 @@ generation, mapper, exit test and compaction, the fixed-schedule generation,
 the BERT-base classification, the tiny f32 decoder, and the CPU oracle on a
 bounded sample.
 
-    python bench.py [--steps K] [--warmup W] [--delta 0.95] [--metric global]
+    python bench.py [--steps K] [--warmup W] [--delta D | --budget 0.2] [--metric global]
 """
 from __future__ import annotations
 
@@ -36,7 +36,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # rocprofv3 traffic summaries: the generation headline (decode attention) and
 # the 8 x 2048 prefill section (GEMMs, prefill attention, exit test, compaction)
 TRAFFIC_FILES = (os.path.join(HERE, "profiles", "llama7b_generation_64x4096_hbm_traffic.json"),
-                 os.path.join(HERE, "profiles", "llama7b_prefill_8x2048_hbm_traffic.json"))
+                 os.path.join(HERE, "profiles", "llama7b_prefill_8x2048_hbm_traffic.json"),
+                 os.path.join(HERE, "profiles", "kvgen_4096tok_32layers_mfma_traffic.json"))
 
 
 # HIP sources each kernel family is built from (its traffic figure is void
@@ -116,7 +117,15 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--prefill-steps", type=int, default=5,
                     help="timed steps of the 8 x 2048 prefill section")
-    ap.add_argument("--delta", type=float, default=0.95)
+    ap.add_argument("--delta", type=float, default=None,
+                    help="exit threshold of the headline generation; default: calibrated on a "
+                         "no-exit pass of the same workload to skip --budget of the token-layers")
+    ap.add_argument("--budget", type=float, default=0.20,
+                    help="skipped fraction of (token, layer) pairs the headline threshold is "
+                         "calibrated to (the paper's operating points are 5-25%%)")
+    ap.add_argument("--prefill-delta", type=float, default=0.95,
+                    help="threshold of the 8 x 2048 prefill section, the classification and "
+                         "the CPU baseline (the prefill configuration's 0.90/0.95/0.99 sweep)")
     ap.add_argument("--metric", choices=("global", "local"), default="global")
     ap.add_argument("--batch", type=int, default=8)
     ap.add_argument("--seq", type=int, default=2048)
@@ -131,10 +140,31 @@ def parse():
     ap.add_argument("--gen-steps", type=int, default=256)
     ap.add_argument("--cpu-tokens", type=int, default=2048)
     ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--sections", default="all",
+                    help="comma list of the parts to run (profiling runs): headline, prefill, "
+                         "variants (prefill no-exit / fixed schedule / sweep), kvgen, hsm, exit, "
+                         "generation, classification, tiny, cpu; default all")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="copy 256 MiB device to device first (a kernel of known traffic "
                          "for scaling hardware byte counters)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    every = {"headline", "prefill", "variants", "kvgen", "hsm", "exit", "generation",
+             "classification", "tiny", "cpu"}
+    sec = every if args.sections == "all" else set(args.sections.split(","))
+    if sec - every:
+        ap.error(f"unknown sections {sorted(sec - every)}")
+    if args.no_extras:
+        sec -= {"variants", "kvgen", "hsm", "exit", "tiny"}
+    if args.no_cpu_baseline:
+        sec.discard("cpu")
+    if args.no_generation:
+        sec.discard("generation")
+    if args.no_classification:
+        sec.discard("classification")
+    if "variants" in sec:
+        sec.add("prefill")
+    args.sec = sec
+    return args
 
 
 def layer_counts(exit_layer, n_layers):
@@ -221,10 +251,24 @@ def main():
         f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated")
 
     # ---- headline: generation (prefill + decode) with the policy's decisions
+    out = {"metric": "tokens/s (prefill+decode) at Llama-7B shape; KV-gen MFMA util %",
+           "value": None, "unit": "tokens/s", "n_gpus": 1, "sections": sorted(args.sec)}
+    if "headline" in args.sec:
+        out = headline(args, model, shape, ai, B, torch, np)
+    run_sections(args, out, model, shape, ai, B, torch, np, Bn, T, n_tok)
+
+
+def headline(args, model, shape, ai, B, torch, np):
     log(f"headline: generation, batch {args.gen_batch}, {args.gen_context}-token prompts, "
-        f"{args.gen_steps} decode steps, delta={args.delta} metric={args.metric}; "
+        f"{args.gen_steps} decode steps, metric={args.metric}, delta "
+        f"{args.delta if args.delta is not None else f'calibrated to skip {args.budget:.0%}'}; "
         f"{args.warmup} warmup + {args.steps} timed passes")
     head = generation_policy(args, model, shape, ai, B, torch, np)
+    if args.delta is None:
+        how = (f"delta {head['delta']:.6f}, calibrated on a no-exit pass of the same workload "
+               f"to skip {args.budget:.0%} of the token-layers")
+    else:
+        how = f"delta {head['delta']}"
     out = {
         "metric": "tokens/s (prefill+decode) at Llama-7B shape; KV-gen MFMA util %",
         "value": head["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -234,13 +278,17 @@ def main():
         "config": {"workload": (f"Llama-7B-shaped decoder generation: batch {args.gen_batch}, "
                                 f"{args.gen_context}-token prompts prefilled, then "
                                 f"{args.gen_steps} greedy decode steps; token-level exit "
-                                f"({args.metric} metric, delta {args.delta})"),
+                                f"with the policy's own decisions ({args.metric} metric, {how})"),
                    "global_batch": args.gen_batch, "seq_len": args.gen_context + args.gen_steps,
                    "parallelism": "none (one GPU)"},
         "roofline": head.pop("roofline"),
         "generation_policy": head,
     }
+    return out
 
+
+def run_sections(args, out, model, shape, ai, B, torch, np, Bn, T, n_tok):
+    N = shape.n_layers
     # ---- prefill 8 x 2048 with the threshold sweep and the per-kernel figures
     ids = torch.from_numpy(ai.token_ids(8, shape.vocab, Bn, T)).cuda()
     cache = model.new_cache(Bn, T)
@@ -264,7 +312,41 @@ def main():
             kern = B.timing_read()
         return e0.elapsed_time(e1) / steps, res, kern
 
-    cfg = B.exit_cfg(args.delta, N, args.metric)
+    cfg = B.exit_cfg(args.prefill_delta, N, args.metric)
+    psteps = args.prefill_steps
+    if "prefill" in args.sec:
+        prefill_section(args, out, run, cfg, model, shape, ai, B, torch, np, Bn, T, n_tok, ids,
+                        cache)
+    if "kvgen" in args.sec:
+        out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
+    if "hsm" in args.sec:
+        out["hsm_standalone"] = hsm_standalone(shape, B, torch, np)
+        log(f"hsm (mapper) 4096 rows: {out['hsm_standalone']['call_ms']:.2f} ms, "
+            f"{out['hsm_standalone']['tflops']:.0f} TFLOP/s")
+    if "exit" in args.sec:
+        out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
+
+    del cache, ids
+    torch.cuda.empty_cache()
+    if "generation" in args.sec:
+        out["generation_fixed_schedule"] = generation(args, model, shape, ai, B, torch, np)
+
+    if "classification" in args.sec:
+        del model
+        torch.cuda.empty_cache()
+        out["classification"] = classification(args, ai, B, torch, np)
+
+    if "tiny" in args.sec:
+        out["tiny_f32"] = tiny_decoder(ai, B, torch, np)
+
+    if "cpu" in args.sec:
+        out["cpu_baseline"] = cpu_baseline(args, shape, ai, np)
+    print(json.dumps(out), flush=True)
+
+
+def prefill_section(args, out, run, cfg, model, shape, ai, B, torch, np, Bn, T, n_tok, ids,
+                    cache):
+    N = shape.n_layers
     psteps = args.prefill_steps
     ms, res, kern = run(cfg, timing=True, warmup=0 if psteps <= 1 else 2)
     tok_s = n_tok / (ms / 1e3)
@@ -280,7 +362,7 @@ def main():
     achieved = d_flops_launch / d_avg_s
     pre = {
         "workload": (f"Llama-7B-shaped decoder prefill, batch {Bn} x {T}, token-level exit "
-                     f"({args.metric} metric, delta {args.delta})"),
+                     f"({args.metric} metric, delta {args.prefill_delta})"),
         "tokens_per_s": tok_s, "ms_per_step": ms, "steps": psteps,
         "dominant_kernel": {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12,
                             "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
@@ -295,7 +377,7 @@ def main():
     }
     out["prefill_8x2048"] = pre
 
-    if not args.no_extras:
+    if "variants" in args.sec:
         # no-exit reference (delta = +inf) and a fixed exit schedule (i* ~ U{8..31})
         ms_inf, _, _ = run(B.exit_cfg(math.inf, N, args.metric), steps=max(2, psteps // 2),
                            warmup=1)
@@ -314,29 +396,14 @@ def main():
             "kernels": kernel_table(kern_f, work_f, ms_f, steps_f),
         }
         log(f"prefill no-exit {ms_inf:.1f} ms/step; fixed schedule {ms_f:.1f} ms/step")
-        pre["delta_sweep"] = delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf)
-        out["kv_generate_standalone"] = kv_generate_standalone(model, shape, ai, B, torch, np)
-        out["hsm_standalone"] = hsm_standalone(shape, B, torch, np)
-        log(f"hsm (mapper) 4096 rows: {out['hsm_standalone']['call_ms']:.2f} ms, "
-            f"{out['hsm_standalone']['tflops']:.0f} TFLOP/s")
-        out["exit_test_standalone"] = exit_test_standalone(shape, ai, B, torch, np, n_tok)
-
-    del cache, ids
-    torch.cuda.empty_cache()
-    if not args.no_generation:
-        out["generation_fixed_schedule"] = generation(args, model, shape, ai, B, torch, np)
-
-    if not args.no_classification:
-        del model
-        torch.cuda.empty_cache()
-        out["classification"] = classification(args, ai, B, torch, np)
-
-    if not args.no_extras:
-        out["tiny_f32"] = tiny_decoder(ai, B, torch, np)
-
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args, shape, ai, np)
-    print(json.dumps(out), flush=True)
+        # similarities of a no-exit pass, for the thresholds calibrated to a budget
+        from paper_2601_03700_amd.calibrate import SimRecorder
+        rec = SimRecorder(N, n_tok, "cuda")
+        model.prefill(ids, B.exit_cfg(math.inf, N, args.metric), cache=cache, logits="last",
+                      on_layer=rec)
+        sims = rec.sims.cpu().numpy()
+        del rec
+        pre["delta_sweep"] = delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf, sims)
 
 
 def skipped_fraction(exit_layer, n_layers):
@@ -359,11 +426,13 @@ def exit_histogram(exit_layer, n_layers):
     return torch.bincount(exit_layer.to("cpu").long(), minlength=n_layers + 1)[1:].tolist()
 
 
-def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf):
+def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf, sims):
     """The policy's own decisions: the threshold set {0.90, 0.95, 0.99} of
-    the prefill configuration, then thresholds calibrated (bisection on
-    delta, the skipped fraction falls as delta rises) so that 10 / 20 / 25 %
-    of the (token, layer) pairs are skipped by the exit test itself."""
+    the prefill configuration, then thresholds calibrated on the no-exit
+    pass's similarities (calibrate.calibrate_delta: the largest delta whose
+    running-max count skips the budget) so that 10 / 20 / 25 % of the
+    (token, layer) pairs are skipped by the exit test itself."""
+    from paper_2601_03700_amd.calibrate import calibrate_delta, skipped_fraction_at
     res_out = {"thresholds": {}, "calibrated": {}}
     for d in (0.90, 0.95, 0.99):
         ms, res, _ = run(B.exit_cfg(d, N, args.metric), steps=2, warmup=1)
@@ -373,21 +442,15 @@ def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf):
             "rdc": reduction(res.exit_layer, shape),
             "exit_layer_histogram": exit_histogram(res.exit_layer, N)}
     for target in (0.10, 0.20, 0.25):
-        lo, hi = -1.0, 1.0          # skipped(lo) >= target > skipped(hi)
-        for _ in range(12):
-            mid = 0.5 * (lo + hi)
-            _, res, _ = run(B.exit_cfg(mid, N, args.metric), steps=1, warmup=0)
-            if skipped_fraction(res.exit_layer, N) >= target:
-                lo = mid
-            else:
-                hi = mid
-        ms, res, _ = run(B.exit_cfg(lo, N, args.metric), steps=2, warmup=1)
+        d = calibrate_delta(sims, target, N)
+        ms, res, _ = run(B.exit_cfg(d, N, args.metric), steps=2, warmup=1)
         frac = skipped_fraction(res.exit_layer, N)
         # the all-at-once variant (Appendix H.2) at the same threshold: each
         # prompt's last token decides for the whole prompt
-        ms_a, res_a, _ = run(B.exit_cfg(lo, N, args.metric, prompt_level=True), steps=2, warmup=1)
+        ms_a, res_a, _ = run(B.exit_cfg(d, N, args.metric, prompt_level=True), steps=2, warmup=1)
         res_out["calibrated"][f"{int(round(target * 100))}%"] = {
-            "delta": lo, "tokens_per_s": n_tok / (ms / 1e3), "ms_per_step": ms,
+            "delta": d, "predicted_skipped_fraction": skipped_fraction_at(sims, d, N),
+            "tokens_per_s": n_tok / (ms / 1e3), "ms_per_step": ms,
             "skipped_fraction": frac, "speedup_vs_no_exit": ms_inf / ms,
             "rdc": reduction(res.exit_layer, shape),
             "exit_layer_histogram": exit_histogram(res.exit_layer, N),
@@ -395,7 +458,7 @@ def delta_sweep(args, run, B, N, n_tok, pos, shape, ms_inf):
                             "skipped_fraction": skipped_fraction(res_a.exit_layer, N),
                             "rdc": reduction(res_a.exit_layer, shape),
                             "exit_layer_histogram": exit_histogram(res_a.exit_layer, N)}}
-        log(f"calibrated delta {lo:.4f}: {frac:.1%} of token-layers skipped, "
+        log(f"calibrated delta {d:.4f}: {frac:.1%} of token-layers skipped, "
             f"{ms:.1f} ms/step ({ms_inf / ms:.2f}x vs no exit)")
     return res_out
 
@@ -430,23 +493,31 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
     written_k = ~torch.isnan(kc).any(dim=(2, 3))
     written_v = ~torch.isnan(vc).any(dim=(2, 3))
     sentinel_ok = bool(torch.equal(written_k, want) and torch.equal(written_v, want))
-    B.timing_reset()
-    B.timing_enable(True)
+    # the whole call without per-launch events, then every launch bracketed
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(reps):
         call()
     e1.record()
     torch.cuda.synchronize()
+    call_ms = e0.elapsed_time(e1) / reps
+    B.timing_reset()
+    B.timing_enable(True)
+    for _ in range(reps):
+        call()
+    torch.cuda.synchronize()
     B.timing_enable(False)
     k = B.timing_read()
     pairs = int((N - el.long()).clamp(min=0).sum())
     flops = 4.0 * D * Dq * pairs
-    call_ms = e0.elapsed_time(e1) / reps
-    g_launch, g_ms = k.get("gemm_kv_grouped_kernel", (reps, call_ms * reps))
+    grouped = [v for kk, v in k.items() if kk.startswith("gemm_kv_grouped_kernel")]
+    assert grouped, f"no grouped KV-generation launch timed: {sorted(k)}"
+    g_launch, g_ms = grouped[0]
     gemm_ms = g_ms / g_launch
+    log(f"kv generation 4096 tokens: call {call_ms:.3f} ms, grouped GEMM {gemm_ms:.3f} ms = "
+        f"{flops / (gemm_ms / 1e3) / PEAK_BF16:.3f} of the bf16 peak")
     return {"tokens": n, "pairs": pairs, "tflop": flops / 1e12, "call_ms": call_ms,
-            "sentinel_ok": sentinel_ok,
+            "sentinel_ok": sentinel_ok, "traffic": measured_traffic("kv_generate"),
             "gemm_ms": gemm_ms, "mfma_util": flops / (gemm_ms / 1e3) / PEAK_BF16,
             "mfma_util_whole_call": flops / (call_ms / 1e3) / PEAK_BF16,
             "kernels": {kk: {"launches": v[0], "avg_us": 1e3 * v[1] / max(v[0], 1)}
@@ -634,26 +705,34 @@ def generation_policy(args, model, shape, ai, B, torch, np):
     decisions.  One step = one pass: prefill of gen_batch prompts of
     gen_context uniform-random tokens, then gen_steps greedy decode steps
     (each new token through the layers with token-level exit, attention over
-    the mixed computed / generated cache).  Timed: `steps` passes after
-    `warmup` untimed ones, each decode-attention launch also timed on its
-    stream; one more pass times every launch for the per-kernel table."""
+    the mixed computed / generated cache).  Unless --delta is given, the
+    threshold is calibrated first (Section 4.1 budget): one untimed pass that
+    never exits records every layer's similarity of every prompt and decode
+    token, and delta is the largest threshold that skips --budget of the
+    (token, layer) pairs on it.  Timed: `steps` passes after `warmup` untimed
+    ones, each decode-attention launch also timed on its stream; one more
+    pass times every launch for the per-kernel table; then the same workload
+    with no exit (delta = +inf) for comparison."""
+    from paper_2601_03700_amd.calibrate import SimRecorder, calibrate_delta, skipped_fraction_at
     N = shape.n_layers
     Bn, T, S = args.gen_batch, args.gen_context, args.gen_steps
     cache = model.new_cache(Bn, T + S)
     ids = torch.from_numpy(ai.token_ids(9, shape.vocab, Bn, T)).cuda()
-    cfg = B.exit_cfg(args.delta, N, args.metric)
+    cfg_inf = B.exit_cfg(math.inf, N, args.metric)
     pos_dec = [torch.full((Bn,), T + k, dtype=torch.int32, device="cuda") for k in range(S)]
 
-    def one_pass(ev=None):
+    def one_pass(cfg, ev=None, rec=None):
         if ev is not None:
             ev[0].record()
-        res, _ = model.prefill(ids, cfg, cache=cache, logits="last")
+        res, _ = model.prefill(ids, cfg, cache=cache, logits="last",
+                               on_layer=None if rec is None else rec[0])
         nxt = model.greedy(res.logits)
         if ev is not None:
             ev[1].record()
         els = []
         for k in range(S):
-            st = model.decode_step(cache, nxt, pos_dec[k], cfg, pos_max=T + k)
+            st = model.decode_step(cache, nxt, pos_dec[k], cfg, pos_max=T + k,
+                                   on_layer=None if rec is None else rec[1 + k])
             nxt = model.greedy(st.logits)
             els.append(st.exit_layer)
         if ev is not None:
@@ -661,8 +740,24 @@ def generation_policy(args, model, shape, ai, B, torch, np):
         return res.exit_layer, torch.stack(els) if els else torch.zeros((0, Bn), dtype=torch.int32)
 
     t0 = time.time()
+    calib = None
+    if args.delta is None:
+        recs = [SimRecorder(N, Bn * T, "cuda")] + [SimRecorder(N, Bn, "cuda") for _ in range(S)]
+        one_pass(cfg_inf, rec=recs)
+        sims = torch.cat([r.sims for r in recs], dim=1).cpu().numpy()
+        delta = calibrate_delta(sims, args.budget, N)
+        calib = {"budget": args.budget, "pass_tokens": int(sims.shape[1]),
+                 "predicted_skipped_fraction": skipped_fraction_at(sims, delta, N),
+                 "method": "largest delta whose running-max similarity count on a no-exit pass "
+                           "of the same workload skips the budget (calibrate.calibrate_delta)"}
+        del recs, sims
+        log(f"headline: delta calibrated to {delta:.6f} for a {args.budget:.0%} budget "
+            f"({time.time() - t0:.1f}s)")
+    else:
+        delta = args.delta
+    cfg = B.exit_cfg(delta, N, args.metric)
     for _ in range(args.warmup):
-        one_pass()
+        one_pass(cfg)
     torch.cuda.synchronize()
     log(f"headline: cache {2 * cache.k.numel() * 2 / 2**30:.0f} GiB, {args.warmup} warmup "
         f"pass(es) in {time.time() - t0:.1f}s")
@@ -676,7 +771,7 @@ def generation_policy(args, model, shape, ai, B, torch, np):
     B.timing_enable(True)
     torch.cuda.synchronize()
     e0.record()
-    passes = [one_pass(evs[k]) for k in range(args.steps)]
+    passes = [one_pass(cfg, evs[k]) for k in range(args.steps)]
     e1.record()
     torch.cuda.synchronize()
     B.timing_enable(False)
@@ -686,7 +781,7 @@ def generation_policy(args, model, shape, ai, B, torch, np):
     B.timing_enable(True)
     i0, i1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     i0.record()
-    one_pass()
+    one_pass(cfg)
     i1.record()
     torch.cuda.synchronize()
     B.timing_enable(False)
@@ -696,6 +791,17 @@ def generation_policy(args, model, shape, ai, B, torch, np):
     prefill_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
     decode_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
     el_prompt, el_dec = passes[-1]
+    # the same workload without exits (no event bracketing)
+    n_inf = max(1, min(2, args.steps))
+    evi = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_inf)]
+    one_pass(cfg_inf)
+    torch.cuda.synchronize()
+    for k in range(n_inf):
+        one_pass(cfg_inf, evi[k])
+    torch.cuda.synchronize()
+    inf_ms = sum(e[0].elapsed_time(e[2]) for e in evi) / n_inf
+    inf_prefill = sum(e[0].elapsed_time(e[1]) for e in evi) / n_inf
+    inf_decode = sum(e[1].elapsed_time(e[2]) for e in evi) / n_inf
     # the dominant kernel over the timed passes and its roofline
     dom = max(kern, key=lambda k: kern[k][1])
     d_launch, d_ms = kern[dom]
@@ -714,25 +820,34 @@ def generation_policy(args, model, shape, ai, B, torch, np):
                     "frac": None, "traffic": None, "avg_launch_us": d_avg_s * 1e6,
                     "launches": d_launch}
     tokens = Bn * (T + S)
+    el_all = torch.cat([el_prompt.reshape(-1), el_dec.reshape(-1)]).to(torch.int64)
     out = {
+        "delta": delta, "calibration": calib,
         "tokens_per_s": tokens / (ms_pass / 1e3), "ms_per_pass": ms_pass,
         "prefill_ms": prefill_ms, "decode_ms": decode_ms,
         "prefill_tokens_per_s": Bn * T / (prefill_ms / 1e3),
         "decode_tokens_per_s": Bn * S / (decode_ms / 1e3) if S else None,
         "decode_ms_per_step": decode_ms / S if S else None,
+        "skipped_fraction": float((N - el_all).clamp(min=0).sum()) / (N * el_all.numel()),
         "prompt_exit_fraction": float((el_prompt < N).to(torch.float64).mean()),
         "prompt_rdc": reduction(el_prompt, shape),
         "decode_exit_fraction": float((el_dec < N).to(torch.float64).mean()) if S else None,
+        "decode_rdc": reduction(el_dec.reshape(-1), shape) if S else None,
+        "exit_layer_histogram": exit_histogram(el_all, N),
         "exited_fraction_by_layer": [float((el_dec <= i).to(torch.float64).mean())
                                      for i in range(1, N + 1)] if S else None,
+        "no_exit": {"tokens_per_s": tokens / (inf_ms / 1e3), "ms_per_pass": inf_ms,
+                    "prefill_ms": inf_prefill, "decode_ms": inf_decode, "passes": n_inf},
+        "speedup_vs_no_exit": inf_ms / ms_pass,
         "roofline": roofline,
         "instrumented_pass_ms": ms_instr,
         "kernels": {k: {"launches": n, "avg_us": ms * 1e3 / n, "share": ms / ms_instr}
                     for k, (n, ms) in sorted(kern_all.items(), key=lambda kv: -kv[1][1])[:16]},
     }
     log(f"headline: {ms_pass:.0f} ms per pass = {out['tokens_per_s']:.0f} tokens/s "
-        f"(prefill {prefill_ms:.0f} ms, decode {decode_ms / max(S, 1):.1f} ms/step); "
-        f"{dom} {roofline.get('frac') or 0:.3f} of its roofline")
+        f"(prefill {prefill_ms:.0f} ms, decode {decode_ms / max(S, 1):.1f} ms/step), "
+        f"{out['skipped_fraction']:.1%} of token-layers skipped; no exit {inf_ms:.0f} ms "
+        f"({out['speedup_vs_no_exit']:.2f}x); {dom} {roofline.get('frac') or 0:.3f} of its roofline")
     del cache, ids
     torch.cuda.empty_cache()
     return out
@@ -750,7 +865,7 @@ def generation(args, model, shape, ai, B, torch, np):
     t0 = time.time()
     cache = model.new_cache(Bn, s_max)
     ids = torch.from_numpy(ai.token_ids(9, shape.vocab, Bn, T)).cuda()
-    cfg = B.exit_cfg(args.delta, N, args.metric)
+    cfg = B.exit_cfg(args.prefill_delta, N, args.metric)
     sched_p = torch.from_numpy(ai.forced_exit_layers(5, Bn * T, 8, 31)).cuda()
     sched_d = torch.from_numpy(ai.forced_exit_layers(6, S * Bn, 8, 31)).cuda().view(S, Bn)
     torch.cuda.synchronize()
@@ -866,8 +981,8 @@ def classification(args, ai, B, torch, np, reps=5):
             kern = B.timing_read()
         return e0.elapsed_time(e1) / reps, out, kern
 
-    ms, out, _ = run(args.delta)
-    _, _, kern = run(args.delta, timing=True)     # per-kernel HIP events (separate run)
+    ms, out, _ = run(args.prefill_delta)
+    _, _, kern = run(args.prefill_delta, timing=True)     # per-kernel HIP events (separate run)
     el = out.exit_layer.to(torch.int64)
     ms_inf, _, _ = run(math.inf)
     sched = torch.from_numpy(ai.forced_exit_layers(19, n, 3, N - 1)).cuda()
@@ -876,7 +991,7 @@ def classification(args, ai, B, torch, np, reps=5):
     res = {
         "workload": (f"BERT-base-shaped encoder classification (12 layers, width 768, 12x64 heads, "
                      f"GELU FFN 3072, 2-class head on [CLS]), batch {Bn} x {T}, token-level exit "
-                     f"({args.metric} metric, delta {args.delta})"),
+                     f"({args.metric} metric, delta {args.prefill_delta})"),
         "sequences_per_s": Bn / (ms / 1e3), "tokens_per_s": n / (ms / 1e3), "ms_per_pass": ms,
         "exit_fraction": float((el < N).to(torch.float64).mean()),
         "no_exit": {"sequences_per_s": Bn / (ms_inf / 1e3), "ms_per_pass": ms_inf},
@@ -950,7 +1065,7 @@ def cpu_baseline(args, shape, ai, np):
     log(f"cpu baseline: drawing {L}-layer oracle weights")
     w = O.as64(ai.decoder_weights(sub, seed=7, dtype="bf16"))
     ids = ai.token_ids(8, shape.vocab, 1, args.cpu_tokens)
-    cfg = O.ExitConfig(delta=args.delta, metric=args.metric)
+    cfg = O.ExitConfig(delta=args.prefill_delta, metric=args.metric)
     t0 = time.perf_counter()
     O.prefill(w, sub, ids, cfg)
     dt = time.perf_counter() - t0
