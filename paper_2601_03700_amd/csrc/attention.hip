@@ -13,9 +13,13 @@
 // 8-byte writes of 4 keys), and the
 // scores are formed transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16 so
 // that each lane owns one query column: the online softmax then needs only
-// two cross-lane steps for the running max, and the probabilities already sit
-// in the B-operand layout of O^T += V^T P^T (the order of keys inside an
-// MFMA's reduction is free, so V^T is read in the same key order).
+// two cross-lane steps (lane swaps) for the running max, and the
+// probabilities already sit in the B-operand layout of O^T += V^T P^T (the
+// order of keys inside an MFMA's reduction is free, so V^T is read in the
+// same key order).  The softmax is the VALU side of the loop, so it is kept
+// short: v_max3 without input quieting, the normaliser as bf16 dot products,
+// and a reference max that moves (and O is rescaled) only when a block's
+// max exceeds it by more than 2^8.
 //
 // Key chunks (bf16, few queries per sequence: decode): see
 // attend_split_kernel.  Generic path (f32): one workgroup per (query, head),
@@ -142,6 +146,30 @@ __global__ __launch_bounds__(1024) void attend_plan_kernel(const int32_t* __rest
 // ---------------------------------------------------------------------------
 // prefill MFMA kernel
 // ---------------------------------------------------------------------------
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+constexpr bf16x2_t kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
+constexpr float kLazy = 8.0f;   // log2 headroom of the reference max
+
+// max(a, b, c) in one v_max3_f32.  The scores come from MFMAs, which the
+// compiler cannot prove canonical, so fmaxf would first quiet each input
+// (one extra v_max per value); finite values and -inf need no quieting.
+__device__ __forceinline__ float max3_raw(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Max over the four lanes l, l^16, l^32, l^48 that hold one column of a
+// 16x16 MFMA result: each lane swap gives every lane its partner row's value
+// in one of its two results.
+__device__ __forceinline__ float max_column(float m) {
+  uint32_t u = __float_as_uint(m);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  m = max3_raw(m, __uint_as_float(a[0]), __uint_as_float(a[1]));
+  u = __float_as_uint(m);
+  const auto b = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return max3_raw(m, __uint_as_float(b[0]), __uint_as_float(b[1]));
+}
 // causal: keys 0..pos of each query; else keys 0..key_len[b]-1 of the
 // sequence, all of them for every query (bidirectional).  key_live
 // (nullable) drops keys whose byte is 0.
@@ -210,7 +238,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
   bool qvalid[QG];
   bf16x8_t qf[QG][DS];
   f32x4_t o[QG][DB];
-  float m_run[QG], l_run[QG];
+  float m_ref[QG], l_run[QG];
 #pragma unroll
   for (int qg = 0; qg < QG; ++qg) {
     const int qi = (wave * QG + qg) * 16 + c16;
@@ -225,7 +253,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
     }
 #pragma unroll
     for (int i = 0; i < DB; ++i) o[qg][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    m_run[qg] = -INFINITY;
+    m_ref[qg] = -INFINITY;
     l_run[qg] = 0.0f;
   }
   // smallest position among the wave's valid queries: blocks of keys at or
@@ -247,19 +275,31 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
   // key: finite values the mask gives weight 0.
   auto fK = [](int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); };
   auto fV = [](int r) { return HD == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); };
+  // Byte offsets of this lane's loads from a block's first key row: the row
+  // part (same for K and V) and the chunk part.  A block's base address is
+  // uniform, so each load is one scalar base plus one 32-bit lane offset.
+  const uint32_t rowb = (uint32_t)(rs * 2);
+  uint32_t lrow[DPW], lcol[2][DPW];
+#pragma unroll
+  for (int j = 0; j < DPW; ++j) {
+    const int r = (wave * DPW + j) * RPI + lane / NCH;
+    lrow[j] = (uint32_t)r * rowb;
+    lcol[0][j] = (uint32_t)(((lane % NCH) ^ fK(r)) * 16);
+    lcol[1][j] = (uint32_t)(((lane % NCH) ^ fV(r)) * 16);
+  }
   auto issue = [&](int kb, int u) {
     const int t0 = kb * KB;
+    // rows past the range re-read its last row (the last block only)
+    const uint32_t lim = t0 + KB > tend ? (uint32_t)(tend - 1 - t0) * rowb : 0xffffffffu;
 #pragma unroll
     for (int op = 0; op < 2; ++op) {
-      const bf16* src = op ? vc : kc;
+      const char* blk = reinterpret_cast<const char*>((op ? vc : kc) + (kbase + t0) * rs + h * HD);
 #pragma unroll
       for (int j = 0; j < DPW; ++j) {
         const int qd = wave * DPW + j;
-        const int r = qd * RPI + lane / NCH;
-        const int c = (lane % NCH) ^ (op ? fV(r) : fK(r));
-        const int t = min(t0 + r, tend - 1);
+        const uint32_t off = min(lrow[j], lim) + lcol[op][j];
         __builtin_amdgcn_global_load_lds(
-            (__attribute__((address_space(1))) void*)(src + (kbase + t) * rs + h * HD + c * 8),
+            (__attribute__((address_space(1))) void*)(blk + off),
             (__attribute__((address_space(3))) void*)(&sKV[u][op][qd * 1024]), 16, 0, 0);
       }
     }
@@ -316,28 +356,49 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
             s[qg][sb][v] = keep ? s[qg][sb][v] : -INFINITY;
           }
     }
-    bf16x8_t pb[QG][2];
-    bool grew = false;
-    float alpha[QG];
+    // ---- running max of the block per query column: each lane folds its 16
+    // scores of a group with v_max3, then the four lanes of the column
+    // (l, l^16, l^32, l^48) by two lane swaps (the max of the raw scores is
+    // taken first and scaled once: scale > 0)
+    float mblk[QG];
+    bool need = false;
 #pragma unroll
     for (int qg = 0; qg < QG; ++qg) {
-      // ---- running max (scale > 0: the max of the raw scores is taken
-      // first and scaled once)
-      float mloc = -INFINITY;
+      float m = max3_raw(s[qg][0][0], s[qg][0][1], s[qg][0][2]);
+      m = max3_raw(m, s[qg][0][3], s[qg][1][0]);
+      m = max3_raw(m, s[qg][1][1], s[qg][1][2]);
+      m = max3_raw(m, s[qg][1][3], s[qg][2][0]);
+      m = max3_raw(m, s[qg][2][1], s[qg][2][2]);
+      m = max3_raw(m, s[qg][2][3], s[qg][3][0]);
+      m = max3_raw(m, s[qg][3][1], s[qg][3][2]);
+      m = max_column(max3_raw(m, s[qg][3][3], m)) * scale_log2;
+      mblk[qg] = m;
+      // the reference max moves only when the block exceeds it by more than
+      // 2^kLazy: the weights exp2(s - m_ref) then stay below 2^kLazy, and
+      // the result (O / l, both taken against the same reference) is the same
+      need |= m > m_ref[qg] + kLazy;
+    }
+    if (__any(need)) {
 #pragma unroll
-      for (int sb = 0; sb < 4; ++sb)
-        mloc = fmaxf(fmaxf(mloc, fmaxf(s[qg][sb][0], s[qg][sb][1])),
-                     fmaxf(s[qg][sb][2], s[qg][sb][3]));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run[qg], mloc * scale_log2);
-      grew |= m_new > m_run[qg];
-      alpha[qg] = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run[qg] - m_new);
-      m_run[qg] = m_new;
-      l_run[qg] *= alpha[qg];
-      // ---- P = exp2(S * scale - m) packed as the B operand (key order:
-      // sub-block pairs); a masked score (-inf) gives exp2(-inf) = 0
-      const float msub = (m_new == -INFINITY) ? 0.0f : m_new;
+      for (int qg = 0; qg < QG; ++qg) {
+        const float m_new = fmaxf(m_ref[qg], mblk[qg]);
+        const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m_ref[qg] - m_new);
+        m_ref[qg] = m_new;
+        l_run[qg] *= alpha;
+#pragma unroll
+        for (int i = 0; i < DB; ++i)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[qg][i][v] *= alpha;
+      }
+    }
+    // ---- P = exp2(S * scale - m_ref) packed as the B operand (key order:
+    // sub-block pairs); a masked score (-inf) gives exp2(-inf) = 0.  The
+    // normaliser sums the rounded weights the MFMA multiplies (a bf16 dot
+    // product of each packed pair with (1, 1)).
+    bf16x8_t pb[QG][2];
+#pragma unroll
+    for (int qg = 0; qg < QG; ++qg) {
+      const float msub = m_ref[qg] == -INFINITY ? 0.0f : m_ref[qg];
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp) {
         uint32_t pw[4];
@@ -350,22 +411,12 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
             const float e1 =
                 __builtin_amdgcn_exp2f(fmaf(s[qg][2 * kp + hh][v + 1], scale_log2, -msub));
             const uint32_t w = pack_bf16x2(e0, e1);
-            // the normaliser sums the rounded weights the MFMA multiplies
-            l_run[qg] += __uint_as_float(w << 16) + __uint_as_float(w & 0xffff0000u);
+            l_run[qg] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), kOnes2,
+                                                        l_run[qg], false);
             pw[hh * 2 + v / 2] = w;
           }
         pb[qg][kp] = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
       }
-    }
-    // ---- rescale O only when some query's running max grew in this block
-    // (alpha = 1 otherwise: skipping the multiply changes nothing)
-    if (__any(grew)) {
-#pragma unroll
-      for (int qg = 0; qg < QG; ++qg)
-#pragma unroll
-        for (int i = 0; i < DB; ++i)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) o[qg][i][v] *= alpha[qg];
     }
     // ---- O^T += V^T P^T; each V^T fragment serves QG groups.  The A operand
     // (16 dims x 32 keys) comes from row-major V by two transpose reads: in

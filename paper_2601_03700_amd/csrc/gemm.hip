@@ -855,6 +855,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kv_grouped_kernel(GP p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int n_work = *p.n_work;
   const int total = n_work * p.tiles_n;
+  if (total == 0) return;   // nothing exited: no counter traffic
   const int chunk = (total + 7) >> 3;
   const int home = blockIdx.x & 7;
   // The item index is passed to all waves through the first word of the LDS
