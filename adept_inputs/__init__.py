@@ -21,15 +21,18 @@ import zlib
 import numpy as np
 
 __all__ = [
-    "DecoderShape", "EncoderShape", "TINY", "LLAMA7B", "BERT_BASE",
-    "rng", "to_bf16_values", "decoder_weights", "encoder_weights",
+    "DecoderShape", "EncoderShape", "TINY", "LLAMA7B", "BERT_BASE", "GPT2_XL",
+    "rng", "to_bf16_values", "decoder_weights", "gpt2_weights", "encoder_weights",
     "token_ids", "normal", "gains",
 ]
 
 
 @dataclasses.dataclass(frozen=True)
 class DecoderShape:
-    """Llama-style pre-norm decoder (RMSNorm, rotary positions, SwiGLU)."""
+    """Pre-norm decoder.  family "llama": RMSNorm, rotary positions, SwiGLU,
+    no biases, untied LM head.  family "gpt2": LayerNorm with bias (eps
+    ln_eps), learned absolute positions (max_pos), tanh-approximated GELU
+    MLP, biases on every projection, LM head tied to the token embedding."""
     n_layers: int
     d_model: int
     n_heads: int
@@ -38,6 +41,9 @@ class DecoderShape:
     vocab: int
     rms_eps: float = 1e-6
     rope_theta: float = 10000.0
+    family: str = "llama"
+    max_pos: int = 0
+    ln_eps: float = 1e-5
 
     @property
     def d_q(self) -> int:
@@ -66,6 +72,11 @@ class EncoderShape:
 # 7B-class decoder (32 layers, width 4096, 32 heads of 128, FFN 11008,
 # vocab 32000) and a BERT-base-class encoder (12 layers, width 768).
 TINY = DecoderShape(n_layers=4, d_model=256, n_heads=4, head_dim=64, d_ff=1024, vocab=1024)
+# GPT2-XL-shaped decoder: 48 layers, width 1600 = 25 heads of 64, MLP 6400,
+# 1024 positions; the vocabulary is padded from 50257 to 50304 (a multiple of
+# 64) as GPT-2 training code commonly does
+GPT2_XL = DecoderShape(n_layers=48, d_model=1600, n_heads=25, head_dim=64, d_ff=6400,
+                       vocab=50304, family="gpt2", max_pos=1024)
 LLAMA7B = DecoderShape(n_layers=32, d_model=4096, n_heads=32, head_dim=128, d_ff=11008, vocab=32000)
 BERT_BASE = EncoderShape(n_layers=12, d_model=768, n_heads=12, head_dim=64, d_ff=3072,
                          vocab=30522, max_pos=512)
@@ -139,6 +150,40 @@ def decoder_weights(shape: DecoderShape, seed: int, dtype: str = "f32", std: flo
             "w_up": normal(seed, p + "w_up", (F, D), std, dtype=dtype),
             "w_down": normal(seed, p + "w_down", (D, F), std, dtype=dtype),
         })
+    return out
+
+
+def gpt2_weights(shape: DecoderShape, seed: int, dtype: str = "f32", std: float = 0.02) -> dict:
+    """Random-init weights of a GPT-2-style decoder (family "gpt2").
+
+    Linear weights, biases and the token / position embeddings N(0, std^2)
+    in nn.Linear [out_features, in_features] order (biases and LayerNorm
+    shifts non-zero on purpose, so that a dropped one is visible); LayerNorm
+    gains 1 + 0.1 N(0,1).  The LM head is the token embedding (tied).
+    Returns {"embed", "pos_embed", "final_ln_g", "final_ln_b", "layers"} with
+    per-layer keys ln1_g, ln1_b, wq, wk, wv, bq, bk, bv, wo, bo, ln2_g, ln2_b,
+    w_fc, b_fc, w_proj, b_proj.
+    """
+    D, Dq, F, V = shape.d_model, shape.d_q, shape.d_ff, shape.vocab
+    out = {
+        "embed": normal(seed, "wte", (V, D), std, dtype=dtype),
+        "pos_embed": normal(seed, "wpe", (shape.max_pos, D), std, dtype=dtype),
+        "final_ln_g": gains(seed, "ln_f.g", (D,), dtype),
+        "final_ln_b": normal(seed, "ln_f.b", (D,), std, dtype=dtype),
+        "layers": [],
+    }
+    for i in range(1, shape.n_layers + 1):
+        p = f"h{i}."
+        lay = {}
+        for nm, shp in (("wq", (Dq, D)), ("wk", (Dq, D)), ("wv", (Dq, D)), ("wo", (D, Dq)),
+                        ("w_fc", (F, D)), ("w_proj", (D, F))):
+            lay[nm] = normal(seed, p + nm, shp, std, dtype=dtype)
+        for nm, n in (("bq", Dq), ("bk", Dq), ("bv", Dq), ("bo", D), ("b_fc", F), ("b_proj", D),
+                      ("ln1_b", D), ("ln2_b", D)):
+            lay[nm] = normal(seed, p + nm, (n,), std, dtype=dtype)
+        lay["ln1_g"] = gains(seed, p + "ln1_g", (D,), dtype)
+        lay["ln2_g"] = gains(seed, p + "ln2_g", (D,), dtype)
+        out["layers"].append(lay)
     return out
 
 

@@ -49,6 +49,8 @@ import numpy as np
 
 F64 = np.float64
 
+GPT2 = "gpt2"       # decoder family: LayerNorm with bias, learned positions, GELU, biases
+
 GLOBAL = "global"   # inertia metric, Section 4.1 Eq. 7-8
 LOCAL = "local"     # consecutive-layer metric, Appendix H.3
 BOTH = "both"       # both of them (Appendix H.3 names the combination, not its rule)
@@ -99,6 +101,13 @@ def apply_rope(x, pos, theta):
 
 def silu(x):
     return x / (1.0 + np.exp(-x))
+
+
+def gelu_tanh(x):
+    """GELU with the tanh approximation (GPT-2's MLP activation):
+    0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))."""
+    x = np.asarray(x, F64)
+    return 0.5 * x * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (x + 0.044715 * x ** 3)))
 
 
 def gelu_erf(x):
@@ -195,13 +204,31 @@ def compact(flags, active):
 # Decoupled KV generation (Section 4, Eq. 6; Section 4.3, Eq. 9).
 # ---------------------------------------------------------------------------
 
+def attn_input_norm(layer_w, shape, x):
+    """The layer's pre-attention norm: RMSNorm (llama family) or LayerNorm
+    with bias (gpt2 family)."""
+    if shape.family == GPT2:
+        return layer_norm(x, layer_w["ln1_g"], layer_w["ln1_b"], shape.ln_eps)
+    return rms_norm(x, layer_w["attn_norm"], shape.rms_eps)
+
+
+def _proj(u, layer_w, w, b, shape):
+    y = u @ layer_w[w].T
+    if shape.family == GPT2:
+        y = y + layer_w[b]
+    return y.reshape(u.shape[0], shape.n_heads, shape.head_dim)
+
+
 def layer_kv(layer_w, x, pos, shape):
-    """Layer r's own key/value path applied to input states x[n, D]:
-    K = RoPE(RMSNorm_r(x) Wk_r^T, pos), V = RMSNorm_r(x) Wv_r^T, as [n, H, hd]."""
-    n = x.shape[0]
-    u = rms_norm(x, layer_w["attn_norm"], shape.rms_eps)
-    k = (u @ layer_w["wk"].T).reshape(n, shape.n_heads, shape.head_dim)
-    v = (u @ layer_w["wv"].T).reshape(n, shape.n_heads, shape.head_dim)
+    """Layer r's own key/value path applied to input states x[n, D], as
+    [n, H, hd]: llama K = RoPE(RMSNorm_r(x) Wk_r^T, pos), V = RMSNorm_r(x) Wv_r^T;
+    gpt2 K = LN1_r(x) Wk_r^T + bk_r, V = LN1_r(x) Wv_r^T + bv_r (positions
+    enter through the embedding, not the keys)."""
+    u = attn_input_norm(layer_w, shape, x)
+    k = _proj(u, layer_w, "wk", "bk", shape)
+    v = _proj(u, layer_w, "wv", "bv", shape)
+    if shape.family == GPT2:
+        return k, v
     return apply_rope(k, pos, shape.rope_theta), v
 
 
@@ -294,22 +321,38 @@ class TokenPassResult:
 
 
 def layer_q(layer_w, shape, h_in, pos):
-    """Layer i's queries of input states h_in[n, D]: RoPE(RMSNorm_i(h_in) Wq_i^T), [n, H, hd]."""
-    n = h_in.shape[0]
-    u = rms_norm(h_in, layer_w["attn_norm"], shape.rms_eps)
-    return apply_rope((u @ layer_w["wq"].T).reshape(n, shape.n_heads, shape.head_dim), pos,
-                      shape.rope_theta)
+    """Layer i's queries of input states h_in[n, D], [n, H, hd]: llama
+    RoPE(RMSNorm_i(h_in) Wq_i^T); gpt2 LN1_i(h_in) Wq_i^T + bq_i."""
+    q = _proj(attn_input_norm(layer_w, shape, h_in), layer_w, "wq", "bq", shape)
+    if shape.family == GPT2:
+        return q
+    return apply_rope(q, pos, shape.rope_theta)
 
 
 def layer_out(layer_w, shape, h_in, o):
     """The rest of a regular layer after attention: output projection and
-    residual, then the SwiGLU FFN on its RMS-normalised input and the second
-    residual.  h_in [n, D] = h_{i-1}, o [n, H, hd] = attention output."""
+    residual, then the FFN on its normalised input and the second residual.
+    llama: RMSNorm and SwiGLU; gpt2: LayerNorm, GELU (tanh form), biases.
+    h_in [n, D] = h_{i-1}, o [n, H, hd] = attention output."""
     n = h_in.shape[0]
     h1 = np.asarray(h_in, F64) + np.asarray(o, F64).reshape(n, -1) @ layer_w["wo"].T
+    if shape.family == GPT2:
+        h1 = h1 + layer_w["bo"]
+        u2 = layer_norm(h1, layer_w["ln2_g"], layer_w["ln2_b"], shape.ln_eps)
+        ff = gelu_tanh(u2 @ layer_w["w_fc"].T + layer_w["b_fc"]) @ layer_w["w_proj"].T
+        return h1 + ff + layer_w["b_proj"]
     u2 = rms_norm(h1, layer_w["ffn_norm"], shape.rms_eps)
     ff = (silu(u2 @ layer_w["w_gate"].T) * (u2 @ layer_w["w_up"].T)) @ layer_w["w_down"].T
     return h1 + ff
+
+
+def embed_rows(weights, shape, ids, pos):
+    """h_0 of token rows: the token embedding, plus the learned position
+    embedding for the gpt2 family."""
+    h0 = np.asarray(weights["embed"], F64)[np.asarray(ids)]
+    if shape.family == GPT2:
+        h0 = h0 + np.asarray(weights["pos_embed"], F64)[np.asarray(pos)]
+    return h0
 
 
 def decoder_layer(layer_w, shape, h_in, pos, seq, cache, layer):
@@ -327,8 +370,12 @@ def decoder_layer(layer_w, shape, h_in, pos, seq, cache, layer):
 
 
 def lm_logits(weights, shape, h_final):
-    """Final RMSNorm and LM head of final states h_final[n, D] (an exited
-    token's final state is its mapped state, Fig. 1 caption)."""
+    """Final norm and LM head of final states h_final[n, D] (an exited
+    token's final state is its mapped state, Fig. 1 caption): llama RMSNorm
+    and an untied head; gpt2 LayerNorm and the token embedding as the head."""
+    if shape.family == GPT2:
+        u = layer_norm(h_final, weights["final_ln_g"], weights["final_ln_b"], shape.ln_eps)
+        return u @ np.asarray(weights["embed"], F64).T
     return rms_norm(h_final, weights["final_norm"], shape.rms_eps) @ weights["lm_head"].T
 
 
@@ -409,7 +456,7 @@ def prefill(weights, shape, ids, cfg, s_max=None, force_layer=None, mapper=None)
     cache = KVCache.empty(shape, B, s_max)
     pos = np.tile(np.arange(T), B)
     seq = np.repeat(np.arange(B), T)
-    h0 = np.asarray(weights["embed"], F64)[ids.reshape(-1)]
+    h0 = embed_rows(weights, shape, ids.reshape(-1), pos)
     res = token_pass(weights, shape, h0, pos, seq, cache, cfg,
                      None if force_layer is None else np.asarray(force_layer).reshape(-1),
                      mapper=mapper)
@@ -426,7 +473,7 @@ def decode_step(weights, shape, cache, ids, pos, cfg, force_layer=None, mapper=N
     at position pos[b] of sequence b; inertia starts empty for the new token."""
     ids = np.asarray(ids)
     B = ids.shape[0]
-    h0 = np.asarray(weights["embed"], F64)[ids]
+    h0 = embed_rows(weights, shape, ids, pos)
     return token_pass(weights, shape, h0, np.asarray(pos), np.arange(B), cache, cfg, force_layer,
                       mapper=mapper)
 

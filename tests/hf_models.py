@@ -70,3 +70,38 @@ def bert(shape, weights, n_layers=None):
             L.output.LayerNorm.weight.copy_(_t(lw["ln2_g"]))
             L.output.LayerNorm.bias.copy_(_t(lw["ln2_b"]))
     return m
+
+
+def gpt2(shape, weights, n_layers=None):
+    """transformers' GPT2LMHeadModel (tanh GELU, LayerNorm with bias, learned
+    positions, head tied to the token embedding) with the seeded weights;
+    Conv1D layers hold their weight as [in, out], the transpose of ours."""
+    from transformers import GPT2Config, GPT2LMHeadModel
+    n_layers = shape.n_layers if n_layers is None else n_layers
+    cfg = GPT2Config(vocab_size=shape.vocab, n_positions=shape.max_pos, n_embd=shape.d_model,
+                     n_layer=n_layers, n_head=shape.n_heads, n_inner=shape.d_ff,
+                     activation_function="gelu_new", resid_pdrop=0.0, embd_pdrop=0.0,
+                     attn_pdrop=0.0, layer_norm_epsilon=shape.ln_eps, tie_word_embeddings=True,
+                     attn_implementation="eager")
+    m = GPT2LMHeadModel(cfg).double().eval()
+    with torch.no_grad():
+        m.transformer.wte.weight.copy_(_t(weights["embed"]))
+        m.transformer.wpe.weight.copy_(_t(weights["pos_embed"]))
+        m.transformer.ln_f.weight.copy_(_t(weights["final_ln_g"]))
+        m.transformer.ln_f.bias.copy_(_t(weights["final_ln_b"]))
+        for i in range(n_layers):
+            lw, L = weights["layers"][i], m.transformer.h[i]
+            L.ln_1.weight.copy_(_t(lw["ln1_g"]))
+            L.ln_1.bias.copy_(_t(lw["ln1_b"]))
+            L.ln_2.weight.copy_(_t(lw["ln2_g"]))
+            L.ln_2.bias.copy_(_t(lw["ln2_b"]))
+            wqkv = np.concatenate([lw["wq"], lw["wk"], lw["wv"]], axis=0)
+            L.attn.c_attn.weight.copy_(_t(wqkv.T))
+            L.attn.c_attn.bias.copy_(_t(np.concatenate([lw["bq"], lw["bk"], lw["bv"]])))
+            L.attn.c_proj.weight.copy_(_t(np.asarray(lw["wo"]).T))
+            L.attn.c_proj.bias.copy_(_t(lw["bo"]))
+            L.mlp.c_fc.weight.copy_(_t(np.asarray(lw["w_fc"]).T))
+            L.mlp.c_fc.bias.copy_(_t(lw["b_fc"]))
+            L.mlp.c_proj.weight.copy_(_t(np.asarray(lw["w_proj"]).T))
+            L.mlp.c_proj.bias.copy_(_t(lw["b_proj"]))
+    return m
