@@ -23,6 +23,7 @@ import numpy as np
 __all__ = [
     "DecoderShape", "EncoderShape", "TINY", "LLAMA7B", "BERT_BASE", "GPT2_XL",
     "rng", "to_bf16_values", "decoder_weights", "gpt2_weights", "encoder_weights",
+    "decoder_weights_torch", "gpt2_weights_torch",
     "token_ids", "normal", "gains",
 ]
 
@@ -221,6 +222,33 @@ def encoder_weights(shape: EncoderShape, seed: int, dtype: str = "f32", std: flo
     return out
 
 
+def _torch_fillers(seed, device, dtype, n_layers):
+    """(single, stacked): N(mean, scale^2) tensors on `device` from torch's
+    counter-based generator, seeded per name (and per layer for stacked
+    [n_layers, ...] tensors, "layer{i}.{name}"), so any slice can be
+    regenerated alone."""
+    import torch
+    g = torch.Generator(device=device)
+
+    def fill(out, name, scale, mean):
+        g.manual_seed((seed * 1000003 + zlib.crc32(name.encode())) & 0x7FFFFFFFFFFFFFFF)
+        tmp = torch.randn(out.shape, generator=g, device=device, dtype=torch.float32)
+        out.copy_(tmp.mul_(scale).add_(mean))
+
+    def stacked(name, shp, scale, mean=0.0):
+        out = torch.empty((n_layers,) + shp, dtype=dtype, device=device)
+        for i in range(n_layers):
+            fill(out[i], f"layer{i + 1}.{name}", scale, mean)
+        return out
+
+    def single(name, shp, scale, mean=0.0):
+        out = torch.empty(shp, dtype=dtype, device=device)
+        fill(out, name, scale, mean)
+        return out
+
+    return single, stacked
+
+
 def decoder_weights_torch(shape: DecoderShape, seed: int, device, dtype=None, std: float = 0.02):
     """Random-init decoder weights generated directly on `device` (torch's
     counter-based generator), stacked over layers: attn_norm/ffn_norm [N, D],
@@ -232,25 +260,8 @@ def decoder_weights_torch(shape: DecoderShape, seed: int, device, dtype=None, st
     """
     import torch
     dtype = torch.bfloat16 if dtype is None else dtype
-    g = torch.Generator(device=device)
     N, D, Dq, F, V = shape.n_layers, shape.d_model, shape.d_q, shape.d_ff, shape.vocab
-
-    def fill(out, name, scale, mean):
-        g.manual_seed((seed * 1000003 + zlib.crc32(name.encode())) & 0x7FFFFFFFFFFFFFFF)
-        tmp = torch.randn(out.shape, generator=g, device=device, dtype=torch.float32)
-        out.copy_(tmp.mul_(scale).add_(mean))
-
-    def stacked(name, shp, scale, mean=0.0):
-        out = torch.empty((N,) + shp, dtype=dtype, device=device)
-        for i in range(N):
-            fill(out[i], f"layer{i + 1}.{name}", scale, mean)
-        return out
-
-    def single(name, shp, scale, mean=0.0):
-        out = torch.empty(shp, dtype=dtype, device=device)
-        fill(out, name, scale, mean)
-        return out
-
+    single, stacked = _torch_fillers(seed, device, dtype, N)
     return {
         "embed": single("embed", (V, D), std),
         "final_norm": single("final_norm", (D,), 0.1, 1.0),
@@ -265,6 +276,33 @@ def decoder_weights_torch(shape: DecoderShape, seed: int, device, dtype=None, st
         "w_up": stacked("w_up", (F, D), std),
         "w_down": stacked("w_down", (D, F), std),
     }
+
+
+def gpt2_weights_torch(shape: DecoderShape, seed: int, device, dtype=None, std: float = 0.02):
+    """gpt2_weights() drawn directly on `device` (torch's generator, as
+    decoder_weights_torch), stacked over layers: ln1_g/ln1_b/ln2_g/ln2_b,
+    bo/b_proj [N, D], wq/wk/wv [N, Dq, D], bq/bk/bv [N, Dq], wo [N, D, Dq],
+    w_fc [N, F, D], b_fc [N, F], w_proj [N, D, F]; embed [V, D] (also the
+    head), pos_embed [max_pos, D], final_ln_g/final_ln_b [D].  For the
+    GPT2-XL shape, whose 1.5 G weights are slow to draw on the host."""
+    import torch
+    dtype = torch.bfloat16 if dtype is None else dtype
+    N, D, Dq, F, V = shape.n_layers, shape.d_model, shape.d_q, shape.d_ff, shape.vocab
+    single, stacked = _torch_fillers(seed, device, dtype, N)
+    out = {
+        "embed": single("wte", (V, D), std),
+        "pos_embed": single("wpe", (shape.max_pos, D), std),
+        "final_ln_g": single("ln_f.g", (D,), 0.1, 1.0),
+        "final_ln_b": single("ln_f.b", (D,), std),
+    }
+    for nm, shp in (("wq", (Dq, D)), ("wk", (Dq, D)), ("wv", (Dq, D)), ("wo", (D, Dq)),
+                    ("w_fc", (F, D)), ("w_proj", (D, F)), ("bq", (Dq,)), ("bk", (Dq,)),
+                    ("bv", (Dq,)), ("bo", (D,)), ("b_fc", (F,)), ("b_proj", (D,)),
+                    ("ln1_b", (D,)), ("ln2_b", (D,))):
+        out[nm] = stacked(nm, shp, std)
+    out["ln1_g"] = stacked("ln1_g", (D,), 0.1, 1.0)
+    out["ln2_g"] = stacked("ln2_g", (D,), 0.1, 1.0)
+    return out
 
 
 def hsm_weights(d_model: int, seed: int, dtype: str = "f32", std: float = 0.02) -> dict:

@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define ADEPT_ABI_VERSION 3
+#define ADEPT_ABI_VERSION 4
 
 typedef enum {
   ADEPT_OK = 0,
@@ -48,6 +48,13 @@ typedef enum {
 } adept_status;
 
 typedef enum { ADEPT_F32 = 0, ADEPT_BF16 = 1 } adept_dtype;
+
+/* Decoder family of adept_layer_step (the paper's base models, Section 5):
+ * LLAMA: RMSNorm, rotary positions, SwiGLU FFN, no biases;
+ * GPT2: LayerNorm with bias, learned absolute positions (added by
+ * adept_embed_positions), tanh-GELU MLP, biases on every projection, LM head
+ * tied to the token embedding (the GPT2-XL shape). */
+typedef enum { ADEPT_FAMILY_LLAMA = 0, ADEPT_FAMILY_GPT2 = 1 } adept_family;
 
 /* Exit metric: GLOBAL compares h_i with the inertia of Section 4.1 (Eq. 7-8);
  * LOCAL compares h_i with h_{i-1} (the "local" metric of Appendix H.3);
@@ -236,6 +243,34 @@ adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_model, int n_
                                size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * adept_kv_generate_layernorm -- decoupled KV generation (Section 4, Eq. 6;
+ * Section 4.3, Eq. 9) for the LayerNorm family: for every listed row j and
+ * every skipped layer r with exit_layer[j] < r <= n_layers, s = s_map[j]:
+ *     xh  = (s - mean(s)) / sqrt(var(s) + eps)            (no affine part)
+ *     K[r][cache_slot[j]] = xh Wk'_r^T + bk'_r,   V[r][cache_slot[j]] = xh Wv'_r^T + bv'_r
+ * where W'_r carries layer r's LayerNorm gain in its columns and b'_r its
+ * shift, b'_r = b_r + W_r beta_r (adept_fold_gain, adept_fold_bias): this is
+ * layer r's own LayerNorm and K/V projection applied to s.  No RoPE (the
+ * family's positions enter through the embedding).  One grouped GEMM.
+ *
+ *  w_kv: layer r's block at w_kv + (r-1)*w_kv_layer_stride elements,
+ *        [2*H*hd][d_model] (K rows then V rows); b_kv: layer r's [2*H*hd] bias
+ *        at b_kv + (r-1)*b_kv_layer_stride.  Other arguments as for
+ *        adept_kv_generate.  bf16; d_model % 64 == 0, H*hd % 32 == 0;
+ *  workspace: adept_kv_generate_layernorm_workspace_bytes(n_layers, max_rows,
+ *        d_model) bytes (the plan plus the normalised rows), 16-byte aligned.
+ * ------------------------------------------------------------------------- */
+size_t adept_kv_generate_layernorm_workspace_bytes(int n_layers, int max_rows, int d_model);
+adept_status adept_kv_generate_layernorm(adept_dtype dt, int n_layers, int d_model, int n_heads,
+                                         int head_dim, float eps, const void* s_map,
+                                         const int32_t* rows, const int32_t* n_rows, int max_rows,
+                                         const int32_t* exit_layer, const int32_t* cache_slot,
+                                         const void* w_kv, int64_t w_kv_layer_stride,
+                                         const void* b_kv, int64_t b_kv_layer_stride,
+                                         void* k_cache, void* v_cache, int64_t n_slots,
+                                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * adept_kv_generate_noalloc -- adept_kv_generate for callers that cannot
  * allocate device memory (code under HIP graph capture, serving loops,
  * harnesses that forbid hipMalloc): same arguments and results, minus the
@@ -292,7 +327,9 @@ adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale
 
 /* ---------------------------------------------------------------------------
  * Whole-layer orchestration of the generative path (Appendix I):
- * adept_layer_step(layer=i) enqueues, for the rows of active[(i-1)&1]:
+ * adept_layer_step(layer=i) enqueues, for the rows of active[(i-1)&1]
+ * (LLAMA family; GPT2: LayerNorm for the norms, biased projections without
+ * RoPE, tanh-GELU MLP, adept_kv_generate_layernorm for the generation):
  *   RMSNorm -> QKV GEMM (+RoPE; own K/V into cache[i]) -> adept_attend ->
  *   O GEMM (+residual: h[i&1] = h[(i-1)&1] + o Wo^T) -> RMSNorm ->
  *   gate/up GEMM (+SwiGLU) -> down GEMM (+residual) -> adept_exit_test ->
@@ -359,6 +396,17 @@ typedef struct {
    * h[i&1] before their K/V are generated (bf16, GLOBAL or BOTH metric: it
    * reads the inertia) */
   const adept_hsm_weights* hsm;
+  /* decoder family (adept_family).  GPT2 (bf16): rms_eps is the LayerNorm
+   * eps; the layer norms run without their affine part, whose gains are
+   * folded into w_qkv (LN1) and w_gate (LN2) and whose shifts into b_qkv and
+   * b_fc; w_gate holds the MLP's first projection W_fc [N][F][D], w_down its
+   * second W_proj [N][D][F], w_up and the rotary table are unused (NULL);
+   * d_model, H*hd and F multiples of 64 */
+  int32_t family;
+  const void* b_qkv;    /* [N][3*H*hd] (GPT2) */
+  const void* b_o;      /* [N][D] */
+  const void* b_fc;     /* [N][F] */
+  const void* b_proj;   /* [N][D] */
 } adept_layer_args;
 
 size_t adept_layer_workspace_bytes(const adept_layer_args* a);
@@ -373,6 +421,34 @@ adept_status adept_layer_step(const adept_layer_args* a, int layer, void* stream
 adept_status adept_fold_gain(adept_dtype dt, int n_mats, int rows, int cols, void* w,
                              int64_t mat_stride, const void* gain, int64_t gain_stride,
                              void* stream);
+
+/* Folds a LayerNorm shift into the bias of the projection that consumes the
+ * normalised vector, in place: bias[l][o] += sum_c w[l][o][c] * shift[l][c]
+ * for l < n_mats, o < rows (w unfolded: run before adept_fold_gain), with
+ * matrix l at w + l*mat_stride, its shift at shift + l*shift_stride and its
+ * bias at bias + l*bias_stride (elements).  (xh g + beta) W^T + b =
+ * xh (W diag g)^T + (b + W beta).  Done once at model load. */
+adept_status adept_fold_bias(adept_dtype dt, int n_mats, int rows, int cols, const void* w,
+                             int64_t mat_stride, const void* shift, int64_t shift_stride,
+                             void* bias, int64_t bias_stride, void* stream);
+
+/* Embedding with learned absolute positions (GPT2 family, before layer 1):
+ * h0[k] = wte[ids[k]] + wpe[pos[k]] (ids and positions clamped into the
+ * tables), wte [vocab][D], wpe [max_pos][D], h0 [n][D] (dtype). */
+adept_status adept_embed_positions(adept_dtype dt, int n, int d_model, int vocab, int max_pos,
+                                   const int32_t* ids, const int32_t* pos, const void* wte,
+                                   const void* wpe, void* h0, void* stream);
+
+/* Final LayerNorm (with gain and shift) and LM head of the GPT2 family, as
+ * adept_final_logits: logits[k] = LN(h[exit_layer[row] & 1][row]; ln_g, ln_b)
+ * lm_head^T (lm_head: the token embedding when tied).  bf16; d_model and
+ * vocab multiples of 64. */
+adept_status adept_final_logits_layernorm(adept_dtype dt, int d_model, int vocab, float eps,
+                                          const void* h0_buf, const void* h1_buf,
+                                          const int32_t* exit_layer, const int32_t* rows,
+                                          const int32_t* n_rows, int max_rows, const void* ln_g,
+                                          const void* ln_b, const void* lm_head, void* x_norm,
+                                          float* logits, void* stream);
 
 /* Embedding gather (support step before layer 1): h0[k] = embed[ids[k]],
  * k < n; embed [vocab][D] (dtype), h0 [n][D] (dtype). */

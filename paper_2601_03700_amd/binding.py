@@ -16,6 +16,7 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadept.so")
 
 F32, BF16 = 0, 1
+FAMILY_LLAMA, FAMILY_GPT2 = 0, 1
 SIM_GLOBAL, SIM_LOCAL, SIM_BOTH = 0, 1, 2
 METRICS = {"global": SIM_GLOBAL, "local": SIM_LOCAL, "both": SIM_BOTH}
 
@@ -55,6 +56,7 @@ class LayerArgs(ctypes.Structure):
         ("k_cache", _vp), ("v_cache", _vp), ("n_slots", _i64),
         ("q_buf", _vp), ("attn_out", _vp), ("ffn_act", _vp),
         ("workspace", _vp), ("workspace_bytes", _sz), ("hsm", _vp),
+        ("family", _i32), ("b_qkv", _vp), ("b_o", _vp), ("b_fc", _vp), ("b_proj", _vp),
     ]
 
 
@@ -95,6 +97,14 @@ _SIGS = {
     "adept_kv_generate_noalloc": (_i32, [_i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp,
                                          _vp, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i32,
                                          _vp, _vp, _i64, _vp]),
+    "adept_kv_generate_layernorm_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "adept_kv_generate_layernorm": (_i32, [_i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp,
+                                           _vp, _i32, _vp, _vp, _vp, _i64, _vp, _i64, _vp, _vp,
+                                           _i64, _vp, _sz, _vp]),
+    "adept_fold_bias": (_i32, [_i32, _i32, _i32, _i32, _vp, _i64, _vp, _i64, _vp, _i64, _vp]),
+    "adept_embed_positions": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "adept_final_logits_layernorm": (_i32, [_i32, _i32, _i32, ctypes.c_float, _vp, _vp, _vp, _vp,
+                                            _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
     "adept_attend_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32]),
     "adept_attend": (_i32, [_i32, _i32, _i32, ctypes.c_float, _i32, _vp, _vp, _vp, _i32, _vp,
                             _vp, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -268,6 +278,52 @@ def kv_generate_noalloc(n_layers, d_model, n_heads, head_dim, eps, s_map, rows, 
                                            ptr(k_cache), ptr(v_cache), n_slots,
                                            stream_handle(stream)),
            "adept_kv_generate_noalloc")
+
+
+def kv_generate_layernorm_workspace_bytes(n_layers, max_rows, d_model):
+    return lib().adept_kv_generate_layernorm_workspace_bytes(n_layers, max_rows, d_model)
+
+
+def kv_generate_layernorm(n_layers, d_model, n_heads, head_dim, eps, s_map, rows, n_rows,
+                          max_rows, exit_layer, cache_slot, w_kv, w_kv_layer_stride, b_kv,
+                          b_kv_layer_stride, k_cache, v_cache, n_slots, workspace=None,
+                          stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().adept_kv_generate_layernorm(dtype_code(s_map), n_layers, d_model, n_heads,
+                                             head_dim, eps, ptr(s_map), ptr(rows), ptr(n_rows),
+                                             max_rows, ptr(exit_layer), ptr(cache_slot),
+                                             ptr(w_kv), w_kv_layer_stride, ptr(b_kv),
+                                             b_kv_layer_stride, ptr(k_cache), ptr(v_cache),
+                                             n_slots, ptr(workspace), ws_bytes,
+                                             stream_handle(stream)),
+           "adept_kv_generate_layernorm")
+
+
+def fold_bias(w, shift, bias, stream=None):
+    """In place: bias[l][o] += sum_c w[l][o][c] * shift[l][c] for a stacked
+    w [L, rows, cols] (rows contiguous), shift [L, cols] and bias [L, rows]
+    (row views with unit column stride)."""
+    L, rows, cols = w.shape
+    assert w.stride(2) == 1 and (rows == 1 or w.stride(1) == cols)
+    assert shift.stride(-1) == 1 and bias.stride(-1) == 1 and bias.shape[-1] == rows
+    _check(lib().adept_fold_bias(dtype_code(w), L, rows, cols, ptr(w), w.stride(0), ptr(shift),
+                                 shift.stride(0), ptr(bias), bias.stride(0),
+                                 stream_handle(stream)), "adept_fold_bias")
+
+
+def embed_positions(n, d_model, vocab, max_pos, ids, pos, wte, wpe, h0, stream=None):
+    _check(lib().adept_embed_positions(dtype_code(wte), n, d_model, vocab, max_pos, ptr(ids),
+                                       ptr(pos), ptr(wte), ptr(wpe), ptr(h0),
+                                       stream_handle(stream)), "adept_embed_positions")
+
+
+def final_logits_layernorm(d_model, vocab, eps, h0, h1, exit_layer, rows, n_rows, max_rows, ln_g,
+                           ln_b, lm_head, x_norm, logits, stream=None):
+    _check(lib().adept_final_logits_layernorm(dtype_code(h0), d_model, vocab, eps, ptr(h0),
+                                              ptr(h1), ptr(exit_layer), ptr(rows), ptr(n_rows),
+                                              max_rows, ptr(ln_g), ptr(ln_b), ptr(lm_head),
+                                              ptr(x_norm), ptr(logits), stream_handle(stream)),
+           "adept_final_logits_layernorm")
 
 
 def attend_workspace_bytes(max_active, n_seq, n_heads, head_dim, s_max):

@@ -206,10 +206,10 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
   __shared__ uint64_t sLive[2];
 
   // Work item of this workgroup.  The hardware deals consecutive workgroup
-  // ids round-robin to the 8 XCDs; when the heads split evenly over them
-  // (1-D grid), XCD x takes heads x, x+8, ... one after another, each head's
-  // tiles longest first, so the tiles in flight on an XCD share a few
-  // sequences' K/V in its L2.  Otherwise blockIdx = (tile, head).
+  // ids round-robin to the 8 XCDs; with several heads (1-D grid, heads
+  // padded to a multiple of 8), XCD x takes heads x, x+8, ... one after
+  // another, each head's tiles longest first, so the tiles in flight on an
+  // XCD share a few sequences' K/V in its L2.  One head: blockIdx.x = tile.
   const int nt = *n_tiles;
   int ti, h;
   if (gridDim.y == 1 && H > 1) {
@@ -324,7 +324,10 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
     const char* cK = sKV[u][0];
     const char* cV = sKV[u][1];
 
-    // ---- S^T = K Q^T: 4 key sub-blocks of 16; each K fragment serves QG groups
+    // ---- S^T = K Q^T: 4 key sub-blocks of 16; each K fragment serves QG groups.
+    // The matrix phases run at a raised wave priority, so the SIMD's other
+    // wave (in its softmax) takes the issue slots the MFMAs leave free.
+    __builtin_amdgcn_s_setprio(1);
     f32x4_t s[QG][4];
 #pragma unroll
     for (int sb = 0; sb < 4; ++sb) {
@@ -340,6 +343,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
           s[qg][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qg][ds], s[qg][sb], 0, 0, 0);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     // ---- mask (only blocks that reach past a query's position, past the
     // range, or under a live-key mask), in the exp2 domain
     const bool full = !key_live && t0 + KB <= tend && t0 + KB - 1 <= wmin;
@@ -418,6 +422,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
         pb[qg][kp] = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
       }
     }
+    __builtin_amdgcn_s_setprio(1);
     // ---- O^T += V^T P^T; each V^T fragment serves QG groups.  The A operand
     // (16 dims x 32 keys) comes from row-major V by two transpose reads: in
     // each 16-lane group, source lane L reads 4 dims of key k0 + L/4 and
@@ -441,6 +446,7 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
         for (int qg = 0; qg < QG; ++qg)
           o[qg][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qg][kp], o[qg][db], 0, 0, 0);
       }
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();   // stage kb+1 landed (every wave waited for its loads); stage u retired
   }
 #pragma unroll
@@ -693,8 +699,10 @@ adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float sc
     ADEPT_LAUNCH(attend_plan_kernel, dim3(1), dim3(1024), 2 * (n_seq + 1) * sizeof(int), s,
                  rows, n_active, max_active, seq, n_seq, tiles, n_tiles);
     ADEPT_CHECK_LAUNCH("attend_plan");
-    // heads that split evenly over the 8 XCDs: 1-D grid, XCD-major order
-    const dim3 grid = n_heads % 8 == 0 ? dim3(max_tiles * n_heads) : dim3(max_tiles, n_heads);
+    // more than one head: 1-D grid in XCD-major order, the heads padded to a
+    // multiple of 8 (the padding's workgroups return at once)
+    const int h8 = (n_heads + 7) / 8 * 8;
+    const dim3 grid = n_heads > 1 ? dim3(max_tiles * h8) : dim3(max_tiles, 1);
     if (head_dim == 128)
       ADEPT_LAUNCH(attend_prefill_kernel<128>, grid, dim3(kPrefillThreads), 0, s, n_heads, sl, causal,
                    (const bf16*)q, rows, pos, seq, (const bf16*)k_layer, (const bf16*)v_layer,

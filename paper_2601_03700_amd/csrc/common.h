@@ -139,6 +139,7 @@ enum EpiKind {
   EPI_SWIGLU = 3,  // B = (gate, up) interleaved per 64 columns; out[k][n] = silu(g) * u
   EPI_KV = 4,      // K/V-only variant of EPI_QKV (KV generation, per-layer groups)
   EPI_GELU = 5,    // C[k][n] = gelu(acc) (exact erf form), dtype
+  EPI_GELU_TANH = 6,  // C[k][n] = gelu(acc) (tanh approximation), dtype
 };
 
 struct GemmArgs {
@@ -167,6 +168,9 @@ struct GemmArgs {
   // f32 workspace of the skinny path (M_max <= 64: decode), nullable; used
   // when at least skinny_ws_bytes(N or 2N for SWIGLU, K) bytes
   float* skinny_ws; size_t skinny_ws_bytes;
+  // grouped KV generation: per-layer bias stride, and A already in the
+  // sorted row order (pre-normalised rows) instead of gathered by token row
+  int64_t bias_layer_stride; int a_sorted;
 };
 size_t skinny_ws_bytes(int n_cols, int K);
 
@@ -193,5 +197,12 @@ adept_status row_rinv(adept_dtype dt, int d, float eps, const void* x, const int
 adept_status rmsnorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
                               const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
                               int max_n, const void* gain, void* out, hipStream_t s);
+// LayerNorm of gathered rows into a compact buffer (csrc/layernorm.hip):
+// out[k] = (x - mean) / sqrt(var + eps) [* gain + bias] (gain NULL: no affine
+// part), x = x1[row] when sel && (sel[row] & 1), else x0[row]; row = rows ? rows[k] : k.
+adept_status layernorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
+                                const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
+                                int max_n, const void* gain, const void* bias, void* out,
+                                hipStream_t s);
 
 }  // namespace adept

@@ -103,6 +103,8 @@ struct GP {
   const int32_t* srows;     // exited rows sorted by exit layer
   int64_t b_layer_stride;
   int64_t cache_layer_stride;
+  int64_t bias_layer_stride; // grouped: layer r's bias at bias + (r-1) * stride
+  int a_sorted;             // grouped: A holds the rows in sorted order (row m), not by token
 };
 
 // x * sigmoid(x) with the hardware reciprocal (about 1 ulp in f32, far below
@@ -114,6 +116,11 @@ __device__ __forceinline__ float silu(float g) {
 // x * Phi(x) with the exact erf form of the normal CDF
 __device__ __forceinline__ float gelu_erf(float x) {
   return 0.5f * x * (1.0f + erff(x * 0.7071067811865476f));
+}
+
+// x * Phi(x) with the tanh approximation of the normal CDF (GPT-2's MLP)
+__device__ __forceinline__ float gelu_tanh(float x) {
+  return 0.5f * x * (1.0f + tanhf(0.7978845608028654f * fmaf(0.044715f * x, x * x, x)));
 }
 
 // Four bias values of columns c..c+3 (zeros when there is no bias).
@@ -191,7 +198,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     const int lchunk = (lane & 7) ^ ((4 * q + (lane >> 4)) & 7);
     int m = m0 + r;
     if (m >= M) m = m0;  // clamp: loaded, never stored
-    const int arow = GROUPED ? p.srows[m] : (p.a_rows ? p.a_rows[m] : m);
+    const int arow = GROUPED ? (p.a_sorted ? m : p.srows[m]) : (p.a_rows ? p.a_rows[m] : m);
     a_src[j] = p.A + (int64_t)arow * p.lda + lchunk * 8;
     const bf16* bbase = Bm;
     int64_t brow;
@@ -200,7 +207,8 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
       bbase = within < 64 ? p.B : p.B2;
       brow = (int64_t)nt * 128 + half * 64 + (within & 63);
     } else {
-      brow = (int64_t)nt * BN + r;
+      // a ragged last column tile re-reads the last row: computed, never stored
+      brow = min((int64_t)nt * BN + r, (int64_t)p.N - 1);
     }
     b_src[j] = bbase + brow * p.ldb + lchunk * 8;
   }
@@ -225,7 +233,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
         pre_row[h] = p.rows[mc];
       } else if (kC) {
         const int row = GROUPED ? p.srows[mc] : p.rows[mc];
-        pre_row[h] = q_sec ? 0 : (p.slot ? p.slot[row] : row);
+        pre_row[h] = (q_sec && p.d_q % 128 == 0) ? 0 : (p.slot ? p.slot[row] : row);
         pre_pos[h] = (v_sec || !p.rope_cos) ? 0 : p.pos[row];
       }
     }
@@ -435,6 +443,11 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   const int row_q = 4 * (lane >> 5);
   const int c4 = (lane & 31) * 4;         // first of the lane's 4 columns (wave space)
   const int nw = nt * BN + wn * 128;      // first output column of this wave
+  // grouped: layer r's bias; a ragged column tile's waves past N store
+  // nothing (SwiGLU tiles are never ragged: 128 outputs of N per tile)
+  const bf16* bias = GROUPED && p.bias ? p.bias + (int64_t)(layer - 1) * p.bias_layer_stride
+                                       : p.bias;
+  const bool wave_out = EPI != EPI_SWIGLU && nw >= p.N;
   constexpr bool kCache = EPI == EPI_QKV || EPI == EPI_KV;
   const int sec = kCache ? nw / p.d_q : 0;    // QKV: 0 q, 1 k, 2 v;  KV: 0 k, 1 v
   const bool is_q = EPI == EPI_QKV && sec == 0;
@@ -465,7 +478,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   auto block = [&](auto ic) {
     constexpr int i = decltype(ic)::value;
     const int mb = m0 + wm * 128 + i * 32;   // first row of the block
-    if (mb >= M) return;                      // the wave's remaining rows are past M
+    if (mb >= M || wave_out) return;          // rows past M / columns past N
     if constexpr (EPI == EPI_SWIGLU) {
       // Gate (blocks j = 0, 1) and up (j = 2, 3) of an output column sit in
       // the same lane, so h = silu(g) * u is formed in registers; lanes 2k
@@ -618,7 +631,8 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     }
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_wave_barrier();
-    if constexpr (EPI == EPI_RESID || EPI == EPI_STORE || EPI == EPI_GELU) {
+    if constexpr (EPI == EPI_RESID || EPI == EPI_STORE || EPI == EPI_GELU ||
+                  EPI == EPI_GELU_TANH) {
       if (EPI != EPI_STORE || !p.c_f32) {   // wave-uniform
         // Row-segment form: 16 lanes per row, 8 consecutive columns per lane
         // (two 16-byte LDS reads of the staged f32 row), so the residual
@@ -628,6 +642,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
         const bool full = mb + 32 <= M;
         const int sg = lane & 15;
         const int col = nw + 8 * sg;
+        const bool col_in = col < p.N;   // N is a multiple of 64: whole 8-column segments
         int drow[8];
         float scv[8];
 #pragma unroll
@@ -641,13 +656,14 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
             const int m = mb + 4 * q + (lane >> 4);
-            rres[q] = (full || m < M) ? *reinterpret_cast<const uint4*>(
+            rres[q] = ((full || m < M) && col_in) ? *reinterpret_cast<const uint4*>(
                                             reinterpret_cast<const bf16*>(p.resid) +
                                             (int64_t)drow[q] * p.ldc + col)
                                       : make_uint4(0, 0, 0, 0);
           }
         }
-        const float4 b0 = bias4(p.bias, col), b1 = bias4(p.bias, col + 4);
+        const float4 b0 = bias4(col_in ? bias : nullptr, col);
+        const float4 b1 = bias4(col_in ? bias : nullptr, col + 4);
         const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
@@ -661,6 +677,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
           for (int e = 0; e < 8; ++e) {
             x[e] = f[e] * scv[q] + bv[e];
             if constexpr (EPI == EPI_GELU) x[e] = gelu_erf(x[e]);
+            if constexpr (EPI == EPI_GELU_TANH) x[e] = gelu_tanh(x[e]);
           }
           if constexpr (EPI == EPI_RESID) {
             const uint32_t rw[4] = {rres[q].x, rres[q].y, rres[q].z, rres[q].w};
@@ -672,7 +689,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
           }
           const uint4 o = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
                                      pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7]));
-          if (full || m < M)
+          if ((full || m < M) && col_in)
             *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + (int64_t)drow[q] * p.ldc +
                                       col) = o;
         }
@@ -720,8 +737,18 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
         constexpr bool kRope = EPI == EPI_QKV || EPI == EPI_KV;
         constexpr int G = kRope ? 4 : 8;
         const bool rope = kRope && !is_v && p.rope_cos;   // wave-uniform
-        const float4 bx = bias4(p.bias, nw + c4);
-        const float4 by = rope ? bias4(p.bias, nw + (c4 ^ half)) : bx;
+        const bool col_in = nw + c4 < p.N;                // N is a multiple of 4
+        const float4 bx = bias4(col_in ? bias : nullptr, nw + c4);
+        const float4 by = rope ? bias4(bias, nw + (c4 ^ half)) : bx;
+        // cache epilogues without RoPE take the section per lane: with d_q
+        // not a multiple of 128 a wave's columns can span Q and K (or K and V)
+        const int secl = kRope ? (nw + c4) / p.d_q : 0;
+        const int cinl = nw + c4 - secl * p.d_q;
+        const bool lq = EPI == EPI_QKV && secl == 0;
+        const bool lv = EPI == EPI_QKV ? secl == 2 : (EPI == EPI_KV && secl == 1);
+        bf16* ldst = lq ? p.q_out
+                        : (lv ? p.v_cache : p.k_cache) +
+                              (GROUPED ? (int64_t)(layer - 1) * p.cache_layer_stride : 0);
 #pragma unroll
         for (int hh = 0; hh < 16 / G; ++hh) {
           float4 x4[G], y4[G], cs[G], sn[G];
@@ -740,7 +767,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
           }
 #pragma unroll
           for (int r = 0; r < G; ++r) {
-            if (EPI == EPI_RESID)
+            if (EPI == EPI_RESID && col_in)
               rv[r] = *reinterpret_cast<const bf16x4_t*>(p.resid + (int64_t)mr[r] * p.ldc + nw + c4);
             if (rope) {
               const int c = (cbase + c4) & (hd - 1);
@@ -755,15 +782,16 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
             const float x[4] = {x4[r].x * sc[r] + bx.x, x4[r].y * sc[r] + bx.y,
                                 x4[r].z * sc[r] + bx.z, x4[r].w * sc[r] + bx.w};
             bf16x4_t o;
-            if (EPI == EPI_GELU) {
+            if (EPI == EPI_GELU || EPI == EPI_GELU_TANH) {
 #pragma unroll
-              for (int e = 0; e < 4; ++e) o[e] = f2bf(gelu_erf(x[e]));
-              if (!kCheck || m < M)
+              for (int e = 0; e < 4; ++e)
+                o[e] = f2bf(EPI == EPI_GELU ? gelu_erf(x[e]) : gelu_tanh(x[e]));
+              if ((!kCheck || m < M) && col_in)
                 *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc +
                                              nw + c4) = o;
             } else if (EPI == EPI_STORE) {
               const int64_t off = (int64_t)m * p.ldc + nw + c4;
-              if (!kCheck || m < M) {
+              if ((!kCheck || m < M) && col_in) {
                 if (p.c_f32) {
                   *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + off) =
                       make_float4(x[0], x[1], x[2], x[3]);
@@ -776,7 +804,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
             } else if (EPI == EPI_RESID) {
 #pragma unroll
               for (int e = 0; e < 4; ++e) o[e] = f2bf(x[e] + bf2f(rv[r][e]));
-              if (!kCheck || m < M)
+              if ((!kCheck || m < M) && col_in)
                 *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) +
                                              (int64_t)mr[r] * p.ldc + nw + c4) = o;
             } else {  // EPI_QKV / EPI_KV
@@ -794,9 +822,15 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
                 for (int e = 0; e < 4; ++e)
                   o[e] = f2bf(c < half ? x[e] * cv[e] - y[e] * sv[e] : x[e] * cv[e] + y[e] * sv[e]);
               }
-              const int64_t drow = is_q ? (int64_t)m : (int64_t)mr[r];
-              if (!kCheck || m < M)
-                *reinterpret_cast<bf16x4_t*>(sec_dst + drow * p.d_q + c4) = o;
+              if (rope) {
+                const int64_t drow = is_q ? (int64_t)m : (int64_t)mr[r];
+                if (!kCheck || m < M)
+                  *reinterpret_cast<bf16x4_t*>(sec_dst + drow * p.d_q + c4) = o;
+              } else {
+                const int64_t drow = lq ? (int64_t)m : (int64_t)mr[r];
+                if ((!kCheck || m < M) && col_in)
+                  *reinterpret_cast<bf16x4_t*>(ldst + drow * p.d_q + cinl) = o;
+              }
             }
           }
         }
@@ -1165,9 +1199,9 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int nout, Sk
   const float4 bx = bias4(p.bias, n);
   const float x[4] = {x4.x * sc + bx.x, x4.y * sc + bx.y, x4.z * sc + bx.z, x4.w * sc + bx.w};
   bf16x4_t o;
-  if (EPI == EPI_GELU) {
+  if (EPI == EPI_GELU || EPI == EPI_GELU_TANH) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = f2bf(gelu_erf(x[e]));
+    for (int e = 0; e < 4; ++e) o[e] = f2bf(EPI == EPI_GELU ? gelu_erf(x[e]) : gelu_tanh(x[e]));
     *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc + n) = o;
   } else if (EPI == EPI_STORE) {
     const int64_t off = (int64_t)m * p.ldc + n;
@@ -1246,6 +1280,7 @@ GP to_gp(const GemmArgs& g) {
   p.bias = (const bf16*)g.bias;
   p.rope_cos = g.rope_cos; p.rope_sin = g.rope_sin; p.head_dim = g.head_dim; p.d_q = g.d_q;
   p.q_out = (bf16*)g.q_out; p.k_cache = (bf16*)g.k_cache; p.v_cache = (bf16*)g.v_cache;
+  p.bias_layer_stride = g.bias_layer_stride; p.a_sorted = g.a_sorted;
   return p;
 }
 
@@ -1272,14 +1307,19 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
     set_error("gemm: K=%d not a positive multiple of %d", g.K, BK);
     return ADEPT_E_UNSUPPORTED;
   }
-  const int ncols = g.epi == EPI_SWIGLU ? 128 : BN;
+  // the last 256-column tile may be ragged (N a multiple of 64); SwiGLU pairs
+  // 64 gate with 64 up columns per wave, so its N is a multiple of 128
+  const int ncols = g.epi == EPI_SWIGLU ? 128 : 64;
   if (g.N <= 0 || g.N % ncols != 0) {
     set_error("gemm: N=%d not a positive multiple of %d", g.N, ncols);
     return ADEPT_E_UNSUPPORTED;
   }
   if ((g.epi == EPI_QKV) &&
-      (g.d_q % 128 != 0 || (g.rope_cos && g.head_dim != 64 && g.head_dim != 128))) {
-    set_error("gemm: QKV epilogue needs d_q %% 128 == 0 (and head_dim 64/128 with RoPE)");
+      (g.d_q % 64 != 0 ||
+       (g.rope_cos && (g.d_q % 128 != 0 || (g.head_dim != 64 && g.head_dim != 128))) ||
+       (!g.rope_cos && !g.bias && g.d_q % 128 != 0))) {
+    set_error("gemm: QKV epilogue needs d_q %% 64 == 0 (d_q %% 128 == 0 and head_dim 64/128 "
+              "with RoPE or without a bias)");
     return ADEPT_E_UNSUPPORTED;
   }
   if (g.bias && (g.epi == EPI_SWIGLU || g.epi == EPI_KV || !aligned8(g.bias))) {
@@ -1300,12 +1340,14 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
         case EPI_RESID: return launch_skinny<EPI_RESID>(p, Nt, g.N, s, g.name, g.skinny_ws);
         case EPI_SWIGLU: return launch_skinny<EPI_SWIGLU>(p, Nt, g.N, s, g.name, g.skinny_ws);
         case EPI_GELU: return launch_skinny<EPI_GELU>(p, Nt, g.N, s, g.name, g.skinny_ws);
+        case EPI_GELU_TANH:
+          return launch_skinny<EPI_GELU_TANH>(p, Nt, g.N, s, g.name, g.skinny_ws);
         default: break;
       }
     }
   }
   p.tiles_m = ceil_div(g.M_max, BM);
-  p.tiles_n = g.N / ncols;
+  p.tiles_n = g.epi == EPI_SWIGLU ? g.N / 128 : ceil_div(g.N, BN);
   switch (g.epi) {
     case EPI_STORE: return launch_bf16<EPI_STORE, 0>(p, s, g.name);
     case EPI_QKV:
@@ -1314,6 +1356,7 @@ adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
     case EPI_RESID: return launch_bf16<EPI_RESID, 0>(p, s, g.name);
     case EPI_SWIGLU: return launch_bf16<EPI_SWIGLU, 0>(p, s, g.name);
     case EPI_GELU: return launch_bf16<EPI_GELU, 0>(p, s, g.name);
+    case EPI_GELU_TANH: return launch_bf16<EPI_GELU_TANH, 0>(p, s, g.name);
     default: set_error("gemm: bad epilogue"); return ADEPT_E_INVALID;
   }
 }
@@ -1360,11 +1403,17 @@ adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32
     set_error("kv_generate: operands must be 16-byte aligned");
     return ADEPT_E_INVALID;
   }
+  if (g.N <= 0 || g.N % 64 != 0 || (g.bias && !aligned8(g.bias)) ||
+      (!g.bias && g.d_q % 128 != 0)) {
+    set_error("kv_generate: 2*H*hd must be a multiple of 64 (128 per section without a bias), "
+              "the bias 8-byte aligned");
+    return ADEPT_E_UNSUPPORTED;
+  }
   GP p = to_gp(g);
   p.work = work; p.n_work = n_work; p.queue = queue; p.grp_m = grp_m; p.srows = srows;
   p.b_layer_stride = b_layer_stride;
   p.cache_layer_stride = cache_layer_stride;
-  p.tiles_n = g.N / BN;
+  p.tiles_n = ceil_div(g.N, BN);
   const int grid = std::min(max_work * p.tiles_n, kPersistentBlocks);
   if (g.head_dim == 128) {
     static bool attr_set = false;

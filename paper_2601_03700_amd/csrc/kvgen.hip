@@ -242,6 +242,84 @@ extern "C" adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_mo
 }
 
 // ---------------------------------------------------------------------------
+// LayerNorm family (GPT-2 style): s~ is normalised once, without the affine
+// part (the same for every skipped layer); layer r's LayerNorm gain is folded
+// into the columns of its Wk / Wv and its shift into their biases
+// (adept_fold_gain, adept_fold_bias), so the grouped GEMM takes the
+// normalised rows (in sorted order) and adds layer r's bias; no RoPE.
+// ---------------------------------------------------------------------------
+namespace adept {
+namespace {
+
+size_t ln_total(int n_layers, int max_rows, int d_model, size_t* xhat_off) {
+  size_t base = 0;
+  carve(nullptr, n_layers, max_rows, &base);
+  *xhat_off = base;
+  return base + align256((size_t)max_rows * d_model * 2);
+}
+
+}  // namespace
+}  // namespace adept
+
+extern "C" size_t adept_kv_generate_layernorm_workspace_bytes(int n_layers, int max_rows,
+                                                              int d_model) {
+  size_t off = 0;
+  return ln_total(n_layers, max_rows, d_model, &off);
+}
+
+extern "C" adept_status adept_kv_generate_layernorm(
+    adept_dtype dt, int n_layers, int d_model, int n_heads, int head_dim, float eps,
+    const void* s_map, const int32_t* rows, const int32_t* n_rows, int max_rows,
+    const int32_t* exit_layer, const int32_t* cache_slot, const void* w_kv,
+    int64_t w_kv_layer_stride, const void* b_kv, int64_t b_kv_layer_stride, void* k_cache,
+    void* v_cache, int64_t n_slots, void* workspace, size_t workspace_bytes, void* stream) {
+  ADEPT_REQUIRE(dt == ADEPT_BF16, "kv_generate_layernorm: bf16 only");
+  ADEPT_REQUIRE(n_layers >= 1 && n_layers <= kMaxLayers, "kv_generate_layernorm: n_layers %d",
+                n_layers);
+  ADEPT_REQUIRE(d_model > 0 && d_model % 64 == 0 && n_heads > 0 && head_dim > 0,
+                "kv_generate_layernorm: d_model must be a multiple of 64");
+  const int dq = n_heads * head_dim;
+  ADEPT_REQUIRE(dq % 32 == 0, "kv_generate_layernorm: H*hd must be a multiple of 32");
+  ADEPT_REQUIRE(max_rows >= 0 && max_rows < (1 << 24) && n_slots > 0,
+                "kv_generate_layernorm: bad sizes");
+  ADEPT_REQUIRE(s_map && rows && n_rows && exit_layer && cache_slot && w_kv && b_kv && k_cache &&
+                    v_cache,
+                "kv_generate_layernorm: NULL tensor");
+  ADEPT_REQUIRE(w_kv_layer_stride >= (int64_t)2 * dq * d_model && w_kv_layer_stride % 8 == 0 &&
+                    b_kv_layer_stride >= 2 * dq && b_kv_layer_stride % 4 == 0,
+                "kv_generate_layernorm: layer strides");
+  ADEPT_REQUIRE(aligned16(s_map) && aligned16(w_kv) && aligned16(workspace) &&
+                    ((uintptr_t)b_kv & 7) == 0,
+                "kv_generate_layernorm: tensors must be 16-byte aligned (bias 8)");
+  if (max_rows == 0) return ADEPT_OK;
+  size_t xoff = 0;
+  const size_t need = ln_total(n_layers, max_rows, d_model, &xoff);
+  if (!workspace || workspace_bytes < need) {
+    set_error("kv_generate_layernorm: workspace of %zu bytes needed", need);
+    return ADEPT_E_WORKSPACE;
+  }
+  hipStream_t s = as_stream(stream);
+  size_t tmp = 0;
+  KvWs w = carve(workspace, n_layers, max_rows, &tmp);
+  void* xhat = (char*)workspace + xoff;
+  ADEPT_LAUNCH(kv_plan_kernel, dim3(1), dim3(1024), 0, s, n_layers, rows, n_rows, max_rows,
+               exit_layer, w);
+  ADEPT_CHECK_LAUNCH("kv_plan");
+  // the exited rows, normalised in sorted order
+  ADEPT_TRY(layernorm_rows_sel(dt, d_model, eps, s_map, s_map, nullptr, w.srows, n_rows, max_rows,
+                               nullptr, nullptr, xhat, s));
+  GemmArgs g{};
+  g.M_max = max_rows; g.N = 2 * dq; g.K = d_model;
+  g.A = xhat; g.lda = d_model; g.a_sorted = 1; g.B = w_kv; g.ldb = d_model;
+  g.epi = EPI_KV; g.slot = cache_slot; g.head_dim = head_dim; g.d_q = dq;
+  g.k_cache = k_cache; g.v_cache = v_cache;
+  g.bias = b_kv; g.bias_layer_stride = b_kv_layer_stride;
+  const int max_work = n_layers * ceil_div(max_rows, kTileM);
+  return gemm_kv_grouped(g, w.work, w.n_work, w.queue, max_work, w.grp_m, w.srows,
+                         w_kv_layer_stride, n_slots * dq, s);
+}
+
+// ---------------------------------------------------------------------------
 // Allocation-free variant: the plan / work-list / row-scale scratch lives in
 // a file-scope device array (one copy per GPU, kept until the process ends).
 // Host code never passes the array's name to a kernel: its device address is

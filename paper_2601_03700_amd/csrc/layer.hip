@@ -27,6 +27,7 @@ struct LayerWs {
   void* hsm;      size_t hsm_bytes;      // mapper activations (when a mapper is given)
   float* skinny;  size_t skinny_bytes;   // GEMM partial sums when n_tok <= 64 (decode)
   float* gemm_tmp;  // f32 path only
+  void* xnorm;      // [n_tok][D] normalised rows (GPT2 family)
   size_t total;
 };
 
@@ -40,8 +41,15 @@ LayerWs carve(const adept_layer_args* a, void* base) {
   w.compact = p + off; off += align256(w.compact_bytes);
   w.attend_bytes = attend_workspace_bytes(a->n_tok, a->n_seq, a->n_heads, a->head_dim, a->s_max);
   w.attend = p + off; off += align256(w.attend_bytes);
-  w.kvgen_bytes = adept_kv_generate_workspace_bytes(a->n_layers, a->n_tok);
+  const bool gpt2 = a->family == ADEPT_FAMILY_GPT2;
+  w.kvgen_bytes = gpt2 ? adept_kv_generate_layernorm_workspace_bytes(a->n_layers, a->n_tok,
+                                                                     a->d_model)
+                       : adept_kv_generate_workspace_bytes(a->n_layers, a->n_tok);
   w.kvgen = p + off; off += align256(w.kvgen_bytes);
+  if (gpt2) {
+    w.xnorm = p + off;
+    off += align256((size_t)a->n_tok * a->d_model * 2);
+  }
   w.all_rows = (int32_t*)(p + off); off += align256(((size_t)a->n_tok + 64) * sizeof(int32_t));
   w.prompt_bytes = adept_exit_prompt_level_workspace_bytes(a->n_seq);
   w.prompt = p + off; off += align256(w.prompt_bytes);
@@ -90,6 +98,27 @@ adept_status run_gemm(adept_dtype dt, const GemmArgs& g, float* tmp, hipStream_t
   return dt == ADEPT_BF16 ? gemm(dt, g, s) : gemm_f32(g, tmp, s);
 }
 
+// Eq. 9 for the rows listed in rows / n_rows: the K and V rows of each
+// layer's stacked QKV weight (and, for the GPT2 family, of its folded bias).
+adept_status kv_generate_family(const adept_layer_args* a, adept_dtype dt, const void* s_map,
+                                const int32_t* rows, const int32_t* n_rows, int max_rows,
+                                const LayerWs& ws, void* stream) {
+  const int N = a->n_layers, D = a->d_model, H = a->n_heads, hd = a->head_dim;
+  const int64_t dq = (int64_t)H * hd;
+  const size_t esz = dt == ADEPT_BF16 ? 2 : 4;
+  const void* wkv = (const char*)a->w_qkv + dq * D * (int64_t)esz;
+  if (a->family == ADEPT_FAMILY_GPT2)
+    return adept_kv_generate_layernorm(dt, N, D, H, hd, a->rms_eps, s_map, rows, n_rows, max_rows,
+                                       a->exit_layer, a->slot, wkv, 3 * dq * D,
+                                       (const char*)a->b_qkv + dq * (int64_t)esz, 3 * dq,
+                                       a->k_cache, a->v_cache, a->n_slots, ws.kvgen,
+                                       ws.kvgen_bytes, stream);
+  return adept_kv_generate(dt, N, D, H, hd, a->rms_eps, s_map, rows, n_rows, max_rows,
+                           a->exit_layer, a->slot, a->pos, wkv, 3 * dq * D, nullptr, a->rope_cos,
+                           a->rope_sin, a->rope_max_pos, a->k_cache, a->v_cache, a->n_slots,
+                           ws.kvgen, ws.kvgen_bytes, stream);
+}
+
 }  // namespace
 }  // namespace adept
 
@@ -111,8 +140,15 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   ADEPT_REQUIRE(a->max_active >= 0 && a->max_active <= a->n_tok, "layer_step: bad max_active");
   ADEPT_REQUIRE(a->n_seq > 0 && a->s_max > 0 && a->n_slots >= (int64_t)a->n_seq * a->s_max,
                 "layer_step: cache smaller than n_seq * s_max");
-  ADEPT_REQUIRE(a->w_qkv && a->w_o && a->w_gate && a->w_up && a->w_down && a->rope_cos &&
-                    a->rope_sin && a->h[0] && a->h[1] && a->pos && a->seq && a->slot &&
+  const bool gpt2 = a->family == ADEPT_FAMILY_GPT2;
+  ADEPT_REQUIRE(a->family == ADEPT_FAMILY_LLAMA || gpt2, "layer_step: bad family %d", a->family);
+  ADEPT_REQUIRE(!gpt2 || (dt == ADEPT_BF16 && a->b_qkv && a->b_o && a->b_fc && a->b_proj &&
+                          D % 64 == 0 && (H * hd) % 64 == 0 && F % 64 == 0 && !a->hsm),
+                "layer_step: the GPT2 family needs bf16, the four biases, no mapper and "
+                "d_model, H*hd, d_ff multiples of 64");
+  ADEPT_REQUIRE(a->w_qkv && a->w_o && a->w_gate && (gpt2 || a->w_up) && a->w_down &&
+                    (gpt2 || (a->rope_cos && a->rope_sin)) && a->h[0] && a->h[1] && a->pos &&
+                    a->seq && a->slot &&
                     a->active[0] && a->active[1] && a->n_active[0] && a->n_active[1] &&
                     a->exited && a->n_exited && a->exit_layer && a->exit_flag && a->k_cache &&
                     a->v_cache && a->q_buf && a->attn_out && a->ffn_act,
@@ -141,12 +177,58 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   const void* wqkv = off(a->w_qkv, li * 3 * dq * D);
   const void* wo = off(a->w_o, li * (int64_t)D * dq);
   const void* wg = off(a->w_gate, li * (int64_t)F * D);
-  const void* wu = off(a->w_up, li * (int64_t)F * D);
+  const void* wu = a->w_up ? off(a->w_up, li * (int64_t)F * D) : nullptr;
   const void* wd = off(a->w_down, li * (int64_t)D * F);
   void* kc = (void*)off(a->k_cache, li * a->n_slots * dq);
   void* vc = (void*)off(a->v_cache, li * a->n_slots * dq);
 
-  if (maxn > 0) {
+  if (maxn > 0 && gpt2) {
+    // LayerNorm family: norms without their affine part (folded into the
+    // weights and biases), biased projections, tanh GELU, no RoPE
+    const void* bqkv = off(a->b_qkv, li * 3 * dq);
+    // 1. LN1 of the active rows (compact order)
+    ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[in], a->h[in], nullptr, act, nact, maxn,
+                                 nullptr, nullptr, ws.xnorm, s));
+    // 2. Q/K/V with bias, own K/V into cache[layer]
+    GemmArgs g{};
+    g.M_max = maxn; g.M_dev = nact; g.N = 3 * dq; g.K = D;
+    g.A = ws.xnorm; g.lda = D; g.B = wqkv; g.ldb = D; g.epi = EPI_QKV; g.bias = bqkv;
+    g.rows = act; g.pos = a->pos; g.slot = a->slot; g.head_dim = hd; g.d_q = dq;
+    g.q_out = a->q_buf; g.k_cache = kc; g.v_cache = vc; g.name = "gemm_qkv";
+    g.skinny_ws = ws.skinny; g.skinny_ws_bytes = ws.skinny_bytes;
+    ADEPT_TRY(gemm(dt, g, s));
+    // 3. attention over the mixed cache
+    ADEPT_TRY(attend_dispatch(dt, H, hd, 1.0f / sqrtf((float)hd), 1, a->q_buf, act, nact, maxn,
+                              a->pos, a->seq, a->n_seq, kc, vc, a->s_max, nullptr, nullptr,
+                              a->attn_out, ws.attend, ws.attend_bytes, a->attn_tiles != 0, s));
+    // 4. output projection + bias + residual: h[out] = h[in] + o Wo^T + bo
+    GemmArgs go{};
+    go.M_max = maxn; go.M_dev = nact; go.N = D; go.K = dq;
+    go.A = a->attn_out; go.lda = dq; go.B = wo; go.ldb = dq; go.epi = EPI_RESID;
+    go.bias = off(a->b_o, li * D);
+    go.C = a->h[out]; go.ldc = D; go.resid = a->h[in]; go.rows = act; go.name = "gemm_o";
+    go.skinny_ws = ws.skinny; go.skinny_ws_bytes = ws.skinny_bytes;
+    ADEPT_TRY(gemm(dt, go, s));
+    // 5. LN2
+    ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[out], a->h[out], nullptr, act, nact,
+                                 maxn, nullptr, nullptr, ws.xnorm, s));
+    // 6. first MLP projection + bias + tanh GELU
+    GemmArgs gf{};
+    gf.M_max = maxn; gf.M_dev = nact; gf.N = F; gf.K = D;
+    gf.A = ws.xnorm; gf.lda = D; gf.B = wg; gf.ldb = D; gf.epi = EPI_GELU_TANH;
+    gf.bias = off(a->b_fc, li * F);
+    gf.C = a->ffn_act; gf.ldc = F; gf.name = "gemm_fc";
+    gf.skinny_ws = ws.skinny; gf.skinny_ws_bytes = ws.skinny_bytes;
+    ADEPT_TRY(gemm(dt, gf, s));
+    // 7. second MLP projection + bias + residual (in place on h[out])
+    GemmArgs gd{};
+    gd.M_max = maxn; gd.M_dev = nact; gd.N = D; gd.K = F;
+    gd.A = a->ffn_act; gd.lda = F; gd.B = wd; gd.ldb = F; gd.epi = EPI_RESID;
+    gd.bias = off(a->b_proj, li * D);
+    gd.C = a->h[out]; gd.ldc = D; gd.resid = a->h[out]; gd.rows = act; gd.name = "gemm_proj";
+    gd.skinny_ws = ws.skinny; gd.skinny_ws_bytes = ws.skinny_bytes;
+    ADEPT_TRY(gemm(dt, gd, s));
+  } else if (maxn > 0) {
     // 1. pre-attention RMSNorm: the gain is folded into W_qkv, the row factor
     //    1/rms(h) scales the GEMM accumulators
     ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[in], act, nact, maxn, ws.rinv, s));
@@ -215,20 +297,11 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
                  a->exit_layer, (const char*)a->h[(N + 1) & 1], (char*)a->h[N & 1], ws.all_rows,
                  ws.all_rows + a->n_tok);
     ADEPT_CHECK_LAUNCH("defer_rows");
-    ADEPT_TRY(adept_kv_generate(dt, N, D, H, hd, a->rms_eps, a->h[N & 1], ws.all_rows,
-                                ws.all_rows + a->n_tok, a->n_tok, a->exit_layer, a->slot, a->pos,
-                                off(a->w_qkv, (int64_t)dq * D), (int64_t)3 * dq * D,
-                                nullptr, a->rope_cos, a->rope_sin, a->rope_max_pos,
-                                a->k_cache, a->v_cache, a->n_slots, ws.kvgen, ws.kvgen_bytes,
-                                stream));
+    ADEPT_TRY(kv_generate_family(a, dt, a->h[N & 1], ws.all_rows, ws.all_rows + a->n_tok,
+                                 a->n_tok, ws, stream));
   }
   if (!defer && layer < N && maxn > 0) {
-    ADEPT_TRY(adept_kv_generate(dt, N, D, H, hd, a->rms_eps, a->h[out], a->exited, a->n_exited,
-                                maxn, a->exit_layer, a->slot, a->pos,
-                                off(a->w_qkv, (int64_t)dq * D), (int64_t)3 * dq * D,
-                                nullptr, a->rope_cos, a->rope_sin, a->rope_max_pos,
-                                a->k_cache, a->v_cache, a->n_slots, ws.kvgen, ws.kvgen_bytes,
-                                stream));
+    ADEPT_TRY(kv_generate_family(a, dt, a->h[out], a->exited, a->n_exited, maxn, ws, stream));
   }
   return ADEPT_OK;
 }

@@ -74,7 +74,11 @@ TimedLaunch::TimedLaunch(const char* name, hipStream_t s) : name_(name), s_(s) {
   if (!g_prefix.empty() && strncmp(name, g_prefix.c_str(), g_prefix.size()) != 0) return;
   a_ = take_event();
   b_ = take_event();
-  if (a_ && b_) hipEventRecord((hipEvent_t)a_, s_);
+  if (a_ && b_ && hipEventRecord((hipEvent_t)a_, s_) == hipSuccess) return;
+  // no timing for this launch: the events go back to the pool
+  if (a_) g_pool.push_back((hipEvent_t)a_);
+  if (b_) g_pool.push_back((hipEvent_t)b_);
+  a_ = b_ = nullptr;
 }
 
 TimedLaunch::~TimedLaunch() {

@@ -7,6 +7,9 @@ sequence ids, cache slots) and calls the C ABI in order:
     adept_embed -> adept_token_init -> adept_layer_step(i), i = 1..N
                 -> adept_final_logits [-> adept_argmax]
 
+(the LayerNorm family: adept_embed_positions and adept_final_logits_layernorm
+in place of the embedding gather and the RMSNorm head).
+
 A prefill runs the rows of a [B, T] prompt batch (row b*T + p); a decode
 step runs one new token per sequence against the cache the prefill (and
 earlier steps) filled, with generated entries for every skipped layer.
@@ -73,10 +76,14 @@ class PassResult:
 
 
 class DecoderModel:
-    """A Llama-style decoder held on the device in the library's layout.
+    """A pre-norm decoder held on the device in the library's layout.
 
-    weights: a dict like adept_inputs.decoder_weights() (numpy, per layer) or
-    adept_inputs.decoder_weights_torch() (stacked torch tensors on device).
+    shape.family "llama": weights like adept_inputs.decoder_weights() (numpy,
+    per layer) or adept_inputs.decoder_weights_torch() (stacked torch tensors
+    on device).  "gpt2": like adept_inputs.gpt2_weights() or
+    gpt2_weights_torch(); the LayerNorm gains and shifts are folded into the
+    projections that follow them (w_qkv / b_qkv, w_fc / b_fc) and the LM
+    head is the token embedding.
     """
 
     def __init__(self, shape, weights, dtype="bf16", device="cuda", rope_max_pos=4096,
@@ -85,6 +92,7 @@ class DecoderModel:
         self.dtype = dtype
         self.tdt = _TORCH_DT[dtype]
         self.device = torch.device(device)
+        self.gpt2 = getattr(shape, "family", "llama") == "gpt2"
         N, D, Dq, F = shape.n_layers, shape.d_model, shape.d_q, shape.d_ff
         dev, tdt = self.device, self.tdt
 
@@ -93,6 +101,13 @@ class DecoderModel:
                 return x.to(dev, tdt).contiguous()
             return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(dev).to(tdt)
 
+        self.hsm, self._hsm_struct = None, None
+        if self.gpt2:
+            if dtype != "bf16" or hsm_weights is not None:
+                raise ValueError("the LayerNorm family runs in bf16 without a mapper")
+            self._init_gpt2(weights, up)
+            return
+        self.b_qkv = self.b_o = self.b_fc = self.b_proj = None
         if isinstance(weights.get("layers"), list):
             L = weights["layers"]
             stack = lambda k: up(np.stack([lw[k] for lw in L]))
@@ -120,7 +135,6 @@ class DecoderModel:
         B.fold_gain(self.w_up, self.ffn_norm)
         # optional hidden state mapper (Section 4.2) of the exiting rows: a dict
         # like adept_inputs.hsm_weights(); None keeps the identity mapper
-        self.hsm, self._hsm_struct = None, None
         if hsm_weights is not None:
             self.hsm = {k: (v if k in ("conv", "conv_b") else up(v)) for k, v in hsm_weights.items()}
             self._hsm_struct = B.hsm_weights(self.hsm)
@@ -129,6 +143,42 @@ class DecoderModel:
         self.rope_cos = torch.empty((rope_max_pos, half), dtype=torch.float32, device=dev)
         self.rope_sin = torch.empty_like(self.rope_cos)
         B.rope_table(rope_max_pos, shape.head_dim, shape.rope_theta, self.rope_cos, self.rope_sin)
+
+    def _init_gpt2(self, weights, up):
+        s = self.shape
+        N, D, Dq, F = s.n_layers, s.d_model, s.d_q, s.d_ff
+        if isinstance(weights.get("layers"), list):
+            L = weights["layers"]
+            stack = lambda k: up(np.stack([lw[k] for lw in L]))
+            cat = lambda ks: up(np.stack([np.concatenate([lw[k] for k in ks]) for lw in L]))
+            ln1_g, ln1_b, ln2_g, ln2_b = (stack("ln1_g"), stack("ln1_b"), stack("ln2_g"),
+                                          stack("ln2_b"))
+            self.w_qkv, self.b_qkv = cat(("wq", "wk", "wv")), cat(("bq", "bk", "bv"))
+            self.w_o, self.b_o = stack("wo"), stack("bo")
+            self.w_gate, self.b_fc = stack("w_fc"), stack("b_fc")
+            self.w_down, self.b_proj = stack("w_proj"), stack("b_proj")
+        else:
+            ln1_g, ln1_b = up(weights["ln1_g"]), up(weights["ln1_b"])
+            ln2_g, ln2_b = up(weights["ln2_g"]), up(weights["ln2_b"])
+            self.w_qkv = torch.cat([up(weights[k]) for k in ("wq", "wk", "wv")], 1).contiguous()
+            self.b_qkv = torch.cat([up(weights[k]) for k in ("bq", "bk", "bv")], 1).contiguous()
+            self.w_o, self.b_o = up(weights["wo"]), up(weights["bo"])
+            self.w_gate, self.b_fc = up(weights["w_fc"]), up(weights["b_fc"])
+            self.w_down, self.b_proj = up(weights["w_proj"]), up(weights["b_proj"])
+        self.w_up = None
+        self.embed, self.pos_embed = up(weights["embed"]), up(weights["pos_embed"])
+        self.final_ln_g, self.final_ln_b = up(weights["final_ln_g"]), up(weights["final_ln_b"])
+        self.lm_head = self.embed      # tied
+        assert self.w_qkv.shape == (N, 3 * Dq, D) and self.b_qkv.shape == (N, 3 * Dq)
+        assert self.w_down.shape == (N, D, F) and self.pos_embed.shape == (s.max_pos, D)
+        # LayerNorm shift into the bias (on the unfolded weights), then the
+        # gain into the weights: LN(x) W^T + b = xh (W diag g)^T + (b + W beta)
+        B.fold_bias(self.w_qkv, ln1_b, self.b_qkv)
+        B.fold_gain(self.w_qkv, ln1_g)
+        B.fold_bias(self.w_gate, ln2_b, self.b_fc)
+        B.fold_gain(self.w_gate, ln2_g)
+        self.rope_cos = self.rope_sin = None
+        self.rope_max_pos = s.max_pos     # the position table bounds the positions
 
     # ------------------------------------------------------------------ buffers
     def new_cache(self, n_seq, s_max, fill=None):
@@ -168,11 +218,15 @@ class DecoderModel:
         a = B.LayerArgs()
         a.dtype = B.dtype_code(self.dtype)
         a.n_layers, a.d_model, a.n_heads = s.n_layers, s.d_model, s.n_heads
-        a.head_dim, a.d_ff, a.rms_eps = s.head_dim, s.d_ff, s.rms_eps
+        a.head_dim, a.d_ff = s.head_dim, s.d_ff
+        a.rms_eps = s.ln_eps if self.gpt2 else s.rms_eps
         a.exit = cfg
         a.w_qkv, a.w_o, a.w_gate = B.ptr(self.w_qkv), B.ptr(self.w_o), B.ptr(self.w_gate)
         a.w_up, a.w_down = B.ptr(self.w_up), B.ptr(self.w_down)
         a.rope_cos, a.rope_sin, a.rope_max_pos = B.ptr(self.rope_cos), B.ptr(self.rope_sin), self.rope_max_pos
+        a.family = B.FAMILY_GPT2 if self.gpt2 else B.FAMILY_LLAMA
+        a.b_qkv, a.b_o = B.ptr(self.b_qkv), B.ptr(self.b_o)
+        a.b_fc, a.b_proj = B.ptr(self.b_fc), B.ptr(self.b_proj)
         a.n_tok, a.max_active, a.n_seq, a.s_max = st.n_tok, st.n_tok, cache.n_seq, cache.s_max
         a.attn_tiles = int(attn_tiles)
         a.h[0], a.h[1] = B.ptr(st.h[0]), B.ptr(st.h[1])
@@ -194,7 +248,7 @@ class DecoderModel:
 
     # ------------------------------------------------------------------ passes
     def _check_positions(self, pos, s_max, pos_max=None):
-        """Positions must lie inside the rotary table and the cache; pos_max
+        """Positions must lie inside the rotary (or position) table and the cache; pos_max
         (a host int, when the caller knows it) avoids reading pos back."""
         pmax = pos_max if pos_max is not None else (int(pos.max()) if pos.numel() else 0)
         if pmax >= self.rope_max_pos or pmax >= s_max:
@@ -207,7 +261,11 @@ class DecoderModel:
         n = int(ids.shape[0])
         slot = (seq * cache.s_max + pos).to(torch.int32)
         st = self.new_state(n, pos, seq, slot, force_layer)
-        B.embed(n, s.d_model, s.vocab, ids, self.embed, st.h[0])
+        if self.gpt2:
+            B.embed_positions(n, s.d_model, s.vocab, s.max_pos, ids, pos, self.embed,
+                              self.pos_embed, st.h[0])
+        else:
+            B.embed(n, s.d_model, s.vocab, ids, self.embed, st.h[0])
         B.token_init(n, s.n_layers, s.d_model, st.active[0], st.counts, st.exit_layer, st.inertia)
         args = self.layer_args(st, cache, cfg, attn_tiles)
         for i in range(1, s.n_layers + 1):
@@ -221,8 +279,13 @@ class DecoderModel:
         n_rows = torch.tensor([nr], dtype=torch.int32, device=self.device)
         logits = torch.empty((nr, s.vocab), dtype=torch.float32, device=self.device)
         xn = torch.empty((nr, s.d_model), dtype=self.tdt, device=self.device)
-        B.final_logits(s.d_model, s.vocab, s.rms_eps, st.h[0], st.h[1], st.exit_layer, rows,
-                       n_rows, nr, self.final_norm, self.lm_head, xn, logits)
+        if self.gpt2:
+            B.final_logits_layernorm(s.d_model, s.vocab, s.ln_eps, st.h[0], st.h[1],
+                                     st.exit_layer, rows, n_rows, nr, self.final_ln_g,
+                                     self.final_ln_b, self.lm_head, xn, logits)
+        else:
+            B.final_logits(s.d_model, s.vocab, s.rms_eps, st.h[0], st.h[1], st.exit_layer, rows,
+                           n_rows, nr, self.final_norm, self.lm_head, xn, logits)
         return PassResult(logits, rows, st.exit_layer, st)
 
     def prefill(self, ids, cfg, s_max=None, force_layer=None, logits="all", cache=None,
