@@ -16,7 +16,7 @@ kernel (timed live with HIP events inside the timed passes), the 8 x 2048
 prefill section (threshold sweep, calibrated thresholds, the no-exit and
 fixed-schedule variants, per-kernel MFMA figures), the standalone KV
 generation, mapper, exit test and compaction, the fixed-schedule generation,
-the BERT-base classification, the tiny f32 decoder, and the CPU oracle on a
+the GPT2-XL-shaped generation, the BERT-base classification, the tiny f32 decoder, and the CPU oracle on a
 bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--delta D | --budget 0.2] [--metric global]
@@ -143,12 +143,12 @@ def parse():
     ap.add_argument("--sections", default="all",
                     help="comma list of the parts to run (profiling runs): headline, prefill, "
                          "variants (prefill no-exit / fixed schedule / sweep), kvgen, hsm, exit, "
-                         "generation, classification, tiny, cpu; default all")
+                         "generation, gpt2, classification, tiny, cpu; default all")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="copy 256 MiB device to device first (a kernel of known traffic "
                          "for scaling hardware byte counters)")
     args = ap.parse_args()
-    every = {"headline", "prefill", "variants", "kvgen", "hsm", "exit", "generation",
+    every = {"headline", "prefill", "variants", "kvgen", "hsm", "exit", "generation", "gpt2",
              "classification", "tiny", "cpu"}
     sec = every if args.sections == "all" else set(args.sections.split(","))
     if sec - every:
@@ -331,6 +331,9 @@ def run_sections(args, out, model, shape, ai, B, torch, np, Bn, T, n_tok):
     if "generation" in args.sec:
         out["generation_fixed_schedule"] = generation(args, model, shape, ai, B, torch, np)
 
+    if "gpt2" in args.sec:
+        out["gpt2_xl_generation"] = gpt2_generation(args, ai, B, torch, np)
+
     if "classification" in args.sec:
         del model
         torch.cuda.empty_cache()
@@ -414,11 +417,11 @@ def skipped_fraction(exit_layer, n_layers):
 
 def reduction(exit_layer, shape):
     """Compute reduction (RDC) of a run's exit layers, three K/V charges
-    (none / the paper's / algorithmic); dense projections of a SwiGLU layer
-    plus the LM head once per token."""
+    (none / the paper's / algorithmic); dense projections of a layer (SwiGLU:
+    three FFN matrices, the GELU MLP two) plus the LM head once per token."""
     from paper_2601_03700_amd.accounting import rdc
     return rdc(exit_layer.to("cpu").numpy(), shape.n_layers, shape.d_model, shape.d_q,
-               shape.d_ff, shape.vocab, ffn_mats=3)
+               shape.d_ff, shape.vocab, ffn_mats=2 if shape.family == "gpt2" else 3)
 
 
 def exit_histogram(exit_layer, n_layers):
@@ -700,7 +703,7 @@ def decode_attention_bytes(shape, el_steps, T):
     return total
 
 
-def generation_policy(args, model, shape, ai, B, torch, np):
+def generation_policy(args, model, shape, ai, B, torch, np, tag="headline"):
     """The headline: generation at the 7B shape with the policy's own exit
     decisions.  One step = one pass: prefill of gen_batch prompts of
     gen_context uniform-random tokens, then gen_steps greedy decode steps
@@ -751,7 +754,7 @@ def generation_policy(args, model, shape, ai, B, torch, np):
                  "method": "largest delta whose running-max similarity count on a no-exit pass "
                            "of the same workload skips the budget (calibrate.calibrate_delta)"}
         del recs, sims
-        log(f"headline: delta calibrated to {delta:.6f} for a {args.budget:.0%} budget "
+        log(f"{tag}: delta calibrated to {delta:.6f} for a {args.budget:.0%} budget "
             f"({time.time() - t0:.1f}s)")
     else:
         delta = args.delta
@@ -759,7 +762,7 @@ def generation_policy(args, model, shape, ai, B, torch, np):
     for _ in range(args.warmup):
         one_pass(cfg)
     torch.cuda.synchronize()
-    log(f"headline: cache {2 * cache.k.numel() * 2 / 2**30:.0f} GiB, {args.warmup} warmup "
+    log(f"{tag}: cache {2 * cache.k.numel() * 2 / 2**30:.0f} GiB, {args.warmup} warmup "
         f"pass(es) in {time.time() - t0:.1f}s")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -844,7 +847,7 @@ def generation_policy(args, model, shape, ai, B, torch, np):
         "kernels": {k: {"launches": n, "avg_us": ms * 1e3 / n, "share": ms / ms_instr}
                     for k, (n, ms) in sorted(kern_all.items(), key=lambda kv: -kv[1][1])[:16]},
     }
-    log(f"headline: {ms_pass:.0f} ms per pass = {out['tokens_per_s']:.0f} tokens/s "
+    log(f"{tag}: {ms_pass:.0f} ms per pass = {out['tokens_per_s']:.0f} tokens/s "
         f"(prefill {prefill_ms:.0f} ms, decode {decode_ms / max(S, 1):.1f} ms/step), "
         f"{out['skipped_fraction']:.1%} of token-layers skipped; no exit {inf_ms:.0f} ms "
         f"({out['speedup_vs_no_exit']:.2f}x); {dom} {roofline.get('frac') or 0:.3f} of its roofline")
@@ -941,6 +944,35 @@ def generation(args, model, shape, ai, B, torch, np):
         f"no-exit {kinf_s * 1e3 / n_inf:.1f} ms/step; decode attention "
         f"{out['decode_attention']['gbs'] or 0:.0f} GB/s")
     del cache
+    torch.cuda.empty_cache()
+    return out
+
+
+def gpt2_generation(args, ai, B, torch, np, batch=64, context=768, steps=256):
+    """GPT2-XL-shaped decoder (48 layers, width 1600, 25 heads of 64, GELU MLP
+    6400, learned positions up to 1024, vocab 50304 tied; bf16, random-init
+    weights) generating with the policy's own decisions, as the headline:
+    batch 64 prompts of 768 uniform-random tokens prefilled, then 256 greedy
+    decode steps (1024 positions, the model's limit), the threshold
+    calibrated on a no-exit pass to skip --budget of the token-layers, and
+    the same workload without exits beside it."""
+    from paper_2601_03700_amd.model import DecoderModel
+    shape = ai.GPT2_XL
+    t0 = time.time()
+    w = ai.gpt2_weights_torch(shape, seed=27, device="cuda")
+    model = DecoderModel(shape, w, dtype="bf16")
+    del w
+    torch.cuda.empty_cache()
+    log(f"gpt2-xl: weights ready in {time.time() - t0:.1f}s")
+    sub = argparse.Namespace(**vars(args))
+    sub.gen_batch, sub.gen_context, sub.gen_steps = batch, context, steps
+    sub.steps, sub.warmup, sub.delta = 1, 1, None
+    out = generation_policy(sub, model, shape, ai, B, torch, np, tag="gpt2-xl")
+    out = {"workload": (f"GPT2-XL-shaped decoder generation: batch {batch}, {context}-token "
+                        f"prompts prefilled, then {steps} greedy decode steps; token-level exit "
+                        f"with the policy's own decisions ({args.metric} metric, delta "
+                        f"{out['delta']:.6f} calibrated to skip {args.budget:.0%})"), **out}
+    del model
     torch.cuda.empty_cache()
     return out
 
