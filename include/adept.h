@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define ADEPT_ABI_VERSION 4
+#define ADEPT_ABI_VERSION 5
 
 typedef enum {
   ADEPT_OK = 0,
@@ -337,7 +337,8 @@ adept_status adept_attend(adept_dtype dt, int n_heads, int head_dim, float scale
  *   [adept_hsm_forward on the exited rows, when `hsm` is set] ->
  *   adept_kv_generate for the rows exited at i (layers i+1..N); with
  *   attn_tiles = 0 (decode) the generation of every exited row is enqueued
- *   once, by the step of layer N, after copying the exit states into h[N&1].
+ *   once, by the step of layer N, after copying the exit states into h[N&1]
+ *   (or, with kv_fused, done by the QKV GEMM of each later layer).
  * The residual stream ping-pongs between h[0] and h[1]: a token's final
  * state is h[exit_layer & 1][row] (its state at exit, the identity mapped
  * state).  Before layer 1 the caller puts h_0 in h[0], zeroes the inertia,
@@ -367,8 +368,9 @@ typedef struct {
   int32_t attn_tiles;    /* 1: prompt rows (prefill): attention by query tiles, K/V of
                             the rows that exit at layer i generated right after layer i;
                             0: one row per sequence (decode): attention by key chunks,
-                            K/V of all exited rows generated after layer N (no row of
-                            the pass reads them); the pass must then run all N layers */
+                            K/V of all exited rows generated after layer N or, with
+                            kv_fused, inside the later layers (no row of the pass
+                            reads them); the pass must then run all N layers */
   void* h[2];            /* [n_tok][D] residual stream ping-pong */
   float* inertia;        /* [n_tok][D] (GLOBAL and BOTH metrics) */
   const int32_t* pos;    /* [n_tok] */
@@ -407,6 +409,13 @@ typedef struct {
   const void* b_o;      /* [N][D] */
   const void* b_fc;     /* [N][F] */
   const void* b_proj;   /* [N][D] */
+  /* decode passes (attn_tiles = 0), bf16: 1 = generate the K/V of exited rows
+   * inside each later layer's QKV GEMM (the GEMM's rows are the active rows
+   * followed by the rows that exited at a layer below it, each read from its
+   * exit state; W_k / W_v are then read once per pass with no extra launch),
+   * 0 = one grouped generation after layer N.  Same cache contents either way
+   * (Eq. 6 leaves the order of the generation free). */
+  int32_t kv_fused;
 } adept_layer_args;
 
 size_t adept_layer_workspace_bytes(const adept_layer_args* a);

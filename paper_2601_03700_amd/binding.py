@@ -57,6 +57,7 @@ class LayerArgs(ctypes.Structure):
         ("q_buf", _vp), ("attn_out", _vp), ("ffn_act", _vp),
         ("workspace", _vp), ("workspace_bytes", _sz), ("hsm", _vp),
         ("family", _i32), ("b_qkv", _vp), ("b_o", _vp), ("b_fc", _vp), ("b_proj", _vp),
+        ("kv_fused", _i32),
     ]
 
 

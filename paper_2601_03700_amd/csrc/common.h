@@ -171,6 +171,9 @@ struct GemmArgs {
   // grouped KV generation: per-layer bias stride, and A already in the
   // sorted row order (pre-normalised rows) instead of gathered by token row
   int64_t bias_layer_stride; int a_sorted;
+  // per-row second A buffer (bf16 paths): token row r = a_rows[m] reads A2
+  // instead of A when a_sel[r] & 1; nullable
+  const void* A2; const int32_t* a_sel;
 };
 size_t skinny_ws_bytes(int n_cols, int K);
 
@@ -194,6 +197,10 @@ adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32
 // out[k] = 1/sqrt(mean(x[rows[k]]^2) + eps) for k < min(*n_dev, max_n) (rows nullable: k).
 adept_status row_rinv(adept_dtype dt, int d, float eps, const void* x, const int32_t* rows,
                       const int32_t* n_dev, int max_n, float* out, hipStream_t s);
+// row_rinv of x1[row] where sel && (sel[row] & 1), else of x0[row]
+adept_status row_rinv_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
+                          const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
+                          int max_n, float* out, hipStream_t s);
 adept_status rmsnorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
                               const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
                               int max_n, const void* gain, void* out, hipStream_t s);

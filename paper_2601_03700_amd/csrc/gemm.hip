@@ -105,6 +105,9 @@ struct GP {
   int64_t cache_layer_stride;
   int64_t bias_layer_stride; // grouped: layer r's bias at bias + (r-1) * stride
   int a_sorted;             // grouped: A holds the rows in sorted order (row m), not by token
+  // per-row second A buffer: token row r reads A2 when a_sel[r] & 1 (nullable)
+  const bf16* A2;
+  const int32_t* a_sel;
 };
 
 // x * sigmoid(x) with the hardware reciprocal (about 1 ulp in f32, far below
@@ -199,7 +202,8 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     int m = m0 + r;
     if (m >= M) m = m0;  // clamp: loaded, never stored
     const int arow = GROUPED ? (p.a_sorted ? m : p.srows[m]) : (p.a_rows ? p.a_rows[m] : m);
-    a_src[j] = p.A + (int64_t)arow * p.lda + lchunk * 8;
+    const bf16* abase = (!GROUPED && p.a_sel && (p.a_sel[arow] & 1)) ? p.A2 : p.A;
+    a_src[j] = abase + (int64_t)arow * p.lda + lchunk * 8;
     const bf16* bbase = Bm;
     int64_t brow;
     if (EPI == EPI_SWIGLU) {
@@ -1122,7 +1126,8 @@ __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int nb, SkSpl
       if (wave < 2) {
         const int m = min(r, M - 1);   // clamped: loaded, never stored
         const int row = p.a_rows ? p.a_rows[m] : m;
-        src[j] = p.A + (int64_t)row * p.lda + ch * 8 + k0;
+        const bf16* abase = (p.a_sel && (p.a_sel[row] & 1)) ? p.A2 : p.A;
+        src[j] = abase + (int64_t)row * p.lda + ch * 8 + k0;
       } else {
         const int n = n0 + r;
         src[j] = (n >= nb ? p.B2 + (int64_t)(n - nb) * p.ldb : p.B + (int64_t)n * p.ldb) +
@@ -1281,13 +1286,15 @@ GP to_gp(const GemmArgs& g) {
   p.rope_cos = g.rope_cos; p.rope_sin = g.rope_sin; p.head_dim = g.head_dim; p.d_q = g.d_q;
   p.q_out = (bf16*)g.q_out; p.k_cache = (bf16*)g.k_cache; p.v_cache = (bf16*)g.v_cache;
   p.bias_layer_stride = g.bias_layer_stride; p.a_sorted = g.a_sorted;
+  p.A2 = (const bf16*)g.A2; p.a_sel = g.a_sel;
   return p;
 }
 
 bool aligned8(const void* p) { return ((uintptr_t)p & 7u) == 0; }
 
 bool aligned_operands(const GemmArgs& g) {
-  return aligned16(g.A) && aligned16(g.B) && (!g.B2 || aligned16(g.B2)) && g.lda % 8 == 0 &&
+  return aligned16(g.A) && aligned16(g.B) && (!g.B2 || aligned16(g.B2)) &&
+         (!g.a_sel || (g.A2 && aligned16(g.A2))) && g.lda % 8 == 0 &&
          g.ldb % 8 == 0;
 }
 

@@ -5,9 +5,15 @@
 //
 // With one query row per sequence (decode) no row of the pass reads another
 // row's cache entries, so the K/V a row generates for its skipped layers
-// (Eq. 9) are needed only by later passes: the generation of all rows is
-// then deferred to the end of layer N, as one grouped GEMM in which each
-// skipped layer's Wk/Wv is read once, instead of once per exit layer.
+// (Eq. 9) are needed only by later passes.  Two schedules use that:
+//  * deferred: the generation of all rows runs after layer N, as one grouped
+//    GEMM in which each skipped layer's Wk/Wv is read once;
+//  * fused (kv_fused): layer r's QKV GEMM also takes the rows that exited
+//    before r, reading their exit state, so their K/V at layer r come out of
+//    the GEMM that reads layer r's weights anyway (Eq. 6 leaves the order of
+//    the generation free); the Q columns of those rows are computed and
+//    ignored.  In a decode pass the GEMM streams its weights once whatever
+//    its row count, so the generation costs no weight traffic.
 #include <algorithm>
 
 #include "common.h"
@@ -22,7 +28,8 @@ struct LayerWs {
   void* compact;  size_t compact_bytes;
   void* attend;   size_t attend_bytes;
   void* kvgen;    size_t kvgen_bytes;
-  int32_t* all_rows;  // [n_tok + 64]: rows 0..n_tok-1 and their count (deferred KV generation)
+  int32_t* all_rows;  // [n_tok + 64]: row list and its count (deferred / fused KV generation)
+  int32_t* fsel;      // [n_tok]: fused schedule, 1 where a row's exit state is in h[layer & 1]
   void* prompt;   size_t prompt_bytes;   // per-sequence keys of the all-at-once variant
   void* hsm;      size_t hsm_bytes;      // mapper activations (when a mapper is given)
   float* skinny;  size_t skinny_bytes;   // GEMM partial sums when n_tok <= 64 (decode)
@@ -51,6 +58,7 @@ LayerWs carve(const adept_layer_args* a, void* base) {
     off += align256((size_t)a->n_tok * a->d_model * 2);
   }
   w.all_rows = (int32_t*)(p + off); off += align256(((size_t)a->n_tok + 64) * sizeof(int32_t));
+  w.fsel = (int32_t*)(p + off); off += align256((size_t)a->n_tok * sizeof(int32_t));
   w.prompt_bytes = adept_exit_prompt_level_workspace_bytes(a->n_seq);
   w.prompt = p + off; off += align256(w.prompt_bytes);
   w.hsm_bytes = a->hsm ? adept_hsm_workspace_bytes(a->d_model, a->n_tok) : 0;
@@ -92,6 +100,36 @@ __global__ __launch_bounds__(64) void defer_rows_kernel(int n_tok, int n_layers,
   const int64_t base = (int64_t)j * row_bytes;
   for (int o = threadIdx.x * 16; o < row_bytes; o += 64 * 16)
     *reinterpret_cast<uint4*>(h_last + base + o) = *reinterpret_cast<const uint4*>(h_other + base + o);
+}
+
+// Fused schedule, the row list of layer `layer`'s QKV GEMM: the active rows
+// (as listed) followed by the rows that exited at a layer below `layer`
+// (ascending), and its count; sel[row] = 1 where the row's state (its exit
+// state) sits in h[layer & 1] rather than h[(layer-1) & 1].  One workgroup;
+// wave 0 walks the rows 64 at a time with a ballot.
+__global__ __launch_bounds__(256) void fused_rows_kernel(int n_tok, int layer,
+                                                         const int32_t* __restrict__ exit_layer,
+                                                         const int32_t* __restrict__ act,
+                                                         const int32_t* __restrict__ n_act,
+                                                         int max_act, int32_t* __restrict__ list,
+                                                         int32_t* __restrict__ count,
+                                                         int32_t* __restrict__ sel) {
+  const int na = min(*n_act, max_act);
+  for (int k = threadIdx.x; k < na; k += blockDim.x) list[k] = act[k];
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  const int par = (layer - 1) & 1;
+  int off = 0;
+  for (int base = 0; base < n_tok; base += 64) {
+    const int row = base + lane;
+    const int el = row < n_tok ? exit_layer[row] : INT_MAX;
+    const bool ex = el < layer;
+    const uint64_t m = __ballot(ex);
+    if (ex) list[na + off + __popcll(m & ((1ull << lane) - 1))] = row;
+    if (row < n_tok) sel[row] = ex && (el & 1) != par;
+    off += __popcll(m);
+  }
+  if (lane == 0) *count = na + off;
 }
 
 adept_status run_gemm(adept_dtype dt, const GemmArgs& g, float* tmp, hipStream_t s) {
@@ -153,6 +191,8 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
                     a->exited && a->n_exited && a->exit_layer && a->exit_flag && a->k_cache &&
                     a->v_cache && a->q_buf && a->attn_out && a->ffn_act,
                 "layer_step: NULL pointer in args");
+  ADEPT_REQUIRE(!a->kv_fused || (dt == ADEPT_BF16 && a->attn_tiles == 0),
+                "layer_step: kv_fused needs bf16 and a decode pass (attn_tiles = 0)");
   ADEPT_REQUIRE(a->exit.metric == ADEPT_SIM_LOCAL || a->inertia,
                 "layer_step: GLOBAL/BOTH metrics need inertia");
   ADEPT_REQUIRE(!a->hsm || (dt == ADEPT_BF16 && a->exit.metric != ADEPT_SIM_LOCAL && a->inertia),
@@ -182,18 +222,31 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   void* kc = (void*)off(a->k_cache, li * a->n_slots * dq);
   void* vc = (void*)off(a->v_cache, li * a->n_slots * dq);
 
-  if (maxn > 0 && gpt2) {
+  // fused schedule: the QKV GEMM's rows are the active rows, then the rows
+  // that exited earlier in the pass (their K/V at this layer, Eq. 9)
+  const bool fused = a->kv_fused != 0;
+  const int32_t* qrows = act;         // rows of the QKV GEMM
+  const int32_t* nq = nact;
+  const int qmax = fused ? a->n_tok : maxn;
+  if (fused) {
+    ADEPT_LAUNCH(fused_rows_kernel, dim3(1), dim3(256), 0, s, a->n_tok, layer, a->exit_layer, act,
+                 nact, maxn, ws.all_rows, ws.all_rows + a->n_tok, ws.fsel);
+    ADEPT_CHECK_LAUNCH("fused_rows");
+    qrows = ws.all_rows;
+    nq = ws.all_rows + a->n_tok;
+  }
+  if (qmax > 0 && gpt2) {
     // LayerNorm family: norms without their affine part (folded into the
     // weights and biases), biased projections, tanh GELU, no RoPE
     const void* bqkv = off(a->b_qkv, li * 3 * dq);
-    // 1. LN1 of the active rows (compact order)
-    ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[in], a->h[in], nullptr, act, nact, maxn,
-                                 nullptr, nullptr, ws.xnorm, s));
+    // 1. LN1 of the QKV rows (compact order; an exited row from its exit state)
+    ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[in], a->h[out], fused ? ws.fsel : nullptr,
+                                 qrows, nq, qmax, nullptr, nullptr, ws.xnorm, s));
     // 2. Q/K/V with bias, own K/V into cache[layer]
     GemmArgs g{};
-    g.M_max = maxn; g.M_dev = nact; g.N = 3 * dq; g.K = D;
+    g.M_max = qmax; g.M_dev = nq; g.N = 3 * dq; g.K = D;
     g.A = ws.xnorm; g.lda = D; g.B = wqkv; g.ldb = D; g.epi = EPI_QKV; g.bias = bqkv;
-    g.rows = act; g.pos = a->pos; g.slot = a->slot; g.head_dim = hd; g.d_q = dq;
+    g.rows = qrows; g.pos = a->pos; g.slot = a->slot; g.head_dim = hd; g.d_q = dq;
     g.q_out = a->q_buf; g.k_cache = kc; g.v_cache = vc; g.name = "gemm_qkv";
     g.skinny_ws = ws.skinny; g.skinny_ws_bytes = ws.skinny_bytes;
     ADEPT_TRY(gemm(dt, g, s));
@@ -228,16 +281,18 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     gd.C = a->h[out]; gd.ldc = D; gd.resid = a->h[out]; gd.rows = act; gd.name = "gemm_proj";
     gd.skinny_ws = ws.skinny; gd.skinny_ws_bytes = ws.skinny_bytes;
     ADEPT_TRY(gemm(dt, gd, s));
-  } else if (maxn > 0) {
+  } else if (qmax > 0) {
     // 1. pre-attention RMSNorm: the gain is folded into W_qkv, the row factor
     //    1/rms(h) scales the GEMM accumulators
-    ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[in], act, nact, maxn, ws.rinv, s));
-    // 2. Q/K/V projections of the gathered active rows, RoPE, own K/V into cache[layer]
+    ADEPT_TRY(row_rinv_sel(dt, D, a->rms_eps, a->h[in], a->h[out], fused ? ws.fsel : nullptr,
+                           qrows, nq, qmax, ws.rinv, s));
+    // 2. Q/K/V projections of the gathered rows, RoPE, own K/V into cache[layer]
     GemmArgs g{};
-    g.M_max = maxn; g.M_dev = nact; g.N = 3 * dq; g.K = D;
-    g.A = a->h[in]; g.a_rows = act; g.lda = D; g.B = wqkv; g.ldb = D; g.epi = EPI_QKV;
+    g.M_max = qmax; g.M_dev = nq; g.N = 3 * dq; g.K = D;
+    g.A = a->h[in]; g.a_rows = qrows; g.lda = D; g.B = wqkv; g.ldb = D; g.epi = EPI_QKV;
+    if (fused) { g.A2 = a->h[out]; g.a_sel = ws.fsel; }
     g.row_scale = ws.rinv;
-    g.rows = act; g.pos = a->pos; g.slot = a->slot;
+    g.rows = qrows; g.pos = a->pos; g.slot = a->slot;
     g.rope_cos = a->rope_cos; g.rope_sin = a->rope_sin; g.head_dim = hd; g.d_q = dq;
     g.q_out = a->q_buf; g.k_cache = kc; g.v_cache = vc; g.name = "gemm_qkv";
     g.skinny_ws = ws.skinny; g.skinny_ws_bytes = ws.skinny_bytes;
@@ -291,7 +346,7 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   // 10. K/V of the skipped layers of the rows that exited here (Eq. 9); in
   //     decode, of every row that exited in the pass, after layer N
   const bool defer = a->attn_tiles == 0;
-  if (defer && layer == N) {
+  if (defer && !fused && layer == N) {
     const int rb = D * (dt == ADEPT_BF16 ? 2 : 4);
     ADEPT_LAUNCH(defer_rows_kernel, dim3(a->n_tok), dim3(64), 0, s, a->n_tok, N, rb,
                  a->exit_layer, (const char*)a->h[(N + 1) & 1], (char*)a->h[N & 1], ws.all_rows,

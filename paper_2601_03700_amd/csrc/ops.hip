@@ -67,9 +67,12 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int d, float eps, const T*
   for (int c = lane; c < d; c += 64) st(o + c, ld(x + c) * r * ld(gain + c));
 }
 
-// One wave per row: out[k] = 1/sqrt(mean(x[row]^2) + eps).
+// One wave per row: out[k] = 1/sqrt(mean(x[row]^2) + eps), x = x1 when
+// sel && (sel[row] & 1), else x0.
 template <typename T>
-__global__ __launch_bounds__(256) void row_rinv_kernel(int d, float eps, const T* __restrict__ x,
+__global__ __launch_bounds__(256) void row_rinv_kernel(int d, float eps, const T* __restrict__ x0,
+                                                       const T* __restrict__ x1,
+                                                       const int32_t* __restrict__ sel,
                                                        const int32_t* __restrict__ rows,
                                                        const int32_t* __restrict__ n_dev,
                                                        int max_n, float* __restrict__ out) {
@@ -77,7 +80,8 @@ __global__ __launch_bounds__(256) void row_rinv_kernel(int d, float eps, const T
   const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int n = n_dev ? min(*n_dev, max_n) : max_n;
   if (k >= n) return;
-  const T* xr = x + (int64_t)(rows ? rows[k] : k) * d;
+  const int row = rows ? rows[k] : k;
+  const T* xr = ((sel && (sel[row] & 1)) ? x1 : x0) + (int64_t)row * d;
   float ss = 0.0f;
   constexpr int V = 16 / sizeof(T);   // elements per 16-byte load
   if (d % V == 0 && ((uintptr_t)xr & 15) == 0) {
@@ -180,17 +184,23 @@ adept_status rmsnorm_rows(adept_dtype dt, int d, float eps, const void* x, const
   return rmsnorm_rows_sel(dt, d, eps, x, x, nullptr, rows, n_dev, max_n, gain, out, s);
 }
 
-adept_status row_rinv(adept_dtype dt, int d, float eps, const void* x, const int32_t* rows,
-                      const int32_t* n_dev, int max_n, float* out, hipStream_t s) {
+adept_status row_rinv_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
+                          const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
+                          int max_n, float* out, hipStream_t s) {
   if (max_n <= 0) return ADEPT_OK;
   dim3 grid(ceil_div(max_n, 4)), block(256);
   if (dt == ADEPT_BF16)
-    ADEPT_LAUNCH(row_rinv_kernel<bf16>, grid, block, 0, s, d, eps, (const bf16*)x, rows, n_dev,
-                 max_n, out);
+    ADEPT_LAUNCH(row_rinv_kernel<bf16>, grid, block, 0, s, d, eps, (const bf16*)x0,
+                 (const bf16*)x1, sel, rows, n_dev, max_n, out);
   else
-    ADEPT_LAUNCH(row_rinv_kernel<float>, grid, block, 0, s, d, eps, (const float*)x, rows, n_dev,
-                 max_n, out);
+    ADEPT_LAUNCH(row_rinv_kernel<float>, grid, block, 0, s, d, eps, (const float*)x0,
+                 (const float*)x1, sel, rows, n_dev, max_n, out);
   return launch_status("row_rinv");
+}
+
+adept_status row_rinv(adept_dtype dt, int d, float eps, const void* x, const int32_t* rows,
+                      const int32_t* n_dev, int max_n, float* out, hipStream_t s) {
+  return row_rinv_sel(dt, d, eps, x, x, nullptr, rows, n_dev, max_n, out, s);
 }
 
 }  // namespace adept

@@ -87,8 +87,11 @@ class DecoderModel:
     """
 
     def __init__(self, shape, weights, dtype="bf16", device="cuda", rope_max_pos=4096,
-                 hsm_weights=None):
+                 hsm_weights=None, kv_fused=True):
         self.shape = shape
+        # decode passes in bf16: exited rows' K/V from the later layers' QKV
+        # GEMMs (True) or one grouped generation after the last layer (False)
+        self.kv_fused = kv_fused
         self.dtype = dtype
         self.tdt = _TORCH_DT[dtype]
         self.device = torch.device(device)
@@ -229,6 +232,7 @@ class DecoderModel:
         a.b_fc, a.b_proj = B.ptr(self.b_fc), B.ptr(self.b_proj)
         a.n_tok, a.max_active, a.n_seq, a.s_max = st.n_tok, st.n_tok, cache.n_seq, cache.s_max
         a.attn_tiles = int(attn_tiles)
+        a.kv_fused = int(bool(self.kv_fused) and not attn_tiles and self.dtype == "bf16")
         a.h[0], a.h[1] = B.ptr(st.h[0]), B.ptr(st.h[1])
         a.inertia, a.pos, a.seq, a.slot = B.ptr(st.inertia), B.ptr(st.pos), B.ptr(st.seq), B.ptr(st.slot)
         a.active[0], a.active[1] = B.ptr(st.active[0]), B.ptr(st.active[1])

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), f"{n} declared in adept.h but not exported"
     assert set(names) == set(B.EXPORTED), "binding signatures and header differ"
-    assert lib.adept_abi_version() == 4
+    assert lib.adept_abi_version() == 5
 
 
 @pytest.mark.parametrize("cname,pyname", [("adept_layer_args", "LayerArgs"),

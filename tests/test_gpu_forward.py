@@ -191,12 +191,14 @@ def test_small_bf16_prefill_teacher_forced(metric):
     assert policy_exits > 0 and np.sum(el < shape.n_layers) < el.size
 
 
-def test_small_bf16_decode_teacher_forced():
+@pytest.mark.parametrize("kv_fused", [True, False])
+def test_small_bf16_decode_teacher_forced(kv_fused):
     """bf16 generation: a prompt with a seeded schedule, then six decode
-    passes (one row per sequence: key-chunked attention, skinny GEMMs, KV
-    generation deferred to the end of the pass), each pass checked layer by
+    passes (one row per sequence: key-chunked attention, skinny GEMMs, the
+    K/V of exited rows from the later layers' QKV GEMMs or deferred to one
+    grouped generation after the last layer), each pass checked layer by
     layer on the GPU's own inputs, generated K/V included."""
-    say("small bf16 decode teacher-forced")
+    say(f"small bf16 decode teacher-forced kv_fused={kv_fused}")
     shape = SMALL_BF16
     N = shape.n_layers
     w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
@@ -207,7 +209,7 @@ def test_small_bf16_decode_teacher_forced():
     rng = np.random.default_rng(6)
     force_p = rng.integers(0, N + 1, size=ids.shape).astype(np.int32)
     force_s = rng.integers(1, N + 1, size=(S, Bn)).astype(np.int32)   # every step token exits
-    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512)
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=512, kv_fused=kv_fused)
     cfg_g = B.exit_cfg(math.inf, N, "global")
     cfg_o = O.ExitConfig(delta=math.inf)
     rep = LC.Report(say)
@@ -282,13 +284,14 @@ def test_7b_prefill_teacher_forced(w7b):
     torch.cuda.empty_cache()
 
 
-def test_7b_width_decode_teacher_forced(w7b):
+@pytest.mark.parametrize("kv_fused", [True, False])
+def test_7b_width_decode_teacher_forced(w7b, kv_fused):
     """Decode at the 7B layer shapes (64 sequences): the skinny stream-K GEMMs
     at their real shapes (ranges straddling column tiles for QKV, gate/up and
     down), key-chunked attention, the deferred KV generation; prompt and
     decode pass checked layer by layer on the GPU's own inputs."""
     shape = SHAPE_7B_4L
-    say("7B-width decode teacher-forced")
+    say(f"7B-width decode teacher-forced kv_fused={kv_fused}")
     w32, w = w7b
     N = shape.n_layers
     Bn, T = 64, 2
@@ -297,7 +300,7 @@ def test_7b_width_decode_teacher_forced(w7b):
     rng = np.random.default_rng(24)
     force_p = rng.integers(0, N + 1, size=ids.shape).astype(np.int32)
     force_s = rng.integers(1, N + 1, size=Bn).astype(np.int32)
-    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=64)
+    model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=64, kv_fused=kv_fused)
     cfg_g = B.exit_cfg(math.inf, N, "global")
     cfg_o = O.ExitConfig(delta=math.inf)
     rep = LC.Report(say)
@@ -307,6 +310,63 @@ def test_7b_width_decode_teacher_forced(w7b):
                         force=force_s, rep=rep)
     rep.summary()
     assert 0 < int(np.sum(chk.exit_layer < N)) < Bn
+
+
+def test_decode_schedules_agree():
+    """The fused and the deferred decode schedules fill the same cache: a
+    prompt, then three decode passes with a seeded schedule, run once per
+    schedule from the same prompt cache.  After the first pass every cache
+    entry is within one bf16 rounding of the other schedule's (the two GEMMs
+    sum in different orders); later passes attend to those entries, so after
+    the last one the bound is the per-element bf16 bound; exit layers equal,
+    logits within 2e-2; the entries no pass wrote stay as the prompt left
+    them."""
+    say("decode schedules agree")
+    shape = SMALL_BF16
+    N = shape.n_layers
+    w32 = ai.decoder_weights(shape, seed=9, dtype="bf16", std=0.03)
+    Bn, T, S = 5, 24, 3
+    ids = ai.token_ids(15, shape.vocab, Bn, T)
+    step_ids = ai.token_ids(16, shape.vocab, S, Bn)
+    rng = np.random.default_rng(17)
+    force_s = rng.integers(1, N + 1, size=(S, Bn)).astype(np.int32)
+    cfg = B.exit_cfg(math.inf, N, "global")
+    outs = []
+    base = None
+    for fused in (True, False):
+        model = DecoderModel(shape, w32, dtype="bf16", rope_max_pos=64, kv_fused=fused)
+        _, cache = model.prefill(ids, cfg, s_max=T + S, logits="last")
+        if base is None:
+            base = (cache.k.clone(), cache.v.clone())
+        logits, els, first = [], [], None
+        for s in range(S):
+            r = model.decode_step(cache, torch.from_numpy(step_ids[s]).to("cuda", torch.int32),
+                                  torch.full((Bn,), T + s, dtype=torch.int32, device="cuda"), cfg,
+                                  force_layer=torch.from_numpy(force_s[s]).to("cuda", torch.int32),
+                                  pos_max=T + s)
+            logits.append(r.logits.clone())
+            els.append(r.exit_layer.clone())
+            if s == 0:
+                first = (cache.k.clone(), cache.v.clone())
+        torch.cuda.synchronize()
+        outs.append((cache, logits, els, first))
+    (c1, l1, e1, f1), (c2, l2, e2, f2) = outs
+    for a, b in zip(e1, e2):
+        assert torch.equal(a, b)
+    for a, b in zip(l1, l2):
+        assert float((a - b).abs().max()) <= 2e-2
+    for a, b in zip(f1, f2):
+        a, b = a.float(), b.float()
+        ulp = torch.maximum(b.abs(), torch.full_like(b, 2.0 ** -126)) * 2.0 ** -7
+        assert bool(((a - b).abs() <= ulp).all())
+        assert int((a != b).sum()) <= a.numel() // 100
+    for x1, x2, x0 in ((c1.k, c2.k, base[0]), (c1.v, c2.v, base[1])):
+        a, b = x1.float(), x2.float()
+        assert bool(((a - b).abs() <= torch.clamp(b.abs() * 2.0 ** -7, min=2e-2)).all())
+        untouched = torch.ones(N, Bn, T + S, dtype=torch.bool, device=a.device)
+        untouched[:, :, T:] = False     # decode slots (written by one schedule or the other)
+        u = untouched.reshape(N, Bn * (T + S))
+        assert torch.equal(x1[u], x0[u]) and torch.equal(x2[u], x0[u])
 
 
 def test_timing_select_prefix():

@@ -164,19 +164,20 @@ def test_gpt2_small_prefill_teacher_forced(w_small, metric):
     assert policy_exits > 0 and np.sum(el == SMALL.n_layers) > 0
 
 
-def test_gpt2_small_decode_teacher_forced(w_small):
+@pytest.mark.parametrize("kv_fused", [True, False])
+def test_gpt2_small_decode_teacher_forced(w_small, kv_fused):
     """Decode at the small shape: a prompt of 24 sequences x 9 rows, then one
     step per sequence (skinny GEMMs with biases and the tanh-GELU epilogue,
     key-chunked attention, the deferred LayerNorm KV generation), both
     checked layer by layer; then a second step over the generated entries."""
-    say("gpt2 small decode teacher-forced")
+    say(f"gpt2 small decode teacher-forced kv_fused={kv_fused}")
     w, w64 = w_small
     N = SMALL.n_layers
     Bn, T = 24, 9
     ids = ai.token_ids(45, SMALL.vocab, Bn, T)
     rng = np.random.default_rng(46)
     force_p = rng.integers(0, N + 1, size=ids.shape).astype(np.int32)
-    model = DecoderModel(SMALL, w, dtype="bf16")
+    model = DecoderModel(SMALL, w, dtype="bf16", kv_fused=kv_fused)
     rep = LC.Report(say)
     _, cache, _ = _tf_prefill(model, w64, SMALL, ids, math.inf, "global", force_p, rep,
                               s_max=T + 2, logits="last")
