@@ -575,13 +575,31 @@ def classify_logits(weights, cls_states):
             + np.asarray(weights["cls_b"], F64))
 
 
-def classify(weights, shape, ids, cfg, force_layer=None):
+def cls_stop(flags, active, seq_len):
+    """Early stop of a classification sequence (Section 4.3: the computation
+    ends once the state that feeds the classifier has exited): a row leaves
+    at the layer where its sequence's [CLS] row (row b * seq_len, position 0)
+    exits, or at once if that row is no longer active.  flags [n] over the
+    active rows (ascending)."""
+    act = np.asarray(active)
+    flags = np.asarray(flags, bool)
+    if act.size == 0:
+        return flags
+    cls = (act // seq_len) * seq_len
+    k = np.minimum(np.searchsorted(act, cls), act.size - 1)
+    present = act[k] == cls
+    return flags | ~present | flags[k]
+
+
+def classify(weights, shape, ids, cfg, force_layer=None, stop_at_cls=True):
     """Token-level exit in an encoder classifier.
 
     Readings: exited tokens stop entirely (no KV generation) and leave the
     key set of later layers; a sequence's output is the [CLS] (position 0)
     state at its exit, fed to the linear head.  Tokens of a sequence whose
-    [CLS] has exited no longer influence the output."""
+    [CLS] has exited no longer influence the output, so with stop_at_cls
+    they leave at that layer too (cls_stop); the logits are the same either
+    way."""
     ids = np.asarray(ids)
     B, T = ids.shape
     N, D, H, hd = shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim
@@ -611,6 +629,8 @@ def classify(weights, shape, ids, cfg, force_layer=None):
             f = np.asarray(force_layer).reshape(-1)[active]
             forced = f > 0
             flags = np.where(forced, (f == i) & (i <= N - 1), flags)
+        if stop_at_cls:
+            flags = cls_stop(flags, active, T)
         if cfg.metric != LOCAL and active.size:
             inertia[active] = inertia_update(inertia[active], h[active])
         active, exited = compact(flags, active)

@@ -444,6 +444,48 @@ def test_classify_exits_drop_tokens_from_later_keys():
     np.testing.assert_allclose(res.h_final.reshape(B, T, -1), h.numpy(), rtol=0, atol=1e-12)
 
 
+@pytest.mark.parametrize("force", [False, True])
+def test_classify_stop_at_cls(force):
+    """Stopping a sequence when its [CLS] row exits changes nothing the
+    classifier sees: the logits are identical to the run that keeps the other
+    tokens going, and each token's exit layer is the smaller of its own (in
+    that run) and its [CLS] row's; with the policy, some tokens are stopped
+    early and some exit on their own before their [CLS]."""
+    w = O.as64(ai.encoder_weights(ENC, seed=24))
+    ids = ai.token_ids(25, ENC.vocab, 4, 12)
+    B, T = ids.shape
+    fl = None
+    if force:
+        fl = np.random.default_rng(26).integers(0, ENC.n_layers + 1, size=ids.shape)
+        fl[:, 0] = [1, 2, 3, 0]
+        delta = math.inf
+    else:
+        full = O.classify(w, ENC, ids, O.ExitConfig(delta=math.inf), stop_at_cls=False)
+        fin = np.sort(full.sims[:ENC.n_layers - 1][np.isfinite(full.sims[:ENC.n_layers - 1])])
+        q = fin.size // 2
+        delta = float(0.5 * (fin[q - 1] + fin[q]))      # between two similarities
+    cfg = O.ExitConfig(delta=delta)
+    go = O.classify(w, ENC, ids, cfg, force_layer=fl, stop_at_cls=False)
+    st = O.classify(w, ENC, ids, cfg, force_layer=fl, stop_at_cls=True)
+    # equal up to the summation order of the batched products (fewer rows)
+    np.testing.assert_allclose(st.logits, go.logits, rtol=0, atol=1e-14)
+    np.testing.assert_array_equal(st.cls_exit_layer, go.cls_exit_layer)
+    el_go, el_st = go.exit_layer.reshape(B, T), st.exit_layer.reshape(B, T)
+    np.testing.assert_array_equal(el_st, np.minimum(el_go, el_go[:, :1]))
+    assert (el_st < el_go).any() and ((el_st < el_st[:, :1]).any() or force)
+
+
+def test_cls_stop_rule():
+    """cls_stop on a hand-made list: rows 0..3 are sequence 0, 4..7 sequence 1,
+    8..11 sequence 2 (seq_len 4).  Sequence 0's [CLS] (row 0) exits now,
+    sequence 1's [CLS] (row 4) has already left, sequence 2's stays."""
+    active = np.array([0, 2, 3, 5, 7, 8, 9, 11])
+    flags = np.array([1, 0, 0, 0, 0, 0, 1, 0], bool)
+    out = O.cls_stop(flags, active, 4)
+    np.testing.assert_array_equal(out, [1, 1, 1, 1, 1, 0, 1, 0])
+    assert O.cls_stop(np.zeros(0, bool), np.zeros(0, np.int64), 4).size == 0
+
+
 # --------------------------------------------------------------------------
 # Section 6 accounting (values printed in the paper)
 # --------------------------------------------------------------------------
