@@ -499,8 +499,9 @@ adept_status adept_argmax(int n, int vocab, const float* logits, int32_t* out, v
  * key_live byte is 1 (bidirectional, keys < key_len[b]) -> O GEMM + bias +
  * residual into y_buf -> LayerNorm 1 (in place) -> GEMM + bias + GELU into
  * ffn_act -> GEMM + bias + residual into h[i&1] -> LayerNorm 2 (in place)
- * -> adept_exit_test -> adept_compact -> key_live[row] = 0 for the rows that
- * exited.  Before layer 1 the caller runs adept_encoder_embed into h[0],
+ * -> adept_exit_test -> [cls_stop: the flags of rows whose sequence's [CLS]
+ * row exits here or has left are set] -> adept_compact -> key_live[row] = 0
+ * for the rows that exited.  Before layer 1 the caller runs adept_encoder_embed into h[0],
  * adept_token_init, and sets key_live to 1 for every row.  A row's final
  * state is h[exit_layer & 1][row].
  * ------------------------------------------------------------------------- */
@@ -523,7 +524,9 @@ typedef struct {
   const void* ln2_g;    /* [N][D] */
   const void* ln2_b;    /* [N][D] */
   int32_t n_tok, n_seq, seq_len;   /* n_tok = n_seq * seq_len */
-  int32_t reserved;
+  int32_t cls_stop;     /* 1: a row also leaves at the layer where its sequence's
+                           [CLS] row exits (or at once if that row is no longer
+                           active): the output no longer depends on it */
   void* h[2];            /* [n_tok][D] residual stream ping-pong */
   float* inertia;        /* [n_tok][D] (GLOBAL and BOTH metrics) */
   const int32_t* pos;    /* [n_tok] position of row j (j mod seq_len) */

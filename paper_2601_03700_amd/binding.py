@@ -68,7 +68,7 @@ class EncoderArgs(ctypes.Structure):
         ("w_qkv", _vp), ("b_qkv", _vp), ("w_o", _vp), ("b_o", _vp), ("ln1_g", _vp),
         ("ln1_b", _vp), ("w_in", _vp), ("b_in", _vp), ("w_out", _vp), ("b_out", _vp),
         ("ln2_g", _vp), ("ln2_b", _vp),
-        ("n_tok", _i32), ("n_seq", _i32), ("seq_len", _i32), ("reserved", _i32),
+        ("n_tok", _i32), ("n_seq", _i32), ("seq_len", _i32), ("cls_stop", _i32),
         ("h", _vp * 2), ("inertia", _vp), ("pos", _vp), ("seq", _vp),
         ("active", _vp * 2), ("n_active", _vp * 2), ("exited", _vp), ("n_exited", _vp),
         ("exit_layer", _vp), ("exit_flag", _vp), ("sim_out", _vp), ("force_layer", _vp),

@@ -211,5 +211,11 @@ adept_status layernorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0
                                 const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
                                 int max_n, const void* gain, const void* bias, void* out,
                                 hipStream_t s);
+// the same, writing out[row] instead of out[k] when out_by_row (bf16 rows of
+// a multiple of 8 elements up to 4096, 16-byte aligned; may run in place)
+adept_status layernorm_rows_any(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
+                                const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
+                                int max_n, const void* gain, const void* bias, void* out,
+                                bool out_by_row, hipStream_t s);
 
 }  // namespace adept

@@ -74,6 +74,28 @@ __global__ __launch_bounds__(256) void encoder_embed_kernel(
   for (int c = lane; c < d; c += 64) o[c] = f2bf((val(c) - mean) * r * bf2f(g[c]) + bf2f(b[c]));
 }
 
+// Early stop of a sequence (the computation ends once the state that feeds
+// the classifier has exited): the flag of active row k is set when its
+// sequence's [CLS] row (row b * seq_len) is flagged at this layer or is no
+// longer active.  The list is ascending, so the [CLS] row, when active, is
+// found by binary search; only the [CLS] row's own thread could write the
+// flag that others read, and it writes back the value it read.
+__global__ void cls_stop_kernel(const int32_t* __restrict__ act, const int32_t* __restrict__ n_act,
+                                int max_n, int seq_len, uint8_t* __restrict__ flag) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = min(*n_act, max_n);
+  if (k >= n) return;
+  const int row = act[k];
+  const int cls = row - row % seq_len;
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (act[mid] < cls) lo = mid + 1; else hi = mid;
+  }
+  const bool stop = lo >= n || act[lo] != cls || flag[lo] != 0;
+  if (stop) flag[k] = 1;
+}
+
 // key_live[exited[k]] = 0 for k < min(*n_exited, max_n).
 __global__ void mark_dead_kernel(const int32_t* __restrict__ exited,
                                  const int32_t* __restrict__ n_exited, int max_n,
@@ -101,6 +123,9 @@ adept_status layernorm_rows(int d, float eps, const void* x, const int32_t* rows
                             const int32_t* n_dev, int max_n, const void* g, const void* b,
                             void* out, hipStream_t s) {
   if (max_n <= 0) return ADEPT_OK;
+  if (d % 8 == 0 && d <= 4096 && aligned16(x) && aligned16(out) && aligned16(g) && aligned16(b))
+    return layernorm_rows_any(ADEPT_BF16, d, eps, x, x, nullptr, rows, n_dev, max_n, g, b, out,
+                              true, s);
   ADEPT_LAUNCH(layernorm_kernel, dim3(ceil_div(max_n, 4)), dim3(256), 0, s, d, eps,
                (const bf16*)x, rows, n_dev, max_n, (const bf16*)g, (const bf16*)b, (bf16*)out);
   return launch_status("layernorm");
@@ -260,6 +285,11 @@ extern "C" adept_status adept_encoder_layer_step(const adept_encoder_args* a, in
   // 6. exit test (Eq. 7-8), active-list update, exited keys leave the key set
   ADEPT_TRY(adept_exit_test(ADEPT_BF16, D, layer, &a->exit, act, nact, maxn, a->h[out], a->h[in],
                             a->inertia, a->force_layer, a->exit_flag, a->sim_out, stream));
+  if (a->cls_stop && maxn > 0) {
+    ADEPT_LAUNCH(cls_stop_kernel, dim3(ceil_div(maxn, 256)), dim3(256), 0, s, act, nact, maxn,
+                 a->seq_len, a->exit_flag);
+    ADEPT_CHECK_LAUNCH("cls_stop");
+  }
   ADEPT_TRY(adept_compact(layer, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
                           a->exited, a->n_exited, a->exit_layer, ws.compact, ws.compact_bytes,
                           stream));

@@ -51,6 +51,75 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(
   }
 }
 
+// The same for bf16 rows held in registers: lane l holds the 8-element
+// chunks l, l+64, ..., (R of them; d a multiple of 8, rows 16-byte aligned),
+// so the row crosses HBM once each way and every access is a 16-byte
+// vector.  Mean and variance in f32 from the registers (two passes);
+// out row = out_by_row ? row : k (in place when out == x0 == x1).
+template <int R>
+__global__ __launch_bounds__(256) void layernorm_vec_kernel(
+    int d, float eps, const bf16* x0, const bf16* x1, const int32_t* __restrict__ sel,
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ n_dev, int max_n,
+    const bf16* __restrict__ gain, const bf16* __restrict__ bias, bf16* out, int out_by_row) {
+  const int lane = threadIdx.x & 63;
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int n = n_dev ? min(*n_dev, max_n) : max_n;
+  if (k >= n) return;
+  const int row = rows ? rows[k] : k;
+  const bf16* x = ((sel && (sel[row] & 1)) ? x1 : x0) + (int64_t)row * d;
+  float v[R][8];
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int c = (lane + 64 * j) * 8;
+    uint4 w = make_uint4(0, 0, 0, 0);
+    if (c < d) w = *reinterpret_cast<const uint4*>(x + c);
+    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[j][2 * e] = __uint_as_float(u[e] << 16);
+      v[j][2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+      s += v[j][2 * e] + v[j][2 * e + 1];
+    }
+  }
+  const float mean = wave_sum_f32(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    if ((lane + 64 * j) * 8 >= d) continue;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float t = v[j][e] - mean;
+      q = fmaf(t, t, q);
+    }
+  }
+  const float r = 1.0f / sqrtf(wave_sum_f32(q) / (float)d + eps);
+  bf16* o = out + (int64_t)(out_by_row ? row : k) * d;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int c = (lane + 64 * j) * 8;
+    if (c >= d) continue;
+    float y[8];
+    if (gain) {
+      const uint4 gw = *reinterpret_cast<const uint4*>(gain + c);
+      const uint4 bw = *reinterpret_cast<const uint4*>(bias + c);
+      const uint32_t gu[4] = {gw.x, gw.y, gw.z, gw.w}, bu[4] = {bw.x, bw.y, bw.z, bw.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y[2 * e] = fmaf((v[j][2 * e] - mean) * r, __uint_as_float(gu[e] << 16),
+                        __uint_as_float(bu[e] << 16));
+        y[2 * e + 1] = fmaf((v[j][2 * e + 1] - mean) * r, __uint_as_float(gu[e] & 0xffff0000u),
+                            __uint_as_float(bu[e] & 0xffff0000u));
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * r;
+    }
+    *reinterpret_cast<uint4*>(o + c) = make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]),
+                                                  pack_bf16x2(y[4], y[5]), pack_bf16x2(y[6], y[7]));
+  }
+}
+
 // h0[k][c] = wte[ids[k]][c] + wpe[pos[k]][c] (ids and positions clamped
 // into the tables), summed in f32 and rounded once.
 template <typename T>
@@ -93,12 +162,39 @@ __global__ __launch_bounds__(256) void fold_bias_kernel(int rows, int cols,
 
 }  // namespace
 
-adept_status layernorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
+adept_status layernorm_rows_any(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
                                 const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
                                 int max_n, const void* gain, const void* bias, void* out,
-                                hipStream_t s) {
+                                bool out_by_row, hipStream_t s) {
   if (max_n <= 0) return ADEPT_OK;
   dim3 grid(ceil_div(max_n, 4)), block(256);
+  const bool vec = dt == ADEPT_BF16 && d % 8 == 0 && d <= 64 * 8 * 8 && aligned16(x0) &&
+                   aligned16(x1) && aligned16(out) && (!gain || (aligned16(gain) && bias &&
+                                                                 aligned16(bias)));
+  if (vec) {
+    const int chunks = ceil_div(d / 8, 64);
+    const bf16 *a0 = (const bf16*)x0, *a1 = (const bf16*)x1;
+    const bf16 *g = (const bf16*)gain, *b = (const bf16*)bias;
+    const int obr = out_by_row ? 1 : 0;
+    if (chunks <= 1)
+      ADEPT_LAUNCH(layernorm_vec_kernel<1>, grid, block, 0, s, d, eps, a0, a1, sel, rows, n_dev,
+                   max_n, g, b, (bf16*)out, obr);
+    else if (chunks <= 2)
+      ADEPT_LAUNCH(layernorm_vec_kernel<2>, grid, block, 0, s, d, eps, a0, a1, sel, rows, n_dev,
+                   max_n, g, b, (bf16*)out, obr);
+    else if (chunks <= 4)
+      ADEPT_LAUNCH(layernorm_vec_kernel<4>, grid, block, 0, s, d, eps, a0, a1, sel, rows, n_dev,
+                   max_n, g, b, (bf16*)out, obr);
+    else
+      ADEPT_LAUNCH(layernorm_vec_kernel<8>, grid, block, 0, s, d, eps, a0, a1, sel, rows, n_dev,
+                   max_n, g, b, (bf16*)out, obr);
+    return launch_status("layernorm_rows");
+  }
+  if (out_by_row) {
+    set_error("layernorm: the in-place form needs bf16 rows of a multiple of 8 up to 4096, "
+              "16-byte aligned");
+    return ADEPT_E_UNSUPPORTED;
+  }
   if (dt == ADEPT_BF16)
     ADEPT_LAUNCH(layernorm_rows_kernel<bf16>, grid, block, 0, s, d, eps, (const bf16*)x0,
                  (const bf16*)x1, sel, rows, n_dev, max_n, (const bf16*)gain, (const bf16*)bias,
@@ -108,6 +204,14 @@ adept_status layernorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0
                  (const float*)x1, sel, rows, n_dev, max_n, (const float*)gain,
                  (const float*)bias, (float*)out);
   return launch_status("layernorm_rows");
+}
+
+adept_status layernorm_rows_sel(adept_dtype dt, int d, float eps, const void* x0, const void* x1,
+                                const int32_t* sel, const int32_t* rows, const int32_t* n_dev,
+                                int max_n, const void* gain, const void* bias, void* out,
+                                hipStream_t s) {
+  return layernorm_rows_any(dt, d, eps, x0, x1, sel, rows, n_dev, max_n, gain, bias, out, false,
+                            s);
 }
 
 }  // namespace adept

@@ -402,10 +402,11 @@ class EncoderModel:
         self.eln_g, self.eln_b = up(weights["embed_ln_g"]), up(weights["embed_ln_b"])
         self.cls_w, self.cls_b = up(weights["cls_w"]), up(weights["cls_b"])
 
-    def classify(self, ids, cfg, force_layer=None, state=None, on_layer=None):
+    def classify(self, ids, cfg, force_layer=None, state=None, on_layer=None, stop_at_cls=True):
         """ids [B, T] (numpy or tensor); cfg from binding.exit_cfg.  A state
         dict from an earlier call of the same shape is reused (no allocation).
-        on_layer(i, state) is called after each layer step (read-back hook)."""
+        on_layer(i, state) is called after each layer step (read-back hook).
+        stop_at_cls: a sequence's rows leave when its [CLS] row exits."""
         s, dev = self.shape, self.device
         ids = torch.as_tensor(np.asarray(ids) if not isinstance(ids, torch.Tensor) else ids)
         Bn, T = ids.shape
@@ -446,6 +447,7 @@ class EncoderModel:
                   "b_out", "ln2_g", "ln2_b"):
             setattr(a, k, B.ptr(getattr(self, k)))
         a.n_tok, a.n_seq, a.seq_len = n, Bn, T
+        a.cls_stop = int(bool(stop_at_cls))
         a.h[0], a.h[1] = B.ptr(st["h"][0]), B.ptr(st["h"][1])
         a.inertia, a.pos, a.seq = B.ptr(st["inertia"]), B.ptr(st["pos"]), B.ptr(st["seq"])
         a.active[0], a.active[1] = B.ptr(st["active"][0]), B.ptr(st["active"][1])

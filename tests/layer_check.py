@@ -277,8 +277,9 @@ class EncoderLayerCheck:
     GPU's layer input (the live rows of each sequence), then the exit test,
     the active-list update and the exit layers as for the decoder."""
 
-    def __init__(self, w, shape, cfg, force_layer=None, report=None):
+    def __init__(self, w, shape, cfg, force_layer=None, report=None, stop_at_cls=True):
         self.w, self.shape, self.cfg = w, shape, cfg
+        self.stop_at_cls = stop_at_cls
         self.force = None if force_layer is None else np.asarray(force_layer).reshape(-1)
         self.rep = report if report is not None else Report()
 
@@ -335,6 +336,9 @@ class EncoderLayerCheck:
             flags_o = np.where(policy, flags_o, (f == i) & (i <= N - 1))
         if cfg.min_exit_layer <= i <= N - 1:
             assert not (policy & fin & (np.abs(sims_o - cfg.delta) <= 1e-11)).any()
+        if self.stop_at_cls:
+            seq_len = st["n"] // (int(self.seq.max()) + 1)
+            flags_o = O.cls_stop(flags_o, act, seq_len)
         flags_g = st["exit_flag"][:n_in].cpu().numpy().astype(bool)
         np.testing.assert_array_equal(flags_g, flags_o, err_msg=f"layer {i} exit flags")
         if self.inertia is not None:
