@@ -39,6 +39,13 @@ Readings of the paper taken here (where it is silent or ambiguous):
   * the "both" metric of Appendix H.3 (not defined there) exits only when
     the global and the local cosine both reach delta; its similarity is
     the smaller of the two, and the inertia is kept as for the global one.
+  * the GPT-2-style family (Section 5's GPT2-XL): Eq. 9 applies layer r's
+    first LayerNorm (gain and shift) and its biased K/V projections to s~;
+    positions enter through the learned position embedding only, so no
+    rotation is applied to generated keys.
+  * classification (Section 4.3): exited tokens leave the key set of later
+    layers and, once a sequence's [CLS] row has exited, its other rows stop
+    with it (the classifier only reads that row).
 """
 from __future__ import annotations
 

@@ -177,7 +177,11 @@ __device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "
 
 // One 256x256 output tile: rows [mt*256, M) against column tile nt of Bm.
 // HD (64 or 128) is the head size of the rotary epilogues (0 otherwise).
-template <int EPI, bool GROUPED, int HD>
+// EXT: the shapes and inputs beyond the plain case -- a ragged last column
+// tile (N not a multiple of 256), cache sections that do not align with the
+// 128-column waves (H*hd not a multiple of 128), a per-row second A buffer;
+// the plain instantiation carries none of their per-lane tests (registers).
+template <int EPI, bool GROUPED, int HD, bool EXT>
 __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, int mt, int nt,
                                           int M, const bf16* Bm) {
   // the wave index in a scalar register: LDS destinations of the direct
@@ -202,7 +206,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
     int m = m0 + r;
     if (m >= M) m = m0;  // clamp: loaded, never stored
     const int arow = GROUPED ? (p.a_sorted ? m : p.srows[m]) : (p.a_rows ? p.a_rows[m] : m);
-    const bf16* abase = (!GROUPED && p.a_sel && (p.a_sel[arow] & 1)) ? p.A2 : p.A;
+    const bf16* abase = (EXT && !GROUPED && p.a_sel && (p.a_sel[arow] & 1)) ? p.A2 : p.A;
     a_src[j] = abase + (int64_t)arow * p.lda + lchunk * 8;
     const bf16* bbase = Bm;
     int64_t brow;
@@ -212,7 +216,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
       brow = (int64_t)nt * 128 + half * 64 + (within & 63);
     } else {
       // a ragged last column tile re-reads the last row: computed, never stored
-      brow = min((int64_t)nt * BN + r, (int64_t)p.N - 1);
+      brow = EXT ? min((int64_t)nt * BN + r, (int64_t)p.N - 1) : (int64_t)nt * BN + r;
     }
     b_src[j] = bbase + brow * p.ldb + lchunk * 8;
   }
@@ -449,9 +453,9 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
   const int nw = nt * BN + wn * 128;      // first output column of this wave
   // grouped: layer r's bias; a ragged column tile's waves past N store
   // nothing (SwiGLU tiles are never ragged: 128 outputs of N per tile)
-  const bf16* bias = GROUPED && p.bias ? p.bias + (int64_t)(layer - 1) * p.bias_layer_stride
+  const bf16* bias = GROUPED && EXT && p.bias ? p.bias + (int64_t)(layer - 1) * p.bias_layer_stride
                                        : p.bias;
-  const bool wave_out = EPI != EPI_SWIGLU && nw >= p.N;
+  const bool wave_out = EXT && EPI != EPI_SWIGLU && nw >= p.N;
   constexpr bool kCache = EPI == EPI_QKV || EPI == EPI_KV;
   const int sec = kCache ? nw / p.d_q : 0;    // QKV: 0 q, 1 k, 2 v;  KV: 0 k, 1 v
   const bool is_q = EPI == EPI_QKV && sec == 0;
@@ -646,7 +650,7 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
         const bool full = mb + 32 <= M;
         const int sg = lane & 15;
         const int col = nw + 8 * sg;
-        const bool col_in = col < p.N;   // N is a multiple of 64: whole 8-column segments
+        const bool col_in = !EXT || col < p.N;   // N is a multiple of 64: whole 8-column segments
         int drow[8];
         float scv[8];
 #pragma unroll
@@ -741,18 +745,12 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
         constexpr bool kRope = EPI == EPI_QKV || EPI == EPI_KV;
         constexpr int G = kRope ? 4 : 8;
         const bool rope = kRope && !is_v && p.rope_cos;   // wave-uniform
-        const bool col_in = nw + c4 < p.N;                // N is a multiple of 4
+        const bool col_in = !EXT || nw + c4 < p.N;        // N is a multiple of 4
         const float4 bx = bias4(col_in ? bias : nullptr, nw + c4);
         const float4 by = rope ? bias4(bias, nw + (c4 ^ half)) : bx;
-        // cache epilogues without RoPE take the section per lane: with d_q
-        // not a multiple of 128 a wave's columns can span Q and K (or K and V)
-        const int secl = kRope ? (nw + c4) / p.d_q : 0;
-        const int cinl = nw + c4 - secl * p.d_q;
-        const bool lq = EPI == EPI_QKV && secl == 0;
-        const bool lv = EPI == EPI_QKV ? secl == 2 : (EPI == EPI_KV && secl == 1);
-        bf16* ldst = lq ? p.q_out
-                        : (lv ? p.v_cache : p.k_cache) +
-                              (GROUPED ? (int64_t)(layer - 1) * p.cache_layer_stride : 0);
+        // a wave's 128 columns lie in one section (Q, K or V) when d_q is a
+        // multiple of 128; otherwise (no RoPE then) each lane finds its own
+        const bool sec_wave = !EXT || p.d_q % 128 == 0;     // wave-uniform
 #pragma unroll
         for (int hh = 0; hh < 16 / G; ++hh) {
           float4 x4[G], y4[G], cs[G], sn[G];
@@ -826,14 +824,20 @@ __device__ __forceinline__ void gemm_tile(const GP& p, char* smem, int layer, in
                 for (int e = 0; e < 4; ++e)
                   o[e] = f2bf(c < half ? x[e] * cv[e] - y[e] * sv[e] : x[e] * cv[e] + y[e] * sv[e]);
               }
-              if (rope) {
+              if (rope || sec_wave) {
                 const int64_t drow = is_q ? (int64_t)m : (int64_t)mr[r];
-                if (!kCheck || m < M)
+                if ((!kCheck || m < M) && col_in)
                   *reinterpret_cast<bf16x4_t*>(sec_dst + drow * p.d_q + c4) = o;
               } else {
+                const int secl = (nw + c4) / p.d_q;
+                const bool lq = EPI == EPI_QKV && secl == 0;
+                const bool lv = EPI == EPI_QKV ? secl == 2 : (EPI == EPI_KV && secl == 1);
+                bf16* ldst = lq ? p.q_out
+                                : (lv ? p.v_cache : p.k_cache) +
+                                      (GROUPED ? (int64_t)(layer - 1) * p.cache_layer_stride : 0);
                 const int64_t drow = lq ? (int64_t)m : (int64_t)mr[r];
                 if ((!kCheck || m < M) && col_in)
-                  *reinterpret_cast<bf16x4_t*>(ldst + drow * p.d_q + cinl) = o;
+                  *reinterpret_cast<bf16x4_t*>(ldst + drow * p.d_q + nw + c4 - secl * p.d_q) = o;
               }
             }
           }
@@ -867,7 +871,7 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int* 
 // The grid is sized for M_max; the tiles are numbered over the rows that are
 // actually active (device count), so when tokens exit the remaining tiles
 // still spread over all XCDs and the surplus workgroups return at once.
-template <int EPI, int HD>
+template <int EPI, int HD, bool EXT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GP p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
@@ -875,7 +879,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GP p) {
   if ((int)blockIdx.x >= tiles_m * p.tiles_n) return;
   int mt, nt;
   tile_of(blockIdx.x, tiles_m, p.tiles_n, &mt, &nt);
-  gemm_tile<EPI, false, HD>(p, smem, 0, mt, nt, M, p.B);
+  gemm_tile<EPI, false, HD, EXT>(p, smem, 0, mt, nt, M, p.B);
 }
 
 // Persistent grouped GEMM over the device-built list of (layer, row tile)
@@ -888,7 +892,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GP p) {
 // Taking items from counters rather than a fixed stride keeps the
 // workgroups busy until the last items: item times vary with the clock and
 // with how much of a layer's weights come from HBM.
-template <int HD>
+template <int HD, bool EXT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kv_grouped_kernel(GP p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int n_work = *p.n_work;
@@ -925,7 +929,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kv_grouped_kernel(GP p) {
     const int packed = p.work[w];
     const int layer = packed >> 16, mt = packed & 0xffff;
     const int M = p.grp_m[layer];
-    gemm_tile<EPI_KV, true, HD>(p, smem, layer, mt, nt, M,
+    gemm_tile<EPI_KV, true, HD, EXT>(p, smem, layer, mt, nt, M,
                                 p.B + (int64_t)(layer - 1) * p.b_layer_stride);
     __syncthreads();  // LDS is reused by the next item
   }
@@ -1034,16 +1038,29 @@ adept_status allow_lds(const void* kernel, bool* done, const char* what) {
   return ADEPT_OK;
 }
 
-template <int EPI, int HD>
-adept_status launch_bf16(const GP& p, hipStream_t s, const char* name) {
+template <int EPI, int HD, bool EXT>
+adept_status launch_bf16_x(const GP& p, hipStream_t s, const char* name) {
   static bool attr_set = false;
-  ADEPT_TRY(allow_lds((const void*)gemm_bf16_kernel<EPI, HD>, &attr_set, "gemm_bf16 LDS limit"));
+  ADEPT_TRY(allow_lds((const void*)gemm_bf16_kernel<EPI, HD, EXT>, &attr_set,
+                      "gemm_bf16 LDS limit"));
   {
     TimedLaunch tl(name ? name : "gemm_bf16", s);
-    hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD>), dim3(p.tiles_m * p.tiles_n), dim3(kThreads),
-                       kLdsBytes, s, p);
+    hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD, EXT>), dim3(p.tiles_m * p.tiles_n),
+                       dim3(kThreads), kLdsBytes, s, p);
   }
   return launch_status("gemm_bf16");
+}
+
+// the extended instantiation only where the shape or the inputs need it
+bool needs_ext(const GP& p, int epi) {
+  return (epi != EPI_SWIGLU && p.N % BN != 0) ||
+         ((epi == EPI_QKV || epi == EPI_KV) && p.d_q % 128 != 0) || p.a_sel != nullptr;
+}
+
+template <int EPI, int HD>
+adept_status launch_bf16(const GP& p, hipStream_t s, const char* name) {
+  return needs_ext(p, EPI) ? launch_bf16_x<EPI, HD, true>(p, s, name)
+                           : launch_bf16_x<EPI, HD, false>(p, s, name);
 }
 
 // ---------------------------------------------------------------------------
@@ -1422,14 +1439,23 @@ adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32
   p.cache_layer_stride = cache_layer_stride;
   p.tiles_n = ceil_div(g.N, BN);
   const int grid = std::min(max_work * p.tiles_n, kPersistentBlocks);
-  if (g.head_dim == 128) {
+  const bool ext = needs_ext(p, EPI_KV) || (g.bias != nullptr);
+  if (g.head_dim == 128 && !ext) {
     static bool attr_set = false;
-    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<128>, &attr_set, "kv LDS limit"));
-    ADEPT_LAUNCH(gemm_kv_grouped_kernel<128>, dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<128, false>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_grouped_kernel<128, false>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+  } else if (g.head_dim == 128) {
+    static bool attr_set = false;
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<128, true>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_grouped_kernel<128, true>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+  } else if (!ext) {
+    static bool attr_set = false;
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<64, false>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_grouped_kernel<64, false>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
   } else {
     static bool attr_set = false;
-    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<64>, &attr_set, "kv LDS limit"));
-    ADEPT_LAUNCH(gemm_kv_grouped_kernel<64>, dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<64, true>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_grouped_kernel<64, true>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
   }
   return launch_status("gemm_kv_grouped");
 }
