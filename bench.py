@@ -595,7 +595,7 @@ def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
 
     def call():
         B.exit_test(D, 5, cfg, rows, cnt, n_tok, h, None, inertia, None, flag)
-        B.compact(5, flag, rows, cnt, n_tok, nxt, cnt2[0:1], ext, cnt2[1:2], el)
+        B.compact(5, N, flag, rows, cnt, n_tok, nxt, cnt2[0:1], ext, cnt2[1:2], el)
     call()
     torch.cuda.synchronize()
     B.timing_reset()
@@ -637,7 +637,7 @@ def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
     n_big = 1 << 26
     rows_b = torch.arange(n_big, dtype=torch.int32, device="cuda")
     nxt_b, ext_b = torch.empty_like(rows_b), torch.empty_like(rows_b)
-    el_b = torch.empty_like(rows_b)
+    el_b = torch.full_like(rows_b, N)        # every listed row holds "never exited"
     cnt_b = torch.tensor([n_big, 0, 0], dtype=torch.int32, device="cuda")
     ws_b = torch.empty(B.compact_workspace_bytes(n_big), dtype=torch.uint8, device="cuda")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -647,7 +647,7 @@ def exit_test_standalone(shape, ai, B, torch, np, n_tok, reps=20):
         flags_b = (torch.rand(n_big, generator=g2, device="cuda") < frac).to(torch.uint8)
 
         def big():
-            B.compact(5, flags_b, rows_b, cnt_b[0:1], n_big, nxt_b, cnt_b[1:2], ext_b,
+            B.compact(5, N, flags_b, rows_b, cnt_b[0:1], n_big, nxt_b, cnt_b[1:2], ext_b,
                       cnt_b[2:3], el_b, ws_b)
         big()
         torch.cuda.synchronize()

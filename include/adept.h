@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define ADEPT_ABI_VERSION 5
+#define ADEPT_ABI_VERSION 6
 
 typedef enum {
   ADEPT_OK = 0,
@@ -193,7 +193,10 @@ adept_status adept_hsm_forward(adept_dtype dt, int d_model, float eps, const ade
  *  exit_flag[k], active_rows[k] for k < *n_active.
  *  next_rows / *n_next out: rows with flag 0, in the order of active_rows.
  *  exited_rows / *n_exited out: rows with flag 1, same order.
- *  exit_layer [n_tok] int32: exit_layer[row] = layer for every exited row.
+ *  exit_layer [n_tok] int32: exit_layer[row] = layer for every exited row;
+ *  every listed row that continues must hold n_layers (never exited, as
+ *  adept_token_init sets it): the multi-pass form writes dense stretches of
+ *  the list (64 consecutive rows) as whole lines, n_layers included.
  *  Counts are exact; with an ascending active list both outputs are ascending.
  *  next_rows / exited_rows must not alias active_rows.
  *  workspace: adept_compact_workspace_bytes(max_active) bytes, 8-byte aligned
@@ -202,7 +205,8 @@ adept_status adept_hsm_forward(adept_dtype dt, int d_model, float eps, const ade
  *  there.  ADEPT_E_WORKSPACE if it is missing or too small.
  * ------------------------------------------------------------------------- */
 size_t adept_compact_workspace_bytes(int max_active);
-adept_status adept_compact(int layer, const uint8_t* exit_flag, const int32_t* active_rows,
+adept_status adept_compact(int layer, int n_layers, const uint8_t* exit_flag,
+                           const int32_t* active_rows,
                            const int32_t* n_active, int max_active, int32_t* next_rows,
                            int32_t* n_next, int32_t* exited_rows, int32_t* n_exited,
                            int32_t* exit_layer, void* workspace, size_t workspace_bytes,

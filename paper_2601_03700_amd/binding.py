@@ -90,7 +90,8 @@ _SIGS = {
                                  _i32, _vp, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
     "adept_exit_prompt_level_workspace_bytes": (_sz, [_i32]),
     "adept_exit_prompt_level": (_i32, [_vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
-    "adept_compact": (_i32, [_i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "adept_compact": (_i32, [_i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
+                             _vp]),
     "adept_kv_generate_workspace_bytes": (_sz, [_i32, _i32]),
     "adept_kv_generate": (_i32, [_i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp, _vp,
                                  _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _vp,
@@ -242,10 +243,10 @@ def compact_workspace_bytes(max_active):
     return lib().adept_compact_workspace_bytes(max_active)
 
 
-def compact(layer, exit_flag, active_rows, n_active, max_active, next_rows, n_next, exited_rows,
-            n_exited, exit_layer, workspace=None, stream=None):
+def compact(layer, n_layers, exit_flag, active_rows, n_active, max_active, next_rows, n_next,
+            exited_rows, n_exited, exit_layer, workspace=None, stream=None):
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().adept_compact(layer, ptr(exit_flag), ptr(active_rows), ptr(n_active), max_active,
+    _check(lib().adept_compact(layer, n_layers, ptr(exit_flag), ptr(active_rows), ptr(n_active), max_active,
                                ptr(next_rows), ptr(n_next), ptr(exited_rows), ptr(n_exited),
                                ptr(exit_layer), ptr(workspace), ws_bytes, stream_handle(stream)),
            "adept_compact")

@@ -237,7 +237,7 @@ __global__ __launch_bounds__(kThreads) void compact_scan(const int32_t* __restri
 // 64-entry steps are in flight together.  Each step is one store per lane,
 // to the exit list or to the kept list, and the exit layer of the exits.
 __global__ __launch_bounds__(kThreads) void compact_scatter(
-    int layer, const uint64_t* __restrict__ masks, const int32_t* __restrict__ active,
+    int layer, int n_layers, const uint64_t* __restrict__ masks, const int32_t* __restrict__ active,
     const int32_t* __restrict__ n_active, const int32_t* __restrict__ tile_ex,
     int32_t* __restrict__ next, int32_t* __restrict__ exited, int32_t* __restrict__ exit_layer,
     int max_n) {
@@ -289,9 +289,25 @@ __global__ __launch_bounds__(kThreads) void compact_scatter(
     const int below = __popcll(mm & lt);
     const bool gone = (mm >> lane) & 1ull;
     int32_t* dst = gone ? exited + (ex_off + below) : next + (keep_off + lane - below);
+    // A step whose 64 entries all go to one list stores one contiguous run
+    // (non-temporal: whole lines, streamed); a mixed step stores two shorter
+    // runs through the cache, which merges the neighbouring steps' pieces of
+    // a line before it reaches HBM.  A step of 64 consecutive rows (a dense
+    // stretch of the list) with exits writes the exit layers of all of them,
+    // n_layers for the rows that continue (the value they hold), so its
+    // 256 bytes go out as whole lines instead of a partial-line scatter.
+    const bool one_list = mm == 0ull || mm == ~0ull;                // wave-uniform
+    const int r0 = __builtin_amdgcn_readfirstlane(r[st]);
+    const bool dense = mm != 0ull && base + 64 <= hi && __ballot(r[st] == r0 + lane) == ~0ull;
     if (base + lane < hi) {
-      __builtin_nontemporal_store(r[st], dst);
-      if (gone) exit_layer[r[st]] = layer;
+      if (one_list)
+        __builtin_nontemporal_store(r[st], dst);
+      else
+        *dst = r[st];
+      if (dense)
+        __builtin_nontemporal_store(gone ? layer : n_layers, exit_layer + r[st]);
+      else if (gone)
+        exit_layer[r[st]] = layer;
     }
     const int me = __popcll(mm);
     ex_off += me;
@@ -311,13 +327,14 @@ extern "C" size_t adept_compact_workspace_bytes(int max_active) {
   return ((tiles * sizeof(int32_t) + 255) & ~size_t(255)) + tiles * (kTile / 64) * sizeof(uint64_t);
 }
 
-extern "C" adept_status adept_compact(int layer, const uint8_t* exit_flag,
+extern "C" adept_status adept_compact(int layer, int n_layers, const uint8_t* exit_flag,
                                       const int32_t* active_rows, const int32_t* n_active,
                                       int max_active, int32_t* next_rows, int32_t* n_next,
                                       int32_t* exited_rows, int32_t* n_exited,
                                       int32_t* exit_layer, void* workspace,
                                       size_t workspace_bytes, void* stream) {
   ADEPT_REQUIRE(max_active >= 0, "compact: max_active < 0");
+  ADEPT_REQUIRE(layer >= 1 && layer <= n_layers, "compact: layer %d outside 1..%d", layer, n_layers);
   ADEPT_REQUIRE(exit_flag && active_rows && n_active && next_rows && n_next && exited_rows &&
                     n_exited && exit_layer,
                 "compact: NULL tensor");
@@ -350,7 +367,7 @@ extern "C" adept_status adept_compact(int layer, const uint8_t* exit_flag,
   ADEPT_LAUNCH(compact_scan, dim3(1), dim3(kThreads), 0, s, n_active, tile_ex, n_next,
                      n_exited, max_active);
   ADEPT_CHECK_LAUNCH("compact_scan");
-  ADEPT_LAUNCH(compact_scatter, dim3(tiles), dim3(kThreads), 0, s, layer, masks,
+  ADEPT_LAUNCH(compact_scatter, dim3(tiles), dim3(kThreads), 0, s, layer, n_layers, masks,
                      active_rows, n_active, tile_ex, next_rows, exited_rows, exit_layer,
                      max_active);
   return launch_status("compact_scatter");

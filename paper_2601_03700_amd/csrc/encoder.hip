@@ -290,7 +290,8 @@ extern "C" adept_status adept_encoder_layer_step(const adept_encoder_args* a, in
                  a->seq_len, a->exit_flag);
     ADEPT_CHECK_LAUNCH("cls_stop");
   }
-  ADEPT_TRY(adept_compact(layer, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
+  ADEPT_TRY(adept_compact(layer, a->n_layers, a->exit_flag, act, nact, maxn, a->active[out],
+                          a->n_active[out],
                           a->exited, a->n_exited, a->exit_layer, ws.compact, ws.compact_bytes,
                           stream));
   ADEPT_LAUNCH(mark_dead_kernel, dim3(ceil_div(maxn, 256)), dim3(256), 0, s, a->exited,

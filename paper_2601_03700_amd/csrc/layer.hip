@@ -334,7 +334,7 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     ADEPT_TRY(adept_exit_prompt_level(act, nact, maxn, a->seq, a->pos, a->n_seq, a->exit_flag,
                                       ws.prompt, ws.prompt_bytes, stream));
   // 9. active-list update
-  ADEPT_TRY(adept_compact(layer, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
+  ADEPT_TRY(adept_compact(layer, N, a->exit_flag, act, nact, maxn, a->active[out], a->n_active[out],
                           a->exited, a->n_exited, a->exit_layer, ws.compact, ws.compact_bytes,
                           stream));
   // 9b. mapper (Section 4.2) of the rows that exited here: s~ replaces h_i

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), f"{n} declared in adept.h but not exported"
     assert set(names) == set(B.EXPORTED), "binding signatures and header differ"
-    assert lib.adept_abi_version() == 5
+    assert lib.adept_abi_version() == 6
 
 
 @pytest.mark.parametrize("cname,pyname", [("adept_layer_args", "LayerArgs"),
@@ -88,7 +88,9 @@ def test_host_validation_rejects_bad_arguments():
     _expect_invalid(L.adept_exit_test(1, 256, 1, ctypes.byref(bad), 16, 16, 4, 16, 16, 16, None,
                                       16, None, None))
     # compaction output aliasing its input
-    _expect_invalid(L.adept_compact(1, 16, 32, 16, 8, 32, 16, 48, 16, 64, None, 0, None))
+    _expect_invalid(L.adept_compact(1, 4, 16, 32, 16, 8, 32, 16, 48, 16, 64, None, 0, None))
+    # compaction at a layer outside 1..n_layers
+    _expect_invalid(L.adept_compact(5, 4, 16, 32, 16, 8, 48, 16, 64, 16, 80, None, 0, None))
     # KV generation: layer stride smaller than one [2*H*hd][D] block
     _expect_invalid(L.adept_kv_generate(1, 4, 256, 2, 128, 1e-6, 16, 16, 16, 8, 16, 16, 16, 16,
                                         100, 16, 16, 16, 8, 16, 16, 8, None, 0, None))

@@ -191,6 +191,7 @@ def test_exit_test_window_and_special_thresholds():
     (16, 16, 0.5, 0), (5000, 4097, 0.3, 0), (16384, 16384, 0.1, 0), (16384, 9000, 0.0, 0),
     (16384, 9000, 1.0, 0), (300000, 200003, 0.4, 0),
     (300000, 300000, 0.0, 0), (300000, 299999, 1.0, 0),   # multi-pass, no / all exits
+    (200000, 200000, 0.3, 0),        # multi-pass over a dense list (whole-line exit layers)
     (70000, 65536, 0.5, 0),          # largest single-workgroup list
     (70000, 65537, 0.5, 0),          # smallest multi-pass list
     (1000, 0, 0.5, 64),              # empty list
@@ -213,7 +214,7 @@ def test_compact_matches_oracle(n_tok, n_act, p_exit, slack):
     el = i32(el0)
     wsb = B.compact_workspace_bytes(max_act)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=DEV) if wsb else None
-    B.compact(layer, flag_d, act_d, n_d, max_act, nxt, cnt[0:1], ext, cnt[1:2], el, ws)
+    B.compact(layer, 32, flag_d, act_d, n_d, max_act, nxt, cnt[0:1], ext, cnt[1:2], el, ws)
     torch.cuda.synchronize()
     still, gone = O.compact(flags.astype(bool), active)
     c = cnt.cpu().numpy()
@@ -233,10 +234,10 @@ def test_compact_worked_example():
     n = count(4)
     el = i32([4, 4, 4, 4])
     nxt1, ex1, c1 = (torch.empty(4, dtype=torch.int32, device=DEV) for _ in range(3))
-    B.compact(1, dev(np.array([0, 1, 0, 0, 0, 0, 0, 0], np.uint8)), act, n, 4, nxt1, c1[0:1],
+    B.compact(1, 4, dev(np.array([0, 1, 0, 0, 0, 0, 0, 0], np.uint8)), act, n, 4, nxt1, c1[0:1],
               ex1, c1[1:2], el)
     nxt2, ex2, c2 = (torch.empty(4, dtype=torch.int32, device=DEV) for _ in range(3))
-    B.compact(2, dev(np.array([0, 1, 0, 0, 0, 0, 0, 0], np.uint8)), nxt1, c1[0:1], 4, nxt2,
+    B.compact(2, 4, dev(np.array([0, 1, 0, 0, 0, 0, 0, 0], np.uint8)), nxt1, c1[0:1], 4, nxt2,
               c2[0:1], ex2, c2[1:2], el)
     torch.cuda.synchronize()
     assert int(c1[0]) == 3 and int(c2[0]) == 2
