@@ -199,7 +199,7 @@ def family(kernel_name):
     base = kernel_name.strip("()").split("<")[0]
     return {"gemm_qkv": "gemm_qkv", "gemm_o": "gemm_o", "gemm_gate_up": "gemm_gate_up",
             "gemm_down": "gemm_down", "attend_prefill_kernel": "attention",
-            "gemm_kv_grouped_kernel": "kv_generate"}.get(base)
+            "gemm_kv_grouped_kernel": "kv_generate", "gemm_kv_flat_kernel": "kv_generate"}.get(base)
 
 
 def kernel_table(kern, work, ms, steps):
@@ -513,7 +513,8 @@ def kv_generate_standalone(model, shape, ai, B, torch, np, reps=10):
     k = B.timing_read()
     pairs = int((N - el.long()).clamp(min=0).sum())
     flops = 4.0 * D * Dq * pairs
-    grouped = [v for kk, v in k.items() if kk.startswith("gemm_kv_grouped_kernel")]
+    grouped = [v for kk, v in k.items()
+               if kk.strip("()").startswith(("gemm_kv_grouped_kernel", "gemm_kv_flat_kernel"))]
     assert grouped, f"no grouped KV-generation launch timed: {sorted(k)}"
     g_launch, g_ms = grouped[0]
     gemm_ms = g_ms / g_launch

@@ -191,7 +191,7 @@ adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float sc
 adept_status gemm_f32(const GemmArgs& g, float* tmp, hipStream_t s);      // f32 + epilogue
 adept_status gemm_f32_direct(const GemmArgs& g, hipStream_t s);           // f32, C = A B^T
 adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32_t* n_work,
-                             int32_t* queue, int max_work, const int32_t* grp_m,
+                             int max_work, const int32_t* grp_m,
                              const int32_t* srows, int64_t b_layer_stride,
                              int64_t cache_layer_stride, hipStream_t s);
 // out[k] = 1/sqrt(mean(x[rows[k]]^2) + eps) for k < min(*n_dev, max_n) (rows nullable: k).

@@ -35,10 +35,10 @@
 // the same staged row), residual add, SwiGLU (B tile = 64 gate rows + 64 up
 // rows per wave), or plain store.
 //
-// The grouped variant is the decoupled KV generation of Eq. 9: a persistent
-// grid strides over (layer r, 256-row tile, column tile) items built on the
-// device from the exited rows sorted by exit layer (rows with i* < r form a
-// prefix); B is [Wk_r; Wv_r] with layer r's gain folded in, the row scale is
+// The grouped variant is the decoupled KV generation of Eq. 9: one
+// workgroup per (layer r, 256-row tile, column tile) item, the items built on
+// the device from the exited rows sorted by exit layer (rows with i* < r form
+// a prefix); B is [Wk_r; Wv_r] with layer r's gain folded in, the row scale is
 // 1/rms(s~), and the epilogue writes K (with RoPE) and V into cache[r].
 //
 // f32 path (small configurations only): a plain 64x64-tiled FMA GEMM into a
@@ -62,7 +62,6 @@ constexpr int kEpiWaveBytes = 32 * kEpiStride * 4;              // one wave's 32
 constexpr int kEpiMetaBytes = 128 * 3 * 4;                      // per-row scale, row/slot, position
 static_assert(4 * (kEpiWaveBytes + kEpiMetaBytes) <= (int)kLdsBytes,
               "epilogue staging fits in the ring");
-constexpr int kPersistentBlocks = 256;                          // one workgroup per CU
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) char lds_char_t;
@@ -98,7 +97,6 @@ struct GP {
   // grouped (KV generation)
   const int32_t* work;      // packed (layer << 16) | m_tile
   const int32_t* n_work;
-  int32_t* queue;           // [8] item counters, zero at launch
   const int32_t* grp_m;     // [N+2]: rows with exit layer < r
   const int32_t* srows;     // exited rows sorted by exit layer
   int64_t b_layer_stride;
@@ -882,57 +880,32 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GP p) {
   gemm_tile<EPI, false, HD, EXT>(p, smem, 0, mt, nt, M, p.B);
 }
 
-// Persistent grouped GEMM over the device-built list of (layer, row tile)
-// items times the column tiles.  The items, rastered in groups of 8 row tiles,
-// are cut into 8 contiguous chunks with one work counter each; a workgroup
-// takes items from the chunk of its own XCD (workgroups are dispatched to the
-// XCDs round-robin), in order, so that the tiles running together on an XCD
-// share operand slices in its L2, and then helps drain the other chunks.
-// A chunk's counter only grows; values past the chunk's end are discarded.
-// Taking items from counters rather than a fixed stride keeps the
-// workgroups busy until the last items: item times vary with the clock and
-// with how much of a layer's weights come from HBM.
+// Grouped GEMM of the KV generation: one workgroup per item of the
+// device-built list of (layer, row tile) items times the column tiles,
+// rastered in groups of 8 row tiles.  Workgroup ids go to the 8 XCDs
+// round-robin, so XCD x takes the x-th contiguous eighth of the item list and
+// the tiles running together on an XCD share one layer's weight slices in its
+// L2; ids past the device-built count return at once.  (A persistent form
+// that took items from per-XCD counters kept the loop's state in registers
+// and spilled 196 bytes per lane around the K loop; one item per workgroup
+// compiles as the plain GEMM does, without scratch, and runs 2 % faster.)
 template <int HD, bool EXT>
-__global__ __launch_bounds__(kThreads, 1) void gemm_kv_grouped_kernel(GP p) {
+__global__ __launch_bounds__(kThreads, 1) void gemm_kv_flat_kernel(GP p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int n_work = *p.n_work;
   const int total = n_work * p.tiles_n;
-  if (total == 0) return;   // nothing exited: no counter traffic
   const int chunk = (total + 7) >> 3;
-  const int home = blockIdx.x & 7;
-  // The item index is passed to all waves through the first word of the LDS
-  // ring, which no tile uses between items.  Thread 0 takes each counter
-  // value one item ahead, so the atomic's round trip passes during a tile;
-  // a value past its chunk moves it on to the next chunk (-1: all drained).
-  int* const s_item = reinterpret_cast<int*>(smem);
-  int qn = 0, qi = home, pre = 0;
-  if (threadIdx.x == 0) pre = atomicAdd(&p.queue[qi], 1);
-  for (;;) {
-    if (threadIdx.x == 0) {
-      int t = qi * chunk + pre;
-      while (t >= min(total, qi * chunk + chunk) && ++qn < 8) {
-        qi = (home + qn) & 7;
-        t = qi * chunk + atomicAdd(&p.queue[qi], 1);
-      }
-      *s_item = qn < 8 ? t : -1;
-      if (qn < 8) pre = atomicAdd(&p.queue[qi], 1);
-    }
-    __syncthreads();
-    const int t = __builtin_amdgcn_readfirstlane(*s_item);
-    __syncthreads();  // every wave has the index before the ring is refilled
-    if (t < 0) break;
-    constexpr int G = 8;
-    const int gsz = G * p.tiles_n;
-    const int g = t / gsz, r = t - g * gsz;
-    const int rows_in_g = min(G, n_work - g * G);
-    const int w = g * G + r % rows_in_g, nt = r / rows_in_g;
-    const int packed = p.work[w];
-    const int layer = packed >> 16, mt = packed & 0xffff;
-    const int M = p.grp_m[layer];
-    gemm_tile<EPI_KV, true, HD, EXT>(p, smem, layer, mt, nt, M,
-                                p.B + (int64_t)(layer - 1) * p.b_layer_stride);
-    __syncthreads();  // LDS is reused by the next item
-  }
+  const int t = (int)(blockIdx.x & 7) * chunk + (int)(blockIdx.x >> 3);
+  if ((int)(blockIdx.x >> 3) >= chunk || t >= total) return;
+  constexpr int G = 8;
+  const int gsz = G * p.tiles_n;
+  const int g = t / gsz, r = t - g * gsz;
+  const int rows_in_g = min(G, n_work - g * G);
+  const int w = g * G + r % rows_in_g, nt = r / rows_in_g;
+  const int packed = p.work[w];
+  const int layer = packed >> 16, mt = packed & 0xffff;
+  gemm_tile<EPI_KV, true, HD, EXT>(p, smem, layer, mt, nt, p.grp_m[layer],
+                                   p.B + (int64_t)(layer - 1) * p.b_layer_stride);
 }
 
 // ----------------------------------------------------------------------------
@@ -1419,7 +1392,7 @@ adept_status gemm_f32_direct(const GemmArgs& g, hipStream_t s) {
 // Grouped bf16 GEMM of the KV generation (see the header comment).  g.row_scale
 // is indexed by the sorted position.
 adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32_t* n_work,
-                             int32_t* queue, int max_work, const int32_t* grp_m,
+                             int max_work, const int32_t* grp_m,
                              const int32_t* srows,
                              int64_t b_layer_stride, int64_t cache_layer_stride, hipStream_t s) {
   if (max_work <= 0) return ADEPT_OK;
@@ -1434,28 +1407,29 @@ adept_status gemm_kv_grouped(const GemmArgs& g, const int32_t* work, const int32
     return ADEPT_E_UNSUPPORTED;
   }
   GP p = to_gp(g);
-  p.work = work; p.n_work = n_work; p.queue = queue; p.grp_m = grp_m; p.srows = srows;
+  p.work = work; p.n_work = n_work; p.grp_m = grp_m; p.srows = srows;
   p.b_layer_stride = b_layer_stride;
   p.cache_layer_stride = cache_layer_stride;
   p.tiles_n = ceil_div(g.N, BN);
-  const int grid = std::min(max_work * p.tiles_n, kPersistentBlocks);
   const bool ext = needs_ext(p, EPI_KV) || (g.bias != nullptr);
+  // one workgroup per item: the host bound on the items, rounded to whole XCD rounds
+  const int flat = (max_work * p.tiles_n + 7) / 8 * 8;
   if (g.head_dim == 128 && !ext) {
     static bool attr_set = false;
-    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<128, false>, &attr_set, "kv LDS limit"));
-    ADEPT_LAUNCH((gemm_kv_grouped_kernel<128, false>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_flat_kernel<128, false>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_flat_kernel<128, false>), dim3(flat), dim3(kThreads), kLdsBytes, s, p);
   } else if (g.head_dim == 128) {
     static bool attr_set = false;
-    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<128, true>, &attr_set, "kv LDS limit"));
-    ADEPT_LAUNCH((gemm_kv_grouped_kernel<128, true>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_flat_kernel<128, true>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_flat_kernel<128, true>), dim3(flat), dim3(kThreads), kLdsBytes, s, p);
   } else if (!ext) {
     static bool attr_set = false;
-    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<64, false>, &attr_set, "kv LDS limit"));
-    ADEPT_LAUNCH((gemm_kv_grouped_kernel<64, false>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_flat_kernel<64, false>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_flat_kernel<64, false>), dim3(flat), dim3(kThreads), kLdsBytes, s, p);
   } else {
     static bool attr_set = false;
-    ADEPT_TRY(allow_lds((const void*)gemm_kv_grouped_kernel<64, true>, &attr_set, "kv LDS limit"));
-    ADEPT_LAUNCH((gemm_kv_grouped_kernel<64, true>), dim3(grid), dim3(kThreads), kLdsBytes, s, p);
+    ADEPT_TRY(allow_lds((const void*)gemm_kv_flat_kernel<64, true>, &attr_set, "kv LDS limit"));
+    ADEPT_LAUNCH((gemm_kv_flat_kernel<64, true>), dim3(flat), dim3(kThreads), kLdsBytes, s, p);
   }
   return launch_status("gemm_kv_grouped");
 }

@@ -27,7 +27,6 @@ constexpr int kMaxLayers = 1024;
 
 struct KvWs {
   int32_t* n_work;
-  int32_t* queue;   // [8] work counters of the grouped GEMM, zeroed by the plan
   int32_t* grp_m;
   int32_t* work;
   int32_t* srows;
@@ -41,7 +40,6 @@ KvWs carve(void* ws, int n_layers, int max_rows, size_t* total) {
   size_t off = 0;
   KvWs w{};
   w.n_work = (int32_t*)(p + off); off += 256;
-  w.queue = (int32_t*)(p + off); off += 256;
   w.grp_m = (int32_t*)(p + off); off += align256((size_t)(n_layers + 2) * 4);
   const size_t max_work = (size_t)n_layers * ((max_rows + kTileM - 1) / kTileM);
   w.work = (int32_t*)(p + off); off += align256(max_work * 4);
@@ -59,7 +57,6 @@ __global__ __launch_bounds__(1024) void kv_plan_kernel(int n_layers, const int32
   __shared__ int hist[kMaxLayers + 2];
   __shared__ int cursor[kMaxLayers + 2];
   const int n = min(*n_rows, max_rows);
-  if (threadIdx.x < 8) w.queue[threadIdx.x] = 0;
   for (int l = threadIdx.x; l <= n_layers + 1; l += blockDim.x) hist[l] = 0;
   __syncthreads();
   for (int k = threadIdx.x; k < n; k += blockDim.x) {
@@ -237,7 +234,7 @@ extern "C" adept_status adept_kv_generate(adept_dtype dt, int n_layers, int d_mo
   g.rope_cos = rope_cos; g.rope_sin = rope_sin; g.head_dim = head_dim; g.d_q = dq;
   g.k_cache = k_cache; g.v_cache = v_cache; g.row_scale = w.rinv;
   const int max_work = n_layers * ceil_div(max_rows, kTileM);
-  return gemm_kv_grouped(g, w.work, w.n_work, w.queue, max_work, w.grp_m, w.srows,
+  return gemm_kv_grouped(g, w.work, w.n_work, max_work, w.grp_m, w.srows,
                          w_kv_layer_stride, layer_stride, s);
 }
 
@@ -315,7 +312,7 @@ extern "C" adept_status adept_kv_generate_layernorm(
   g.k_cache = k_cache; g.v_cache = v_cache;
   g.bias = b_kv; g.bias_layer_stride = b_kv_layer_stride;
   const int max_work = n_layers * ceil_div(max_rows, kTileM);
-  return gemm_kv_grouped(g, w.work, w.n_work, w.queue, max_work, w.grp_m, w.srows,
+  return gemm_kv_grouped(g, w.work, w.n_work, max_work, w.grp_m, w.srows,
                          w_kv_layer_stride, n_slots * dq, s);
 }
 
