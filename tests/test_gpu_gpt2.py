@@ -190,6 +190,33 @@ def test_gpt2_small_decode_teacher_forced(w_small, kv_fused):
     rep.summary()
 
 
+@pytest.mark.parametrize("metric", ["global", "local"])
+def test_gpt2_small_free_running_decisions(w_small, metric):
+    """The policy end to end (no teacher forcing): a threshold half-way between
+    two of the oracle's similarities of a pass without exits; every token whose
+    oracle margin |sim - delta| exceeds 5e-3 at all its tested layers exits at
+    the same layer on the GPU."""
+    say(f"gpt2 small free running metric={metric}")
+    w, w64 = w_small
+    ids = ai.token_ids(54, SMALL.vocab, 2, 128)
+    N = SMALL.n_layers
+    full, _ = O.prefill(w64, SMALL, ids, O.ExitConfig(delta=math.inf, metric=metric))
+    sims = np.sort(full.sims[:N - 1][np.isfinite(full.sims[:N - 1])])
+    q = int((0.6 if metric == "global" else 0.9) * sims.size)   # both: some tokens never exit
+    delta = float(0.5 * (sims[q] + sims[q + 1]))
+    model = DecoderModel(SMALL, w, dtype="bf16")
+    res_g, _ = model.prefill(ids, B.exit_cfg(delta, N, metric), logits="all")
+    torch.cuda.synchronize()
+    res_o, _ = O.prefill(w64, SMALL, ids, O.ExitConfig(delta=delta, metric=metric))
+    el_g, el_o = res_g.exit_layer.cpu().numpy(), res_o.exit_layer
+    m = np.abs(res_o.sims - delta)
+    safe = np.nanmin(np.where(np.isfinite(m), m, np.inf), axis=0) > 5e-3
+    say(f"  delta {delta:.6f}: {int(safe.sum())} of {safe.size} tokens decided with margin, "
+        f"{int(np.sum(el_o < N))} exits")
+    assert safe.sum() > 0.3 * safe.size and 0 < np.sum(el_o < N) < el_o.size
+    np.testing.assert_array_equal(el_g[safe], el_o[safe])
+
+
 def test_gpt2_xl_width_prefill_teacher_forced(w_xl):
     """Prefill at the GPT2-XL layer shapes (width 1600, 25 heads of 64, MLP
     6400; three layers): 2 x 520 rows (five 256-row tiles, the last ragged;
