@@ -474,9 +474,31 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
 // split-K kernel (decode and bidirectional): HBM-bound streaming of K/V rows
 // ---------------------------------------------------------------------------
 constexpr int kSplitThreads = 256;
+constexpr int kSplitTarget = 8192;   // workgroups of a decode attention launch
+
+// Chunks per (query entry, head) for n entries: about kSplitTarget
+// workgroups, at most one chunk per 256 keys of s_max.  The host sizes the
+// grid and the workspace for max_active entries (nc_host chunks); the
+// kernels take the chunk count from the device count n <= max_active, which
+// gives more chunks when fewer entries are active (a fuller grid), within the
+// grid and workspace capacity max_active * nc_host.  nc_host == 1 (the output
+// is written directly, no combine) stays 1.
+__host__ __device__ inline int split_nc(int n, int H, int s_max) {
+  const int64_t pairs = (int64_t)(n > 1 ? n : 1) * H;
+  const int64_t want = (kSplitTarget + pairs - 1) / pairs;
+  const int64_t most = (s_max + 255) / 256;
+  return (int)(want < 1 ? 1 : (want < most ? want : (most < 1 ? 1 : most)));
+}
+__device__ inline int split_nc_dev(int n, int max_active, int nc_host, int H, int s_max) {
+  if (nc_host == 1 || n <= 0) return nc_host;
+  const int cap = (int)(((int64_t)max_active * nc_host) / n);
+  const int f = split_nc(n, H, s_max);
+  return max(nc_host, min(f, cap));
+}
 
 // Workgroup (k, c, h): keys [c*CK, min(L, (c+1)*CK)) of query entry k, head
-// h, CK = ceil(L / nc).  A key's row of head h (HD bf16 = HD*2 bytes) is read
+// h, CK = ceil(L / nc), nc = split_nc_dev of the device count (nc_host: the
+// count the grid was sized with).  A key's row of head h (HD bf16 = HD*2 bytes) is read
 // by LPK = HD/8 lanes, 16 bytes each (non-temporal: nothing reads it again
 // while cached), so every load instruction covers whole rows; the wave's GPW lane groups take different keys, four per group in
 // flight.  Scores are q.k over the group (xor shuffles), and each group keeps
@@ -488,7 +510,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 template <int HD>
 __global__ __launch_bounds__(kSplitThreads) void attend_split_kernel(
-    int H, float scale_log2, int causal, int nc, const bf16* __restrict__ q,
+    int H, float scale_log2, int causal, int nc_host, const bf16* __restrict__ q,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ n_active, int max_active,
     const int32_t* __restrict__ pos, const int32_t* __restrict__ seq,
     const bf16* __restrict__ kc, const bf16* __restrict__ vc, int s_max,
@@ -499,8 +521,10 @@ __global__ __launch_bounds__(kSplitThreads) void attend_split_kernel(
   constexpr int G = GPW * (kSplitThreads / 64);
   __shared__ float gm[G], gl[G];
   __shared__ float go[G][HD + 4];
+  const int na = min(*n_active, max_active);
+  const int nc = split_nc_dev(na, max_active, nc_host, H, s_max);
   const int k = blockIdx.x / nc, c = blockIdx.x - (blockIdx.x / nc) * nc, h = blockIdx.y;
-  if (k >= min(*n_active, max_active)) return;
+  if (k >= na) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int grp = (tid >> 6) * GPW + lane / LPK;   // key group in the workgroup
   const int sub = lane % LPK;                      // 8-dim slice of the row
@@ -612,13 +636,15 @@ __global__ __launch_bounds__(kSplitThreads) void attend_split_kernel(
 
 // Merges the nc partial results of each (query entry, head).
 template <int HD>
-__global__ __launch_bounds__(HD) void attend_combine_kernel(int H, int nc,
+__global__ __launch_bounds__(HD) void attend_combine_kernel(int H, int nc_host,
                                                            const int32_t* __restrict__ n_active,
-                                                           int max_active,
+                                                           int max_active, int s_max,
                                                            const float* __restrict__ part,
                                                            bf16* __restrict__ out) {
   const int k = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
-  if (k >= min(*n_active, max_active)) return;
+  const int na = min(*n_active, max_active);
+  if (k >= na) return;
+  const int nc = split_nc_dev(na, max_active, nc_host, H, s_max);
   const int64_t pq = (int64_t)k * H + h;
   const float* pp = part + pq * nc * (HD + 2);
   // the chunks' loads are independent: unrolled so that they are in flight together
@@ -638,13 +664,8 @@ __global__ __launch_bounds__(HD) void attend_combine_kernel(int H, int nc,
   out[pq * HD + d] = f2bf(O / Ls);
 }
 
-// Chunks per (query entry, head) of the split kernel: about 32K workgroups
-// in all, at most one chunk per 256 keys of s_max.
-int split_chunks(int max_active, int H, int s_max) {
-  const int64_t pairs = (int64_t)std::max(max_active, 1) * H;
-  const int64_t want = std::max<int64_t>(1, 32768 / pairs);
-  return (int)std::max<int64_t>(1, std::min<int64_t>(want, (s_max + 255) / 256));
-}
+// Chunks per (query entry, head) the split kernel's grid is sized with.
+int split_chunks(int max_active, int H, int s_max) { return split_nc(max_active, H, s_max); }
 
 size_t split_workspace_bytes(int max_active, int H, int hd, int s_max) {
   const int nc = split_chunks(max_active, H, s_max);
@@ -732,10 +753,10 @@ adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float sc
       dim3 g2(max_active, n_heads);
       if (head_dim == 128)
         ADEPT_LAUNCH(attend_combine_kernel<128>, g2, dim3(128), 0, s, n_heads, nc, n_active,
-                     max_active, part, (bf16*)out);
+                     max_active, s_max, part, (bf16*)out);
       else
         ADEPT_LAUNCH(attend_combine_kernel<64>, g2, dim3(64), 0, s, n_heads, nc, n_active,
-                     max_active, part, (bf16*)out);
+                     max_active, s_max, part, (bf16*)out);
     }
     return launch_status("attend_split");
   }
