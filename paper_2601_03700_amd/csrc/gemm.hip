@@ -1085,8 +1085,11 @@ SkSplit skinny_split(int Nt, int K) {
 // pass streams B (the weights) once, so it is HBM-bound: A and B reach LDS by
 // direct loads of whole 128-byte rows (eight lanes per row, one cache line),
 // four stages deep, and the four waves each take a 32x32 block of the 64x64
-// tile.  Every iteration issues the same loads (the stage index clamped past
-// the segment's last stage), so the vmcnt accounting is uniform.
+// tile.  The two segments of a range share one load pipeline (the second
+// tile's first stages are in flight while the first tile's last ones are
+// multiplied); the first segment's accumulators are held in registers and
+// both partial tiles are written at the end, so no store sits among the
+// loads that the stage waits count.
 __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int nb, SkSplit sp,
                                                              float* __restrict__ part) {
   __shared__ __attribute__((aligned(1024))) char sm[kSkStages * kSkStage];
@@ -1095,52 +1098,57 @@ __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int nb, SkSpl
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int64_t u_end = min(sp.total, (int64_t)(blockIdx.x + 1) * sp.U);
-  int64_t u = (int64_t)blockIdx.x * sp.U;
+  const int64_t u0 = (int64_t)blockIdx.x * sp.U;
+  const int n = (int)(min(sp.total, u0 + sp.U) - u0);   // >= 1: G = ceil(total / U)
+  // a range is never longer than a tile's k extent (U <= KT): tiles t0, t1
+  const int t0 = (int)(u0 / sp.KT), kb0 = (int)(u0 - (int64_t)t0 * sp.KT);
+  const int n0 = min(n, sp.KT - kb0);   // k steps in tile t0; the rest are in t0 + 1
   const int rA = wm * 32 + (lane & 31), rB = wn * 32 + (lane & 31);
   const int swz = (lane >> 1) & 7;
-  for (int seg = 0; seg < 2 && u < u_end; ++seg) {
-    const int tile = (int)(u / sp.KT), kb = (int)(u - (int64_t)tile * sp.KT);
-    const int KT = (int)min<int64_t>(sp.KT - kb, u_end - u);
-    u += KT;
-    const int n0 = tile * kSkinnyBN, k0 = kb * BK;
-    // direct-load instruction j (0..3) of wave w: operand (A for waves 0-1,
-    // B for 2-3), rows 8q .. 8q+7 with q = (4w + j) mod 8; lane l -> row
-    // 8q + l/8, stored position l%8, logical chunk (l%8) ^ ((row >> 1) & 7)
-    const bf16* src[4];
+  // direct-load instruction j (0..3) of wave w: operand (A for waves 0-1, B
+  // for 2-3), rows 8q .. 8q+7 with q = (4w + j) mod 8; lane l -> row 8q + l/8,
+  // stored position l%8, logical chunk (l%8) ^ ((row >> 1) & 7).  src0 / src1
+  // point at k step 0 of tile t0 / t0 + 1 (the same A row for both), so the
+  // loop only selects one and adds the k offset.
+  const bf16* src0[4];
+  const bf16* src1[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int q = (4 * wave + j) & 7;
-      const int r = 8 * q + (lane >> 3);
-      const int ch = (lane & 7) ^ ((r >> 1) & 7);
-      if (wave < 2) {
-        const int m = min(r, M - 1);   // clamped: loaded, never stored
-        const int row = p.a_rows ? p.a_rows[m] : m;
-        const bf16* abase = (p.a_sel && (p.a_sel[row] & 1)) ? p.A2 : p.A;
-        src[j] = abase + (int64_t)row * p.lda + ch * 8 + k0;
-      } else {
-        const int n = n0 + r;
-        src[j] = (n >= nb ? p.B2 + (int64_t)(n - nb) * p.ldb : p.B + (int64_t)n * p.ldb) +
-                 ch * 8 + k0;
-      }
+  for (int j = 0; j < 4; ++j) {
+    const int q = (4 * wave + j) & 7;
+    const int r = 8 * q + (lane >> 3);
+    const int ch = (lane & 7) ^ ((r >> 1) & 7);
+    if (wave < 2) {
+      const int m = min(r, M - 1);   // clamped: loaded, never stored
+      const int row = p.a_rows ? p.a_rows[m] : m;
+      const bf16* abase = (p.a_sel && (p.a_sel[row] & 1)) ? p.A2 : p.A;
+      src0[j] = src1[j] = abase + (int64_t)row * p.lda + ch * 8;
+    } else {
+      // tile t0 + 1 past the last tile (then n0 == n) is never loaded
+      const int na = t0 * kSkinnyBN + r;
+      const int nb1 = (int64_t)(t0 + 1) * sp.KT < sp.total ? na + kSkinnyBN : na;
+      src0[j] = (na >= nb ? p.B2 + (int64_t)(na - nb) * p.ldb : p.B + (int64_t)na * p.ldb) + ch * 8;
+      src1[j] = (nb1 >= nb ? p.B2 + (int64_t)(nb1 - nb) * p.ldb : p.B + (int64_t)nb1 * p.ldb) +
+                ch * 8;
     }
-    auto issue = [&](int kt) {
-      const int k = min(kt, KT - 1) * BK;
-      char* slot = sm + (kt % kSkStages) * kSkStage + (wave >> 1) * 8192;
+  }
+  auto issue = [&](int i) {   // stage i of the range into ring slot i % kSkStages
+    const bool second = i >= n0;
+    const int k = (second ? i - n0 : kb0 + i) * BK;
+    char* slot = sm + (i % kSkStages) * kSkStage + (wave >> 1) * 8192;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) dma16(src[j] + k, slot + ((4 * wave + j) & 7) * 1024);
-    };
-    f32x16_t acc;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
-#pragma unroll
-    for (int s = 0; s < kSkStages - 1; ++s) issue(s);
-    for (int kt = 0; kt < KT; ++kt) {
-      // stage kt has landed once at most the later stages' loads are in flight
-      wait_vm<4 * (kSkStages - 2)>();
-      stage_barrier();   // publishes stage kt; every wave is done with stage kt-1
-      issue(kt + kSkStages - 1);   // into stage kt-1's slot
-      const char* st = sm + (kt % kSkStages) * kSkStage;
+    for (int j = 0; j < 4; ++j)
+      dma16((second ? src1[j] : src0[j]) + k, slot + ((4 * wave + j) & 7) * 1024);
+  };
+  // the stages [i0, i1) of the range into acc
+  auto run = [&](f32x16_t& acc, int i0, int i1) {
+    for (int it = i0; it < i1; ++it) {
+      // stage it has landed once at most the later stages' loads are in
+      // flight; near the end of the range fewer stages follow it
+      if (it + kSkStages - 2 < n) wait_vm<4 * (kSkStages - 2)>();
+      else wait_dma();
+      stage_barrier();   // publishes stage it; every wave is done with stage it-1
+      if (it + kSkStages - 1 < n) issue(it + kSkStages - 1);   // into stage it-1's slot
+      const char* st = sm + (it % kSkStages) * kSkStage;
 #pragma unroll
       for (int ks = 0; ks < BK / 16; ++ks) {
         const int ch = (2 * ks + (lane >> 5)) ^ swz;
@@ -1149,14 +1157,28 @@ __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GP p, int nb, SkSpl
         acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
       }
     }
-    wait_dma();        // the clamped loads land before the ring is reused
-    stage_barrier();   // every wave is done reading the ring
-    // C layout: value v is row 8*(v/4) + 4*(lane/32) + v%4 of the block, column lane%32
-    float* dst = part + ((int64_t)blockIdx.x * 2 + seg) * kSkPart;
+  };
+  f32x16_t acc0, acc1;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc0[v] = acc1[v] = 0.0f;
+#pragma unroll
+  for (int s = 0; s < kSkStages - 1; ++s)
+    if (s < n) issue(s);
+  run(acc0, 0, n0);
+  run(acc1, n0, n);
+  // every load has landed (the last stage waited for all of them)
+  // C layout: value v is row 8*(v/4) + 4*(lane/32) + v%4 of the block, column lane%32
+  float* dst = part + (int64_t)blockIdx.x * 2 * kSkPart;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int r = wm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+    dst[r * kSkinnyBN + wn * 32 + (lane & 31)] = acc0[v];
+  }
+  if (n0 < n) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int r = wm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-      dst[r * kSkinnyBN + wn * 32 + (lane & 31)] = acc[v];
+      dst[kSkPart + r * kSkinnyBN + wn * 32 + (lane & 31)] = acc1[v];
     }
   }
 }
