@@ -67,6 +67,41 @@ __device__ __forceinline__ float wave_max_f32(float v) {
   return v;
 }
 
+// 1/sqrt(mean(x^2) + eps) of one row of d elements, by one wave (every lane
+// returns it): squares summed in f32 lane by lane (16-byte loads when the row
+// allows, several in flight), then across the wave.
+template <typename T>
+__device__ __forceinline__ float row_rinv_wave(const T* __restrict__ xr, int d, float eps,
+                                               int lane) {
+  float ss = 0.0f;
+  constexpr int V = 16 / sizeof(T);   // elements per 16-byte load
+  if (d % V == 0 && ((uintptr_t)xr & 15) == 0) {
+#pragma unroll 4
+    for (int c = lane * V; c < d; c += 64 * V) {
+      const uint4 w = *reinterpret_cast<const uint4*>(xr + c);
+      const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if constexpr (sizeof(T) == 2) {
+          const float lo = __uint_as_float(u[e] << 16), hi = __uint_as_float(u[e] & 0xffff0000u);
+          ss = fmaf(lo, lo, ss);
+          ss = fmaf(hi, hi, ss);
+        } else {
+          const float v = __uint_as_float(u[e]);
+          ss = fmaf(v, v, ss);
+        }
+      }
+    }
+  } else {
+    for (int c = lane; c < d; c += 64) {
+      const float v = ld(xr + c);
+      ss = fmaf(v, v, ss);
+    }
+  }
+  ss = wave_sum_f32(ss);
+  return 1.0f / sqrtf(ss / (float)d + eps);
+}
+
 // ---------------------------------------------------------------------------
 // host-side error plumbing
 // ---------------------------------------------------------------------------

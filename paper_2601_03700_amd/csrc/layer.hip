@@ -132,6 +132,65 @@ __global__ __launch_bounds__(256) void fused_rows_kernel(int n_tok, int layer,
   if (lane == 0) *count = na + off;
 }
 
+// fused_rows_kernel and the QKV GEMM's row factors in one launch (RMSNorm
+// family): workgroup 0 writes the list, its count and the selectors as
+// fused_rows_kernel does; every wave also finds list entry k itself from the
+// same ballots (entries past the active rows are the rows that exited earlier,
+// ascending) and writes rinv[k] = 1/rms of that row's state, so no workgroup
+// waits for another.  A kernel boundary costs more than the few ballots each
+// wave repeats.
+template <typename T>
+__global__ __launch_bounds__(256) void fused_rows_rinv_kernel(
+    int n_tok, int layer, int d, float eps, const int32_t* __restrict__ exit_layer,
+    const int32_t* __restrict__ act, const int32_t* __restrict__ n_act, int max_act,
+    const T* __restrict__ x_in, const T* __restrict__ x_out, int32_t* __restrict__ list,
+    int32_t* __restrict__ count, int32_t* __restrict__ sel, float* __restrict__ rinv) {
+  const int lane = threadIdx.x & 63;
+  const int na = min(*n_act, max_act);
+  const int par = (layer - 1) & 1;
+  if (blockIdx.x == 0) {
+    for (int k = threadIdx.x; k < na; k += blockDim.x) list[k] = act[k];
+    if (threadIdx.x < 64) {
+      int off = 0;
+      for (int base = 0; base < n_tok; base += 64) {
+        const int row = base + lane;
+        const int el = row < n_tok ? exit_layer[row] : INT_MAX;
+        const bool ex = el < layer;
+        const uint64_t m = __ballot(ex);
+        if (ex) list[na + off + __popcll(m & ((1ull << lane) - 1))] = row;
+        if (row < n_tok) sel[row] = ex && (el & 1) != par;
+        off += __popcll(m);
+      }
+      if (lane == 0) *count = na + off;
+    }
+  }
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+  int row = -1;
+  bool from_out = false;
+  if (k < na) {
+    row = act[k];
+  } else {
+    const int want = k - na;   // the want-th row that exited before this layer
+    int off = 0;
+    for (int base = 0; base < n_tok; base += 64) {
+      const int r = base + lane;
+      const bool ex = r < n_tok && exit_layer[r] < layer;
+      const uint64_t m = __ballot(ex);
+      const int c = __popcll(m);
+      if (want < off + c) {
+        const uint64_t hit = __ballot(ex && __popcll(m & ((1ull << lane) - 1)) == want - off);
+        row = base + __ffsll((unsigned long long)hit) - 1;
+        break;
+      }
+      off += c;
+    }
+    if (row >= 0) from_out = (exit_layer[row] & 1) != par;
+  }
+  if (row < 0) return;   // past the list
+  const float r = row_rinv_wave((from_out ? x_out : x_in) + (int64_t)row * d, d, eps, lane);
+  if (lane == 0) rinv[k] = r;
+}
+
 adept_status run_gemm(adept_dtype dt, const GemmArgs& g, float* tmp, hipStream_t s) {
   return dt == ADEPT_BF16 ? gemm(dt, g, s) : gemm_f32(g, tmp, s);
 }
@@ -228,10 +287,20 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   const int32_t* qrows = act;         // rows of the QKV GEMM
   const int32_t* nq = nact;
   const int qmax = fused ? a->n_tok : maxn;
-  if (fused) {
+  // RMSNorm family, fused schedule: the row list and the QKV rows' factors
+  // come from one kernel
+  const bool rinv_fused = fused && !gpt2 && dt == ADEPT_BF16 && qmax > 0;
+  if (rinv_fused) {
+    ADEPT_LAUNCH(fused_rows_rinv_kernel<bf16>, dim3(ceil_div(qmax, 4)), dim3(256), 0, s, a->n_tok,
+                 layer, D, a->rms_eps, a->exit_layer, act, nact, maxn, (const bf16*)a->h[in],
+                 (const bf16*)a->h[out], ws.all_rows, ws.all_rows + a->n_tok, ws.fsel, ws.rinv);
+    ADEPT_CHECK_LAUNCH("fused_rows_rinv");
+  } else if (fused) {
     ADEPT_LAUNCH(fused_rows_kernel, dim3(1), dim3(256), 0, s, a->n_tok, layer, a->exit_layer, act,
                  nact, maxn, ws.all_rows, ws.all_rows + a->n_tok, ws.fsel);
     ADEPT_CHECK_LAUNCH("fused_rows");
+  }
+  if (fused) {
     qrows = ws.all_rows;
     nq = ws.all_rows + a->n_tok;
   }
@@ -284,8 +353,9 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   } else if (qmax > 0) {
     // 1. pre-attention RMSNorm: the gain is folded into W_qkv, the row factor
     //    1/rms(h) scales the GEMM accumulators
-    ADEPT_TRY(row_rinv_sel(dt, D, a->rms_eps, a->h[in], a->h[out], fused ? ws.fsel : nullptr,
-                           qrows, nq, qmax, ws.rinv, s));
+    if (!rinv_fused)
+      ADEPT_TRY(row_rinv_sel(dt, D, a->rms_eps, a->h[in], a->h[out], fused ? ws.fsel : nullptr,
+                             qrows, nq, qmax, ws.rinv, s));
     // 2. Q/K/V projections of the gathered rows, RoPE, own K/V into cache[layer]
     GemmArgs g{};
     g.M_max = qmax; g.M_dev = nq; g.N = 3 * dq; g.K = D;

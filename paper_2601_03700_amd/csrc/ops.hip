@@ -82,34 +82,8 @@ __global__ __launch_bounds__(256) void row_rinv_kernel(int d, float eps, const T
   if (k >= n) return;
   const int row = rows ? rows[k] : k;
   const T* xr = ((sel && (sel[row] & 1)) ? x1 : x0) + (int64_t)row * d;
-  float ss = 0.0f;
-  constexpr int V = 16 / sizeof(T);   // elements per 16-byte load
-  if (d % V == 0 && ((uintptr_t)xr & 15) == 0) {
-    // 16-byte loads, several in flight per lane
-#pragma unroll 4
-    for (int c = lane * V; c < d; c += 64 * V) {
-      const uint4 w = *reinterpret_cast<const uint4*>(xr + c);
-      const uint32_t u[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if constexpr (sizeof(T) == 2) {
-          const float lo = __uint_as_float(u[e] << 16), hi = __uint_as_float(u[e] & 0xffff0000u);
-          ss = fmaf(lo, lo, ss);
-          ss = fmaf(hi, hi, ss);
-        } else {
-          const float v = __uint_as_float(u[e]);
-          ss = fmaf(v, v, ss);
-        }
-      }
-    }
-  } else {
-    for (int c = lane; c < d; c += 64) {
-      const float v = ld(xr + c);
-      ss = fmaf(v, v, ss);
-    }
-  }
-  ss = wave_sum_f32(ss);
-  if (lane == 0) out[k] = 1.0f / sqrtf(ss / (float)d + eps);
+  const float r = row_rinv_wave(xr, d, eps, lane);
+  if (lane == 0) out[k] = r;
 }
 
 // w[l][o][c] *= gain[l][c] (in place, rounded to the element type).
