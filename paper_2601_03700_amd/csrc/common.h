@@ -209,8 +209,14 @@ struct GemmArgs {
   // per-row second A buffer (bf16 paths): token row r = a_rows[m] reads A2
   // instead of A when a_sel[r] & 1; nullable
   const void* A2; const int32_t* a_sel;
+  // RESID on the skinny path only (gemm_skinny_rinv says when): also
+  // rinv_out[m] = 1/sqrt(mean(C row^2) + rinv_eps) of each result row, from
+  // its bf16 values; nullable
+  float* rinv_out; float rinv_eps;
 };
 size_t skinny_ws_bytes(int n_cols, int K);
+// whether gemm() runs g on the skinny path and can fill g.rinv_out there
+bool gemm_skinny_rinv(const GemmArgs& g);
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s);       // bf16 MFMA path
 // attention (csrc/attention.hip): adept_attend with a switch that can forbid

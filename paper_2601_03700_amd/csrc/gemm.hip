@@ -106,6 +106,8 @@ struct GP {
   // per-row second A buffer: token row r reads A2 when a_sel[r] & 1 (nullable)
   const bf16* A2;
   const int32_t* a_sel;
+  float* rinv_out;          // skinny RESID: 1/rms of each result row (nullable)
+  float rinv_eps;
 };
 
 // x * sigmoid(x) with the hardware reciprocal (about 1 ulp in f32, far below
@@ -1271,6 +1273,46 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int nout, Sk
   }
 }
 
+// The residual epilogue with the row factor of its result (the next
+// RMSNorm's 1/rms): one workgroup of 1024 threads per row m, thread t owning
+// columns 4t + 4096j (one pass for rows of up to 4096, so every partial of
+// the row is in flight at once); the squares of the bf16 results (the values
+// a separate pass would read back) are summed in f32, across the wave, then
+// across the 16 waves in a fixed order.
+__global__ __launch_bounds__(1024) void skinny_resid_rinv_kernel(GP p, int nout, SkSplit sp,
+                                                                 const float* __restrict__ part) {
+  __shared__ float wsum[16];
+  const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
+  const int m = blockIdx.x;
+  if (m >= M) return;
+  const float sc = p.row_scale ? p.row_scale[m] : 1.0f;
+  float ss = 0.0f;
+  for (int n = threadIdx.x * 4; n < nout; n += 4096) {
+    const float4 x4 = skinny_sum(part, sp, m, n);
+    const float4 bx = bias4(p.bias, n);
+    const float x[4] = {x4.x * sc + bx.x, x4.y * sc + bx.y, x4.z * sc + bx.z, x4.w * sc + bx.w};
+    const int64_t off = (int64_t)p.rows[m] * p.ldc + n;
+    const bf16x4_t r = *reinterpret_cast<const bf16x4_t*>(p.resid + off);
+    bf16x4_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] = f2bf(x[e] + bf2f(r[e]));
+      const float v = bf2f(o[e]);
+      ss = fmaf(v, v, ss);
+    }
+    *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
+  }
+  ss = wave_sum_f32(ss);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) t += wsum[w];
+    p.rinv_out[m] = 1.0f / sqrtf(t / (float)nout + p.rinv_eps);
+  }
+}
+
 template <int EPI>
 adept_status launch_skinny(const GP& p, int Nt, int nout, hipStream_t s, const char* name,
                            float* part) {
@@ -1281,6 +1323,10 @@ adept_status launch_skinny(const GP& p, int Nt, int nout, hipStream_t s, const c
                        EPI == EPI_SWIGLU ? nout : Nt, sp, part);
   }
   ADEPT_CHECK_LAUNCH("gemm_skinny");
+  if (EPI == EPI_RESID && p.rinv_out) {
+    ADEPT_LAUNCH(skinny_resid_rinv_kernel, dim3(p.M_max), dim3(1024), 0, s, p, nout, sp, part);
+    return launch_status("skinny_resid_rinv");
+  }
   const int64_t total = (int64_t)p.M_max * (nout / 4);
   ADEPT_LAUNCH(skinny_epilogue_kernel<EPI>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
                s, p, nout, sp, part);
@@ -1299,6 +1345,7 @@ GP to_gp(const GemmArgs& g) {
   p.q_out = (bf16*)g.q_out; p.k_cache = (bf16*)g.k_cache; p.v_cache = (bf16*)g.v_cache;
   p.bias_layer_stride = g.bias_layer_stride; p.a_sorted = g.a_sorted;
   p.A2 = (const bf16*)g.A2; p.a_sel = g.a_sel;
+  p.rinv_out = g.rinv_out; p.rinv_eps = g.rinv_eps;
   return p;
 }
 
@@ -1316,8 +1363,19 @@ size_t skinny_ws_bytes(int Nt, int K) {
   return (size_t)skinny_split(Nt, K).G * 2 * kSkPart * sizeof(float);
 }
 
+bool gemm_skinny_rinv(const GemmArgs& g) {
+  const int Nt = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
+  return g.epi == EPI_RESID && g.M_max > 0 && g.M_max <= kSkinnyM && g.skinny_ws && g.N > 0 &&
+         g.N % 1024 == 0 && g.K > 0 && g.K % BK == 0 &&
+         skinny_ws_bytes(Nt, g.K) <= g.skinny_ws_bytes;
+}
+
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
   if (g.M_max <= 0) return ADEPT_OK;
+  if (g.rinv_out && !gemm_skinny_rinv(g)) {
+    set_error("gemm: rinv_out only on the skinny residual path (see gemm_skinny_rinv)");
+    return ADEPT_E_INVALID;
+  }
   if (dt != ADEPT_BF16) {
     set_error("gemm: bf16 entry called with another dtype");
     return ADEPT_E_INVALID;

@@ -377,9 +377,14 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     go.A = a->attn_out; go.lda = dq; go.B = wo; go.ldb = dq; go.epi = EPI_RESID;
     go.C = a->h[out]; go.ldc = D; go.resid = a->h[in]; go.rows = act; go.name = "gemm_o";
     go.skinny_ws = ws.skinny; go.skinny_ws_bytes = ws.skinny_bytes;
+    // 5. pre-FFN RMSNorm (gain folded into W_gate / W_up): its row factors
+    //    come from the projection's epilogue on the skinny path
+    if (dt == ADEPT_BF16 && gemm_skinny_rinv(go)) {
+      go.rinv_out = ws.rinv;
+      go.rinv_eps = a->rms_eps;
+    }
     ADEPT_TRY(run_gemm(dt, go, ws.gemm_tmp, s));
-    // 5. pre-FFN RMSNorm (gain folded into W_gate / W_up)
-    ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[out], act, nact, maxn, ws.rinv, s));
+    if (!go.rinv_out) ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[out], act, nact, maxn, ws.rinv, s));
     // 6. gate/up projections with SwiGLU
     GemmArgs gu{};
     gu.M_max = maxn; gu.M_dev = nact; gu.N = F; gu.K = D;
