@@ -474,25 +474,29 @@ __global__ __launch_bounds__(kPrefillThreads, 2) void attend_prefill_kernel(
 // split-K kernel (decode and bidirectional): HBM-bound streaming of K/V rows
 // ---------------------------------------------------------------------------
 constexpr int kSplitThreads = 256;
-constexpr int kSplitTarget = 8192;   // workgroups of a decode attention launch
 
-// Chunks per (query entry, head) for n entries: about kSplitTarget
+// Workgroups of a decode attention launch: about 8192 for 128-wide heads and
+// 2048 for 64-wide ones (a workgroup then takes twice the keys per pass of
+// its lane groups; measured best for each width).
+__host__ __device__ inline int64_t split_target(int hd) { return hd <= 64 ? 2048 : 8192; }
+
+// Chunks per (query entry, head) for n entries: about split_target(hd)
 // workgroups, at most one chunk per 256 keys of s_max.  The host sizes the
 // grid and the workspace for max_active entries (nc_host chunks); the
 // kernels take the chunk count from the device count n <= max_active, which
 // gives more chunks when fewer entries are active (a fuller grid), within the
 // grid and workspace capacity max_active * nc_host.  nc_host == 1 (the output
 // is written directly, no combine) stays 1.
-__host__ __device__ inline int split_nc(int n, int H, int s_max) {
+__host__ __device__ inline int split_nc(int n, int H, int hd, int s_max) {
   const int64_t pairs = (int64_t)(n > 1 ? n : 1) * H;
-  const int64_t want = (kSplitTarget + pairs - 1) / pairs;
+  const int64_t want = (split_target(hd) + pairs - 1) / pairs;
   const int64_t most = (s_max + 255) / 256;
   return (int)(want < 1 ? 1 : (want < most ? want : (most < 1 ? 1 : most)));
 }
-__device__ inline int split_nc_dev(int n, int max_active, int nc_host, int H, int s_max) {
+__device__ inline int split_nc_dev(int n, int max_active, int nc_host, int H, int hd, int s_max) {
   if (nc_host == 1 || n <= 0) return nc_host;
   const int cap = (int)(((int64_t)max_active * nc_host) / n);
-  const int f = split_nc(n, H, s_max);
+  const int f = split_nc(n, H, hd, s_max);
   return max(nc_host, min(f, cap));
 }
 
@@ -522,7 +526,7 @@ __global__ __launch_bounds__(kSplitThreads) void attend_split_kernel(
   __shared__ float gm[G], gl[G];
   __shared__ float go[G][HD + 4];
   const int na = min(*n_active, max_active);
-  const int nc = split_nc_dev(na, max_active, nc_host, H, s_max);
+  const int nc = split_nc_dev(na, max_active, nc_host, H, HD, s_max);
   const int k = blockIdx.x / nc, c = blockIdx.x - (blockIdx.x / nc) * nc, h = blockIdx.y;
   if (k >= na) return;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -644,7 +648,7 @@ __global__ __launch_bounds__(HD) void attend_combine_kernel(int H, int nc_host,
   const int k = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
   const int na = min(*n_active, max_active);
   if (k >= na) return;
-  const int nc = split_nc_dev(na, max_active, nc_host, H, s_max);
+  const int nc = split_nc_dev(na, max_active, nc_host, H, HD, s_max);
   const int64_t pq = (int64_t)k * H + h;
   const float* pp = part + pq * nc * (HD + 2);
   // the chunks' loads are independent: unrolled so that they are in flight together
@@ -665,10 +669,12 @@ __global__ __launch_bounds__(HD) void attend_combine_kernel(int H, int nc_host,
 }
 
 // Chunks per (query entry, head) the split kernel's grid is sized with.
-int split_chunks(int max_active, int H, int s_max) { return split_nc(max_active, H, s_max); }
+int split_chunks(int max_active, int H, int hd, int s_max) {
+  return split_nc(max_active, H, hd, s_max);
+}
 
 size_t split_workspace_bytes(int max_active, int H, int hd, int s_max) {
-  const int nc = split_chunks(max_active, H, s_max);
+  const int nc = split_chunks(max_active, H, hd, s_max);
   return nc == 1 ? 0 : (size_t)max_active * H * nc * (hd + 2) * sizeof(float);
 }
 
@@ -735,7 +741,7 @@ adept_status attend_dispatch(adept_dtype dt, int n_heads, int head_dim, float sc
     return launch_status("attend_prefill");
   }
   if (fast) {
-    const int nc = split_chunks(max_active, n_heads, s_max);
+    const int nc = split_chunks(max_active, n_heads, head_dim, s_max);
     float* part = (float*)workspace;
     dim3 grid(max_active * nc, n_heads);
     if (head_dim == 128)
