@@ -67,6 +67,68 @@ __device__ __forceinline__ float wave_max_f32(float v) {
   return v;
 }
 
+// LayerNorm of one bf16 row by one wave, the row held in registers: lane l
+// holds the 8-element chunks l, l+64, ..., (R of them; d a multiple of 8 up to
+// 512 R, rows 16-byte aligned), so the row crosses HBM once each way and every
+// access is a 16-byte vector.  Mean and variance in f32 from the registers
+// (two passes); o = (x - mean) / sqrt(var + eps) [* gain + bias].  o may be x.
+template <int R>
+__device__ __forceinline__ void layernorm_row_vec(const bf16* x, int d, float eps,
+                                                  const bf16* __restrict__ gain,
+                                                  const bf16* __restrict__ bias, bf16* o,
+                                                  int lane) {
+  float v[R][8];
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int c = (lane + 64 * j) * 8;
+    uint4 w = make_uint4(0, 0, 0, 0);
+    if (c < d) w = *reinterpret_cast<const uint4*>(x + c);
+    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[j][2 * e] = __uint_as_float(u[e] << 16);
+      v[j][2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+      s += v[j][2 * e] + v[j][2 * e + 1];
+    }
+  }
+  const float mean = wave_sum_f32(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    if ((lane + 64 * j) * 8 >= d) continue;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float t = v[j][e] - mean;
+      q = fmaf(t, t, q);
+    }
+  }
+  const float r = 1.0f / sqrtf(wave_sum_f32(q) / (float)d + eps);
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int c = (lane + 64 * j) * 8;
+    if (c >= d) continue;
+    float y[8];
+    if (gain) {
+      const uint4 gw = *reinterpret_cast<const uint4*>(gain + c);
+      const uint4 bw = *reinterpret_cast<const uint4*>(bias + c);
+      const uint32_t gu[4] = {gw.x, gw.y, gw.z, gw.w}, bu[4] = {bw.x, bw.y, bw.z, bw.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y[2 * e] = fmaf((v[j][2 * e] - mean) * r, __uint_as_float(gu[e] << 16),
+                        __uint_as_float(bu[e] << 16));
+        y[2 * e + 1] = fmaf((v[j][2 * e + 1] - mean) * r, __uint_as_float(gu[e] & 0xffff0000u),
+                            __uint_as_float(bu[e] & 0xffff0000u));
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * r;
+    }
+    *reinterpret_cast<uint4*>(o + c) = make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]),
+                                                  pack_bf16x2(y[4], y[5]), pack_bf16x2(y[6], y[7]));
+  }
+}
+
 // 1/sqrt(mean(x^2) + eps) of one row of d elements, by one wave (every lane
 // returns it): squares summed in f32 lane by lane (16-byte loads when the row
 // allows, several in flight), then across the wave.
@@ -209,14 +271,15 @@ struct GemmArgs {
   // per-row second A buffer (bf16 paths): token row r = a_rows[m] reads A2
   // instead of A when a_sel[r] & 1; nullable
   const void* A2; const int32_t* a_sel;
-  // RESID on the skinny path only (gemm_skinny_rinv says when): also
-  // rinv_out[m] = 1/sqrt(mean(C row^2) + rinv_eps) of each result row, from
-  // its bf16 values; nullable
-  float* rinv_out; float rinv_eps;
+  // RESID on the skinny path only (gemm_skinny_row_norm says when), at most
+  // one of: rinv_out[m] = 1/sqrt(mean(v^2) + row_eps), or ln_out[m] (bf16,
+  // [M][N]) = (v - mean) / sqrt(var + row_eps), of each result row v (its
+  // bf16 values); nullable
+  float* rinv_out; void* ln_out; float row_eps;
 };
 size_t skinny_ws_bytes(int n_cols, int K);
-// whether gemm() runs g on the skinny path and can fill g.rinv_out there
-bool gemm_skinny_rinv(const GemmArgs& g);
+// whether gemm() runs g on the skinny path and can fill g.rinv_out / g.ln_out
+bool gemm_skinny_row_norm(const GemmArgs& g);
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s);       // bf16 MFMA path
 // attention (csrc/attention.hip): adept_attend with a switch that can forbid

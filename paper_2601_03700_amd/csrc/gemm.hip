@@ -107,7 +107,8 @@ struct GP {
   const bf16* A2;
   const int32_t* a_sel;
   float* rinv_out;          // skinny RESID: 1/rms of each result row (nullable)
-  float rinv_eps;
+  bf16* ln_out;             // skinny RESID: LayerNorm of each result row (nullable)
+  float row_eps;
 };
 
 // x * sigmoid(x) with the hardware reciprocal (about 1 ulp in f32, far below
@@ -1273,21 +1274,27 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int nout, Sk
   }
 }
 
-// The residual epilogue with the row factor of its result (the next
-// RMSNorm's 1/rms): one workgroup of 1024 threads per row m, thread t owning
-// columns 4t + 4096j (one pass for rows of up to 4096, so every partial of
-// the row is in flight at once); the squares of the bf16 results (the values
-// a separate pass would read back) are summed in f32, across the wave, then
-// across the 16 waves in a fixed order.
-__global__ __launch_bounds__(1024) void skinny_resid_rinv_kernel(GP p, int nout, SkSplit sp,
-                                                                 const float* __restrict__ part) {
+// The residual epilogue with the next norm of its result rows: one
+// workgroup of 1024 threads per row m (rows of at most 4096; thread t owns
+// columns 4t..4t+3, so every partial of the row is in flight at once).  From
+// the bf16 results (the values a separate norm pass would read back), summed
+// in f32 lane by lane, across the wave, then over the 16 waves in order:
+// LN == false: rinv_out[m] = 1/sqrt(mean(v^2) + eps) (the next RMSNorm's
+// factor); LN == true: ln_out[m] = (v - mean) / sqrt(var + eps) (LayerNorm
+// without its affine part, two passes over the registers).
+template <bool LN>
+__global__ __launch_bounds__(1024) void skinny_resid_row_kernel(GP p, int nout, SkSplit sp,
+                                                                const float* __restrict__ part) {
   __shared__ float wsum[16];
+  __shared__ float total;
   const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
   const int m = blockIdx.x;
   if (m >= M) return;
   const float sc = p.row_scale ? p.row_scale[m] : 1.0f;
-  float ss = 0.0f;
-  for (int n = threadIdx.x * 4; n < nout; n += 4096) {
+  const int n = threadIdx.x * 4;
+  const bool live = n < nout;
+  float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (live) {
     const float4 x4 = skinny_sum(part, sp, m, n);
     const float4 bx = bias4(p.bias, n);
     const float x[4] = {x4.x * sc + bx.x, x4.y * sc + bx.y, x4.z * sc + bx.z, x4.w * sc + bx.w};
@@ -1297,19 +1304,48 @@ __global__ __launch_bounds__(1024) void skinny_resid_rinv_kernel(GP p, int nout,
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       o[e] = f2bf(x[e] + bf2f(r[e]));
-      const float v = bf2f(o[e]);
-      ss = fmaf(v, v, ss);
+      v[e] = bf2f(o[e]);
     }
     *reinterpret_cast<bf16x4_t*>(reinterpret_cast<bf16*>(p.C) + off) = o;
   }
-  ss = wave_sum_f32(ss);
-  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float t = 0.0f;
+  auto block_sum = [&](float x) {
+    x = wave_sum_f32(x);
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float t = 0.0f;
 #pragma unroll
-    for (int w = 0; w < 16; ++w) t += wsum[w];
-    p.rinv_out[m] = 1.0f / sqrtf(t / (float)nout + p.rinv_eps);
+      for (int w = 0; w < 16; ++w) t += wsum[w];
+      total = t;
+    }
+    __syncthreads();
+    const float t = total;
+    __syncthreads();   // wsum and total are reused by the next sum
+    return t;
+  };
+  if (!LN) {
+    float ss = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ss = fmaf(v[e], v[e], ss);
+    const float t = block_sum(ss);
+    if (threadIdx.x == 0) p.rinv_out[m] = 1.0f / sqrtf(t / (float)nout + p.row_eps);
+  } else {
+    const float mean = block_sum((v[0] + v[1]) + (v[2] + v[3])) / (float)nout;
+    float q = 0.0f;
+    if (live) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float t = v[e] - mean;
+        q = fmaf(t, t, q);
+      }
+    }
+    const float r = 1.0f / sqrtf(block_sum(q) / (float)nout + p.row_eps);
+    if (live) {
+      bf16x4_t y;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = f2bf((v[e] - mean) * r);
+      *reinterpret_cast<bf16x4_t*>(p.ln_out + (int64_t)m * nout + n) = y;
+    }
   }
 }
 
@@ -1323,8 +1359,13 @@ adept_status launch_skinny(const GP& p, int Nt, int nout, hipStream_t s, const c
                        EPI == EPI_SWIGLU ? nout : Nt, sp, part);
   }
   ADEPT_CHECK_LAUNCH("gemm_skinny");
+  if (EPI == EPI_RESID && p.ln_out) {
+    ADEPT_LAUNCH(skinny_resid_row_kernel<true>, dim3(p.M_max), dim3(1024), 0, s, p, nout, sp, part);
+    return launch_status("skinny_resid_ln");
+  }
   if (EPI == EPI_RESID && p.rinv_out) {
-    ADEPT_LAUNCH(skinny_resid_rinv_kernel, dim3(p.M_max), dim3(1024), 0, s, p, nout, sp, part);
+    ADEPT_LAUNCH(skinny_resid_row_kernel<false>, dim3(p.M_max), dim3(1024), 0, s, p, nout, sp,
+                 part);
     return launch_status("skinny_resid_rinv");
   }
   const int64_t total = (int64_t)p.M_max * (nout / 4);
@@ -1345,7 +1386,7 @@ GP to_gp(const GemmArgs& g) {
   p.q_out = (bf16*)g.q_out; p.k_cache = (bf16*)g.k_cache; p.v_cache = (bf16*)g.v_cache;
   p.bias_layer_stride = g.bias_layer_stride; p.a_sorted = g.a_sorted;
   p.A2 = (const bf16*)g.A2; p.a_sel = g.a_sel;
-  p.rinv_out = g.rinv_out; p.rinv_eps = g.rinv_eps;
+  p.rinv_out = g.rinv_out; p.ln_out = (bf16*)g.ln_out; p.row_eps = g.row_eps;
   return p;
 }
 
@@ -1363,17 +1404,18 @@ size_t skinny_ws_bytes(int Nt, int K) {
   return (size_t)skinny_split(Nt, K).G * 2 * kSkPart * sizeof(float);
 }
 
-bool gemm_skinny_rinv(const GemmArgs& g) {
-  const int Nt = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
+bool gemm_skinny_row_norm(const GemmArgs& g) {
   return g.epi == EPI_RESID && g.M_max > 0 && g.M_max <= kSkinnyM && g.skinny_ws && g.N > 0 &&
-         g.N % 1024 == 0 && g.K > 0 && g.K % BK == 0 &&
-         skinny_ws_bytes(Nt, g.K) <= g.skinny_ws_bytes;
+         g.N % 64 == 0 && g.N <= 4096 && g.K > 0 && g.K % BK == 0 &&
+         skinny_ws_bytes(g.N, g.K) <= g.skinny_ws_bytes;
 }
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
   if (g.M_max <= 0) return ADEPT_OK;
-  if (g.rinv_out && !gemm_skinny_rinv(g)) {
-    set_error("gemm: rinv_out only on the skinny residual path (see gemm_skinny_rinv)");
+  if ((g.rinv_out || g.ln_out) && (!gemm_skinny_row_norm(g) || (g.rinv_out && g.ln_out) ||
+                                    (g.ln_out && !aligned8(g.ln_out)))) {
+    set_error("gemm: rinv_out / ln_out (one of them, ln_out 8-byte aligned) only on the skinny "
+              "residual path (see gemm_skinny_row_norm)");
     return ADEPT_E_INVALID;
   }
   if (dt != ADEPT_BF16) {

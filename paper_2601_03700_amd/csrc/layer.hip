@@ -105,16 +105,14 @@ __global__ __launch_bounds__(64) void defer_rows_kernel(int n_tok, int n_layers,
 // Fused schedule, the row list of layer `layer`'s QKV GEMM: the active rows
 // (as listed) followed by the rows that exited at a layer below `layer`
 // (ascending), and its count; sel[row] = 1 where the row's state (its exit
-// state) sits in h[layer & 1] rather than h[(layer-1) & 1].  One workgroup;
-// wave 0 walks the rows 64 at a time with a ballot.
-__global__ __launch_bounds__(256) void fused_rows_kernel(int n_tok, int layer,
-                                                         const int32_t* __restrict__ exit_layer,
-                                                         const int32_t* __restrict__ act,
-                                                         const int32_t* __restrict__ n_act,
-                                                         int max_act, int32_t* __restrict__ list,
-                                                         int32_t* __restrict__ count,
-                                                         int32_t* __restrict__ sel) {
-  const int na = min(*n_act, max_act);
+// state) sits in h[layer & 1] rather than h[(layer-1) & 1].  Written by one
+// workgroup; wave 0 walks the rows 64 at a time with a ballot.
+__device__ __forceinline__ void fused_rows_write(int n_tok, int layer, int na,
+                                                 const int32_t* __restrict__ exit_layer,
+                                                 const int32_t* __restrict__ act,
+                                                 int32_t* __restrict__ list,
+                                                 int32_t* __restrict__ count,
+                                                 int32_t* __restrict__ sel) {
   for (int k = threadIdx.x; k < na; k += blockDim.x) list[k] = act[k];
   if (threadIdx.x >= 64) return;
   const int lane = threadIdx.x;
@@ -132,63 +130,79 @@ __global__ __launch_bounds__(256) void fused_rows_kernel(int n_tok, int layer,
   if (lane == 0) *count = na + off;
 }
 
-// fused_rows_kernel and the QKV GEMM's row factors in one launch (RMSNorm
-// family): workgroup 0 writes the list, its count and the selectors as
-// fused_rows_kernel does; every wave also finds list entry k itself from the
-// same ballots (entries past the active rows are the rows that exited earlier,
-// ascending) and writes rinv[k] = 1/rms of that row's state, so no workgroup
-// waits for another.  A kernel boundary costs more than the few ballots each
-// wave repeats.
+// Entry k of that list, found by one wave from the same ballots (-1 past its
+// end), and whether the row's state is in h[layer & 1].
+__device__ __forceinline__ int fused_row_of(int k, int n_tok, int layer, int na,
+                                            const int32_t* __restrict__ exit_layer,
+                                            const int32_t* __restrict__ act, bool* from_out) {
+  const int lane = threadIdx.x & 63;
+  *from_out = false;
+  if (k < na) return act[k];
+  const int want = k - na;   // the want-th row that exited before this layer
+  int off = 0;
+  for (int base = 0; base < n_tok; base += 64) {
+    const int r = base + lane;
+    const bool ex = r < n_tok && exit_layer[r] < layer;
+    const uint64_t m = __ballot(ex);
+    const int c = __popcll(m);
+    if (want < off + c) {
+      const uint64_t hit = __ballot(ex && __popcll(m & ((1ull << lane) - 1)) == want - off);
+      const int row = base + __ffsll((unsigned long long)hit) - 1;
+      *from_out = (exit_layer[row] & 1) != ((layer - 1) & 1);
+      return row;
+    }
+    off += c;
+  }
+  return -1;
+}
+
+__global__ __launch_bounds__(256) void fused_rows_kernel(int n_tok, int layer,
+                                                         const int32_t* __restrict__ exit_layer,
+                                                         const int32_t* __restrict__ act,
+                                                         const int32_t* __restrict__ n_act,
+                                                         int max_act, int32_t* __restrict__ list,
+                                                         int32_t* __restrict__ count,
+                                                         int32_t* __restrict__ sel) {
+  fused_rows_write(n_tok, layer, min(*n_act, max_act), exit_layer, act, list, count, sel);
+}
+
+// The list and the QKV GEMM's row factors in one launch (RMSNorm family):
+// workgroup 0 writes the list, every wave finds its own entry k and writes
+// rinv[k] = 1/rms of that row's state, so no workgroup waits for another.
+// A kernel boundary costs more than the few ballots each wave repeats.
 template <typename T>
 __global__ __launch_bounds__(256) void fused_rows_rinv_kernel(
     int n_tok, int layer, int d, float eps, const int32_t* __restrict__ exit_layer,
     const int32_t* __restrict__ act, const int32_t* __restrict__ n_act, int max_act,
     const T* __restrict__ x_in, const T* __restrict__ x_out, int32_t* __restrict__ list,
     int32_t* __restrict__ count, int32_t* __restrict__ sel, float* __restrict__ rinv) {
-  const int lane = threadIdx.x & 63;
   const int na = min(*n_act, max_act);
-  const int par = (layer - 1) & 1;
-  if (blockIdx.x == 0) {
-    for (int k = threadIdx.x; k < na; k += blockDim.x) list[k] = act[k];
-    if (threadIdx.x < 64) {
-      int off = 0;
-      for (int base = 0; base < n_tok; base += 64) {
-        const int row = base + lane;
-        const int el = row < n_tok ? exit_layer[row] : INT_MAX;
-        const bool ex = el < layer;
-        const uint64_t m = __ballot(ex);
-        if (ex) list[na + off + __popcll(m & ((1ull << lane) - 1))] = row;
-        if (row < n_tok) sel[row] = ex && (el & 1) != par;
-        off += __popcll(m);
-      }
-      if (lane == 0) *count = na + off;
-    }
-  }
+  if (blockIdx.x == 0) fused_rows_write(n_tok, layer, na, exit_layer, act, list, count, sel);
   const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
-  int row = -1;
-  bool from_out = false;
-  if (k < na) {
-    row = act[k];
-  } else {
-    const int want = k - na;   // the want-th row that exited before this layer
-    int off = 0;
-    for (int base = 0; base < n_tok; base += 64) {
-      const int r = base + lane;
-      const bool ex = r < n_tok && exit_layer[r] < layer;
-      const uint64_t m = __ballot(ex);
-      const int c = __popcll(m);
-      if (want < off + c) {
-        const uint64_t hit = __ballot(ex && __popcll(m & ((1ull << lane) - 1)) == want - off);
-        row = base + __ffsll((unsigned long long)hit) - 1;
-        break;
-      }
-      off += c;
-    }
-    if (row >= 0) from_out = (exit_layer[row] & 1) != par;
-  }
+  bool from_out;
+  const int row = fused_row_of(k, n_tok, layer, na, exit_layer, act, &from_out);
   if (row < 0) return;   // past the list
+  const int lane = threadIdx.x & 63;
   const float r = row_rinv_wave((from_out ? x_out : x_in) + (int64_t)row * d, d, eps, lane);
   if (lane == 0) rinv[k] = r;
+}
+
+// The same for the LayerNorm family: each wave writes the normalised row k
+// (no affine part: folded into the projection) into xnorm[k].
+template <int R>
+__global__ __launch_bounds__(256) void fused_rows_ln_kernel(
+    int n_tok, int layer, int d, float eps, const int32_t* __restrict__ exit_layer,
+    const int32_t* __restrict__ act, const int32_t* __restrict__ n_act, int max_act,
+    const bf16* __restrict__ x_in, const bf16* __restrict__ x_out, int32_t* __restrict__ list,
+    int32_t* __restrict__ count, int32_t* __restrict__ sel, bf16* __restrict__ xnorm) {
+  const int na = min(*n_act, max_act);
+  if (blockIdx.x == 0) fused_rows_write(n_tok, layer, na, exit_layer, act, list, count, sel);
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+  bool from_out;
+  const int row = fused_row_of(k, n_tok, layer, na, exit_layer, act, &from_out);
+  if (row < 0) return;
+  layernorm_row_vec<R>((from_out ? x_out : x_in) + (int64_t)row * d, d, eps, nullptr, nullptr,
+                       xnorm + (int64_t)k * d, threadIdx.x & 63);
 }
 
 adept_status run_gemm(adept_dtype dt, const GemmArgs& g, float* tmp, hipStream_t s) {
@@ -287,14 +301,37 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
   const int32_t* qrows = act;         // rows of the QKV GEMM
   const int32_t* nq = nact;
   const int qmax = fused ? a->n_tok : maxn;
-  // RMSNorm family, fused schedule: the row list and the QKV rows' factors
-  // come from one kernel
+  // fused schedule: the row list and the QKV rows' norm (the RMSNorm
+  // factors, or the LayerNorm rows when they fit one wave's registers) come
+  // from one kernel
   const bool rinv_fused = fused && !gpt2 && dt == ADEPT_BF16 && qmax > 0;
+  const int ln_r = ceil_div(ceil_div(D, 8), 64);   // 16-byte chunks per lane
+  const bool ln_fused = fused && gpt2 && dt == ADEPT_BF16 && qmax > 0 && D % 8 == 0 &&
+                        ln_r <= 8 && aligned16(a->h[0]) && aligned16(a->h[1]) &&
+                        aligned16(ws.xnorm);
+  const dim3 fgrid(ceil_div(std::max(qmax, 1), 4));
   if (rinv_fused) {
-    ADEPT_LAUNCH(fused_rows_rinv_kernel<bf16>, dim3(ceil_div(qmax, 4)), dim3(256), 0, s, a->n_tok,
-                 layer, D, a->rms_eps, a->exit_layer, act, nact, maxn, (const bf16*)a->h[in],
+    ADEPT_LAUNCH(fused_rows_rinv_kernel<bf16>, fgrid, dim3(256), 0, s, a->n_tok, layer, D,
+                 a->rms_eps, a->exit_layer, act, nact, maxn, (const bf16*)a->h[in],
                  (const bf16*)a->h[out], ws.all_rows, ws.all_rows + a->n_tok, ws.fsel, ws.rinv);
     ADEPT_CHECK_LAUNCH("fused_rows_rinv");
+  } else if (ln_fused) {
+    const bf16 *xi = (const bf16*)a->h[in], *xo = (const bf16*)a->h[out];
+    int32_t *lst = ws.all_rows, *cnt = ws.all_rows + a->n_tok;
+    bf16* xn = (bf16*)ws.xnorm;
+    if (ln_r <= 1)
+      ADEPT_LAUNCH(fused_rows_ln_kernel<1>, fgrid, dim3(256), 0, s, a->n_tok, layer, D,
+                   a->rms_eps, a->exit_layer, act, nact, maxn, xi, xo, lst, cnt, ws.fsel, xn);
+    else if (ln_r <= 2)
+      ADEPT_LAUNCH(fused_rows_ln_kernel<2>, fgrid, dim3(256), 0, s, a->n_tok, layer, D,
+                   a->rms_eps, a->exit_layer, act, nact, maxn, xi, xo, lst, cnt, ws.fsel, xn);
+    else if (ln_r <= 4)
+      ADEPT_LAUNCH(fused_rows_ln_kernel<4>, fgrid, dim3(256), 0, s, a->n_tok, layer, D,
+                   a->rms_eps, a->exit_layer, act, nact, maxn, xi, xo, lst, cnt, ws.fsel, xn);
+    else
+      ADEPT_LAUNCH(fused_rows_ln_kernel<8>, fgrid, dim3(256), 0, s, a->n_tok, layer, D,
+                   a->rms_eps, a->exit_layer, act, nact, maxn, xi, xo, lst, cnt, ws.fsel, xn);
+    ADEPT_CHECK_LAUNCH("fused_rows_ln");
   } else if (fused) {
     ADEPT_LAUNCH(fused_rows_kernel, dim3(1), dim3(256), 0, s, a->n_tok, layer, a->exit_layer, act,
                  nact, maxn, ws.all_rows, ws.all_rows + a->n_tok, ws.fsel);
@@ -309,8 +346,10 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     // weights and biases), biased projections, tanh GELU, no RoPE
     const void* bqkv = off(a->b_qkv, li * 3 * dq);
     // 1. LN1 of the QKV rows (compact order; an exited row from its exit state)
-    ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[in], a->h[out], fused ? ws.fsel : nullptr,
-                                 qrows, nq, qmax, nullptr, nullptr, ws.xnorm, s));
+    if (!ln_fused)
+      ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[in], a->h[out],
+                                   fused ? ws.fsel : nullptr, qrows, nq, qmax, nullptr, nullptr,
+                                   ws.xnorm, s));
     // 2. Q/K/V with bias, own K/V into cache[layer]
     GemmArgs g{};
     g.M_max = qmax; g.M_dev = nq; g.N = 3 * dq; g.K = D;
@@ -330,10 +369,15 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     go.bias = off(a->b_o, li * D);
     go.C = a->h[out]; go.ldc = D; go.resid = a->h[in]; go.rows = act; go.name = "gemm_o";
     go.skinny_ws = ws.skinny; go.skinny_ws_bytes = ws.skinny_bytes;
+    // 5. LN2: on the skinny path the projection's epilogue writes it
+    if (gemm_skinny_row_norm(go)) {
+      go.ln_out = ws.xnorm;
+      go.row_eps = a->rms_eps;
+    }
     ADEPT_TRY(gemm(dt, go, s));
-    // 5. LN2
-    ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[out], a->h[out], nullptr, act, nact,
-                                 maxn, nullptr, nullptr, ws.xnorm, s));
+    if (!go.ln_out)
+      ADEPT_TRY(layernorm_rows_sel(dt, D, a->rms_eps, a->h[out], a->h[out], nullptr, act, nact,
+                                   maxn, nullptr, nullptr, ws.xnorm, s));
     // 6. first MLP projection + bias + tanh GELU
     GemmArgs gf{};
     gf.M_max = maxn; gf.M_dev = nact; gf.N = F; gf.K = D;
@@ -379,9 +423,9 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     go.skinny_ws = ws.skinny; go.skinny_ws_bytes = ws.skinny_bytes;
     // 5. pre-FFN RMSNorm (gain folded into W_gate / W_up): its row factors
     //    come from the projection's epilogue on the skinny path
-    if (dt == ADEPT_BF16 && gemm_skinny_rinv(go)) {
+    if (dt == ADEPT_BF16 && gemm_skinny_row_norm(go)) {
       go.rinv_out = ws.rinv;
-      go.rinv_eps = a->rms_eps;
+      go.row_eps = a->rms_eps;
     }
     ADEPT_TRY(run_gemm(dt, go, ws.gemm_tmp, s));
     if (!go.rinv_out) ADEPT_TRY(row_rinv(dt, D, a->rms_eps, a->h[out], act, nact, maxn, ws.rinv, s));

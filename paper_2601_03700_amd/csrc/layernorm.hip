@@ -51,11 +51,9 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(
   }
 }
 
-// The same for bf16 rows held in registers: lane l holds the 8-element
-// chunks l, l+64, ..., (R of them; d a multiple of 8, rows 16-byte aligned),
-// so the row crosses HBM once each way and every access is a 16-byte
-// vector.  Mean and variance in f32 from the registers (two passes);
-// out row = out_by_row ? row : k (in place when out == x0 == x1).
+// The same for bf16 rows held in registers (layernorm_row_vec, shared with
+// the layer step); out row = out_by_row ? row : k (in place when
+// out == x0 == x1).
 template <int R>
 __global__ __launch_bounds__(256) void layernorm_vec_kernel(
     int d, float eps, const bf16* x0, const bf16* x1, const int32_t* __restrict__ sel,
@@ -67,57 +65,7 @@ __global__ __launch_bounds__(256) void layernorm_vec_kernel(
   if (k >= n) return;
   const int row = rows ? rows[k] : k;
   const bf16* x = ((sel && (sel[row] & 1)) ? x1 : x0) + (int64_t)row * d;
-  float v[R][8];
-  float s = 0.0f;
-#pragma unroll
-  for (int j = 0; j < R; ++j) {
-    const int c = (lane + 64 * j) * 8;
-    uint4 w = make_uint4(0, 0, 0, 0);
-    if (c < d) w = *reinterpret_cast<const uint4*>(x + c);
-    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      v[j][2 * e] = __uint_as_float(u[e] << 16);
-      v[j][2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
-      s += v[j][2 * e] + v[j][2 * e + 1];
-    }
-  }
-  const float mean = wave_sum_f32(s) / (float)d;
-  float q = 0.0f;
-#pragma unroll
-  for (int j = 0; j < R; ++j) {
-    if ((lane + 64 * j) * 8 >= d) continue;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float t = v[j][e] - mean;
-      q = fmaf(t, t, q);
-    }
-  }
-  const float r = 1.0f / sqrtf(wave_sum_f32(q) / (float)d + eps);
-  bf16* o = out + (int64_t)(out_by_row ? row : k) * d;
-#pragma unroll
-  for (int j = 0; j < R; ++j) {
-    const int c = (lane + 64 * j) * 8;
-    if (c >= d) continue;
-    float y[8];
-    if (gain) {
-      const uint4 gw = *reinterpret_cast<const uint4*>(gain + c);
-      const uint4 bw = *reinterpret_cast<const uint4*>(bias + c);
-      const uint32_t gu[4] = {gw.x, gw.y, gw.z, gw.w}, bu[4] = {bw.x, bw.y, bw.z, bw.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        y[2 * e] = fmaf((v[j][2 * e] - mean) * r, __uint_as_float(gu[e] << 16),
-                        __uint_as_float(bu[e] << 16));
-        y[2 * e + 1] = fmaf((v[j][2 * e + 1] - mean) * r, __uint_as_float(gu[e] & 0xffff0000u),
-                            __uint_as_float(bu[e] & 0xffff0000u));
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * r;
-    }
-    *reinterpret_cast<uint4*>(o + c) = make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]),
-                                                  pack_bf16x2(y[4], y[5]), pack_bf16x2(y[6], y[7]));
-  }
+  layernorm_row_vec<R>(x, d, eps, gain, bias, out + (int64_t)(out_by_row ? row : k) * d, lane);
 }
 
 // h0[k][c] = wte[ids[k]][c] + wpe[pos[k]][c] (ids and positions clamped
