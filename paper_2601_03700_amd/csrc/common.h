@@ -67,6 +67,20 @@ __device__ __forceinline__ float wave_max_f32(float v) {
   return v;
 }
 
+// The exit decision of Eq. 8 for one row: the test passed (the cosine
+// reached delta), inside the window min_exit_layer <= layer <= n_layers - 1;
+// a forced schedule (force_layer[row] > 0) overrides it with "exit exactly at
+// that layer".
+__device__ __forceinline__ bool exit_decision(bool pass, int layer, int min_exit_layer,
+                                              int n_layers, const int32_t* force_layer, int row) {
+  bool ex = (layer >= min_exit_layer) && (layer <= n_layers - 1) && pass;
+  if (force_layer) {
+    const int f = force_layer[row];
+    if (f > 0) ex = (layer == f) && (layer <= n_layers - 1);
+  }
+  return ex;
+}
+
 // LayerNorm of one bf16 row by one wave, the row held in registers: lane l
 // holds the 8-element chunks l, l+64, ..., (R of them; d a multiple of 8 up to
 // 512 R, rows 16-byte aligned), so the row crosses HBM once each way and every
@@ -274,11 +288,25 @@ struct GemmArgs {
   // RESID on the skinny path only (gemm_skinny_row_norm says when), at most
   // one of: rinv_out[m] = 1/sqrt(mean(v^2) + row_eps), or ln_out[m] (bf16,
   // [M][N]) = (v - mean) / sqrt(var + row_eps), of each result row v (its
-  // bf16 values); nullable
+  // bf16 values); nullable.  Or exit (nullable): the GLOBAL exit test of
+  // each result row (as adept_exit_test: flags, similarities, inertia update).
   float* rinv_out; void* ln_out; float row_eps;
+  const struct RowExit* exit;
+};
+// The GLOBAL-metric exit test (Eq. 7-8) run by a residual epilogue over its
+// result rows m (token rows rows[m]): flags and similarities by m, the
+// inertia by token row.
+struct RowExit {
+  double delta;
+  int layer, min_exit_layer, n_layers;
+  float* inertia;               // [n_tok][N] f32, updated in place
+  const int32_t* force_layer;   // nullable
+  uint8_t* exit_flag;           // [M]
+  double* sim_out;              // [M], nullable
 };
 size_t skinny_ws_bytes(int n_cols, int K);
 // whether gemm() runs g on the skinny path and can fill g.rinv_out / g.ln_out
+// or run g.exit
 bool gemm_skinny_row_norm(const GemmArgs& g);
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s);       // bf16 MFMA path

@@ -127,11 +127,7 @@ void exit_test_kernel(
     pass = pass && sim_l >= p.delta;
     sim = (sim != sim || sim_l != sim_l) ? kNaN : fmin(sim, sim_l);
   }
-  bool ex = (p.layer >= p.min_exit_layer) && (p.layer <= p.n_layers - 1) && pass;
-  if (force_layer) {
-    const int f = force_layer[row];
-    if (f > 0) ex = (p.layer == f) && (p.layer <= p.n_layers - 1);
-  }
+  const bool ex = exit_decision(pass, p.layer, p.min_exit_layer, p.n_layers, force_layer, row);
   if (lane == 0) {
     exit_flag[k] = ex ? 1 : 0;
     if (sim_out) sim_out[k] = sim;

@@ -109,6 +109,8 @@ struct GP {
   float* rinv_out;          // skinny RESID: 1/rms of each result row (nullable)
   bf16* ln_out;             // skinny RESID: LayerNorm of each result row (nullable)
   float row_eps;
+  RowExit ex;               // skinny RESID: the exit test of each result row (has_exit)
+  int has_exit;
 };
 
 // x * sigmoid(x) with the hardware reciprocal (about 1 ulp in f32, far below
@@ -1274,19 +1276,26 @@ __global__ __launch_bounds__(256) void skinny_epilogue_kernel(GP p, int nout, Sk
   }
 }
 
-// The residual epilogue with the next norm of its result rows: one
+// The residual epilogue with the next step over its result rows: one
 // workgroup of 1024 threads per row m (rows of at most 4096; thread t owns
 // columns 4t..4t+3, so every partial of the row is in flight at once).  From
-// the bf16 results (the values a separate norm pass would read back), summed
-// in f32 lane by lane, across the wave, then over the 16 waves in order:
-// LN == false: rinv_out[m] = 1/sqrt(mean(v^2) + eps) (the next RMSNorm's
-// factor); LN == true: ln_out[m] = (v - mean) / sqrt(var + eps) (LayerNorm
-// without its affine part, two passes over the registers).
-template <bool LN>
+// the bf16 results (the values a separate pass would read back), summed lane
+// by lane, across the wave, then over the 16 waves in order:
+//  * ROW_RINV: rinv_out[m] = 1/sqrt(mean(v^2) + eps) (the next RMSNorm's
+//    factor), f32;
+//  * ROW_LN: ln_out[m] = (v - mean) / sqrt(var + eps) (LayerNorm without its
+//    affine part, two passes over the registers), f32;
+//  * ROW_EXIT: the GLOBAL exit test of the row against its inertia I:
+//    <v,v>, <I,I>, <v,I> in double (every product of two floats is exact),
+//    the decision of Eq. 8, then I += v/|v| (as adept_exit_test).
+enum { ROW_RINV = 0, ROW_LN = 1, ROW_EXIT = 2 };
+template <int MODE>
 __global__ __launch_bounds__(1024) void skinny_resid_row_kernel(GP p, int nout, SkSplit sp,
                                                                 const float* __restrict__ part) {
   __shared__ float wsum[16];
   __shared__ float total;
+  __shared__ double dsum[16][3];
+  __shared__ double dtot[3];
   const int M = p.M_dev ? min(*p.M_dev, p.M_max) : p.M_max;
   const int m = blockIdx.x;
   if (m >= M) return;
@@ -1323,7 +1332,50 @@ __global__ __launch_bounds__(1024) void skinny_resid_row_kernel(GP p, int nout, 
     __syncthreads();   // wsum and total are reused by the next sum
     return t;
   };
-  if (!LN) {
+  if (MODE == ROW_EXIT) {
+    const int row = p.rows[m];
+    float* ir = p.ex.inertia + (int64_t)row * nout;
+    f32x4_t i4 = {0.f, 0.f, 0.f, 0.f};
+    if (live) i4 = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(ir + n));
+    const float iv[4] = {i4[0], i4[1], i4[2], i4[3]};
+    double s3[3] = {0.0, 0.0, 0.0};   // <v,v>, <I,I>, <v,I>
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double a = v[e], b = iv[e];
+      s3[0] = fma(a, a, s3[0]);
+      s3[1] = fma(b, b, s3[1]);
+      s3[2] = fma(a, b, s3[2]);
+    }
+#pragma unroll
+    for (int q = 0; q < 3; ++q) s3[q] = wave_sum_f64(s3[q]);
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+      for (int q = 0; q < 3; ++q) dsum[threadIdx.x >> 6][q] = s3[q];
+    }
+    __syncthreads();
+    if (threadIdx.x < 3) {
+      double t = 0.0;
+#pragma unroll
+      for (int w = 0; w < 16; ++w) t += dsum[w][threadIdx.x];
+      dtot[threadIdx.x] = t;
+    }
+    __syncthreads();
+    const double nh = sqrt(dtot[0]), nr = sqrt(dtot[1]);
+    const double den = nh * nr;
+    const double sim = den > 0.0 ? dtot[2] / den : __longlong_as_double(0x7ff8000000000000ll);
+    if (threadIdx.x == 0) {
+      p.ex.exit_flag[m] = exit_decision(sim >= p.ex.delta, p.ex.layer, p.ex.min_exit_layer,
+                                        p.ex.n_layers, p.ex.force_layer, row) ? 1 : 0;
+      if (p.ex.sim_out) p.ex.sim_out[m] = sim;
+    }
+    if (live && nh > 0.0) {
+      const double inv = 1.0 / nh;
+      f32x4_t o4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o4[e] = (float)((double)iv[e] + (double)v[e] * inv);
+      __builtin_nontemporal_store(o4, reinterpret_cast<f32x4_t*>(ir + n));
+    }
+  } else if (MODE == ROW_RINV) {
     float ss = 0.0f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) ss = fmaf(v[e], v[e], ss);
@@ -1359,14 +1411,15 @@ adept_status launch_skinny(const GP& p, int Nt, int nout, hipStream_t s, const c
                        EPI == EPI_SWIGLU ? nout : Nt, sp, part);
   }
   ADEPT_CHECK_LAUNCH("gemm_skinny");
-  if (EPI == EPI_RESID && p.ln_out) {
-    ADEPT_LAUNCH(skinny_resid_row_kernel<true>, dim3(p.M_max), dim3(1024), 0, s, p, nout, sp, part);
-    return launch_status("skinny_resid_ln");
-  }
-  if (EPI == EPI_RESID && p.rinv_out) {
-    ADEPT_LAUNCH(skinny_resid_row_kernel<false>, dim3(p.M_max), dim3(1024), 0, s, p, nout, sp,
-                 part);
-    return launch_status("skinny_resid_rinv");
+  if (EPI == EPI_RESID && (p.ln_out || p.rinv_out || p.has_exit)) {
+    const dim3 g(p.M_max), b(1024);
+    if (p.has_exit)
+      ADEPT_LAUNCH(skinny_resid_row_kernel<ROW_EXIT>, g, b, 0, s, p, nout, sp, part);
+    else if (p.ln_out)
+      ADEPT_LAUNCH(skinny_resid_row_kernel<ROW_LN>, g, b, 0, s, p, nout, sp, part);
+    else
+      ADEPT_LAUNCH(skinny_resid_row_kernel<ROW_RINV>, g, b, 0, s, p, nout, sp, part);
+    return launch_status("skinny_resid_row");
   }
   const int64_t total = (int64_t)p.M_max * (nout / 4);
   ADEPT_LAUNCH(skinny_epilogue_kernel<EPI>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
@@ -1387,6 +1440,8 @@ GP to_gp(const GemmArgs& g) {
   p.bias_layer_stride = g.bias_layer_stride; p.a_sorted = g.a_sorted;
   p.A2 = (const bf16*)g.A2; p.a_sel = g.a_sel;
   p.rinv_out = g.rinv_out; p.ln_out = (bf16*)g.ln_out; p.row_eps = g.row_eps;
+  p.has_exit = g.exit != nullptr;
+  if (g.exit) p.ex = *g.exit;
   return p;
 }
 
@@ -1412,10 +1467,12 @@ bool gemm_skinny_row_norm(const GemmArgs& g) {
 
 adept_status gemm(adept_dtype dt, const GemmArgs& g, hipStream_t s) {
   if (g.M_max <= 0) return ADEPT_OK;
-  if ((g.rinv_out || g.ln_out) && (!gemm_skinny_row_norm(g) || (g.rinv_out && g.ln_out) ||
-                                    (g.ln_out && !aligned8(g.ln_out)))) {
-    set_error("gemm: rinv_out / ln_out (one of them, ln_out 8-byte aligned) only on the skinny "
-              "residual path (see gemm_skinny_row_norm)");
+  if ((g.rinv_out || g.ln_out || g.exit) &&
+      (!gemm_skinny_row_norm(g) || (!!g.rinv_out + !!g.ln_out + !!g.exit) > 1 ||
+       (g.ln_out && !aligned8(g.ln_out)) ||
+       (g.exit && (!g.exit->inertia || !aligned16(g.exit->inertia) || !g.exit->exit_flag)))) {
+    set_error("gemm: one of rinv_out / ln_out (8-byte aligned) / exit (16-byte aligned inertia, "
+              "flags) only on the skinny residual path (see gemm_skinny_row_norm)");
     return ADEPT_E_INVALID;
   }
   if (dt != ADEPT_BF16) {

@@ -310,6 +310,21 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
                         ln_r <= 8 && aligned16(a->h[0]) && aligned16(a->h[1]) &&
                         aligned16(ws.xnorm);
   const dim3 fgrid(ceil_div(std::max(qmax, 1), 4));
+  // the GLOBAL exit test (step 8) can run in the down projection's epilogue
+  // on the skinny path (each result row tested as it is formed)
+  RowExit rx{a->exit.delta, layer, a->exit.min_exit_layer, a->exit.n_layers, a->inertia,
+             a->force_layer, a->exit_flag, a->sim_out};
+  bool exit_done = false;
+  auto exit_in_epilogue = [&](GemmArgs& g) -> adept_status {
+    if (dt != ADEPT_BF16 || a->exit.metric != ADEPT_SIM_GLOBAL || !gemm_skinny_row_norm(g))
+      return ADEPT_OK;
+    // the exit test's argument checks, with no rows to test
+    ADEPT_TRY(adept_exit_test(dt, D, layer, &a->exit, act, nact, 0, a->h[out], a->h[in],
+                              a->inertia, a->force_layer, a->exit_flag, a->sim_out, stream));
+    g.exit = &rx;
+    exit_done = true;
+    return ADEPT_OK;
+  };
   if (rinv_fused) {
     ADEPT_LAUNCH(fused_rows_rinv_kernel<bf16>, fgrid, dim3(256), 0, s, a->n_tok, layer, D,
                  a->rms_eps, a->exit_layer, act, nact, maxn, (const bf16*)a->h[in],
@@ -393,6 +408,7 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     gd.bias = off(a->b_proj, li * D);
     gd.C = a->h[out]; gd.ldc = D; gd.resid = a->h[out]; gd.rows = act; gd.name = "gemm_proj";
     gd.skinny_ws = ws.skinny; gd.skinny_ws_bytes = ws.skinny_bytes;
+    ADEPT_TRY(exit_in_epilogue(gd));
     ADEPT_TRY(gemm(dt, gd, s));
   } else if (qmax > 0) {
     // 1. pre-attention RMSNorm: the gain is folded into W_qkv, the row factor
@@ -443,11 +459,13 @@ extern "C" adept_status adept_layer_step(const adept_layer_args* a, int layer, v
     gd.A = a->ffn_act; gd.lda = F; gd.B = wd; gd.ldb = F; gd.epi = EPI_RESID;
     gd.C = a->h[out]; gd.ldc = D; gd.resid = a->h[out]; gd.rows = act; gd.name = "gemm_down";
     gd.skinny_ws = ws.skinny; gd.skinny_ws_bytes = ws.skinny_bytes;
+    ADEPT_TRY(exit_in_epilogue(gd));
     ADEPT_TRY(run_gemm(dt, gd, ws.gemm_tmp, s));
   }
-  // 8. exit test (Eq. 7-8)
-  ADEPT_TRY(adept_exit_test(dt, D, layer, &a->exit, act, nact, maxn, a->h[out], a->h[in],
-                            a->inertia, a->force_layer, a->exit_flag, a->sim_out, stream));
+  // 8. exit test (Eq. 7-8), unless the down projection's epilogue ran it
+  if (!exit_done)
+    ADEPT_TRY(adept_exit_test(dt, D, layer, &a->exit, act, nact, maxn, a->h[out], a->h[in],
+                              a->inertia, a->force_layer, a->exit_flag, a->sim_out, stream));
   // all-at-once variant (Appendix H.2): a prompt's last token decides for all of it
   if (a->exit.prompt_level && a->attn_tiles)
     ADEPT_TRY(adept_exit_prompt_level(act, nact, maxn, a->seq, a->pos, a->n_seq, a->exit_flag,
